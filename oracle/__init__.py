@@ -1,0 +1,275 @@
+"""WUSH-KV CPU oracle -- test infrastructure only.
+
+Python view of the plain C reference in ``wushkv_oracle.c``.  Only the tests,
+``__graft_entry__.smoke()`` and the benchmark's ``cpu_baseline`` leg may
+import this package; the GPU library and its Python binding never do, and
+this package imports nothing from them.
+
+The oracle works on a *logical* cache: per (sequence, kv-head) it keeps the
+bf16 value of every position plus the codes and fp16 (scale, zero) of the
+quantised positions.  It knows nothing of pages, rings or kernel layouts.
+
+Paper references: Eq. (2) attention, Eq. (3) transform insertion, Eq. (7)
+quantiser, Sec. 3.4 windows, Alg. 2 cache management.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "wushkv_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "_build", "liboracle.so")
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (fp-contract off: the quantiser's fp32
+    sequence must not be fused)."""
+    if not force and os.path.exists(_LIB_PATH):
+        return _LIB_PATH
+    os.makedirs(os.path.dirname(_LIB_PATH), exist_ok=True)
+    tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-std=c11", "-O2", "-ffp-contract=off", "-fno-fast-math",
+           "-fPIC", "-shared", "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build()
+        _lib = ctypes.CDLL(_LIB_PATH)
+        _declare(_lib)
+    return _lib
+
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+_F32 = ctypes.c_float
+
+
+def _declare(L):
+    L.orc_bf16_to_f32.argtypes = [ctypes.c_uint16]
+    L.orc_bf16_to_f32.restype = _F32
+    L.orc_f32_to_bf16.argtypes = [_F32]
+    L.orc_f32_to_bf16.restype = ctypes.c_uint16
+    L.orc_f32_to_f16.argtypes = [_F32]
+    L.orc_f32_to_f16.restype = ctypes.c_uint16
+    L.orc_f16_to_f32.argtypes = [ctypes.c_uint16]
+    L.orc_f16_to_f32.restype = _F32
+    for name in ("orc_f32_to_bf16_array", "orc_f32_to_f16_array",
+                 "orc_f16_to_f32_array", "orc_f64_to_bf16_array"):
+        getattr(L, name).argtypes = [_P, _P, _I64]
+        getattr(L, name).restype = None
+    L.orc_kappa_position.argtypes = [_F32, ctypes.c_int, _P, _P]
+    L.orc_kappa_position.restype = None
+    L.orc_quantile_abs.argtypes = [_P, ctypes.c_int, _I32, _F32]
+    L.orc_quantile_abs.restype = _F32
+    L.orc_quantize_groups.argtypes = [_P, _I64, ctypes.c_int, ctypes.c_int, _F32, _P, _P]
+    L.orc_quantize_groups.restype = None
+    L.orc_dequant.argtypes = [ctypes.c_uint8, ctypes.c_uint16, ctypes.c_uint16]
+    L.orc_dequant.restype = _F32
+    L.orc_next_quant_end.argtypes = [_I32] * 5
+    L.orc_next_quant_end.restype = _I32
+    L.orc_append_head.argtypes = [ctypes.c_int] * 5 + [_F32, _F32, _I32, _I32, _I32,
+                                                       _P, _I64, _P, _I64, _P,
+                                                       _P, _P, _P, _P, _P, _P]
+    L.orc_append_head.restype = _I32
+    L.orc_attend.argtypes = [ctypes.c_int, _I64, _P, _P, _P, ctypes.c_double, _P]
+    L.orc_attend.restype = None
+    L.orc_decode_head.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, _I32, _I32,
+                                  _P, _P, _P, _P, _P, _P, _P, _P, _F32, _P]
+    L.orc_decode_head.restype = None
+
+
+def _ptr(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"], "oracle arrays must be C-contiguous"
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+# --------------------------------------------------------------------------
+# Number formats
+# --------------------------------------------------------------------------
+
+def _conv(x, in_dtype, out_dtype, fn_name):
+    a = np.asarray(x, dtype=in_dtype)
+    flat = np.ascontiguousarray(a.reshape(-1))
+    y = np.empty(flat.shape, dtype=out_dtype)
+    getattr(lib(), fn_name)(_ptr(flat), _ptr(y), flat.size)
+    return y.reshape(a.shape)
+
+
+def f32_to_bf16(x) -> np.ndarray:
+    """fp32 -> bf16 bit patterns (uint16), round to nearest even."""
+    return _conv(x, np.float32, np.uint16, "orc_f32_to_bf16_array")
+
+
+def f64_to_bf16(x) -> np.ndarray:
+    """fp64 -> bf16 bit patterns in a single rounding."""
+    return _conv(x, np.float64, np.uint16, "orc_f64_to_bf16_array")
+
+
+def bf16_to_f32(h) -> np.ndarray:
+    a = np.asarray(h, dtype=np.uint16)
+    return (a.astype(np.uint32) << 16).view(np.float32)
+
+
+def f32_to_f16(x) -> np.ndarray:
+    """fp32 -> fp16 bit patterns (uint16), round to nearest even."""
+    return _conv(x, np.float32, np.uint16, "orc_f32_to_f16_array")
+
+
+def f16_to_f32(h) -> np.ndarray:
+    return _conv(h, np.uint16, np.float32, "orc_f16_to_f32_array")
+
+
+# --------------------------------------------------------------------------
+# Quantiser, Eq. (7)
+# --------------------------------------------------------------------------
+
+def kappa_position(kappa: float, d: int):
+    lo = ctypes.c_int32()
+    t = ctypes.c_float()
+    lib().orc_kappa_position(kappa, d, ctypes.byref(lo), ctypes.byref(t))
+    return lo.value, t.value
+
+
+def quantile_abs(x, kappa: float) -> float:
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    lo, t = kappa_position(kappa, x.size)
+    return lib().orc_quantile_abs(_ptr(x), x.size, lo, t)
+
+
+def quantize_groups(x, bits: int, kappa: float):
+    """x [..., d] fp32 -> (codes uint8 [..., d], scale16 uint16 [...], zero16 uint16 [...])."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    d = x.shape[-1]
+    n = x.size // d
+    codes = np.empty(x.shape, dtype=np.uint8)
+    params = np.empty(x.shape[:-1] + (2,), dtype=np.uint16)
+    lib().orc_quantize_groups(_ptr(x), n, d, bits, kappa, _ptr(codes), _ptr(params))
+    return codes, params[..., 0].copy(), params[..., 1].copy()
+
+
+def dequant(codes, s16, z16) -> np.ndarray:
+    """fp32 reconstruction scale * code + zero (one rounding)."""
+    codes = np.asarray(codes, dtype=np.uint8)
+    s = f16_to_f32(np.asarray(s16, dtype=np.uint16))[..., None]
+    z = f16_to_f32(np.asarray(z16, dtype=np.uint16))[..., None]
+    # s * code is exact in fp32 (11-bit significand times a <= 4-bit integer),
+    # so the fp64 sum rounded once to fp32 equals fmaf(s, code, z).
+    return (s.astype(np.float64) * codes + z.astype(np.float64)).astype(np.float32)
+
+
+# --------------------------------------------------------------------------
+# Windows and bookkeeping, Sec. 3.4 / Alg. 2
+# --------------------------------------------------------------------------
+
+def next_quant_end(s_new: int, s_quant: int, s_sink: int, s_keep: int, s_flush: int) -> int:
+    return lib().orc_next_quant_end(s_new, s_quant, s_sink, s_keep, s_flush)
+
+
+class OracleCache:
+    """Logical WUSH-KV cache for ``batch`` sequences and ``n_kv`` heads.
+
+    Holds, per (sequence, head), the bf16 pattern of every cached position and
+    the codes / fp16 params of the quantised ones.  ``append`` follows Alg. 2
+    steps 3-4 and 7-11; ``decode`` follows Eq. (2) with the Eq. (3) query
+    compensation.
+    """
+
+    def __init__(self, batch, n_kv, d, bits, s_sink, s_keep, s_flush,
+                 kappa_k, kappa_v, capacity):
+        self.batch, self.n_kv, self.d, self.bits = batch, n_kv, d, bits
+        self.s_sink, self.s_keep, self.s_flush = s_sink, s_keep, s_flush
+        self.kappa_k, self.kappa_v = float(kappa_k), float(kappa_v)
+        self.cap = capacity
+        shp = (batch, n_kv, capacity, d)
+        self.kbits = np.zeros(shp, np.uint16)
+        self.vbits = np.zeros(shp, np.uint16)
+        self.kc = np.zeros(shp, np.uint8)
+        self.vc = np.zeros(shp, np.uint8)
+        self.kp = np.zeros((batch, n_kv, capacity, 2), np.uint16)
+        self.vp = np.zeros((batch, n_kv, capacity, 2), np.uint16)
+        self.seq_len = np.zeros(batch, np.int32)
+        self.quant_end = np.zeros(batch, np.int32)
+
+    def append(self, k_new, v_new, n_new, tk):
+        """k_new, v_new: bf16 patterns [batch][max_new][n_kv][d];
+        n_new: [batch] ints; tk: bf16 patterns [n_kv][d][d] (k~ = T_K k)."""
+        k_new = np.ascontiguousarray(k_new, dtype=np.uint16)
+        v_new = np.ascontiguousarray(v_new, dtype=np.uint16)
+        tk = np.ascontiguousarray(tk, dtype=np.uint16)
+        L = lib()
+        d, nkv = self.d, self.n_kv
+        row_stride = nkv * d
+        for b in range(self.batch):
+            n = int(n_new[b])
+            s_old, q_old = int(self.seq_len[b]), int(self.quant_end[b])
+            assert s_old + n <= self.cap, "oracle cache capacity exceeded"
+            q_new = q_old
+            for h in range(nkv):
+                # pointer to (b, token 0, head h); token rows are row_stride apart
+                kptr = ctypes.c_void_p(k_new.ctypes.data + (b * k_new.shape[1] * nkv + h) * d * 2)
+                vptr = ctypes.c_void_p(v_new.ctypes.data + (b * v_new.shape[1] * nkv + h) * d * 2)
+                q_new = L.orc_append_head(
+                    d, self.bits, self.s_sink, self.s_keep, self.s_flush,
+                    self.kappa_k, self.kappa_v, s_old, q_old, n,
+                    kptr, row_stride, vptr, row_stride,
+                    _ptr(tk[h]),
+                    _ptr(self.kbits[b, h]), _ptr(self.vbits[b, h]),
+                    _ptr(self.kc[b, h]), _ptr(self.kp[b, h]),
+                    _ptr(self.vc[b, h]), _ptr(self.vp[b, h]))
+            self.seq_len[b] = s_old + n
+            self.quant_end[b] = q_new
+
+    def decode(self, q, tinv, sm_scale, heads=None):
+        """q: bf16 patterns [batch][n_q][d]; tinv: fp32 [n_kv][d][d].
+        Returns fp64 [batch][n_q][d].  ``heads`` optionally restricts the work
+        to a list of (b, h) pairs (other rows are left NaN)."""
+        q = np.ascontiguousarray(q, dtype=np.uint16)
+        tinv = np.ascontiguousarray(tinv, dtype=np.float32)
+        nq = q.shape[1]
+        G = nq // self.n_kv
+        out = np.full((self.batch, nq, self.d), np.nan, np.float64)
+        pairs = heads if heads is not None else [(b, h) for b in range(self.batch)
+                                                 for h in range(self.n_kv)]
+        for b, h in pairs:
+            o = np.empty((G, self.d), np.float64)
+            qg = np.ascontiguousarray(q[b, h * G:(h + 1) * G])
+            decode_head(self.d, G, self.s_sink, int(self.seq_len[b]), int(self.quant_end[b]),
+                        self.kbits[b, h], self.vbits[b, h], self.kc[b, h], self.kp[b, h],
+                        self.vc[b, h], self.vp[b, h], qg, tinv[h], sm_scale, o)
+            out[b, h * G:(h + 1) * G] = o
+        return out
+
+
+def decode_head(d, G, s_sink, S, q_end, kbits, vbits, kc, kp, vc, vp, q, tinv, sm_scale, out):
+    """Thin wrapper over orc_decode_head; arrays are per (sequence, head):
+    kbits/vbits [cap][d] uint16, kc/vc [cap][d] uint8, kp/vp [cap][2] uint16,
+    q [G][d] uint16 (bf16), tinv [d][d] fp32, out [G][d] fp64 (written)."""
+    args = [np.ascontiguousarray(a) for a in (kbits, vbits, kc, kp, vc, vp, q, tinv)]
+    assert out.flags["C_CONTIGUOUS"] and out.dtype == np.float64
+    lib().orc_decode_head(d, G, s_sink, S, q_end, *[_ptr(a) for a in args],
+                          float(sm_scale), _ptr(out))
+    return out
+
+
+def attend(q, K, V, scale: float) -> np.ndarray:
+    """fp64 softmax attention of one query q [d] over K, V [S][d]."""
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    K = np.ascontiguousarray(K, dtype=np.float64)
+    V = np.ascontiguousarray(V, dtype=np.float64)
+    d = q.shape[0]
+    out = np.empty(d, np.float64)
+    lib().orc_attend(d, K.shape[0], _ptr(q), _ptr(K), _ptr(V), float(scale), _ptr(out))
+    return out
