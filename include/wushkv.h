@@ -1,0 +1,237 @@
+/*
+ * wushkv.h -- C ABI of the WUSH-KV online hot path on AMD Instinct MI355X
+ * (gfx950).
+ *
+ * WUSH-KV ("KV Cache Quantization with Data-Adaptive Transforms") caches, for
+ * every key/value head h of a grouped-query attention layer, the quantised
+ * transformed keys Q(T_K(h) k) and values Q(T_V(h) v) (Eq. (3)).  The value
+ * transform is folded into the projection weights offline, so values arrive
+ * here already transformed; the key transform is applied online after norm
+ * and RoPE.  Queries are compensated with T_K^{-T} (Alg. 2, step 3).  The
+ * quantiser is the per-token percentile-clipped affine quantiser of Eq. (7)
+ * and the cache keeps two bf16 windows, a sink and a recent window, with
+ * quantisation in multiples of S_flush (Sec. 3.4, Alg. 2).
+ *
+ * Entry points:
+ *   wushkv_append            Alg. 2 steps 3 (keys), 4 and 7-11
+ *   wushkv_decode_attention  Alg. 2 steps 3 (queries) and 5, Eq. (2)
+ *   wushkv_dequant           the reconstruction of Eq. (7) for stored tokens
+ *
+ * Conventions
+ *   - Every pointer is a DEVICE pointer unless marked (host), and must be
+ *     16-byte aligned.  bf16 and fp16 values are passed as uint16_t bit
+ *     patterns.
+ *   - The caller owns all memory.  The library never allocates device memory
+ *     on these paths, never frees and never synchronises; all work is
+ *     enqueued on the caller's stream.  No call mutates library state, so
+ *     calls on different streams with disjoint caches may run concurrently.
+ *   - Argument checks happen on the host before anything is enqueued; a
+ *     failing check returns a negative status and enqueues nothing.
+ *   - Device-resident values (seq_len, quant_end, n_new, page_table) cannot
+ *     be checked on the host.  The kernels never access memory outside the
+ *     bounds the descriptor states (a page index outside [0, n_pages) or a
+ *     logical page beyond max_pages_per_seq is skipped), but the results of
+ *     a call that breaks the capacity contract are unspecified.
+ *
+ * Status codes: WUSHKV_OK (0) or a negative WUSHKV_E* value;
+ * wushkv_status_string() names them.
+ */
+#ifndef WUSHKV_H
+#define WUSHKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t *wushkv_stream_t; /* same type as hipStream_t */
+
+enum {
+    WUSHKV_OK = 0,
+    WUSHKV_EINVAL = -1,       /* null pointer or value out of range */
+    WUSHKV_EUNSUPPORTED = -2, /* valid per the paper but not built here */
+    WUSHKV_EWORKSPACE = -3,   /* workspace too small */
+    WUSHKV_ELAUNCH = -4,      /* the HIP runtime refused a launch */
+    WUSHKV_ENODEVICE = -5     /* no usable gfx950 device */
+};
+
+#define WUSHKV_PAGE_TOKENS 64
+#define WUSHKV_ABI_VERSION 1
+
+/*
+ * Cache descriptor.  Sizes are host values; the arrays are device memory.
+ *
+ * Positions p of sequence b are counted from 0.  With S = seq_len[b] and
+ * S_quant = quant_end[b] (the paper's inclusive 1-based boundary is the same
+ * integer as this exclusive 0-based end):
+ *   p <  s_sink                       sink window, bf16, slot p
+ *   s_sink <= p < max(S_quant,s_sink) quantised (Eq. (7)), in pages
+ *   max(S_quant, s_sink) <= p < S     recent window, bf16, ring slot
+ *                                     s_sink + (p - s_sink) mod R,
+ *                                     R = win_slots - s_sink
+ *
+ * Quantised positions live in pages of 64 tokens.  Logical page i of
+ * sequence b holds positions s_sink + 64 i .. s_sink + 64 i + 63 and is
+ * physical page page_table[b * max_pages_per_seq + i].
+ *
+ * pages: uint8 [n_pages][n_kv_heads][page_bytes], page_bytes =
+ *   wushkv_page_bytes(head_dim, bits) = 64 * (2 * head_dim * bits / 8 + 8).
+ *   One (page, head) block is, in order:
+ *     K codes   8 * head_dim * bits bytes
+ *     V codes   8 * head_dim * bits bytes
+ *     K params  64 tokens x 4 bytes: fp16 scale, fp16 zero (token t at 4 t)
+ *     V params  64 tokens x 4 bytes, same form
+ *   Reconstruction of a stored entry: x = scale * code + zero (fp32 fma).
+ *
+ *   Code words.  Both code regions are arrays of little-endian 32-bit words.
+ *   A word holds B = 32 / bits codes, "elements" e = 0 .. B-1; element e sits
+ *   at bit 16 * (e % 2) + bits * (e / 2): even elements fill the low half
+ *   word, odd elements the high half, each in increasing order.  Element e
+ *   belongs to operand o = e / 8, slot i = e % 8.  With nw = head_dim * bits
+ *   / 128, each region holds 64 "lanes" L = 16 j + m (j = 0..3, m = 0..15)
+ *   of 4 nw words each:
+ *
+ *   K word at index L * 4nw + tau * nw + w   (tau = 0..3, w = 0..nw-1)
+ *     token    32 (tau / 2) + 8 (m / 4) + 4 (tau % 2) + (m % 4)
+ *     channel  32 c + 8 j + i,  c = w * (B / 8) + o
+ *   V word at index L * 4nw + kc * 2nw + u   (kc = 0..1, u = 0..2nw-1)
+ *     token    32 kc + 8 j + i
+ *     channel  16 nt + m,  nt = u * (B / 8) + o
+ *
+ *   (This is the operand order of the 16x16x32 bf16 matrix instructions the
+ *   decode kernel feeds: a lane loads its words with 128-bit loads and
+ *   widens two codes per 32-bit operand register.)
+ *
+ * win_k: bf16 [batch][n_kv_heads][win_slots][head_dim]   (token-major)
+ * win_v: bf16 [batch][n_kv_heads][head_dim][win_slots]   (channel-major)
+ *   Keys in transformed coordinates (T_K k, rounded to bf16), values as
+ *   given (already transformed).  Slots that hold no live position may hold
+ *   any bit pattern, NaN included; they are never read into a result.
+ */
+typedef struct wushkv_cache {
+    int32_t batch;             /* sequences, >= 1 */
+    int32_t n_kv_heads;        /* >= 1 */
+    int32_t head_dim;          /* 64 or 128 */
+    int32_t bits;              /* 2 or 4, for keys and values */
+    int32_t s_sink;            /* >= 0 */
+    int32_t s_keep;            /* >= 0 */
+    int32_t s_flush;           /* >= 1 */
+    int32_t win_slots;         /* multiple of 64, >= s_sink + max(1, s_keep + s_flush - 1) */
+    int32_t max_pages_per_seq; /* row length of page_table, >= 0 */
+    int32_t n_pages;           /* pages in the pool, >= 0 */
+    float kappa_k;             /* Eq. (7) clipping quantile for keys, (0, 1] */
+    float kappa_v;             /* same for values */
+    uint8_t *pages;
+    int32_t *page_table;       /* [batch][max_pages_per_seq] */
+    uint16_t *win_k;
+    uint16_t *win_v;
+    int32_t *seq_len;          /* [batch] S; read and advanced by wushkv_append */
+    int32_t *quant_end;        /* [batch] S_quant; read and advanced by wushkv_append */
+} wushkv_cache;
+
+/* Bytes of one (page, head) block, or 0 for unsupported (head_dim, bits). */
+size_t wushkv_page_bytes(int32_t head_dim, int32_t bits);
+
+/*
+ * wushkv_append -- append new tokens to every sequence (Alg. 2 steps 3-4)
+ * and quantise the newly eligible positions (Alg. 2 steps 7-11).
+ *
+ *   k_new   bf16 [batch][max_new][n_kv_heads][head_dim]: keys after headwise
+ *           norm and RoPE.  Row t of sequence b is position seq_len[b] + t.
+ *   v_new   bf16, same shape: values, already in transformed coordinates.
+ *   n_new   int32 [batch]: tokens appended to each sequence, 0..max_new.
+ *   max_new (host) upper bound of n_new, sizes the grid; 0 is a no-op.
+ *   t_k     bf16 [n_kv_heads][head_dim][head_dim] row-major: the stored key
+ *           is k~ = T_K k, i.e. k~[o] = sum_i t_k[o][i] k[i], accumulated in
+ *           fp32 and rounded once to bf16 (Alg. 2 step 3).
+ *   k_tilde_out  nullable; bf16 of k_new's shape: receives k~ for every
+ *           appended token (a verification aid; costs one extra write).
+ *
+ * Effect, per sequence b with S = seq_len[b], S' = n_new[b]:
+ *   S_new = S + S'; S_start = max(S_quant, s_sink);
+ *   S_quant_new = max(S_quant, S_start + floor((S_new - s_keep - S_start)
+ *                 / s_flush) * s_flush)          (floor toward -infinity);
+ *   positions [S_start, S_quant_new) are quantised with Eq. (7) from their
+ *   bf16 values (kappa_k for keys, kappa_v for values); new positions below
+ *   s_sink go to the sink, new positions at or after S_quant_new go to the
+ *   recent ring; seq_len[b] = S_new; quant_end[b] = S_quant_new.
+ * Capacity (caller's contract): page_table holds valid pages for every
+ *   logical page the new S_quant reaches.
+ */
+int wushkv_append(const wushkv_cache *c,
+                  const uint16_t *k_new, const uint16_t *v_new,
+                  const int32_t *n_new, int32_t max_new,
+                  const uint16_t *t_k, uint16_t *k_tilde_out,
+                  wushkv_stream_t stream);
+
+/*
+ * wushkv_decode_attention -- one decode query per query head (Eq. (2)).
+ *
+ *   q          bf16 [batch][n_q_heads][head_dim]: queries after norm and RoPE.
+ *              Query head (h, g) is flat index h * G + g, G = n_q / n_kv.
+ *   n_q_heads  (host) multiple of n_kv_heads; G <= 8.
+ *   max_seq_len (host) >= every seq_len[b]; sizes the split-K grid.
+ *   t_k_inv    fp32 [n_kv_heads][head_dim][head_dim] row-major T_K^{-1}:
+ *              the compensated query is q~[j] = sum_i q[i] t_k_inv[i][j]
+ *              (the row form of T_K^{-T} q, Eq. (3)).
+ *   sm_scale   softmax scale 1 / tau (usually 1 / sqrt(head_dim)).
+ *   out        fp32 [batch][n_q_heads][head_dim]: attention output in
+ *              transformed value coordinates (the folded W_O consumes it).
+ *              A sequence with seq_len 0 gets zeros.
+ *   workspace  device scratch of at least wushkv_decode_workspace_bytes();
+ *              contents need not be initialised and are clobbered.
+ *
+ * The query of sequence b attends to all positions [0, seq_len[b]): sink
+ * and recent windows at bf16, the middle through the stored codes.
+ */
+int wushkv_decode_attention(const wushkv_cache *c,
+                            const uint16_t *q, int32_t n_q_heads,
+                            int32_t max_seq_len,
+                            const float *t_k_inv, float sm_scale,
+                            float *out, void *workspace,
+                            size_t workspace_bytes,
+                            wushkv_stream_t stream);
+
+/* Workspace bytes wushkv_decode_attention needs for these sizes (0 on bad
+ * arguments). */
+size_t wushkv_decode_workspace_bytes(const wushkv_cache *c,
+                                     int32_t n_q_heads, int32_t max_seq_len);
+
+/*
+ * wushkv_dequant -- reconstruct stored entries x = scale * code + zero
+ * (Eq. (7), last term) of sequence b, positions [start, start + count).
+ *   k_out, v_out  fp32 [n_kv_heads][count][head_dim] (either may be null).
+ * Positions must satisfy start >= s_sink and start + count <= s_sink + 64 *
+ * max_pages_per_seq (host-checked).  The pages are decoded as stored,
+ * whether or not quant_end has reached the position; a logical page whose
+ * physical index lies outside [0, n_pages) yields NaN.
+ */
+int wushkv_dequant(const wushkv_cache *c, int32_t b, int32_t start,
+                   int32_t count, float *k_out, float *v_out,
+                   wushkv_stream_t stream);
+
+/* Name of a status code. */
+const char *wushkv_status_string(int status);
+
+/* WUSHKV_ABI_VERSION of the loaded library. */
+int wushkv_abi_version(void);
+
+/*
+ * Kernel timing for measurement.  While enabled (slots > 0), every launch
+ * the library makes is bracketed by a pair of HIP events on its stream, for
+ * up to `slots` launches; disabling (slots = 0) releases the events.  This
+ * is the only library state and it is not thread-safe; leave it off in
+ * production.  wushkv_timing_read synchronises on the recorded events and
+ * returns, for launches whose kernel name contains `name_substr`, the count
+ * and the summed milliseconds, then clears the record.
+ */
+int wushkv_timing_enable(int32_t slots);
+int wushkv_timing_read(const char *name_substr, int32_t *count, double *total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WUSHKV_H */

@@ -1,0 +1,551 @@
+// wushkv_append: online key transform, window routing and per-token
+// percentile-clipped quantisation into packed pages (Alg. 2 steps 3-4 and
+// 7-11; quantiser Eq. (7); windows Sec. 3.4).
+//
+// One workgroup (256 threads, four waves) owns one tile of up to 64
+// consecutive positions of one (sequence, kv head): either a chunk of the
+// sink window or exactly one logical page of the quantised region.  Owning a
+// whole page means the read-modify-write of shared value-code words never
+// races inside a launch.
+//
+//   phase A  new keys k (bf16) x T_K^T on the 16x16x32 bf16 matrix cores,
+//            fp32 accumulate, rounded once to bf16 -> LDS.  Keys that are
+//            flushed from the recent ring are copied from it instead.
+//            Values (new or ring) -> LDS.
+//   phase B  one thread per (token, K|V) group: exact top-k of |x| with a
+//            median-of-three insertion network, the type-7 quantile, fp16
+//            scale/zero and the codes.  Key codes go straight to their words;
+//            value codes go to LDS.
+//   phase C  value-code words (each spans 8 tokens) are assembled from LDS;
+//            words only partly covered by this call are merged with what the
+//            page already holds.
+//   phase D  bf16 window writes (sink and ring) and the optional k~ output.
+#include "common.h"
+
+namespace wushkv {
+
+enum { kModeFlush = 1, kModeNew = 2 };
+
+struct AppendArgs {
+    uint8_t *pages;
+    const int32_t *page_table;
+    uint16_t *win_k;
+    uint16_t *win_v;
+    const int32_t *seq_len;
+    const int32_t *quant_end;
+    int32_t n_kv, s_sink, s_keep, s_flush, win_slots, max_pages, n_pages;
+    int32_t lo_k, lo_v;  // quantile positions: lo = floor(kappa (d-1))
+    float t_k, t_v;      // and t = kappa (d-1) - lo
+    const uint16_t *k_new;
+    const uint16_t *v_new;
+    const int32_t *n_new;
+    int32_t max_new;
+    const uint16_t *tk;
+    uint16_t *k_tilde_out;
+    int32_t mode;
+    int32_t sink_tiles;  // ceil(s_sink / 64)
+};
+
+// Descending top-KMAX of the values pushed so far; t[0] is the largest.
+// Inserting a into a sorted list is one median-of-three per slot:
+// new t[i] = med3(t[i-1], t[i], a).
+template <int KMAX>
+struct TopK {
+    float t[KMAX];
+    __device__ __forceinline__ void init()
+    {
+#pragma unroll
+        for (int i = 0; i < KMAX; ++i) t[i] = -1.0f;
+    }
+    __device__ __forceinline__ void push(float a)
+    {
+#pragma unroll
+        for (int i = KMAX - 1; i >= 1; --i) t[i] = __builtin_amdgcn_fmed3f(t[i - 1], t[i], a);
+        t[0] = fmaxf(t[0], a);
+    }
+    __device__ __forceinline__ float get(int k) const
+    {
+        float r = t[0];
+#pragma unroll
+        for (int i = 1; i < KMAX; ++i) r = (k == i) ? t[i] : r;
+        return r;
+    }
+};
+
+// a_lo and a_{lo+1} of the ascending sort of |x| over a bf16 row in LDS,
+// for lo >= D - KMAX.
+template <int D, int KMAX>
+__device__ __forceinline__ void order_stats_topk(const uint16_t *row, int lo, float &a_lo,
+                                                 float &a_hi, float &mn, float &mx)
+{
+    TopK<KMAX> tk;
+    tk.init();
+    mn = INFINITY;
+    mx = -INFINITY;
+#pragma unroll 4
+    for (int c8 = 0; c8 < D / 8; ++c8) {
+        uint4 v = *reinterpret_cast<const uint4 *>(row + 8 * c8);
+        uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+                float x = bf16_bits_to_f32(hh ? (w[q] >> 16) : (w[q] & 0xFFFFu));
+                mn = fminf(mn, x);
+                mx = fmaxf(mx, x);
+                tk.push(fabsf(x));
+            }
+        }
+    }
+    const int K = D - lo;  // a_lo is the K-th largest
+    a_lo = tk.get(K - 1);
+    a_hi = (K >= 2) ? tk.get(K - 2) : a_lo;
+}
+
+// Same order statistics by counting ranks: any lo, O(D^2) work.  Used when
+// kappa is small enough that the top-k list would not fit in registers.
+template <int D>
+__device__ __noinline__ void order_stats_rank(const uint16_t *row, int lo, float &a_lo,
+                                              float &a_hi, float &mn, float &mx)
+{
+    mn = INFINITY;
+    mx = -INFINITY;
+    a_lo = 0.0f;
+    a_hi = 0.0f;
+    for (int e = 0; e < D; ++e) {
+        float xe = bf16_bits_to_f32(row[e]);
+        mn = fminf(mn, xe);
+        mx = fmaxf(mx, xe);
+        float ae = fabsf(xe);
+        int less = 0, le = 0;
+        for (int f = 0; f < D; ++f) {
+            float af = fabsf(bf16_bits_to_f32(row[f]));
+            less += (af < ae);
+            le += (af <= ae);
+        }
+        // |x_e| occupies ascending ranks [less, le)
+        if (less <= lo && lo < le) a_lo = ae;
+        if (less <= lo + 1 && lo + 1 < le) a_hi = ae;
+    }
+    if (lo + 1 >= D) a_hi = a_lo;
+}
+
+// Eq. (7) parameters from the order statistics.  Every operation is a single
+// correctly rounded fp32 operation (the file is built without contraction).
+__device__ __forceinline__ void quant_params(float a_lo, float a_hi, float t, bool interp,
+                                             float mn, float mx, int levels, uint32_t &s16,
+                                             uint32_t &z16, float &z, float &inv)
+{
+    float q = a_lo;
+    if (interp) {
+        float diff = a_hi - a_lo;
+        float prod = t * diff;
+        q = a_lo + prod;
+    }
+    float x_min = (mn > -q) ? mn : -q;
+    float x_max = (mx < q) ? mx : q;
+    float delta = (x_max - x_min) / (float)levels;
+    s16 = f32_to_f16_bits(delta);
+    z16 = f32_to_f16_bits(x_min);
+    float s = f16_bits_to_f32(s16);
+    z = f16_bits_to_f32(z16);
+    inv = (s > 0.0f) ? 1.0f / s : 0.0f;
+}
+
+__device__ __forceinline__ uint32_t code_of(float x, float z, float inv, float levels)
+{
+    float y = (x - z) * inv;
+    float r = rintf(y);
+    r = fminf(fmaxf(r, 0.0f), levels);
+    return (uint32_t)r;
+}
+
+template <int D, int BITS>
+__device__ void order_stats(const uint16_t *row, int lo, float &a_lo, float &a_hi, float &mn,
+                            float &mx)
+{
+    const int K = D - lo;
+    if (K <= 2) order_stats_topk<D, 2>(row, lo, a_lo, a_hi, mn, mx);
+    else if (K <= 4) order_stats_topk<D, 4>(row, lo, a_lo, a_hi, mn, mx);
+    else if (K <= 8) order_stats_topk<D, 8>(row, lo, a_lo, a_hi, mn, mx);
+    else if (K <= 12) order_stats_topk<D, 12>(row, lo, a_lo, a_hi, mn, mx);
+    else if (K <= 16) order_stats_topk<D, 16>(row, lo, a_lo, a_hi, mn, mx);
+    else order_stats_rank<D>(row, lo, a_lo, a_hi, mn, mx);
+}
+
+template <int D, int BITS>
+__global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
+{
+    using L = Layout<D, BITS>;
+    constexpr int kPitch = D + 8;  // bf16 elements per LDS row (16 B pad)
+    __shared__ __attribute__((aligned(16))) uint16_t kt[kPage * kPitch];
+    __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * kPitch];
+    __shared__ __attribute__((aligned(16))) uint8_t vcodes[kPage * D];
+    __shared__ int32_t sh_page;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int h = blockIdx.y, b = blockIdx.z;
+
+    // ---- per-sequence bookkeeping (identical in every workgroup)
+    const int32_t s_old = a.seq_len[b];
+    const int32_t q_old = a.quant_end[b];
+    int32_t nn = a.n_new[b];
+    nn = nn < 0 ? 0 : (nn > a.max_new ? a.max_new : nn);
+    const int32_t s_new = s_old + nn;
+    const int32_t q_new = next_quant_end(s_new, q_old, a.s_sink, a.s_keep, a.s_flush);
+    const int32_t start_old = q_old > a.s_sink ? q_old : a.s_sink;
+    const int32_t first = s_old < start_old ? s_old : start_old;
+    const int32_t ring = a.win_slots - a.s_sink;
+
+    // ---- which tile
+    int k0 = first < a.s_sink ? (first / kPage) - a.sink_tiles : (first - a.s_sink) / kPage;
+    const int k = k0 + (int)blockIdx.x;
+    int32_t blk_lo, blk_hi;
+    if (k < 0) {
+        blk_lo = (k + a.sink_tiles) * kPage;
+        blk_hi = min(blk_lo + kPage, a.s_sink);
+    } else {
+        blk_lo = a.s_sink + k * kPage;
+        blk_hi = blk_lo + kPage;
+    }
+    const int32_t lo = max(blk_lo, first), hi = min(blk_hi, s_new);
+    if (lo >= hi) return;
+
+    const bool do_new = (a.mode & kModeNew) != 0, do_flush = (a.mode & kModeFlush) != 0;
+    // position p (lo <= p < hi) is: new if p >= s_old; quantised now if
+    // start_old <= p < q_new; otherwise a window entry (sink, or ring if new).
+    auto is_new = [&](int32_t p) { return p >= s_old; };
+    auto quant_now = [&](int32_t p) {
+        return p >= start_old && p < q_new && (is_new(p) ? do_new : do_flush);
+    };
+    auto window_write = [&](int32_t p) {
+        return do_new && is_new(p) && (p < a.s_sink || p >= q_new);
+    };
+
+    if (tid == 0) {
+        int32_t phys = -1;
+        if (k >= 0 && k < a.max_pages) {
+            phys = a.page_table[(int64_t)b * a.max_pages + k];
+            if (phys < 0 || phys >= a.n_pages) phys = -1;
+        }
+        sh_page = phys;
+    }
+
+    const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;  // win_k row base (slots)
+    const uint16_t *tk_h = a.tk + (int64_t)h * D * D;
+
+    // ---- phase A: transformed keys -> kt, values -> vt
+    bool any_new = false;
+    for (int32_t p = lo; p < hi; ++p) any_new |= (do_new && is_new(p));
+    if (any_new) {
+        // Wave w produces output channels [w D/4, (w+1) D/4) for all 64 rows.
+        constexpr int kNtW = D / 64;  // N-tiles per wave
+        const int j = lane >> 4, n = lane & 15;
+        bf16x8 bop[kNtW][L::kChunks];
+#pragma unroll
+        for (int nt = 0; nt < kNtW; ++nt) {
+            const int o = (wave * kNtW + nt) * 16 + n;
+#pragma unroll
+            for (int c = 0; c < L::kChunks; ++c)
+                bop[nt][c] = *reinterpret_cast<const bf16x8 *>(tk_h + (int64_t)o * D + 32 * c + 8 * j);
+        }
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+            const int r = 16 * mt + n;  // A row handled by this lane
+            const int32_t p = blk_lo + r;
+            const bool ld = (p >= lo && p < hi && is_new(p) && do_new);
+            const uint16_t *krow = a.k_new + (((int64_t)b * a.max_new + (p - s_old)) * a.n_kv + h) * D;
+            f32x4 acc[kNtW];
+#pragma unroll
+            for (int nt = 0; nt < kNtW; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int c = 0; c < L::kChunks; ++c) {
+                u32x4 av = {0u, 0u, 0u, 0u};
+                if (ld) av = *reinterpret_cast<const u32x4 *>(krow + 32 * c + 8 * j);
+                bf16x8 aop = __builtin_bit_cast(bf16x8, av);
+#pragma unroll
+                for (int nt = 0; nt < kNtW; ++nt) acc[nt] = mfma16(aop, bop[nt][c], acc[nt]);
+            }
+#pragma unroll
+            for (int nt = 0; nt < kNtW; ++nt) {
+                const int ch = (wave * kNtW + nt) * 16 + n;
+#pragma unroll
+                for (int rr = 0; rr < 4; rr += 2) {
+                    uint32_t pr = pack_bf16_rne(acc[nt][rr], acc[nt][rr + 1]);
+                    const int row = 16 * mt + 4 * j + rr;
+                    kt[row * kPitch + ch] = (uint16_t)(pr & 0xFFFFu);
+                    kt[(row + 1) * kPitch + ch] = (uint16_t)(pr >> 16);
+                }
+            }
+        }
+    }
+    // ring-sourced keys (flush) and all values, 16 B per thread-step
+    {
+        constexpr int kVec = D / 8;  // uint4 per row
+        for (int idx = tid; idx < kPage * kVec; idx += 256) {
+            const int r = idx / kVec, cv = idx % kVec;
+            const int32_t p = blk_lo + r;
+            if (p < lo || p >= hi) continue;
+            const bool nw = is_new(p);
+            if (nw ? !do_new : !quant_now(p)) continue;
+            uint4 vv;
+            if (nw) {
+                vv = *reinterpret_cast<const uint4 *>(
+                    a.v_new + (((int64_t)b * a.max_new + (p - s_old)) * a.n_kv + h) * D + 8 * cv);
+            } else {
+                const int32_t slot = ring_slot(p, a.s_sink, ring);
+                const uint16_t *vsrc = a.win_v + (head_win * D) + slot;  // channel-major
+                uint16_t e[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) e[q] = vsrc[(int64_t)(8 * cv + q) * a.win_slots];
+                vv.x = e[0] | ((uint32_t)e[1] << 16);
+                vv.y = e[2] | ((uint32_t)e[3] << 16);
+                vv.z = e[4] | ((uint32_t)e[5] << 16);
+                vv.w = e[6] | ((uint32_t)e[7] << 16);
+                *reinterpret_cast<uint4 *>(kt + r * kPitch + 8 * cv) =
+                    *reinterpret_cast<const uint4 *>(a.win_k + (head_win + slot) * D + 8 * cv);
+            }
+            *reinterpret_cast<uint4 *>(vt + r * kPitch + 8 * cv) = vv;
+        }
+    }
+    __syncthreads();
+    const int32_t page = sh_page;
+    uint8_t *pg = page >= 0 ? a.pages + ((int64_t)page * a.n_kv + h) * L::kPageBytes : nullptr;
+
+    // ---- phase B: quantise (threads 0-63 keys, 64-127 values)
+    if (tid < 2 * kPage) {
+        const bool is_v = tid >= kPage;
+        const int r = tid & (kPage - 1);
+        const int32_t p = blk_lo + r;
+        if (p >= lo && p < hi && quant_now(p) && pg != nullptr) {
+            const uint16_t *row = (is_v ? vt : kt) + r * kPitch;
+            const int qlo = is_v ? a.lo_v : a.lo_k;
+            const float qt = is_v ? a.t_v : a.t_k;
+            float a_lo, a_hi, mn, mx;
+            order_stats<D, BITS>(row, qlo, a_lo, a_hi, mn, mx);
+            uint32_t s16, z16;
+            float z, inv;
+            constexpr int kLevels = (1 << BITS) - 1;
+            quant_params(a_lo, a_hi, qt, qlo + 1 < D, mn, mx, kLevels, s16, z16, z, inv);
+            *reinterpret_cast<uint32_t *>(pg + L::kParamOffset + 4 * r + (is_v ? 4 * kPage : 0)) =
+                s16 | (z16 << 16);
+            if (!is_v) {
+                // key words of this token: word (j, w) holds channels
+                // 32 c + 8 j + i with c = w (B/8) + o.
+                uint32_t kw[4][L::kNw];
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+                    for (int w = 0; w < L::kNw; ++w) kw[jj][w] = 0u;
+#pragma unroll
+                for (int c8 = 0; c8 < D / 8; ++c8) {
+                    uint4 v = *reinterpret_cast<const uint4 *>(row + 8 * c8);
+                    uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+                    const int c = c8 >> 2, jj = c8 & 3;
+                    const int w = c / L::kOpsPerWord, o = c % L::kOpsPerWord;
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        uint32_t hb = (i & 1) ? (wv[i >> 1] >> 16) : (wv[i >> 1] & 0xFFFFu);
+                        uint32_t code = code_of(bf16_bits_to_f32(hb), z, inv, (float)kLevels);
+                        kw[jj][w] |= code << L::elem_bit(8 * o + i);
+                    }
+                }
+                const int tau = 2 * (r >> 5) + ((r >> 2) & 1);
+                const int m = 4 * ((r >> 3) & 3) + (r & 3);
+                uint32_t *kreg = reinterpret_cast<uint32_t *>(pg);
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+                    for (int w = 0; w < L::kNw; ++w)
+                        kreg[(16 * jj + m) * L::kWordsPerLane + tau * L::kNw + w] = kw[jj][w];
+            } else {
+#pragma unroll
+                for (int c8 = 0; c8 < D / 8; ++c8) {
+                    uint4 v = *reinterpret_cast<const uint4 *>(row + 8 * c8);
+                    uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+                    uint32_t lo4 = 0, hi4 = 0;
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        uint32_t hb = (i & 1) ? (wv[i >> 1] >> 16) : (wv[i >> 1] & 0xFFFFu);
+                        uint32_t code = code_of(bf16_bits_to_f32(hb), z, inv, (float)kLevels);
+                        if (i < 4) lo4 |= code << (8 * i);
+                        else hi4 |= code << (8 * (i - 4));
+                    }
+                    *reinterpret_cast<uint2 *>(vcodes + r * D + 8 * c8) = make_uint2(lo4, hi4);
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    // ---- phase C: value-code words
+    if (pg != nullptr) {
+        uint32_t *vreg = reinterpret_cast<uint32_t *>(pg + L::kRegionBytes);
+        constexpr int kWords = 64 * L::kWordsPerLane;
+        for (int widx = tid; widx < kWords; widx += 256) {
+            const int Ln = widx / L::kWordsPerLane, rem = widx % L::kWordsPerLane;
+            const int kc = rem / (2 * L::kNw), u = rem % (2 * L::kNw);
+            const int j = Ln >> 4, m = Ln & 15;
+            uint32_t mask = 0, bits = 0;
+#pragma unroll
+            for (int e = 0; e < L::kCodesPerWord; ++e) {
+                const int o = e >> 3, i = e & 7;
+                const int t = 32 * kc + 8 * j + i;
+                const int32_t p = blk_lo + t;
+                if (p >= lo && p < hi && quant_now(p)) {
+                    const int ch = 16 * (u * L::kOpsPerWord + o) + m;
+                    const int bit = L::elem_bit(e);
+                    mask |= ((1u << BITS) - 1u) << bit;
+                    bits |= (uint32_t)vcodes[t * D + ch] << bit;
+                }
+            }
+            if (mask == 0u) continue;
+            if (mask != 0xFFFFFFFFu) bits |= vreg[widx] & ~mask;
+            vreg[widx] = bits;
+        }
+    }
+
+    // ---- phase D: bf16 windows and the optional k~ output
+    {
+        constexpr int kVec = D / 8;
+        for (int idx = tid; idx < kPage * kVec; idx += 256) {
+            const int r = idx / kVec, cv = idx % kVec;
+            const int32_t p = blk_lo + r;
+            if (p < lo || p >= hi || !(do_new && is_new(p))) continue;
+            const uint4 kv = *reinterpret_cast<const uint4 *>(kt + r * kPitch + 8 * cv);
+            if (a.k_tilde_out != nullptr)
+                *reinterpret_cast<uint4 *>(
+                    a.k_tilde_out + (((int64_t)b * a.max_new + (p - s_old)) * a.n_kv + h) * D + 8 * cv) = kv;
+            if (window_write(p)) {
+                const int32_t slot = p < a.s_sink ? p : ring_slot(p, a.s_sink, ring);
+                *reinterpret_cast<uint4 *>(a.win_k + (head_win + slot) * D + 8 * cv) = kv;
+            }
+        }
+        // values, channel-major: consecutive threads write consecutive slots
+        for (int idx = tid; idx < kPage * D; idx += 256) {
+            const int ch = idx / kPage, r = idx % kPage;
+            const int32_t p = blk_lo + r;
+            if (p < lo || p >= hi || !window_write(p)) continue;
+            const int32_t slot = p < a.s_sink ? p : ring_slot(p, a.s_sink, ring);
+            a.win_v[(head_win * D) + (int64_t)ch * a.win_slots + slot] = vt[r * kPitch + ch];
+        }
+    }
+}
+
+// Advance seq_len / quant_end after the append kernels have read them.
+__global__ void append_commit_kernel(int32_t *seq_len, int32_t *quant_end, const int32_t *n_new,
+                                     int32_t batch, int32_t max_new, int32_t s_sink,
+                                     int32_t s_keep, int32_t s_flush)
+{
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= batch) return;
+    int32_t nn = n_new[b];
+    nn = nn < 0 ? 0 : (nn > max_new ? max_new : nn);
+    const int32_t s_new = seq_len[b] + nn;
+    quant_end[b] = next_quant_end(s_new, quant_end[b], s_sink, s_keep, s_flush);
+    seq_len[b] = s_new;
+}
+
+template <int D, int BITS>
+static hipError_t launch_append(const AppendArgs &a, dim3 grid, hipStream_t s)
+{
+    timing_begin("append_kernel", s);
+    hipLaunchKernelGGL((append_kernel<D, BITS>), grid, dim3(256), 0, s, a);
+    timing_end(s);
+    return hipGetLastError();
+}
+
+}  // namespace wushkv
+
+using namespace wushkv;
+
+// Host-side position of the kappa-quantile (fp64, as in the definition of
+// the quantile: pos = kappa (d - 1), lo = floor(pos), t = pos - lo).
+static void kappa_position(float kappa, int d, int32_t &lo, float &t)
+{
+    double pos = (double)kappa * (double)(d - 1);
+    double fl = std::floor(pos);
+    if (fl < 0.0) fl = 0.0;
+    if (fl > (double)(d - 1)) fl = (double)(d - 1);
+    lo = (int32_t)fl;
+    t = (float)(pos - fl);
+}
+
+int wushkv_validate_cache(const wushkv_cache *c);  // api.hip
+
+extern "C" int wushkv_append(const wushkv_cache *c, const uint16_t *k_new, const uint16_t *v_new,
+                             const int32_t *n_new, int32_t max_new, const uint16_t *t_k,
+                             uint16_t *k_tilde_out, wushkv_stream_t stream)
+{
+    int st = wushkv_validate_cache(c);
+    if (st != WUSHKV_OK) return st;
+    if (max_new < 0) return WUSHKV_EINVAL;
+    if (max_new == 0) return WUSHKV_OK;
+    if (!k_new || !v_new || !n_new || !t_k) return WUSHKV_EINVAL;
+
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    AppendArgs a{};
+    a.pages = c->pages;
+    a.page_table = c->page_table;
+    a.win_k = c->win_k;
+    a.win_v = c->win_v;
+    a.seq_len = c->seq_len;
+    a.quant_end = c->quant_end;
+    a.n_kv = c->n_kv_heads;
+    a.s_sink = c->s_sink;
+    a.s_keep = c->s_keep;
+    a.s_flush = c->s_flush;
+    a.win_slots = c->win_slots;
+    a.max_pages = c->max_pages_per_seq;
+    a.n_pages = c->n_pages;
+    kappa_position(c->kappa_k, c->head_dim, a.lo_k, a.t_k);
+    kappa_position(c->kappa_v, c->head_dim, a.lo_v, a.t_v);
+    a.k_new = k_new;
+    a.v_new = v_new;
+    a.n_new = n_new;
+    a.max_new = max_new;
+    a.tk = t_k;
+    a.k_tilde_out = k_tilde_out;
+    a.sink_tiles = (c->s_sink + kPage - 1) / kPage;
+
+    // Tiles a sequence can touch: the sink tiles, plus the span from the
+    // oldest unflushed position (at most s_keep + s_flush - 1 back) to the
+    // new end.
+    const int64_t span = (int64_t)max_new + c->s_keep + c->s_flush - 1;
+    const int64_t tiles = a.sink_tiles + (span + kPage - 1) / kPage + 1;
+    if (tiles > 0x7FFFFFFF) return WUSHKV_EINVAL;
+    dim3 grid((unsigned)tiles, (unsigned)c->n_kv_heads, (unsigned)c->batch);
+
+    // Flushed ring slots may be reused by new tokens of the same call only if
+    // the ring is shorter than the span; then flush first, in its own launch.
+    const int64_t ring = (int64_t)c->win_slots - c->s_sink;
+    const bool fused = ring >= span;
+
+    auto go = [&](int mode) -> hipError_t {
+        a.mode = mode;
+        const int key = c->head_dim * 10 + c->bits;
+        switch (key) {
+            case 1282: return launch_append<128, 2>(a, grid, s);
+            case 1284: return launch_append<128, 4>(a, grid, s);
+            case 642: return launch_append<64, 2>(a, grid, s);
+            case 644: return launch_append<64, 4>(a, grid, s);
+        }
+        return hipErrorInvalidValue;
+    };
+    hipError_t e;
+    if (fused) {
+        e = go(kModeFlush | kModeNew);
+    } else {
+        e = go(kModeFlush);
+        if (e == hipSuccess) e = go(kModeNew);
+    }
+    if (e != hipSuccess) return WUSHKV_ELAUNCH;
+    timing_begin("append_commit_kernel", s);
+    hipLaunchKernelGGL(append_commit_kernel, dim3((c->batch + 255) / 256), dim3(256), 0, s,
+                       c->seq_len, c->quant_end, n_new, c->batch, max_new, c->s_sink, c->s_keep,
+                       c->s_flush);
+    timing_end(s);
+    if (hipGetLastError() != hipSuccess) return WUSHKV_ELAUNCH;
+    return WUSHKV_OK;
+}

@@ -1,0 +1,84 @@
+// wushkv_dequant: reconstruct stored entries x = scale * code + zero
+// (Eq. (7), last term) straight from the packed pages.  One thread per
+// (position, channel); reads the page layout of include/wushkv.h.
+#include "common.h"
+
+namespace wushkv {
+
+template <int D, int BITS>
+__global__ void __launch_bounds__(256) dequant_kernel(const uint8_t *pages, const int32_t *page_table,
+                                                      int32_t n_kv, int32_t s_sink, int32_t max_pages,
+                                                      int32_t n_pages, int32_t b, int32_t start,
+                                                      int32_t count, float *k_out, float *v_out)
+{
+    using L = Layout<D, BITS>;
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int h = blockIdx.y;
+    if (idx >= (int64_t)count * D) return;
+    const int32_t pos = start + (int32_t)(idx / D);
+    const int ch = (int)(idx % D);
+    const int32_t rel = pos - s_sink;
+    const int32_t lp = rel / kPage, t = rel % kPage;
+    const int32_t phys = lp < max_pages ? page_table[(int64_t)b * max_pages + lp] : -1;
+    const int64_t o = ((int64_t)h * count + (pos - start)) * D + ch;
+    if (phys < 0 || phys >= n_pages) {
+        if (k_out) k_out[o] = NAN;
+        if (v_out) v_out[o] = NAN;
+        return;
+    }
+    const uint8_t *pg = pages + ((int64_t)phys * n_kv + h) * L::kPageBytes;
+    const uint32_t *w = reinterpret_cast<const uint32_t *>(pg);
+    const uint32_t *pk = reinterpret_cast<const uint32_t *>(pg + L::kParamOffset);
+    const uint32_t mask = (1u << BITS) - 1u;
+    int word, bit;
+    if (k_out) {
+        L::k_pos(t, ch, word, bit);
+        const uint32_t code = (w[word] >> bit) & mask;
+        const uint32_t prm = pk[t];
+        k_out[o] = fmaf(f16_bits_to_f32(prm & 0xFFFFu), (float)code, f16_bits_to_f32(prm >> 16));
+    }
+    if (v_out) {
+        L::v_pos(t, ch, word, bit);
+        const uint32_t code = (w[L::kRegionBytes / 4 + word] >> bit) & mask;
+        const uint32_t prm = pk[kPage + t];
+        v_out[o] = fmaf(f16_bits_to_f32(prm & 0xFFFFu), (float)code, f16_bits_to_f32(prm >> 16));
+    }
+}
+
+}  // namespace wushkv
+
+using namespace wushkv;
+
+int wushkv_validate_cache(const wushkv_cache *c);  // api.hip
+
+extern "C" int wushkv_dequant(const wushkv_cache *c, int32_t b, int32_t start, int32_t count,
+                              float *k_out, float *v_out, wushkv_stream_t stream)
+{
+    int st = wushkv_validate_cache(c);
+    if (st != WUSHKV_OK) return st;
+    if (b < 0 || b >= c->batch || count < 0 || start < c->s_sink) return WUSHKV_EINVAL;
+    if ((int64_t)start + count > (int64_t)c->s_sink + (int64_t)kPage * c->max_pages_per_seq)
+        return WUSHKV_EINVAL;
+    if (count == 0 || (!k_out && !v_out)) return WUSHKV_OK;
+    if (((uintptr_t)k_out | (uintptr_t)v_out) & 3u) return WUSHKV_EINVAL;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const int64_t n = (int64_t)count * c->head_dim;
+    if ((n + 255) / 256 > 0x7FFFFFFF) return WUSHKV_EINVAL;
+    dim3 grid((unsigned)((n + 255) / 256), (unsigned)c->n_kv_heads);
+    const int key = c->head_dim * 10 + c->bits;
+    timing_begin("dequant_kernel", s);
+#define WUSHKV_DQ(D_, B_)                                                                        \
+    hipLaunchKernelGGL((dequant_kernel<D_, B_>), grid, dim3(256), 0, s, c->pages, c->page_table, \
+                       c->n_kv_heads, c->s_sink, c->max_pages_per_seq, c->n_pages, b, start,     \
+                       count, k_out, v_out)
+    switch (key) {
+        case 1282: WUSHKV_DQ(128, 2); break;
+        case 1284: WUSHKV_DQ(128, 4); break;
+        case 642: WUSHKV_DQ(64, 2); break;
+        case 644: WUSHKV_DQ(64, 4); break;
+    }
+#undef WUSHKV_DQ
+    timing_end(s);
+    if (hipGetLastError() != hipSuccess) return WUSHKV_ELAUNCH;
+    return WUSHKV_OK;
+}

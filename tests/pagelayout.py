@@ -1,0 +1,109 @@
+"""Test-side reader of the packed page layout, written from the description
+in include/wushkv.h (not from the kernels), so a layout slip on the GPU side
+shows up as a parity failure rather than cancelling out.
+
+One (page, head) block: K code words, V code words, K params, V params.
+A word holds B = 32 / bits elements; element e sits at bit
+16 * (e % 2) + bits * (e // 2) and is slot i = e % 8 of operand o = e // 8.
+Lane L = 16 j + m owns 4 nw consecutive words, nw = d * bits / 128.
+  K word L*4nw + tau*nw + w : token 32(tau//2) + 8(m//4) + 4(tau%2) + m%4,
+                              channel 32 c + 8 j + i, c = w (B/8) + o
+  V word L*4nw + kc*2nw + u : token 32 kc + 8 j + i,
+                              channel 16 nt + m, nt = u (B/8) + o
+"""
+from __future__ import annotations
+
+import functools
+
+import numpy as np
+
+PAGE = 64
+
+
+def page_bytes(d: int, bits: int) -> int:
+    return PAGE * (2 * d * bits // 8 + 8)
+
+
+@functools.lru_cache(maxsize=None)
+def _maps(d: int, bits: int):
+    """For every (word, element): (token, channel, bit) for K and for V."""
+    B = 32 // bits
+    nw = d * bits // 128
+    ops = B // 8
+    n_words = 64 * 4 * nw
+    kt = np.empty((n_words, B), np.int64)
+    kc_ = np.empty((n_words, B), np.int64)
+    vt = np.empty((n_words, B), np.int64)
+    vc_ = np.empty((n_words, B), np.int64)
+    bit = np.array([16 * (e % 2) + bits * (e // 2) for e in range(B)], np.int64)
+    for L in range(64):
+        j, m = divmod(L, 16)
+        for tau in range(4):
+            for w in range(nw):
+                widx = L * 4 * nw + tau * nw + w
+                for e in range(B):
+                    o, i = divmod(e, 8)
+                    c = w * ops + o
+                    kt[widx, e] = 32 * (tau // 2) + 8 * (m // 4) + 4 * (tau % 2) + m % 4
+                    kc_[widx, e] = 32 * c + 8 * j + i
+        for kc in range(2):
+            for u in range(2 * nw):
+                widx = L * 4 * nw + kc * 2 * nw + u
+                for e in range(B):
+                    o, i = divmod(e, 8)
+                    nt = u * ops + o
+                    vt[widx, e] = 32 * kc + 8 * j + i
+                    vc_[widx, e] = 16 * nt + m
+    return kt, kc_, vt, vc_, bit
+
+
+def decode_block(block: np.ndarray, d: int, bits: int):
+    """block: uint8 [page_bytes] -> (kcodes [64][d], vcodes [64][d],
+    kparams [64][2], vparams [64][2]) with params as fp16 bit patterns
+    (scale, zero)."""
+    block = np.ascontiguousarray(block, dtype=np.uint8)
+    region = 8 * d * bits
+    kt, kch, vt, vch, bit = _maps(d, bits)
+    mask = (1 << bits) - 1
+    kw = block[:region].view("<u4").astype(np.int64)
+    vw = block[region:2 * region].view("<u4").astype(np.int64)
+    kcodes = np.full((PAGE, d), -1, np.int64)
+    vcodes = np.full((PAGE, d), -1, np.int64)
+    kcodes[kt, kch] = (kw[:, None] >> bit[None, :]) & mask
+    vcodes[vt, vch] = (vw[:, None] >> bit[None, :]) & mask
+    assert (kcodes >= 0).all() and (vcodes >= 0).all(), "layout map is not a bijection"
+    prm = block[2 * region:2 * region + 8 * PAGE].view("<u2").reshape(2, PAGE, 2)
+    return kcodes.astype(np.uint8), vcodes.astype(np.uint8), prm[0].copy(), prm[1].copy()
+
+
+def encode_block(kcodes, vcodes, kparams, vparams, d: int, bits: int) -> np.ndarray:
+    """Inverse of decode_block (used to check the maps form a bijection)."""
+    region = 8 * d * bits
+    kt, kch, vt, vch, bit = _maps(d, bits)
+    kw = (np.asarray(kcodes, np.int64)[kt, kch] << bit[None, :]).sum(axis=1)
+    vw = (np.asarray(vcodes, np.int64)[vt, vch] << bit[None, :]).sum(axis=1)
+    out = np.zeros(page_bytes(d, bits), np.uint8)
+    out[:region] = kw.astype("<u4").view(np.uint8)
+    out[region:2 * region] = vw.astype("<u4").view(np.uint8)
+    prm = np.stack([np.asarray(kparams, np.uint16), np.asarray(vparams, np.uint16)])
+    out[2 * region:] = prm.astype("<u2").reshape(-1).view(np.uint8)
+    return out
+
+
+def gather_sequence(pages: np.ndarray, page_table: np.ndarray, b: int, h: int, n_kv: int,
+                    d: int, bits: int, s_sink: int, q_end: int):
+    """Codes and params of positions [s_sink, q_end) of (sequence b, head h),
+    read from a host copy of the page pool."""
+    pb = page_bytes(d, bits)
+    pool = pages.reshape(-1, n_kv, pb)
+    n = max(0, q_end - s_sink)
+    kc = np.zeros((n, d), np.uint8)
+    vc = np.zeros((n, d), np.uint8)
+    kp = np.zeros((n, 2), np.uint16)
+    vp = np.zeros((n, 2), np.uint16)
+    for lp in range((n + PAGE - 1) // PAGE):
+        k1, v1, kp1, vp1 = decode_block(pool[page_table[b, lp], h], d, bits)
+        lo, hi = lp * PAGE, min(n, (lp + 1) * PAGE)
+        kc[lo:hi], vc[lo:hi] = k1[:hi - lo], v1[:hi - lo]
+        kp[lo:hi], vp[lo:hi] = kp1[:hi - lo], vp1[:hi - lo]
+    return kc, vc, kp, vp

@@ -1,0 +1,143 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every function include/wushkv.h declares, reports sizes in closed form, and
+rejects bad descriptors before anything is enqueued.  Also checks that the
+test-side page decoder's maps are bijections in the documented order."""
+import ctypes
+
+import numpy as np
+import pytest
+
+from conftest import gpu_available
+import pagelayout
+
+wk = pytest.importorskip("paper_2609_38121_amd")
+from paper_2609_38121_amd import _lib  # noqa: E402
+
+
+def test_exports_every_declared_function():
+    names = _lib.header_functions()
+    assert len(names) >= 9
+    L = _lib.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert wk.wushkv_abi_version() == 1
+
+
+@pytest.mark.parametrize("d,bits", [(64, 2), (64, 4), (128, 2), (128, 4)])
+def test_page_bytes_closed_form(d, bits):
+    # per token-head: K and V codes d*bits/8 bytes each, plus 2 x (scale, zero) fp16
+    assert wk.wushkv_page_bytes(d, bits) == 64 * (2 * d * bits // 8 + 8)
+    assert pagelayout.page_bytes(d, bits) == wk.wushkv_page_bytes(d, bits)
+
+
+def test_page_bytes_rejects_unsupported():
+    assert wk.wushkv_page_bytes(96, 2) == 0
+    assert wk.wushkv_page_bytes(128, 3) == 0
+
+
+def test_status_strings():
+    for st in (0, -1, -2, -3, -4, -5):
+        assert wk.wushkv_status_string(st) not in ("", "unknown status")
+    assert wk.wushkv_status_string(-99) == "unknown status"
+
+
+FAKE = 0x10000  # 16-byte aligned, never dereferenced: every case below fails validation
+
+
+def _desc(**over):
+    f = dict(batch=2, n_kv_heads=2, head_dim=128, bits=2, s_sink=4, s_keep=128, s_flush=8,
+             win_slots=192, max_pages_per_seq=4, n_pages=8, kappa_k=0.96, kappa_v=0.92,
+             pages=FAKE, page_table=FAKE, win_k=FAKE, win_v=FAKE, seq_len=FAKE, quant_end=FAKE)
+    f.update(over)
+    return _lib.CacheDesc(**f)
+
+
+BAD = [
+    (dict(batch=0), -1), (dict(n_kv_heads=0), -1), (dict(head_dim=96), -2), (dict(bits=3), -2),
+    (dict(s_sink=-1), -1), (dict(s_flush=0), -1), (dict(win_slots=100), -1),
+    (dict(win_slots=128), -1),  # ring 124 < s_keep + s_flush - 1 = 135
+    (dict(kappa_k=0.0), -1), (dict(kappa_v=1.5), -1), (dict(kappa_k=float("nan")), -1),
+    (dict(win_k=None), -1), (dict(seq_len=None), -1), (dict(pages=None), -1),
+    (dict(win_v=FAKE + 4), -1), (dict(max_pages_per_seq=-1), -1),
+]
+
+
+@pytest.mark.skipif(gpu_available(), reason="fake device pointers: run only where no GPU exists")
+@pytest.mark.parametrize("over,status", BAD)
+def test_validation_rejects_before_launch(over, status):
+    L = _lib.lib()
+    d = _desc(**over)
+    st = L.wushkv_append(ctypes.byref(d), FAKE, FAKE, FAKE, 1, FAKE, None, None)
+    assert st == status
+    st = L.wushkv_decode_attention(ctypes.byref(d), FAKE, 8, 100, FAKE, 0.1, FAKE, FAKE, 1 << 30, None)
+    assert st == status
+    st = L.wushkv_dequant(ctypes.byref(d), 0, 4, 1, FAKE, FAKE, None)
+    assert st == status
+    assert L.wushkv_decode_workspace_bytes(ctypes.byref(d), 8, 100) == 0
+
+
+@pytest.mark.skipif(gpu_available(), reason="fake device pointers: run only where no GPU exists")
+def test_call_specific_validation():
+    L = _lib.lib()
+    d = _desc()
+    by = ctypes.byref(d)
+    # append: null inputs, negative max_new; max_new == 0 is a no-op
+    assert L.wushkv_append(by, None, FAKE, FAKE, 1, FAKE, None, None) == -1
+    assert L.wushkv_append(by, FAKE, FAKE, FAKE, -1, FAKE, None, None) == -1
+    assert L.wushkv_append(by, FAKE, FAKE, FAKE, 0, FAKE, None, None) == 0
+    # decode: n_q not a multiple of n_kv, G too large or not a power of two,
+    # bad scale, small workspace
+    assert L.wushkv_decode_attention(by, FAKE, 7, 100, FAKE, 0.1, FAKE, FAKE, 1 << 30, None) == -1
+    assert L.wushkv_decode_attention(by, FAKE, 32, 100, FAKE, 0.1, FAKE, FAKE, 1 << 30, None) == -2
+    assert L.wushkv_decode_attention(by, FAKE, 6, 100, FAKE, 0.1, FAKE, FAKE, 1 << 30, None) == -2
+    assert L.wushkv_decode_attention(by, FAKE, 8, 100, FAKE, -1.0, FAKE, FAKE, 1 << 30, None) == -1
+    need = L.wushkv_decode_workspace_bytes(by, 8, 100)
+    assert need > 0
+    assert L.wushkv_decode_attention(by, FAKE, 8, 100, FAKE, 0.1, FAKE, FAKE, need - 1, None) == -3
+    # dequant: position before the sink end, past the table, bad sequence
+    assert L.wushkv_dequant(by, 0, 3, 1, FAKE, FAKE, None) == -1
+    assert L.wushkv_dequant(by, 0, 4, 4 * 64 + 1, FAKE, FAKE, None) == -1
+    assert L.wushkv_dequant(by, 2, 4, 1, FAKE, FAKE, None) == -1
+    assert L.wushkv_dequant(by, 0, 4, 0, FAKE, FAKE, None) == 0
+
+
+def test_workspace_bytes_closed_form():
+    L = _lib.lib()
+    d = _desc()
+    # qt: batch * n_q * d * 4 (rounded to 256) + partials heads*splits*G*(d+2)*4
+    ws = L.wushkv_decode_workspace_bytes(ctypes.byref(d), 8, 1000)
+    units = 192 // 64 + (1000 - 4 + 63) // 64
+    ups = max(4, -(-units * 4 // 4096))
+    ups = -(-ups // 4) * 4
+    splits = -(-units // ups)
+    assert ws == -(-(2 * 8 * 128 * 4) // 256) * 256 + 4 * splits * 4 * (128 + 2) * 4
+
+
+@pytest.mark.parametrize("d,bits", [(64, 2), (64, 4), (128, 2), (128, 4)])
+def test_layout_maps_are_bijections(d, bits):
+    rng = np.random.default_rng(d + bits)
+    kc = rng.integers(0, 1 << bits, (64, d))
+    vc = rng.integers(0, 1 << bits, (64, d))
+    kp = rng.integers(0, 1 << 16, (64, 2))
+    vp = rng.integers(0, 1 << 16, (64, 2))
+    blk = pagelayout.encode_block(kc, vc, kp, vp, d, bits)
+    k2, v2, kp2, vp2 = pagelayout.decode_block(blk, d, bits)
+    assert np.array_equal(k2, kc) and np.array_equal(v2, vc)
+    assert np.array_equal(kp2, kp) and np.array_equal(vp2, vp)
+
+
+def test_layout_first_words_as_documented():
+    # K word 0 (lane 0, tile 0): token 0, channels 0..7 then 32..39 (2-bit),
+    # even channels in the low half word.  V word 0: channel 0, tokens 0..7
+    # of the first N-tile and channel 16 for the second operand.
+    d, bits = 128, 2
+    kc = np.zeros((64, d), np.int64)
+    kc[0, 2] = 3   # element e = 2 -> bit 2
+    kc[0, 33] = 1  # channel 33: operand 1, slot 1 -> element 9 -> bit 16 + 8 = 24
+    vc = np.zeros((64, d), np.int64)
+    vc[5, 16] = 2  # token 5 slot 5, channel 16: operand 1 -> element 13 -> bit 16 + 12
+    blk = pagelayout.encode_block(kc, vc, np.zeros((64, 2)), np.zeros((64, 2)), d, bits)
+    w = blk[:8 * d * bits].view("<u4")
+    assert w[0] == (3 << 2) | (1 << 24)
+    vw = blk[8 * d * bits:16 * d * bits].view("<u4")
+    assert vw[0] == 2 << 28
