@@ -1,0 +1,414 @@
+"""Benchmark of the WUSH-KV hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+Workload (one GPU): a Llama-3-8B-shaped attention layer in decode -- batch 8,
+32 query / 8 kv heads, head_dim 128, 8192-token context, 2-bit keys and
+values with 4 sink + 128 recent bf16 tokens and flushes of 8.  One step is
+one pass of the whole hot path: append one new token per sequence (key
+transform, window routing, and the flush quantisation when it falls due),
+then decode attention over the updated cache.  The cache is built by a
+prefill append of the 8192-token context and replicated so that consecutive
+steps touch more than 512 MB (the 256 MB Infinity Cache cannot serve them).
+
+Reported value: algorithmic HBM bytes of a step (packed codes and params of
+every quantised token-head, bf16 windows, queries, transforms, outputs,
+page table, and the append's inputs and writes) over the step time, in GB/s.
+The step loop runs as a captured HIP graph.  The second half of the metric,
+append throughput, is measured on the prefill workload (4 x 16384 new tokens,
+QK-norm + RoPE theta 1e6 inputs, Student-t keys) and reported in tokens/s.
+
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+MALL_BYTES = 256 << 20
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-prefill", action="store_true", help="skip the append-throughput leg")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline leg")
+    ap.add_argument("--seed", type=int, default=0)
+    return ap.parse_args()
+
+
+# ----------------------------------------------------------------- bytes
+
+def decode_bytes(seq_len, quant_end, s_sink, n_kv, n_q, d, bits, page_tokens=64):
+    """Algorithmic bytes one decode call must move."""
+    per_q = 2 * d * bits // 8 + 8          # codes K+V and two fp16 (scale, zero) pairs
+    per_w = 4 * d                          # bf16 K and V
+    q_tok = w_tok = pages = 0
+    for S, Q in zip(seq_len, quant_end):
+        qe = min(max(Q, s_sink), S) if S > s_sink else S
+        nq = max(0, qe - s_sink) if S > s_sink else 0
+        q_tok += nq
+        w_tok += S - nq
+        pages += math.ceil(nq / page_tokens)
+    B = len(seq_len)
+    main = n_kv * (q_tok * per_q + w_tok * per_w)
+    other = B * n_q * d * 2 + n_kv * d * d * 4 + B * n_q * d * 4 + B * pages * 4
+    return main, other
+
+
+def append_step_bytes(B, n_kv, d, bits, n_new, n_flushed):
+    """One append call in which every sequence adds n_new tokens that stay in
+    the bf16 ring and flushes n_flushed ring tokens into pages: bf16 K and V
+    in, the window writes, the flushed tokens' ring reads and packed writes,
+    and T_K once."""
+    per_q = 2 * d * bits // 8 + 8
+    per_seq_head = n_new * 4 * d + n_new * 4 * d + n_flushed * (4 * d + per_q)
+    return B * n_kv * per_seq_head + n_kv * d * d * 2
+
+
+def prefill_bytes(B, n_kv, d, bits, n_new, n_quant):
+    """An append into an empty cache: bf16 K and V in, packed writes of the
+    n_quant quantised tokens, bf16 writes of the rest, T_K once."""
+    per_q = 2 * d * bits // 8 + 8
+    per_seq_head = n_new * 4 * d + n_quant * per_q + (n_new - n_quant) * 4 * d
+    return B * n_kv * per_seq_head + n_kv * d * d * 2
+
+
+def window_quant_end(S, s_sink, s_keep, s_flush):
+    """S_quant of a cache filled to S positions (window rule of Alg. 2,
+    restated here for byte accounting; the kernels compute their own)."""
+    start = s_sink
+    return max(0, start + ((S - s_keep - start) // s_flush) * s_flush)
+
+
+# ----------------------------------------------------------------- main
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(every (sequence, kv head) pair is independent; see the design notes "
+              "for how it would shard).  Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_38121_amd as wk
+    from workloads import synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = synth.CONFIGS["llama8b"]
+    w = synth.Workload(cfg, seed=args.seed)
+    B, H, NQ, D, BITS = cfg["batch"], cfg["n_kv"], cfg["n_q"], cfg["d"], cfg["bits"]
+    ctx = cfg["ctx"]
+    as_dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    # ---- build the cache by a prefill append of the context
+    log("generating %d x %d tokens" % (B, ctx))
+    t0 = time.time()
+    k = np.stack([w.keys(b, 0, ctx) for b in range(B)])
+    v = np.stack([w.values(b, 0, ctx) for b in range(B)])
+    tk_bits, tinv = w.transform()
+    log("  %.1fs" % (time.time() - t0))
+    max_seq = ctx + args.steps + args.warmup + 256
+    base = wk.WushKVCache(B, H, D, BITS, cfg["s_sink"], cfg["s_keep"], cfg["s_flush"],
+                          cfg["kappa_k"], cfg["kappa_v"], max_seq_len=max_seq)
+    tk = as_dev(tk_bits)
+    tinv_d = torch.from_numpy(tinv).to(dev)
+    wk.wushkv_append(base, as_dev(k), as_dev(v), torch.full((B,), ctx, dtype=torch.int32, device=dev), tk)
+    torch.cuda.synchronize()
+    del k, v
+    cache_bytes = base.pages.numel() + 2 * base.win_k.numel() * 2
+    reps = max(1, math.ceil(2 * MALL_BYTES / cache_bytes))
+    caches = [base] + [base.clone() for _ in range(reps - 1)]
+    log("cache %.1f MB x %d replicas" % (cache_bytes / 1e6, reps))
+
+    # per-step inputs: one new token per sequence and the decode query
+    k1 = as_dev(np.stack([w.keys(b, ctx, 1) for b in range(B)]))
+    v1 = as_dev(np.stack([w.values(b, ctx, 1) for b in range(B)]))
+    q = as_dev(w.query(0))
+    ones = torch.ones(B, dtype=torch.int32, device=dev)
+    sm = 1.0 / math.sqrt(D)
+    ws_bytes = wk.wushkv_decode_workspace_bytes(base, NQ, max_seq)
+    work = [torch.empty(ws_bytes, dtype=torch.uint8, device=dev) for _ in range(reps)]
+    outs = [torch.empty(B, NQ, D, dtype=torch.float32, device=dev) for _ in range(reps)]
+
+    def step(i):
+        r = i % reps
+        wk.wushkv_append(caches[r], k1, v1, ones, tk, max_new=1)
+        wk.wushkv_decode_attention(caches[r], q, tinv_d, sm_scale=sm, max_seq_len=max_seq,
+                                   out=outs[r], workspace=work[r])
+
+    def decode_only(i):
+        r = i % reps
+        wk.wushkv_decode_attention(caches[r], q, tinv_d, sm_scale=sm, max_seq_len=max_seq,
+                                   out=outs[r], workspace=work[r])
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    done = args.warmup
+
+    # lengths are the same for every sequence; track them on the host
+    def lengths_at(step_index):
+        """(S, S_quant) of the replica that step step_index runs on, after
+        that step's append: prefill of ctx, then one token per visit."""
+        S = ctx + step_index // reps + 1
+        return S, quant_end_after(S)
+
+    def quant_end_after(S):
+        return window_quant_end(S, cfg["s_sink"], cfg["s_keep"], cfg["s_flush"])
+
+    # ---- timed region, graph-captured steps
+    log("capturing %d steps (one per replica) in a HIP graph" % reps)
+    g = torch.cuda.CUDAGraph()
+    cap_stream = torch.cuda.Stream()
+    cap_stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cap_stream):
+        # replaying the graph runs steps done .. done + reps - 1 again and again;
+        # capture itself must not run the kernels twice, so record only
+        with torch.cuda.graph(g, stream=cap_stream):
+            for i in range(reps):
+                step(done + i)
+    torch.cuda.current_stream().wait_stream(cap_stream)
+    torch.cuda.synchronize()
+    # the capture enqueued nothing; replays advance every replica by one token
+    n_rep = max(1, args.steps // reps)
+    K = n_rep * reps
+    g.replay()  # one untimed replay (warm)
+    torch.cuda.synchronize()
+    done += reps
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(n_rep):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_graph = e0.elapsed_time(e1) / K
+    first_timed = done
+    done += K
+
+    # algorithmic bytes of the timed steps
+    tot_main = tot_other = tot_app = 0
+    for i in range(first_timed, first_timed + K):
+        S, Q = lengths_at(i)
+        main_b, other_b = decode_bytes([S] * B, [Q] * B, cfg["s_sink"], H, NQ, D, BITS)
+        Q_prev = quant_end_after(S - 1)
+        flushed = max(0, Q - max(Q_prev, cfg["s_sink"]))
+        tot_main += main_b
+        tot_other += other_b
+        tot_app += append_step_bytes(B, H, D, BITS, 1, flushed)
+    step_gbs = (tot_main + tot_other + tot_app) / K / (ms_graph * 1e-3) / 1e9
+    log("graph step: %.2f us, %.1f GB/s" % (ms_graph * 1e3, step_gbs))
+
+    # ---- eager steps with per-launch kernel timing (roofline of the decode kernel)
+    wk.wushkv_timing_enable(8 * 64)
+    KT = 64
+    e0.record()
+    for i in range(KT):
+        step(done + i)
+    e1.record()
+    torch.cuda.synchronize()
+    ms_eager = e0.elapsed_time(e1) / KT
+    kernels = {}
+    for name in ("decode_main_kernel", "decode_qt_kernel", "decode_combine_kernel",
+                 "append_kernel", "append_commit_kernel"):
+        n, tot = wk.wushkv_timing_read(name)
+        kernels[name] = (tot / n) if n else None
+    wk.wushkv_timing_enable(0)
+    main_sum = 0
+    for i in range(done, done + KT):
+        S, Q = lengths_at(i)
+        main_b, _ = decode_bytes([S] * B, [Q] * B, cfg["s_sink"], H, NQ, D, BITS)
+        main_sum += main_b
+    done += KT
+    main_per_launch = main_sum / KT
+    t_main = kernels["decode_main_kernel"]
+    achieved = main_per_launch / (t_main * 1e-3) / 1e9
+    log("decode_main_kernel: %.2f us avg, %.1f GB/s (%.1f%% of 8 TB/s); eager step %.2f us"
+        % (t_main * 1e3, achieved, 100 * achieved / PEAK_HBM_GBS, ms_eager * 1e3))
+
+    # ---- decode call alone (graph), for context
+    g2 = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(cap_stream):
+        with torch.cuda.graph(g2, stream=cap_stream):
+            for i in range(reps):
+                decode_only(i)
+    torch.cuda.synchronize()
+    g2.replay()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(n_rep):
+        g2.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_dec = e0.elapsed_time(e1) / K
+    dec_bytes = 0
+    for r in range(reps):
+        S = ctx + (done - r + reps - 1) // reps  # appends replica r has seen
+        mb, ob = decode_bytes([S] * B, [quant_end_after(S)] * B, cfg["s_sink"], H, NQ, D, BITS)
+        dec_bytes += mb + ob
+        # the host-side bookkeeping must agree with the device counters
+        assert int(caches[r].seq_len[0].item()) == S
+        assert int(caches[r].quant_end[0].item()) == quant_end_after(S)
+    dec_gbs = dec_bytes / reps / (ms_dec * 1e-3) / 1e9
+    log("decode call (graph): %.2f us, %.1f GB/s" % (ms_dec * 1e3, dec_gbs))
+
+    # ---- append throughput on the prefill workload
+    prefill = None
+    if not args.no_prefill:
+        prefill = bench_prefill(torch, wk, synth, dev, args)
+
+    # ---- oracle baseline on the host
+    cpu = None
+    if not args.no_cpu:
+        cpu = bench_oracle(cfg, w, tk_bits, tinv, args.cpu_seconds)
+
+    line = {
+        "metric": "decode-attn achieved HBM GB/s (% of peak) on 2-bit cache; append tokens/s",
+        "value": round(step_gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_graph, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "pct_of_peak": round(100 * step_gbs / PEAK_HBM_GBS, 2),
+        "config": {"workload": "llama3-8b-layer-decode-2bit", "batch": B, "n_q_heads": NQ,
+                   "n_kv_heads": H, "head_dim": D, "ctx": ctx, "bits": BITS,
+                   "s_sink": cfg["s_sink"], "s_keep": cfg["s_keep"], "s_flush": cfg["s_flush"],
+                   "kappa_k": cfg["kappa_k"], "kappa_v": cfg["kappa_v"], "replicas": reps,
+                   "step": "append 1 token/seq + decode", "graph": True},
+        "roofline": {"bound": "hbm", "kernel": "decode_main_kernel",
+                     "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "avg_us": round(t_main * 1e3, 3),
+                     "bytes_per_launch": int(main_per_launch)},
+        "cpu_baseline": cpu,
+        "decode_call_gbps": round(dec_gbs, 2),
+        "decode_call_us": round(ms_dec * 1e3, 3),
+        "eager_step_us": round(ms_eager * 1e3, 3),
+        "kernel_avg_us": {k_: (round(v_ * 1e3, 3) if v_ else None) for k_, v_ in kernels.items()},
+        "append": prefill,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def bench_prefill(torch, wk, synth, dev, args):
+    cfg = synth.CONFIGS["prefill"]
+    w = synth.Workload(cfg, seed=args.seed)
+    B, H, D, BITS, n = cfg["batch"], cfg["n_kv"], cfg["d"], cfg["bits"], cfg["ctx"]
+    log("prefill append: generating %d x %d tokens" % (B, n))
+    as_dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+    k = as_dev(np.stack([w.keys(b, 0, n) for b in range(B)]))
+    v = as_dev(np.stack([w.values(b, 0, n) for b in range(B)]))
+    tk_bits, _ = w.transform()
+    tk = as_dev(tk_bits)
+    cache = wk.WushKVCache(B, H, D, BITS, cfg["s_sink"], cfg["s_keep"], cfg["s_flush"],
+                           cfg["kappa_k"], cfg["kappa_v"], max_seq_len=n)
+    nn = torch.full((B,), n, dtype=torch.int32, device=dev)
+    reps = 10
+    wk.wushkv_timing_enable(16 * reps)
+    times = []
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for r in range(reps + 2):
+        cache.seq_len.zero_()
+        cache.quant_end.zero_()
+        torch.cuda.synchronize()
+        e0.record()
+        wk.wushkv_append(cache, k, v, nn, tk)
+        e1.record()
+        torch.cuda.synchronize()
+        if r >= 2:
+            times.append(e0.elapsed_time(e1))
+    cnt, tot = wk.wushkv_timing_read("append_kernel")
+    wk.wushkv_timing_enable(0)
+    ms = float(np.median(times))
+    t_kernel = tot / cnt
+    tokens = B * n
+    Q = int(cache.quant_end[0].item())
+    n_quant = Q - cfg["s_sink"]
+    byts = prefill_bytes(B, H, D, BITS, n, n_quant)
+    ach = byts / (t_kernel * 1e-3) / 1e9
+    log("prefill append: %.1f us/call, %.3g tokens/s, append_kernel %.1f us, %.1f GB/s"
+        % (ms * 1e3, tokens / (ms * 1e-3), t_kernel * 1e3, ach))
+    return {"workload": "prefill-append-4x16384-2bit", "tokens_per_s": round(tokens / (ms * 1e-3), 1),
+            "ms_per_call": round(ms, 4), "bytes_per_call": int(byts),
+            "roofline": {"bound": "hbm", "kernel": "append_kernel", "achieved": round(ach, 2),
+                         "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
+                         "traffic": None, "avg_us": round(t_kernel * 1e3, 3)},
+            "roofline_tokens_per_s": round(tokens / (byts / (PEAK_HBM_GBS * 1e9)), 1)}
+
+
+def bench_oracle(cfg, w, tk_bits, tinv, budget_s):
+    """The oracle as it stands, single-threaded, on a sample of the same
+    workload: two (sequence, kv head) pairs are filled with the 8192-token
+    prefill (untimed), then decode steps -- append one token, decode the
+    pair's query group -- are timed until about budget_s seconds of CPU."""
+    import oracle
+    d, G, ctx = cfg["d"], cfg["n_q"] // cfg["n_kv"], cfg["ctx"]
+    sm = 1.0 / math.sqrt(d)
+    pairs = [(0, 0), (5, 3)]
+    cap = ctx + 1024
+    states = []
+    for b, h in pairs:
+        kk = w.keys(b, 0, ctx)[:, h:h + 1][None]
+        vv = w.values(b, 0, ctx)[:, h:h + 1][None]
+        oc = oracle.OracleCache(1, 1, d, cfg["bits"], cfg["s_sink"], cfg["s_keep"],
+                                cfg["s_flush"], cfg["kappa_k"], cfg["kappa_v"], cap)
+        oc.append(kk, vv, np.array([ctx]), tk_bits[h:h + 1])
+        states.append((b, h, oc))
+    q = w.query(0)
+    spent = 0.0
+    nbytes = 0
+    steps = 0
+    while spent < budget_s and steps < 2 * (cap - ctx):
+        b, h, oc = states[steps % len(states)]
+        S0 = int(oc.seq_len[0])
+        kk = w.keys(b, S0, 1)[:, h:h + 1][None]
+        vv = w.values(b, S0, 1)[:, h:h + 1][None]
+        qq = np.ascontiguousarray(q[b:b + 1, h * G:(h + 1) * G])
+        Q0 = int(oc.quant_end[0])
+        t0 = time.process_time()
+        oc.append(kk, vv, np.array([1]), tk_bits[h:h + 1])
+        oc.decode(qq, tinv[h:h + 1], sm)
+        spent += time.process_time() - t0
+        S, Q = int(oc.seq_len[0]), int(oc.quant_end[0])
+        main_b, other_b = decode_bytes([S], [Q], cfg["s_sink"], 1, G, d, cfg["bits"])
+        flushed = max(0, Q - max(Q0, cfg["s_sink"]))
+        nbytes += main_b + other_b + append_step_bytes(1, 1, d, cfg["bits"], 1, flushed)
+        steps += 1
+    gbs = nbytes / spent / 1e9
+    log("oracle: %d decode steps on %d (sequence, head) pairs in %.1fs CPU -> %.5f GB/s"
+        % (steps, len(pairs), spent, gbs))
+    return {"value": round(gbs, 6), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": "%d decode steps (append 1 token + decode %d query heads) alternating over "
+                      "%d (sequence, kv head) pairs of the %d-token workload, single thread"
+                      % (steps, G, len(pairs), ctx)}
+
+
+if __name__ == "__main__":
+    main()

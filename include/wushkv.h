@@ -224,8 +224,9 @@ int wushkv_abi_version(void);
  * up to `slots` launches; disabling (slots = 0) releases the events.  This
  * is the only library state and it is not thread-safe; leave it off in
  * production.  wushkv_timing_read synchronises on the recorded events and
- * returns, for launches whose kernel name contains `name_substr`, the count
- * and the summed milliseconds, then clears the record.
+ * returns, for launches whose kernel name contains `name_substr` (all
+ * launches for NULL), the count and the summed milliseconds.  Reading does
+ * not clear the record; calling wushkv_timing_enable again does.
  */
 int wushkv_timing_enable(int32_t slots);
 int wushkv_timing_read(const char *name_substr, int32_t *count, double *total_ms);

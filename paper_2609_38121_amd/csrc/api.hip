@@ -132,6 +132,5 @@ extern "C" int wushkv_timing_read(const char *name_substr, int32_t *count, doubl
         *count += 1;
         *total_ms += ms;
     }
-    t.used = 0;
     return WUSHKV_OK;
 }

@@ -8,14 +8,16 @@
 //   decode_main_kernel     grid (splits, kv heads, batch), four waves per
 //                          workgroup.  The "units" of a (sequence, head) are
 //                          the win_slots / 64 window units (bf16 sink + ring)
-//                          followed by the quantised pages; a split owns a
-//                          run of units and each wave every fourth of them.
-//                          Per unit a wave computes 64 scores with the
-//                          16x16x32 bf16 matrix instruction (codes as the A
-//                          operand, the G query heads as columns), keeps an
-//                          online softmax, and accumulates P V with a second
-//                          matrix product.  Partials (m, l, o) go to the
-//                          workspace.
+//                          followed by the quantised pages.  A split owns a
+//                          run of units and each wave a contiguous part of
+//                          it; while a wave computes one page it has the next
+//                          page's words and parameters in flight.  Per unit
+//                          the wave forms 64 scores with the 16x16x32 bf16
+//                          matrix instruction (codes as the A operand, the G
+//                          query heads as columns), keeps an online softmax
+//                          and accumulates P V with a second matrix product.
+//                          The four waves merge in LDS; the workgroup writes
+//                          one partial (m, l, o) per query head.
 //   decode_combine_kernel  log-sum-exp merge of the splits.
 //
 // Scores against codes.  A stored key is k = s c + z per token, so
@@ -23,15 +25,19 @@
 // The codes are widened to bf16 as 128 + c 2^sh (see widen_word), hence
 //   q~' . (128 + c 2^sh) = 128 sum(q~') + q~ . c   with q~' = q~ 2^-sh,
 // and the correction 128 sum(q~') is subtracted per query head.  Values
-// likewise: sum_t p_t (s_t c_t + z_t) = sum_t (p_t s_t) c_t + sum_t p_t z_t.
-// q~' and the weights p_t s_t 2^-sh are split into bf16 hi + lo parts (about
-// 16 significant bits) and both parts go through the matrix cores, so the
-// products carry fp32-level accuracy.
+// likewise: sum_t p_t (s_t c_t + z_t) = sum_t (p_t s_t) c_t + sum_t p_t z_t;
+// value codes are widened to fp16 as 1024 + c 4^p and the weights
+// p_t s_t 4^-p enter the fp16 product as one fp16 operand (11 significant
+// bits, a relative error below 2.5e-4 per weight); the 1024 offset is removed
+// with one more matrix product against a constant-1024 operand, which yields
+// 1024 sum_t A_t per row.  q~' is split into bf16 hi + lo parts (about 16
+// significant bits), so the scores carry fp32-level accuracy.
 #include "common.h"
 
 namespace wushkv {
 
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kMaxSplits = 1024;
 
 struct DecodeArgs {
     const uint8_t *pages;
@@ -42,36 +48,63 @@ struct DecodeArgs {
     const int32_t *quant_end;
     int32_t n_kv, s_sink, win_slots, max_pages, n_pages;
     int32_t G, n_q;
-    int32_t units_per_split, n_splits;
+    int32_t units_per_wave, n_splits;
+    WidenMasks wk, wv;  // key codes to bf16, value codes to fp16
     const float *qt;  // [batch][n_q][D]
     float *part;      // [batch][n_kv][n_splits][G][D + 2]
 };
 
+__device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // ------------------------------------------------------------------ q~
 
+// One workgroup per (kv head, sequence).  Thread (ig, jg) multiplies a block
+// of rows i of T^{-1} (kRows of them) by the G queries for 8 output channels
+// j; all of a thread's loads are independent and issued together, and the
+// row blocks are summed in LDS.
 template <int D>
 __global__ void __launch_bounds__(256) decode_qt_kernel(const uint16_t *q, const float *tinv,
                                                         float *qt, int32_t n_kv, int32_t G,
                                                         float scale)
 {
+    constexpr int kJG = D / 8;        // groups of 8 output channels
+    constexpr int kIG = 256 / kJG;    // groups of rows
+    constexpr int kRows = D / kIG;    // rows per group
     __shared__ float qs[8 * D];
+    __shared__ float red[kIG][8][D];
     const int h = blockIdx.x, b = blockIdx.y;
     const int n_q = n_kv * G;
     const uint16_t *qb = q + ((int64_t)b * n_q + h * G) * D;
-    for (int i = threadIdx.x; i < G * D; i += blockDim.x) qs[i] = bf16_bits_to_f32(qb[i]);
+    for (int i = threadIdx.x; i < G * D; i += 256) qs[i] = bf16_bits_to_f32(qb[i]);
+    const int jg = threadIdx.x % kJG, ig = threadIdx.x / kJG;
+    const float *T = tinv + (int64_t)h * D * D + (int64_t)ig * kRows * D + 8 * jg;
+    f32x4 t[kRows][2];
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) {
+        t[r][0] = *reinterpret_cast<const f32x4 *>(T + (int64_t)r * D);
+        t[r][1] = *reinterpret_cast<const f32x4 *>(T + (int64_t)r * D + 4);
+    }
     __syncthreads();
-    const float *T = tinv + (int64_t)h * D * D;
-    for (int jj = threadIdx.x; jj < D; jj += blockDim.x) {
+    for (int g = 0; g < G; ++g) {
         float acc[8];
 #pragma unroll
-        for (int g = 0; g < 8; ++g) acc[g] = 0.0f;
-        for (int i = 0; i < D; ++i) {
-            const float t = T[(int64_t)i * D + jj];
+        for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
 #pragma unroll
-            for (int g = 0; g < 8; ++g)
-                if (g < G) acc[g] = fmaf(qs[g * D + i], t, acc[g]);
+        for (int r = 0; r < kRows; ++r) {
+            const float qi = qs[g * D + ig * kRows + r];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[e] = fmaf(qi, t[r][e >> 2][e & 3], acc[e]);
         }
-        for (int g = 0; g < G; ++g) qt[((int64_t)b * n_q + h * G + g) * D + jj] = acc[g] * scale;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) red[ig][g][8 * jg + e] = acc[e];
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < G * D; idx += 256) {
+        const int g = idx / D, jj = idx % D;
+        float s = 0.0f;
+#pragma unroll
+        for (int k = 0; k < kIG; ++k) s += red[k][g][jj];
+        qt[((int64_t)b * n_q + h * G + g) * D + jj] = s * scale;
     }
 }
 
@@ -89,23 +122,14 @@ __device__ __forceinline__ float wave_sum_xor_16_32(float x)
     x += __shfl_xor(x, 32);
     return x;
 }
-__device__ __forceinline__ float readlane_f(float x, int l)
-{
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
-}
 
-__device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float bf16_hi_to_f32(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
 // hi = bf16(x) (nearest even), lo = bf16(x - hi), for a pair of values.
-__device__ __forceinline__ void split_hi_lo(float x0, float x1, uint32_t &hi, uint32_t &lo,
-                                            float &h0, float &h1, float &l0, float &l1)
+__device__ __forceinline__ void split_hi_lo(float x0, float x1, uint32_t &hi, uint32_t &lo)
 {
     hi = pack_bf16_rne(x0, x1);
-    h0 = bf16_bits_to_f32(hi & 0xFFFFu);
-    h1 = bf16_bits_to_f32(hi >> 16);
-    lo = pack_bf16_rne(x0 - h0, x1 - h1);
-    l0 = bf16_bits_to_f32(lo & 0xFFFFu);
-    l1 = bf16_bits_to_f32(lo >> 16);
+    lo = pack_bf16_rne(x0 - bf16_bits_to_f32(hi & 0xFFFFu), x1 - bf16_hi_to_f32(hi));
 }
 
 // Token of the page (or window unit) whose score lands in accumulator row
@@ -115,14 +139,96 @@ __device__ __forceinline__ int score_token(int tau, int j, int r)
     return 32 * (tau >> 1) + 8 * j + 4 * (tau & 1) + r;
 }
 
+// Packed operands and parameters of one page, as one lane holds them.
+template <int D, int BITS>
+struct PageRegs {
+    using L = Layout<D, BITS>;
+    uint32_t kw[L::kWordsPerLane];
+    uint32_t vw[L::kWordsPerLane];
+    uint32_t kp[2][8];  // (scale, zero) of tokens 32 kc + 8 j + i
+    uint32_t vp[2][8];
+
+    __device__ __forceinline__ void load(const uint8_t *pgb, int lane, int j)
+    {
+        constexpr int kQ = L::kWordsPerLane / 4;
+        const u32x4 *kr = reinterpret_cast<const u32x4 *>(pgb) + lane * kQ;
+        const u32x4 *vr = reinterpret_cast<const u32x4 *>(pgb + L::kRegionBytes) + lane * kQ;
+#pragma unroll
+        for (int q4 = 0; q4 < kQ; ++q4) {
+            const u32x4 x = kr[q4], y = vr[q4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                kw[4 * q4 + e] = x[e];
+                vw[4 * q4 + e] = y[e];
+            }
+        }
+        const u32x4 *kpr = reinterpret_cast<const u32x4 *>(pgb + L::kParamOffset);
+        const u32x4 *vpr = reinterpret_cast<const u32x4 *>(pgb + L::kParamOffset + 4 * kPage);
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2) {
+                const u32x4 x = kpr[(32 * kc + 8 * j) / 4 + h2];
+                const u32x4 y = vpr[(32 * kc + 8 * j) / 4 + h2];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    kp[kc][4 * h2 + e] = x[e];
+                    vp[kc][4 * h2 + e] = y[e];
+                }
+            }
+    }
+};
+
+// One wave's online softmax and output accumulators.
+template <int D>
+struct WaveState {
+    static constexpr int kNT = D / 16;
+    f32x4 acc[kNT];  // P V accumulators, rows 4 j + r (head g: hi row g, lo row g + G)
+    f32x4 accb;      // 128 sum_t A_t per row (offset of the widened value codes)
+    float m_lane;    // running max of this lane's column
+    float l_lane;    // sum of p over this lane's tokens
+    float z_lane;    // sum of p * value zero over this lane's tokens
+
+    __device__ __forceinline__ void init()
+    {
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        accb = f32x4{0.f, 0.f, 0.f, 0.f};
+        m_lane = -INFINITY;
+        l_lane = 0.0f;
+        z_lane = 0.0f;
+    }
+
+    // Fold a unit's column max into the running max; rescale on change.
+    // Accumulator row 4 j + r belongs to head (4 j + r) mod G, whose factor
+    // lane (4 j + r) mod G holds (every lane of a column has the same max).
+    __device__ __forceinline__ void update_max(float mloc, int j, int G)
+    {
+        const float m_new = fmaxf(m_lane, mloc);
+        if (__any(m_new > m_lane)) {
+            const float al = (m_new == -INFINITY) ? 1.0f : fexp2(m_lane - m_new);
+            l_lane *= al;
+            z_lane *= al;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float ar = __shfl(al, (4 * j + r) & (G - 1));
+#pragma unroll
+                for (int nt = 0; nt < kNT; ++nt) acc[nt][r] *= ar;
+                accb[r] *= ar;
+            }
+        }
+        m_lane = m_new;
+    }
+};
+
 template <int D, int BITS>
 __global__ void __launch_bounds__(256, 2) decode_main_kernel(DecodeArgs a)
 {
     using L = Layout<D, BITS>;
-    constexpr int kC = L::kChunks;    // D / 32
-    constexpr int kNT = L::kNTiles;   // D / 16
+    constexpr int kC = L::kChunks;   // D / 32
+    constexpr int kNT = L::kNTiles;  // D / 16
     constexpr int kNw = L::kNw;
-    constexpr int kWpl = L::kWordsPerLane;
+    constexpr int kOpw = L::kOpsPerWord;
 
     __shared__ float sC[4][16][D];
     __shared__ float sM[4][8], sL[4][8], sZ[4][8];
@@ -140,301 +246,278 @@ __global__ void __launch_bounds__(256, 2) decode_main_kernel(DecodeArgs a)
     const int32_t q_hi = qend > a.s_sink ? qend : a.s_sink;  // quantised: [s_sink, q_hi)
     const int32_t n_qpages = (q_hi - a.s_sink + kPage - 1) / kPage;
     const int32_t n_wunits = a.win_slots / kPage;
-    const int32_t n_units = n_wunits + n_qpages;
+    const int32_t n_units = n_qpages + n_wunits;  // pages first, then the window units
     const int32_t ring = a.win_slots - a.s_sink;
-    // ring holds positions [q_hi, S); the oldest sits at ring index a0
+    // the ring holds positions [q_hi, S); the oldest sits at ring index a0
     const int32_t a0 = S > q_hi ? (q_hi - a.s_sink) % ring : 0;
     const int32_t ring_live = S > q_hi ? S - q_hi : 0;
 
+    // this wave's units
+    const int upw = a.units_per_wave;
+    const int w0 = (split * 4 + wave) * upw;
+    const int w1 = min(w0 + upw, n_units);
+
     const float *qrow = a.qt + ((int64_t)b * a.n_q + h * G + g) * D;
-    float zsum = 0.0f;  // sum of q~ over the channels (zero-point term)
-    if (cls < 2) {
-#pragma unroll
-        for (int c = 0; c < kC; ++c)
-#pragma unroll
-            for (int i = 0; i < 8; ++i) zsum += qrow[32 * c + 8 * j + i];
-    }
-    zsum = wave_sum_xor_16_32(zsum);
-
-    // B operands for the score products (hi and lo parts), rebuilt when the
-    // wave switches between window units (plain q~) and pages (q~ 2^-sh).
-    uint32_t bhi[kC][4], blo[kC][4];
-    float qbias = 0.0f;  // 128 * sum of the operand values, pages only
-    int mode = -1;       // 0 window, 1 pages
-    auto build_b = [&](int m) {
-        float part = 0.0f;
-#pragma unroll
-        for (int c = 0; c < kC; ++c)
-#pragma unroll
-            for (int p = 0; p < 4; ++p) {
-                const float sc = m ? slot_scale<BITS>(2 * p) : 1.0f;
-                float x0 = 0.0f, x1 = 0.0f;
-                if (cls < 2) {
-                    x0 = qrow[32 * c + 8 * j + 2 * p] * sc;
-                    x1 = qrow[32 * c + 8 * j + 2 * p + 1] * sc;
-                }
-                float h0, h1, l0, l1;
-                split_hi_lo(x0, x1, bhi[c][p], blo[c][p], h0, h1, l0, l1);
-                part += (h0 + l0) + (h1 + l1);
-            }
-        qbias = m ? 128.0f * wave_sum_xor_16_32(part) : 0.0f;
-        mode = m;
-    };
-
-    // online-softmax state
-    float m_run[8];
-#pragma unroll
-    for (int gg = 0; gg < 8; ++gg) m_run[gg] = -INFINITY;
-    float m_lane = -INFINITY;  // m_run[g] of this lane's column
-    float l_lane = 0.0f;       // sum of p over this lane's tokens (hi columns only)
-    float z_lane = 0.0f;       // value-side corrections (pages)
-    f32x4 acc[kNT];
-#pragma unroll
-    for (int nt = 0; nt < kNT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int u_begin = split * a.units_per_split;
-    const int u_end = min(u_begin + a.units_per_split, n_units);
     const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;
 
-    for (int u = u_begin + wave; u < u_end; u += 4) {
-        const bool is_win = u < n_wunits;
-        // ---- locate the unit, its valid tokens and load its operands
-        int32_t nvalid = 0;
-        const uint8_t *pgb = nullptr;
-        int32_t slot0 = 0;
-        if (!is_win) {
-            const int32_t lp = u - n_wunits;
-            const int32_t phys = lp < a.max_pages ? a.page_table[(int64_t)b * a.max_pages + lp] : -1;
-            if (phys < 0 || phys >= a.n_pages) continue;
-            pgb = a.pages + ((int64_t)phys * a.n_kv + h) * L::kPageBytes;
-            nvalid = min(kPage, q_hi - (a.s_sink + lp * kPage));
-        } else {
-            slot0 = u * kPage;
-        }
-        auto win_valid = [&](int t) -> bool {
-            const int32_t sl = slot0 + t;
-            if (sl < a.s_sink) return sl < S;
-            const int32_t off = (sl - a.s_sink - a0 + ring) % ring;
-            return off < ring_live;
-        };
-        auto tok_valid = [&](int t) -> bool { return is_win ? win_valid(t) : t < nvalid; };
-        if (is_win) {
-            bool any = false;
-            for (int t = lane; t < kPage; t += 64) any |= win_valid(t);
-            if (!__any(any)) continue;
-        }
-        if (mode != (is_win ? 0 : 1)) build_b(is_win ? 0 : 1);
+    WaveState<D> st;
+    st.init();
 
-        // ---- scores: S^T[token][col] for four tiles of 16 tokens
-        f32x4 sc[4];
-        uint32_t vw[kWpl];
-        uint32_t kp[2][8], vp[2][8];
-        if (!is_win) {
-            const u32x4 *kr = reinterpret_cast<const u32x4 *>(pgb) + lane * (kWpl / 4);
-            const u32x4 *vr = reinterpret_cast<const u32x4 *>(pgb + L::kRegionBytes) + lane * (kWpl / 4);
-            uint32_t kw[kWpl];
+    // B operands of the score products: hi and lo parts of q~ (2^-sh scaled
+    // for pages); columns n < 2G carry query head g = n mod G.
+    uint32_t bhi[kC][4], blo[kC][4];
+    float zsum = 0.0f, qbias = 0.0f;
+    auto build_b = [&](bool pages) {
+        float part = 0.0f, zs = 0.0f;
 #pragma unroll
-            for (int q4 = 0; q4 < kWpl / 4; ++q4) {
-                u32x4 x = kr[q4], y = vr[q4];
+        for (int c = 0; c < kC; ++c) {
+            float x[8];
+            if (cls < 2) {
+                const f32x4 lo4 = *reinterpret_cast<const f32x4 *>(qrow + 32 * c + 8 * j);
+                const f32x4 hi4 = *reinterpret_cast<const f32x4 *>(qrow + 32 * c + 8 * j + 4);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    kw[4 * q4 + e] = x[e];
-                    vw[4 * q4 + e] = y[e];
+                    x[e] = lo4[e];
+                    x[4 + e] = hi4[e];
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[e] = 0.0f;
+            }
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                zs += x[2 * p] + x[2 * p + 1];
+                const float sc = pages ? slot_scale<BITS>(2 * p) : 1.0f;
+                split_hi_lo(x[2 * p] * sc, x[2 * p + 1] * sc, bhi[c][p], blo[c][p]);
+                part += (bf16_bits_to_f32(bhi[c][p] & 0xFFFFu) + bf16_hi_to_f32(bhi[c][p])) +
+                        (bf16_bits_to_f32(blo[c][p] & 0xFFFFu) + bf16_hi_to_f32(blo[c][p]));
+            }
+        }
+        zsum = wave_sum_xor_16_32(zs);
+        qbias = pages ? 128.0f * wave_sum_xor_16_32(part) : 0.0f;
+    };
+    auto bop = [](const uint32_t (&v)[4]) {
+        return __builtin_bit_cast(bf16x8, u32x4{v[0], v[1], v[2], v[3]});
+    };
+
+    // ---------------------------------------------------- quantised pages
+    const int pw1 = min(w1, n_qpages);
+    if (w0 < pw1) {
+        build_b(true);
+        // widening masks in scalar registers and the biases in vector
+        // registers (one v_mov each, opaque to the optimizer), so that
+        // (word & mask) | bias selects v_and_or_b32 with one scalar operand
+        WidenMasks wk = a.wk, wv = a.wv;
+        asm volatile("v_mov_b32 %0, %1" : "=v"(wk.bias) : "s"(a.wk.bias));
+        asm volatile("v_mov_b32 %0, %1" : "=v"(wv.bias) : "s"(a.wv.bias));
+        const f16x8 c1024 = __builtin_bit_cast(f16x8, u32x4{kBiasF16x2, kBiasF16x2, kBiasF16x2, kBiasF16x2});
+        // the wave's page-table entries, one per lane, read once
+        int32_t tbl = -1;
+        if (w0 + lane < pw1 && w0 + lane < a.max_pages)
+            tbl = a.page_table[(int64_t)b * a.max_pages + w0 + lane];
+        auto page_ptr = [&](int u) -> const uint8_t * {
+            const int32_t phys = __builtin_amdgcn_readlane(tbl, u - w0);
+            if (phys < 0 || phys >= a.n_pages) return nullptr;
+            return a.pages + ((int64_t)phys * a.n_kv + h) * L::kPageBytes;
+        };
+        PageRegs<D, BITS> cur, nxt;
+        const uint8_t *pc = page_ptr(w0);
+        if (pc) cur.load(pc, lane, j);
+        for (int u = w0; u < pw1; ++u) {
+            const uint8_t *pn = (u + 1 < pw1) ? page_ptr(u + 1) : nullptr;
+            if (pn) nxt.load(pn, lane, j);
+            if (pc) {
+                const int32_t nvalid = min(kPage, q_hi - (a.s_sink + u * kPage));
+                // scores S^T[token][column] - 128 sum q~', four tiles of 16 tokens
+                f32x4 sc[4];
+#pragma unroll
+                for (int tau = 0; tau < 4; ++tau) {
+                    sc[tau] = f32x4{-qbias, -qbias, -qbias, -qbias};
+#pragma unroll
+                    for (int w = 0; w < kNw; ++w) {
+                        uint32_t op[L::kCodesPerWord / 2];
+                        widen_word<BITS>(cur.kw[tau * kNw + w], op, wk);
+#pragma unroll
+                        for (int o = 0; o < kOpw; ++o) {
+                            const int c = w * kOpw + o;
+                            const bf16x8 A = as_op(op + 4 * o);
+                            sc[tau] = mfma16(A, bop(bhi[c]), sc[tau]);
+                            sc[tau] = mfma16(A, bop(blo[c]), sc[tau]);
+                        }
+                    }
+                }
+                // logits (base 2): s (S - 128 sum q~') + z sum q~
+                float lg[4][4];
+#pragma unroll
+                for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const uint32_t kprm = cur.kp[tau >> 1][4 * (tau & 1) + r];
+                        lg[tau][r] = fmaf(f16_bits_to_f32(kprm & 0xFFFFu), sc[tau][r],
+                                          f16_bits_to_f32(kprm >> 16) * zsum);
+                    }
+                if (nvalid < kPage) {
+#pragma unroll
+                    for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            if (score_token(tau, j, r) >= nvalid) lg[tau][r] = -INFINITY;
+                }
+                float mloc = -INFINITY;
+#pragma unroll
+                for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) mloc = fmaxf(mloc, lg[tau][r]);
+                st.update_max(wave_max_xor_16_32(mloc), j, G);
+                // weights p s 4^-p as fp16, in the A rows g < G
+                uint32_t aop[2][4];
+#pragma unroll
+                for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+                    for (int p = 0; p < 4; ++p) {
+                        float wv2[2];
+#pragma unroll
+                        for (int e = 0; e < 2; ++e) {
+                            const int i = 2 * p + e;  // slot: token 32 kc + 8 j + i
+                            const float pr = fexp2(lg[2 * kc + (i >> 2)][i & 3] - st.m_lane);
+                            const uint32_t vprm = cur.vp[kc][i];
+                            st.l_lane += pr;
+                            st.z_lane = fmaf(pr, f16_bits_to_f32(vprm >> 16), st.z_lane);
+                            wv2[e] = pr * (f16_bits_to_f32(vprm & 0xFFFFu) * slot_scale_f16<BITS>(i));
+                        }
+                        aop[kc][p] = cls == 0 ? pack_f16_rne(wv2[0], wv2[1]) : 0u;
+                    }
+                // P V, plus the row sums that remove the 1024 offset
+#pragma unroll
+                for (int kc = 0; kc < 2; ++kc) {
+                    const f16x8 A = __builtin_bit_cast(f16x8, u32x4{aop[kc][0], aop[kc][1], aop[kc][2], aop[kc][3]});
+#pragma unroll
+                    for (int uu = 0; uu < 2 * kNw; ++uu) {
+                        uint32_t op[L::kCodesPerWord / 2];
+                        widen_word_f16<BITS>(cur.vw[kc * 2 * kNw + uu], op, wv);
+#pragma unroll
+                        for (int o = 0; o < kOpw; ++o) {
+                            const int nt = uu * kOpw + o;
+                            st.acc[nt] = mfma16h(A, as_op_h(op + 4 * o), st.acc[nt]);
+                        }
+                    }
+                    st.accb = mfma16h(A, c1024, st.accb);
                 }
             }
-            const u32x4 *kpr = reinterpret_cast<const u32x4 *>(pgb + L::kParamOffset);
-            const u32x4 *vpr = reinterpret_cast<const u32x4 *>(pgb + L::kParamOffset + 4 * kPage);
+            cur = nxt;
+            pc = pn;
+        }
+    }
+
+    // ---------------------------------------------------- window units
+    const int ww0 = max(w0, n_qpages);
+    if (ww0 < w1) {
+        build_b(false);
+        for (int u = ww0; u < w1; ++u) {
+            const int32_t slot0 = (u - n_qpages) * kPage;
+            // slot validity of the unit, one bit per slot
+            bool mine;
+            {
+                const int32_t sl = slot0 + lane;
+                if (sl < a.s_sink) mine = sl < S;
+                else mine = ((sl - a.s_sink - a0 + ring) % ring) < ring_live;
+            }
+            const uint64_t vmask = __ballot(mine);
+            if (vmask == 0) continue;
+            auto valid = [&](int t) -> bool { return (vmask >> t) & 1u; };
+            const uint16_t *wk = a.win_k + (head_win + slot0) * D;
+            // All loads stay inside this unit's slots, so they are issued
+            // unconditionally (a branch per load would serialise them);
+            // dead slots are zeroed afterwards, whatever bits they held.
+            u32x4 kx[4][kC];
+#pragma unroll
+            for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+                for (int c = 0; c < kC; ++c)
+                    kx[tau][c] = *reinterpret_cast<const u32x4 *>(
+                        wk + (int64_t)score_token(tau, n >> 2, n & 3) * D + 32 * c + 8 * j);
+            const uint16_t *wvp = a.win_v + head_win * D + slot0;
+            u32x4 vx[2][kNT];
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
-                for (int h2 = 0; h2 < 2; ++h2) {
-                    u32x4 x = kpr[(32 * kc + 8 * j) / 4 + h2];
-                    u32x4 y = vpr[(32 * kc + 8 * j) / 4 + h2];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        kp[kc][4 * h2 + e] = x[e];
-                        vp[kc][4 * h2 + e] = y[e];
-                    }
-                }
+                for (int nt = 0; nt < kNT; ++nt)
+                    vx[kc][nt] = *reinterpret_cast<const u32x4 *>(
+                        wvp + (int64_t)(16 * nt + n) * a.win_slots + 32 * kc + 8 * j);
+            f32x4 sc[4];
 #pragma unroll
             for (int tau = 0; tau < 4; ++tau) {
-                sc[tau] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int w = 0; w < kNw; ++w) {
-                    uint32_t op[L::kCodesPerWord / 2];
-                    widen_word<BITS>(kw[tau * kNw + w], op);
-#pragma unroll
-                    for (int o = 0; o < L::kOpsPerWord; ++o) {
-                        const int c = w * L::kOpsPerWord + o;
-                        const bf16x8 A = as_op(op + 4 * o);
-                        sc[tau] = mfma16(A, __builtin_bit_cast(bf16x8, u32x4{bhi[c][0], bhi[c][1], bhi[c][2], bhi[c][3]}), sc[tau]);
-                        sc[tau] = mfma16(A, __builtin_bit_cast(bf16x8, u32x4{blo[c][0], blo[c][1], blo[c][2], blo[c][3]}), sc[tau]);
-                    }
-                }
-            }
-        } else {
-            const uint16_t *wk = a.win_k + (head_win + slot0) * D;
-#pragma unroll
-            for (int tau = 0; tau < 4; ++tau) {
-                const int t = score_token(tau, n >> 2, n & 3);  // A row n of tile tau
-                const bool ok = win_valid(t);
+                // A row n of tile tau is token score_token(tau, n / 4, n % 4)
+                const uint32_t keep = valid(score_token(tau, n >> 2, n & 3)) ? 0xFFFFFFFFu : 0u;
                 sc[tau] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int c = 0; c < kC; ++c) {
-                    u32x4 x = {0u, 0u, 0u, 0u};
-                    if (ok) x = *reinterpret_cast<const u32x4 *>(wk + (int64_t)t * D + 32 * c + 8 * j);
+                    const u32x4 x = {kx[tau][c][0] & keep, kx[tau][c][1] & keep,
+                                     kx[tau][c][2] & keep, kx[tau][c][3] & keep};
                     const bf16x8 A = __builtin_bit_cast(bf16x8, x);
-                    sc[tau] = mfma16(A, __builtin_bit_cast(bf16x8, u32x4{bhi[c][0], bhi[c][1], bhi[c][2], bhi[c][3]}), sc[tau]);
-                    sc[tau] = mfma16(A, __builtin_bit_cast(bf16x8, u32x4{blo[c][0], blo[c][1], blo[c][2], blo[c][3]}), sc[tau]);
+                    sc[tau] = mfma16(A, bop(bhi[c]), sc[tau]);
+                    sc[tau] = mfma16(A, bop(blo[c]), sc[tau]);
                 }
             }
-        }
-
-        // ---- logits (base 2), masked
-        float lg[4][4];
-        float mloc = -INFINITY;
+            float lg[4][4];
+            float mloc = -INFINITY;
 #pragma unroll
-        for (int tau = 0; tau < 4; ++tau)
+            for (int tau = 0; tau < 4; ++tau)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int t = score_token(tau, j, r);
-                float v;
-                if (!is_win) {
-                    const uint32_t kprm = kp[tau >> 1][4 * (tau & 1) + r];
-                    const float ks = f16_bits_to_f32(kprm & 0xFFFFu), kz = f16_bits_to_f32(kprm >> 16);
-                    v = fmaf(ks, sc[tau][r] - qbias, kz * zsum);
-                } else {
-                    v = sc[tau][r];
+                for (int r = 0; r < 4; ++r) {
+                    const float v = valid(score_token(tau, j, r)) ? sc[tau][r] : -INFINITY;
+                    lg[tau][r] = v;
+                    mloc = fmaxf(mloc, v);
                 }
-                v = (cls < 2 && tok_valid(t)) ? v : -INFINITY;
-                lg[tau][r] = v;
-                mloc = fmaxf(mloc, v);
-            }
-        mloc = wave_max_xor_16_32(mloc);
-        const float m_new_lane = fmaxf(m_lane, mloc);
-        // rescale when any column's running max moved
-        bool moved = false;
-        float alpha[8];
+            st.update_max(wave_max_xor_16_32(mloc), j, G);
+            uint32_t aop[2][4];
 #pragma unroll
-        for (int gg = 0; gg < 8; ++gg) {
-            float mn = gg < G ? fmaxf(m_run[gg], readlane_f(mloc, gg)) : -INFINITY;
-            alpha[gg] = (mn == -INFINITY) ? 1.0f : fexp2(m_run[gg] - mn);
-            moved |= (mn != m_run[gg]) && gg < G;
-            m_run[gg] = gg < G ? mn : m_run[gg];
-        }
-        if (moved) {
-            const float al = (m_new_lane == -INFINITY) ? 1.0f : fexp2(m_lane - m_new_lane);
-            l_lane *= al;
-            z_lane *= al;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int gr = (4 * j + r) & (G - 1);
-                float ar = alpha[0];
-#pragma unroll
-                for (int gg = 1; gg < 8; ++gg) ar = (gr == gg) ? alpha[gg] : ar;
-#pragma unroll
-                for (int nt = 0; nt < kNT; ++nt) acc[nt][r] *= ar;
-            }
-        }
-        m_lane = m_new_lane;
-
-        // ---- probabilities -> A operand of the P V product
-        uint32_t aop[2][4];
-#pragma unroll
-        for (int kc = 0; kc < 2; ++kc) {
-#pragma unroll
-            for (int p = 0; p < 4; ++p) {
-                float w2[2], pr2[2], vz2[2];
-#pragma unroll
-                for (int e = 0; e < 2; ++e) {
-                    const int i = 2 * p + e;              // slot: token 32 kc + 8 j + i
-                    const int tau = 2 * kc + (i >> 2), r = i & 3;
-                    const float pr = (lg[tau][r] == -INFINITY) ? 0.0f : fexp2(lg[tau][r] - m_new_lane);
-                    pr2[e] = pr;
-                    if (!is_win) {
-                        const uint32_t vprm = vp[kc][i];
-                        const float vs = f16_bits_to_f32(vprm & 0xFFFFu);
-                        vz2[e] = (pr == 0.0f) ? 0.0f : pr * f16_bits_to_f32(vprm >> 16);
-                        w2[e] = (pr == 0.0f) ? 0.0f : pr * (vs * slot_scale<BITS>(i));
-                    } else {
-                        vz2[e] = 0.0f;
-                        w2[e] = pr;
-                    }
-                }
-                uint32_t hi, lo;
-                float h0, h1, l0, l1;
-                split_hi_lo(w2[0], w2[1], hi, lo, h0, h1, l0, l1);
-                aop[kc][p] = cls == 0 ? hi : (cls == 1 ? lo : 0u);
-                if (cls == 0) {
-                    l_lane += pr2[0] + pr2[1];
-                    if (!is_win) z_lane += (vz2[0] + vz2[1]) - 128.0f * (h0 + h1);
-                } else if (cls == 1 && !is_win) {
-                    z_lane -= 128.0f * (l0 + l1);
-                }
-            }
-        }
-
-        // ---- P V
-        if (!is_win) {
-#pragma unroll
-            for (int kc = 0; kc < 2; ++kc) {
-                const bf16x8 A = as_op(aop[kc]);
-#pragma unroll
-                for (int uu = 0; uu < 2 * kNw; ++uu) {
-                    uint32_t op[L::kCodesPerWord / 2];
-                    widen_word<BITS>(vw[kc * 2 * kNw + uu], op);
-#pragma unroll
-                    for (int o = 0; o < L::kOpsPerWord; ++o) {
-                        const int nt = uu * L::kOpsPerWord + o;
-                        acc[nt] = mfma16(A, as_op(op + 4 * o), acc[nt]);
-                    }
-                }
-            }
-        } else {
-            const uint16_t *wv = a.win_v + head_win * D + slot0;
-#pragma unroll
-            for (int kc = 0; kc < 2; ++kc) {
-                const bf16x8 A = as_op(aop[kc]);
-                uint32_t msk[4];
-                bool anyv = false;
+            for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
                 for (int p = 0; p < 4; ++p) {
-                    const bool v0 = win_valid(32 * kc + 8 * j + 2 * p);
-                    const bool v1 = win_valid(32 * kc + 8 * j + 2 * p + 1);
-                    msk[p] = (v0 ? 0x0000FFFFu : 0u) | (v1 ? 0xFFFF0000u : 0u);
-                    anyv |= v0 | v1;
+                    float pr[2];
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) {
+                        const int i = 2 * p + e;
+                        pr[e] = fexp2(lg[2 * kc + (i >> 2)][i & 3] - st.m_lane);
+                    }
+                    st.l_lane += pr[0] + pr[1];
+                    uint32_t hi, lo;
+                    split_hi_lo(pr[0], pr[1], hi, lo);
+                    aop[kc][p] = cls == 0 ? hi : (cls == 1 ? lo : 0u);
                 }
 #pragma unroll
+            for (int kc = 0; kc < 2; ++kc) {
+                const bf16x8 A = bop(aop[kc]);
+                const uint32_t bits8 = (uint32_t)(vmask >> (32 * kc + 8 * j)) & 0xFFu;
+                uint32_t msk[4];
+#pragma unroll
+                for (int p = 0; p < 4; ++p)
+                    msk[p] = (((bits8 >> (2 * p)) & 1u) ? 0x0000FFFFu : 0u) |
+                             (((bits8 >> (2 * p + 1)) & 1u) ? 0xFFFF0000u : 0u);
+#pragma unroll
                 for (int nt = 0; nt < kNT; ++nt) {
-                    const int ch = 16 * nt + n;
-                    u32x4 x = {0u, 0u, 0u, 0u};
-                    if (anyv)
-                        x = *reinterpret_cast<const u32x4 *>(wv + (int64_t)ch * a.win_slots + 32 * kc + 8 * j);
-                    u32x4 y = {x[0] & msk[0], x[1] & msk[1], x[2] & msk[2], x[3] & msk[3]};
-                    acc[nt] = mfma16(A, __builtin_bit_cast(bf16x8, y), acc[nt]);
+                    const u32x4 x = vx[kc][nt];
+                    const u32x4 y = {x[0] & msk[0], x[1] & msk[1], x[2] & msk[2], x[3] & msk[3]};
+                    st.acc[nt] = mfma16(A, __builtin_bit_cast(bf16x8, y), st.acc[nt]);
                 }
             }
         }
     }
 
-    // ---- combine the four waves of the workgroup through LDS
-    l_lane = wave_sum_xor_16_32(l_lane);
-    z_lane = wave_sum_xor_16_32(z_lane);
+    // ---------------------------------------------------- merge the waves
+    // head g: rows g (pages and window hi parts) and g + G (window lo parts)
+    const float l_col = wave_sum_xor_16_32(st.l_lane);
+    const float z_col = wave_sum_xor_16_32(st.z_lane);
 #pragma unroll
     for (int nt = 0; nt < kNT; ++nt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) sC[wave][4 * j + r][16 * nt + n] = acc[nt][r];
-    if (lane < 8) {
-        sM[wave][lane] = lane < G ? m_run[0] : -INFINITY;
-#pragma unroll
-        for (int gg = 1; gg < 8; ++gg)
-            if (lane == gg) sM[wave][lane] = gg < G ? m_run[gg] : -INFINITY;
+        for (int r = 0; r < 4; ++r) sC[wave][4 * j + r][16 * nt + n] = st.acc[nt][r] - st.accb[r];
+    if (lane < G) {
+        sM[wave][lane] = st.m_lane;
+        sL[wave][lane] = l_col;
+        sZ[wave][lane] = z_col;
     }
-    // lanes n < G (j = 0) hold l for column g; lanes n < 2G hold z parts
-    if (lane < G) sL[wave][lane] = l_lane;
-    if (lane < 2 * G && lane >= G) sZ[wave][lane - G] = z_lane;
-    __syncthreads();
-    if (lane < G) sZ[wave][lane] += z_lane;  // hi part joins the lo part
     __syncthreads();
 
     float *part = a.part + (((int64_t)b * a.n_kv + h) * a.n_splits + split) * G * (D + 2);
@@ -463,27 +546,45 @@ __global__ void __launch_bounds__(256, 2) decode_main_kernel(DecodeArgs a)
 
 // ------------------------------------------------------------------ combine
 
+// One workgroup per (query head, sequence): the split maxima and weights go
+// through LDS, then every channel thread sums its column with the loads
+// unrolled so they are in flight together.
 template <int D>
 __global__ void __launch_bounds__(D) decode_combine_kernel(const float *part, float *out,
                                                            int32_t n_kv, int32_t G,
                                                            int32_t n_splits)
 {
+    __shared__ float fw[kMaxSplits];
+    __shared__ float red[D];
     const int qh = blockIdx.x, b = blockIdx.y;
     const int h = qh / G, g = qh % G;
     const int ch = threadIdx.x;
     const int n_q = n_kv * G;
-    const float *pp = part + (((int64_t)b * n_kv + h) * n_splits) * G * (D + 2) + g * (D + 2);
     const int64_t stride = (int64_t)G * (D + 2);
+    const float *pp = part + (((int64_t)b * n_kv + h) * n_splits) * stride + g * (D + 2);
     float mx = -INFINITY;
-    for (int s = 0; s < n_splits; ++s) mx = fmaxf(mx, pp[s * stride + D]);
+    for (int s = ch; s < n_splits; s += D) {
+        const float m = pp[s * stride + D];
+        fw[s] = m;
+        mx = fmaxf(mx, m);
+    }
+    red[ch] = mx;
+    __syncthreads();
+    for (int off = D / 2; off > 0; off >>= 1) {
+        if (ch < off) red[ch] = fmaxf(red[ch], red[ch + off]);
+        __syncthreads();
+    }
+    const float M = red[0];
+    for (int s = ch; s < n_splits; s += D)
+        fw[s] = (fw[s] == -INFINITY) ? 0.0f : fexp2(fw[s] - M);
+    __syncthreads();
     float o = 0.0f, l = 0.0f;
-    if (mx != -INFINITY) {
+    if (M != -INFINITY) {
+#pragma unroll 8
         for (int s = 0; s < n_splits; ++s) {
-            const float ms = pp[s * stride + D];
-            if (ms == -INFINITY) continue;
-            const float f = fexp2(ms - mx);
-            o += f * pp[s * stride + ch];
-            l += f * pp[s * stride + D + 1];
+            const float f = fw[s];
+            o = fmaf(f, pp[s * stride + ch], o);
+            l = fmaf(f, pp[s * stride + D + 1], l);
         }
     }
     out[((int64_t)b * n_q + qh) * D + ch] = (l > 0.0f) ? o / l : 0.0f;
@@ -492,7 +593,7 @@ __global__ void __launch_bounds__(D) decode_combine_kernel(const float *part, fl
 // ------------------------------------------------------------------ host
 
 struct DecodePlan {
-    int32_t units_per_split, n_splits;
+    int32_t units_per_wave, n_splits;
     size_t qt_bytes, part_bytes;
 };
 
@@ -502,14 +603,18 @@ static bool make_plan(const wushkv_cache *c, int32_t n_q, int32_t max_seq_len, D
     const int64_t qpages = max_seq_len > c->s_sink ? (max_seq_len - c->s_sink + kPage - 1) / kPage : 0;
     const int64_t units = c->win_slots / kPage + qpages;
     const int64_t heads = (int64_t)c->batch * c->n_kv_heads;
-    // aim at about 4096 workgroups, at least 4 units (one per wave) each,
-    // in multiples of 4 so the waves of a split share its units evenly
-    int64_t ups = (units * heads + 4095) / 4096;
-    if (ups < 4) ups = 4;
-    ups = (ups + 3) / 4 * 4;
-    const int64_t splits = (units + ups - 1) / ups;
-    if (splits < 1 || splits > 65535) return false;
-    p.units_per_split = (int32_t)ups;
+    // about one full residency round of waves (256 CUs x 8 waves), with at
+    // least 2 and at most 32 units per wave so ragged lengths still balance
+    int64_t upw = (units * heads + 2047) / 2048;
+    if (upw < 2) upw = 2;
+    if (upw > 32) upw = 32;
+    int64_t splits = (units + 4 * upw - 1) / (4 * upw);
+    if (splits > kMaxSplits) {
+        upw = (units + 4 * kMaxSplits - 1) / (4 * kMaxSplits);
+        splits = (units + 4 * upw - 1) / (4 * upw);
+    }
+    if (splits < 1 || splits > kMaxSplits || upw > 0x7FFFFFFF / 4 / kMaxSplits) return false;
+    p.units_per_wave = (int32_t)upw;
     p.n_splits = (int32_t)splits;
     p.qt_bytes = ((size_t)c->batch * n_q * c->head_dim * 4 + 255) / 256 * 256;
     p.part_bytes = (size_t)heads * splits * G * (c->head_dim + 2) * 4;
@@ -575,8 +680,10 @@ extern "C" int wushkv_decode_attention(const wushkv_cache *c, const uint16_t *q,
     a.n_pages = c->n_pages;
     a.G = G;
     a.n_q = n_q_heads;
-    a.units_per_split = p.units_per_split;
+    a.units_per_wave = p.units_per_wave;
     a.n_splits = p.n_splits;
+    a.wk = widen_masks(c->bits);
+    a.wv = widen_masks_f16(c->bits);
     a.qt = qt;
     a.part = part;
 

@@ -104,13 +104,12 @@ def test_call_specific_validation():
 def test_workspace_bytes_closed_form():
     L = _lib.lib()
     d = _desc()
-    # qt: batch * n_q * d * 4 (rounded to 256) + partials heads*splits*G*(d+2)*4
+    # q~: batch * n_q * d * 4 rounded up to 256; partials: one (o[d], m, l)
+    # per (sequence, kv head, split, query head of the group).  Units per
+    # (sequence, head): 192/64 window units + ceil((1000 - 4)/64) pages = 19;
+    # 2 units per wave, 8 per four-wave split -> 3 splits.
     ws = L.wushkv_decode_workspace_bytes(ctypes.byref(d), 8, 1000)
-    units = 192 // 64 + (1000 - 4 + 63) // 64
-    ups = max(4, -(-units * 4 // 4096))
-    ups = -(-ups // 4) * 4
-    splits = -(-units // ups)
-    assert ws == -(-(2 * 8 * 128 * 4) // 256) * 256 + 4 * splits * 4 * (128 + 2) * 4
+    assert ws == 2 * 8 * 128 * 4 + (2 * 2) * 3 * 4 * (128 + 2) * 4
 
 
 @pytest.mark.parametrize("d,bits", [(64, 2), (64, 4), (128, 2), (128, 4)])
