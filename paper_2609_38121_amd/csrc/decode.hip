@@ -139,6 +139,56 @@ __device__ __forceinline__ int score_token(int tau, int j, int r)
     return 32 * (tau >> 1) + 8 * j + 4 * (tau & 1) + r;
 }
 
+__device__ __forceinline__ void __attribute__((address_space(3))) *lds_ptr(void *p)
+{
+    return (void __attribute__((address_space(3))) *)p;
+}
+
+// 16-byte LDS read of page data staged by the direct-to-LDS loads.  Written
+// as inline assembly because the compiler, unable to tell the staging slots
+// apart, would otherwise wait for every outstanding load before any LDS read
+// and undo the pipelining.  The caller waits for the data with
+// lds_reads_done() before using it; stage_ready() has already ensured the
+// page itself has arrived.
+__device__ __forceinline__ u32x4 lds_read16(const uint8_t *p)
+{
+    u32x4 r;
+    const uint32_t addr = (uint32_t)(uintptr_t)lds_ptr(const_cast<uint8_t *>(p));
+    asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr) : "memory");
+    return r;
+}
+
+// Wait for the LDS reads above.  The read results pass through the asm as
+// read-write operands, so nothing that uses them can be scheduled before it.
+template <int NX>
+__device__ __forceinline__ void lds_reads_done(u32x4 (&x)[NX], u32x4 (&y)[2][2])
+{
+    static_assert(NX == 1 || NX == 2 || NX == 4, "words per lane");
+    if constexpr (NX == 1)
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(x[0]), "+v"(y[0][0]), "+v"(y[0][1]), "+v"(y[1][0]), "+v"(y[1][1])::"memory");
+    else if constexpr (NX == 2)
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(x[0]), "+v"(x[1]), "+v"(y[0][0]), "+v"(y[0][1]), "+v"(y[1][0]),
+                       "+v"(y[1][1])::"memory");
+    else
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]), "+v"(y[0][0]),
+                       "+v"(y[0][1]), "+v"(y[1][0]), "+v"(y[1][1])::"memory");
+}
+
+// Wait until at most `after` direct-to-LDS loads are outstanding.  `after`
+// is a multiple of kDma between 0 and kMaxAhead * kDma; the count must be an
+// immediate, hence the cases.  The memory clobber keeps LDS reads below it.
+template <int kMaxAhead, int kDma>
+__device__ __forceinline__ void wait_vmcnt_at_most(int after)
+{
+    static_assert(kMaxAhead * kDma <= 63, "vmcnt immediate");
+    if (after <= 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    else if (after <= kDma) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kDma) : "memory");
+    else asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kMaxAhead * kDma) : "memory");
+}
+
 // Packed operands and parameters of one page, as one lane holds them.
 template <int D, int BITS>
 struct PageRegs {
@@ -225,12 +275,21 @@ template <int D, int BITS>
 __global__ void __launch_bounds__(256, 2) decode_main_kernel(DecodeArgs a)
 {
     using L = Layout<D, BITS>;
+    // pages per wave in LDS (kStages - 1 in flight): three for pages up to
+    // 5 KB, two for the 8.5 KB 4-bit pages, keeping two workgroups per CU
+    constexpr int kStages = L::kPageBytes <= 5120 ? 3 : 2;
     constexpr int kC = L::kChunks;   // D / 32
     constexpr int kNT = L::kNTiles;  // D / 16
     constexpr int kNw = L::kNw;
     constexpr int kOpw = L::kOpsPerWord;
 
-    __shared__ float sC[4][16][D];
+    // page stages of the four waves; after its loops a wave reuses its own
+    // stage area for its slice of the merge buffer
+    constexpr int kPB = L::kPageBytes;
+    constexpr int kDma = (kPB + 1023) / 1024;  // direct-to-LDS loads per page
+    constexpr int kSlot = kDma * 1024;
+    constexpr int kWaveLds = kStages * kSlot > 16 * D * 4 ? kStages * kSlot : 16 * D * 4;
+    __shared__ __attribute__((aligned(16))) uint8_t lds[4 * kWaveLds];
     __shared__ float sM[4][8], sL[4][8], sZ[4][8];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -301,6 +360,11 @@ __global__ void __launch_bounds__(256, 2) decode_main_kernel(DecodeArgs a)
     };
 
     // ---------------------------------------------------- quantised pages
+    // Pages are copied whole, global -> LDS, by the direct-to-LDS loads
+    // (64 lanes x 16 B per instruction, lane l's bytes at slot + 16 l), so
+    // a stage holds the page block byte for byte.  A wave keeps kStages - 1
+    // pages in flight while it computes the oldest one; the compiler does not
+    // track these loads, so the waits below are explicit.
     const int pw1 = min(w1, n_qpages);
     if (w0 < pw1) {
         build_b(true);
@@ -315,97 +379,163 @@ __global__ void __launch_bounds__(256, 2) decode_main_kernel(DecodeArgs a)
         int32_t tbl = -1;
         if (w0 + lane < pw1 && w0 + lane < a.max_pages)
             tbl = a.page_table[(int64_t)b * a.max_pages + w0 + lane];
-        auto page_ptr = [&](int u) -> const uint8_t * {
-            const int32_t phys = __builtin_amdgcn_readlane(tbl, u - w0);
-            if (phys < 0 || phys >= a.n_pages) return nullptr;
-            return a.pages + ((int64_t)phys * a.n_kv + h) * L::kPageBytes;
+        uint8_t *stage = lds + wave * kWaveLds;
+        // Every page of the run issues exactly kDma loads; a page-table entry
+        // outside the pool loads physical page 0 instead (its data is never
+        // used), which keeps the count of outstanding loads a closed form.
+        auto phys_of = [&](int u) -> int32_t { return __builtin_amdgcn_readlane(tbl, u - w0); };
+        auto issue = [&](int u, int s) {
+            int32_t phys = phys_of(u);
+            if (phys < 0 || phys >= a.n_pages) phys = 0;
+            const uint8_t *src = a.pages + ((int64_t)phys * a.n_kv + h) * L::kPageBytes + 16 * lane;
+            uint8_t *dst = stage + s * kSlot;
+#pragma unroll
+            for (int i = 0; i < kDma; ++i) {
+                if (i + 1 < kDma || 1024 * i + 16 * lane < L::kPageBytes)
+                    __builtin_amdgcn_global_load_lds(src + 1024 * i, lds_ptr(dst + 1024 * i), 16, 0, 0);
+            }
         };
-        PageRegs<D, BITS> cur, nxt;
-        const uint8_t *pc = page_ptr(w0);
-        if (pc) cur.load(pc, lane, j);
+        if (a.n_pages > 0) {
+#pragma unroll
+        for (int s = 0; s < kStages - 1; ++s)
+            if (w0 + s < pw1) issue(w0 + s, s);
         for (int u = w0; u < pw1; ++u) {
-            const uint8_t *pn = (u + 1 < pw1) ? page_ptr(u + 1) : nullptr;
-            if (pn) nxt.load(pn, lane, j);
-            if (pc) {
-                const int32_t nvalid = min(kPage, q_hi - (a.s_sink + u * kPage));
-                // scores S^T[token][column] - 128 sum q~', four tiles of 16 tokens
-                f32x4 sc[4];
+            const int s = (u - w0) % kStages;
+            if (u + kStages - 1 < pw1) issue(u + kStages - 1, (u - w0 + kStages - 1) % kStages);
+            // pages issued after page u: min(kStages - 1, pw1 - 1 - u)
+            // stage_ready: page u has landed in LDS once at most the later
+            // pages' loads are outstanding
+            wait_vmcnt_at_most<kStages - 1, kDma>(kDma * min(kStages - 1, pw1 - 1 - u));
+            {
+                const int32_t phys = phys_of(u);
+                if (phys < 0 || phys >= a.n_pages) continue;
+            }
+            const uint8_t *pg = stage + s * kSlot;
+            const int32_t nvalid = min(kPage, q_hi - (a.s_sink + u * kPage));
+            // scores S^T[token][column] - 128 sum q~', four tiles of 16 tokens
+            uint32_t kw[L::kWordsPerLane];
+            uint32_t kp[2][8];
+            {
+                u32x4 x[L::kWordsPerLane / 4], y[2][2];
 #pragma unroll
-                for (int tau = 0; tau < 4; ++tau) {
-                    sc[tau] = f32x4{-qbias, -qbias, -qbias, -qbias};
-#pragma unroll
-                    for (int w = 0; w < kNw; ++w) {
-                        uint32_t op[L::kCodesPerWord / 2];
-                        widen_word<BITS>(cur.kw[tau * kNw + w], op, wk);
-#pragma unroll
-                        for (int o = 0; o < kOpw; ++o) {
-                            const int c = w * kOpw + o;
-                            const bf16x8 A = as_op(op + 4 * o);
-                            sc[tau] = mfma16(A, bop(bhi[c]), sc[tau]);
-                            sc[tau] = mfma16(A, bop(blo[c]), sc[tau]);
-                        }
-                    }
-                }
-                // logits (base 2): s (S - 128 sum q~') + z sum q~
-                float lg[4][4];
-#pragma unroll
-                for (int tau = 0; tau < 4; ++tau)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const uint32_t kprm = cur.kp[tau >> 1][4 * (tau & 1) + r];
-                        lg[tau][r] = fmaf(f16_bits_to_f32(kprm & 0xFFFFu), sc[tau][r],
-                                          f16_bits_to_f32(kprm >> 16) * zsum);
-                    }
-                if (nvalid < kPage) {
-#pragma unroll
-                    for (int tau = 0; tau < 4; ++tau)
-#pragma unroll
-                        for (int r = 0; r < 4; ++r)
-                            if (score_token(tau, j, r) >= nvalid) lg[tau][r] = -INFINITY;
-                }
-                float mloc = -INFINITY;
-#pragma unroll
-                for (int tau = 0; tau < 4; ++tau)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) mloc = fmaxf(mloc, lg[tau][r]);
-                st.update_max(wave_max_xor_16_32(mloc), j, G);
-                // weights p s 4^-p as fp16, in the A rows g < G
-                uint32_t aop[2][4];
+                for (int q4 = 0; q4 < L::kWordsPerLane / 4; ++q4)
+                    x[q4] = lds_read16(pg + 16 * (lane * (L::kWordsPerLane / 4) + q4));
 #pragma unroll
                 for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
-                    for (int p = 0; p < 4; ++p) {
-                        float wv2[2];
+                    for (int h2 = 0; h2 < 2; ++h2)
+                        y[kc][h2] = lds_read16(pg + L::kParamOffset + 4 * (32 * kc + 8 * j) + 16 * h2);
+                lds_reads_done(x, y);
 #pragma unroll
-                        for (int e = 0; e < 2; ++e) {
-                            const int i = 2 * p + e;  // slot: token 32 kc + 8 j + i
-                            const float pr = fexp2(lg[2 * kc + (i >> 2)][i & 3] - st.m_lane);
-                            const uint32_t vprm = cur.vp[kc][i];
-                            st.l_lane += pr;
-                            st.z_lane = fmaf(pr, f16_bits_to_f32(vprm >> 16), st.z_lane);
-                            wv2[e] = pr * (f16_bits_to_f32(vprm & 0xFFFFu) * slot_scale_f16<BITS>(i));
-                        }
-                        aop[kc][p] = cls == 0 ? pack_f16_rne(wv2[0], wv2[1]) : 0u;
+                for (int q4 = 0; q4 < L::kWordsPerLane / 4; ++q4)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) kw[4 * q4 + e] = x[q4][e];
+#pragma unroll
+                for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+                    for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) kp[kc][4 * h2 + e] = y[kc][h2][e];
+            }
+            f32x4 sc[4];
+#pragma unroll
+            for (int tau = 0; tau < 4; ++tau) {
+                sc[tau] = f32x4{-qbias, -qbias, -qbias, -qbias};
+#pragma unroll
+                for (int w = 0; w < kNw; ++w) {
+                    uint32_t op[L::kCodesPerWord / 2];
+                    widen_word<BITS>(kw[tau * kNw + w], op, wk);
+#pragma unroll
+                    for (int o = 0; o < kOpw; ++o) {
+                        const int c = w * kOpw + o;
+                        const bf16x8 A = as_op(op + 4 * o);
+                        sc[tau] = mfma16(A, bop(bhi[c]), sc[tau]);
+                        sc[tau] = mfma16(A, bop(blo[c]), sc[tau]);
                     }
-                // P V, plus the row sums that remove the 1024 offset
-#pragma unroll
-                for (int kc = 0; kc < 2; ++kc) {
-                    const f16x8 A = __builtin_bit_cast(f16x8, u32x4{aop[kc][0], aop[kc][1], aop[kc][2], aop[kc][3]});
-#pragma unroll
-                    for (int uu = 0; uu < 2 * kNw; ++uu) {
-                        uint32_t op[L::kCodesPerWord / 2];
-                        widen_word_f16<BITS>(cur.vw[kc * 2 * kNw + uu], op, wv);
-#pragma unroll
-                        for (int o = 0; o < kOpw; ++o) {
-                            const int nt = uu * kOpw + o;
-                            st.acc[nt] = mfma16h(A, as_op_h(op + 4 * o), st.acc[nt]);
-                        }
-                    }
-                    st.accb = mfma16h(A, c1024, st.accb);
                 }
             }
-            cur = nxt;
-            pc = pn;
+            // logits (base 2): s (S - 128 sum q~') + z sum q~
+            float lg[4][4];
+#pragma unroll
+            for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const uint32_t kprm = kp[tau >> 1][4 * (tau & 1) + r];
+                    lg[tau][r] = fmaf(f16_bits_to_f32(kprm & 0xFFFFu), sc[tau][r],
+                                      f16_bits_to_f32(kprm >> 16) * zsum);
+                }
+            if (nvalid < kPage) {
+#pragma unroll
+                for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (score_token(tau, j, r) >= nvalid) lg[tau][r] = -INFINITY;
+            }
+            float mloc = -INFINITY;
+#pragma unroll
+            for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) mloc = fmaxf(mloc, lg[tau][r]);
+            st.update_max(wave_max_xor_16_32(mloc), j, G);
+            // weights p s 4^-p as fp16, in the A rows g < G
+            uint32_t vp[2][8];
+            uint32_t vw[L::kWordsPerLane];
+            {
+                u32x4 x[L::kWordsPerLane / 4], y[2][2];
+#pragma unroll
+                for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+                    for (int h2 = 0; h2 < 2; ++h2)
+                        y[kc][h2] = lds_read16(pg + L::kParamOffset + 4 * kPage + 4 * (32 * kc + 8 * j) + 16 * h2);
+#pragma unroll
+                for (int q4 = 0; q4 < L::kWordsPerLane / 4; ++q4)
+                    x[q4] = lds_read16(pg + L::kRegionBytes + 16 * (lane * (L::kWordsPerLane / 4) + q4));
+                lds_reads_done(x, y);
+#pragma unroll
+                for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+                    for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) vp[kc][4 * h2 + e] = y[kc][h2][e];
+#pragma unroll
+                for (int q4 = 0; q4 < L::kWordsPerLane / 4; ++q4)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) vw[4 * q4 + e] = x[q4][e];
+            }
+            uint32_t aop[2][4];
+#pragma unroll
+            for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+                for (int p = 0; p < 4; ++p) {
+                    float wv2[2];
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) {
+                        const int i = 2 * p + e;  // slot: token 32 kc + 8 j + i
+                        const float pr = fexp2(lg[2 * kc + (i >> 2)][i & 3] - st.m_lane);
+                        const uint32_t vprm = vp[kc][i];
+                        st.l_lane += pr;
+                        st.z_lane = fmaf(pr, f16_bits_to_f32(vprm >> 16), st.z_lane);
+                        wv2[e] = pr * (f16_bits_to_f32(vprm & 0xFFFFu) * slot_scale_f16<BITS>(i));
+                    }
+                    aop[kc][p] = cls == 0 ? pack_f16_rne(wv2[0], wv2[1]) : 0u;
+                }
+            // P V, plus the row sums that remove the 1024 offset
+#pragma unroll
+            for (int kc = 0; kc < 2; ++kc) {
+                const f16x8 A = __builtin_bit_cast(f16x8, u32x4{aop[kc][0], aop[kc][1], aop[kc][2], aop[kc][3]});
+#pragma unroll
+                for (int uu = 0; uu < 2 * kNw; ++uu) {
+                    uint32_t op[L::kCodesPerWord / 2];
+                    widen_word_f16<BITS>(vw[kc * 2 * kNw + uu], op, wv);
+#pragma unroll
+                    for (int o = 0; o < kOpw; ++o) {
+                        const int nt = uu * kOpw + o;
+                        st.acc[nt] = mfma16h(A, as_op_h(op + 4 * o), st.acc[nt]);
+                    }
+                }
+                st.accb = mfma16h(A, c1024, st.accb);
+            }
+        }
         }
     }
 
@@ -509,10 +639,17 @@ __global__ void __launch_bounds__(256, 2) decode_main_kernel(DecodeArgs a)
     // head g: rows g (pages and window hi parts) and g + G (window lo parts)
     const float l_col = wave_sum_xor_16_32(st.l_lane);
     const float z_col = wave_sum_xor_16_32(st.z_lane);
+    // this wave's stage reads are complete: every value read was consumed
+    float(*sC)[16][D] = reinterpret_cast<float(*)[16][D]>(lds);
+    auto sCw = [&](int w) -> float(*)[D] { return reinterpret_cast<float(*)[D]>(lds + w * kWaveLds); };
+    {
+        float(*mine)[D] = sCw(wave);
 #pragma unroll
-    for (int nt = 0; nt < kNT; ++nt)
+        for (int nt = 0; nt < kNT; ++nt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) sC[wave][4 * j + r][16 * nt + n] = st.acc[nt][r] - st.accb[r];
+            for (int r = 0; r < 4; ++r) mine[4 * j + r][16 * nt + n] = st.acc[nt][r] - st.accb[r];
+    }
+    (void)sC;
     if (lane < G) {
         sM[wave][lane] = st.m_lane;
         sL[wave][lane] = l_col;
@@ -532,7 +669,7 @@ __global__ void __launch_bounds__(256, 2) decode_main_kernel(DecodeArgs a)
             for (int w = 0; w < 4; ++w) {
                 if (sM[w][gg] == -INFINITY) continue;
                 const float f = fexp2(sM[w][gg] - mx);
-                o += f * (sC[w][gg][ch] + sC[w][gg + G][ch] + sZ[w][gg]);
+                o += f * (sCw(w)[gg][ch] + sCw(w)[gg + G][ch] + sZ[w][gg]);
                 l += f * sL[w][gg];
             }
         }
