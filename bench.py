@@ -51,7 +51,50 @@ def parse():
     ap.add_argument("--no-prefill", action="store_true", help="skip the append-throughput leg")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline leg")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 512 MiB device-to-device copy five times (a known-size "
+                         "reference for the HBM byte counters) and exit")
     return ap.parse_args()
+
+
+def profiled_traffic(summary, csrc):
+    """HBM bytes per launch from a committed counter summary, or None when
+    the kernel sources changed since the counters were taken (the summary
+    records a sha256 prefix of each source it covers)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", summary)
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for ln in open(path):
+        if ":" in ln and not ln.startswith(("|", " ", "#")):
+            k_, v_ = ln.split(":", 1)
+            fields[k_.strip()] = v_.strip()
+    try:
+        value = int(fields["traffic_bytes_per_launch"])
+        want = dict(x.split("=") for x in fields["source_sha256_prefix"].split())
+    except (KeyError, ValueError):
+        return None
+    for name, pre in want.items():
+        with open(os.path.join(csrc, name), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest()[:len(pre)] != pre:
+                return None
+    return value
+
+
+def copy_calibration():
+    """A plain copy of known size: 512 MiB read and 512 MiB written per
+    launch.  Profiling it with the same byte counters as the kernels gives
+    the factor that turns counter readings into bytes."""
+    import torch
+    n = 512 << 20
+    src = torch.randint(0, 255, (n,), dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    assert torch.equal(dst[:4096], src[:4096])
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}), flush=True)
 
 
 # ----------------------------------------------------------------- bytes
@@ -102,6 +145,9 @@ def window_quant_end(S, s_sink, s_keep, s_flush):
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(every (sequence, kv head) pair is independent; see the design notes "
@@ -304,7 +350,9 @@ def main():
                    "step": "append 1 token/seq + decode", "graph": True},
         "roofline": {"bound": "hbm", "kernel": "decode_main_kernel",
                      "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "frac": round(achieved / PEAK_HBM_GBS, 4),
+                     "traffic": profiled_traffic("decode_main_kernel_llama8b_2bit.md",
+                                                 os.path.join(ROOT, "paper_2609_38121_amd", "csrc")),
                      "avg_us": round(t_main * 1e3, 3),
                      "bytes_per_launch": int(main_per_launch)},
         "cpu_baseline": cpu,

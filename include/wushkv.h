@@ -10,7 +10,7 @@
  * and RoPE.  Queries are compensated with T_K^{-T} (Alg. 2, step 3).  The
  * quantiser is the per-token percentile-clipped affine quantiser of Eq. (7)
  * and the cache keeps two bf16 windows, a sink and a recent window, with
- * quantisation in multiples of S_flush (Sec. 3.4, Alg. 2).
+ * quantisation in multiples of S_flush (Sec. 4.4, Alg. 2).
  *
  * Entry points:
  *   wushkv_append            Alg. 2 steps 3 (keys), 4 and 7-11

@@ -10,7 +10,7 @@ bf16 value of every position plus the codes and fp16 (scale, zero) of the
 quantised positions.  It knows nothing of pages, rings or kernel layouts.
 
 Paper references: Eq. (2) attention, Eq. (3) transform insertion, Eq. (7)
-quantiser, Sec. 3.4 windows, Alg. 2 cache management.
+quantiser, Sec. 4.4 windows, Alg. 2 cache management.
 """
 from __future__ import annotations
 
@@ -171,7 +171,7 @@ def dequant(codes, s16, z16) -> np.ndarray:
 
 
 # --------------------------------------------------------------------------
-# Windows and bookkeeping, Sec. 3.4 / Alg. 2
+# Windows and bookkeeping, Sec. 4.4 / Alg. 2
 # --------------------------------------------------------------------------
 
 def next_quant_end(s_new: int, s_quant: int, s_sink: int, s_keep: int, s_flush: int) -> int:

@@ -10,10 +10,10 @@
  *
  * What each function follows:
  *   orc_append_head  Alg. 2 (inference and cache management), steps 3-4 and
- *                    7-11, with the window rules of Sec. 3.4.
+ *                    7-11, with the window rules of Sec. 4.4.
  *   orc_next_quant_end  the S_quant update of Alg. 2 (0-based, exclusive).
  *   orc_quantize_group  Eq. (7): the OSCAR-style percentile-clipped affine
- *                    quantiser used for the end-to-end runs (Sec. 4.3).
+ *                    quantiser used for the end-to-end runs (Sec. 5.3).
  *   orc_dequant      the reconstruction term of Eq. (7).
  *   orc_decode_head  Eq. (2) GQA attention for one query per query head,
  *                    with the query compensation of Eq. (3) (q -> T_K^{-T} q,
@@ -220,7 +220,7 @@ float orc_dequant(uint8_t code, uint16_t s16, uint16_t z16)
 }
 
 /* ------------------------------------------------------------------------ */
-/* Cache windows, Sec. 3.4 and Alg. 2.                                       */
+/* Cache windows, Sec. 4.4 and Alg. 2.                                       */
 /* ------------------------------------------------------------------------ */
 
 static int64_t floor_div(int64_t a, int64_t b)

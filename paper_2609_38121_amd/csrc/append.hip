@@ -1,6 +1,6 @@
 // wushkv_append: online key transform, window routing and per-token
 // percentile-clipped quantisation into packed pages (Alg. 2 steps 3-4 and
-// 7-11; quantiser Eq. (7); windows Sec. 3.4).
+// 7-11; quantiser Eq. (7); windows Sec. 4.4).
 //
 // One workgroup (256 threads, four waves) owns one tile of up to 64
 // consecutive positions of one (sequence, kv head): either a chunk of the

@@ -1,4 +1,4 @@
-"""Pins of the oracle's cache management (Sec. 3.4, Alg. 2) and attention
+"""Pins of the oracle's cache management (Sec. 4.4, Alg. 2) and attention
 (Eq. (2), Eq. (3)): hand-worked window examples, window invariants over
 random schedules, flush-time independence, the transform-insertion identity,
 and closed-form special cases of softmax attention."""
