@@ -58,7 +58,7 @@ enum {
 };
 
 #define WUSHKV_PAGE_TOKENS 64
-#define WUSHKV_ABI_VERSION 1
+#define WUSHKV_ABI_VERSION 2
 
 /*
  * Cache descriptor.  Sizes are host values; the arrays are device memory.
@@ -85,24 +85,31 @@ enum {
  *     V params  64 tokens x 4 bytes, same form
  *   Reconstruction of a stored entry: x = scale * code + zero (fp32 fma).
  *
- *   Code words.  Both code regions are arrays of little-endian 32-bit words.
- *   A word holds B = 32 / bits codes, "elements" e = 0 .. B-1; element e sits
- *   at bit 16 * (e % 2) + bits * (e / 2): even elements fill the low half
- *   word, odd elements the high half, each in increasing order.  Element e
- *   belongs to operand o = e / 8, slot i = e % 8.  With nw = head_dim * bits
- *   / 128, each region holds 64 "lanes" L = 16 j + m (j = 0..3, m = 0..15)
- *   of 4 nw words each:
+ *   Code words.  Both code regions are arrays of little-endian 32-bit
+ *   words; a word holds B = 32 / bits codes.
  *
- *   K word at index L * 4nw + tau * nw + w   (tau = 0..3, w = 0..nw-1)
- *     token    32 (tau / 2) + 8 (m / 4) + 4 (tau % 2) + (m % 4)
- *     channel  32 c + 8 j + i,  c = w * (B / 8) + o
+ *   K region: 16 * head_dim / 32 "lanes" L = 16 j + n (j < head_dim / 32,
+ *   n = 0..15) of 4 * bits words each.  K word L * 4 bits + bits * t + w
+ *   (t = 0..3, w = 0..bits-1) holds token 4 n + t, channels
+ *   32 j + B w + e for e = 0..B-1; code e = h * B/2 + i (h = 0, 1) sits at
+ *   bit 2 * bits * i + bits * h.  A mask then spreads a word, or the word
+ *   shifted right by bits, into one code per nibble (2-bit) or per byte
+ *   (4-bit): the fp4 / fp8 operands of the decode kernel's scaled matrix
+ *   instruction.
+ *
+ *   V region: element e of a word is slot i = e % 8 of operand o = e / 8
+ *   and sits at bit 16 * (i % 2) + F(o, i / 2): slot pairs share a field
+ *   position, the even slot in the low half word.  F = (6, 10, 8, 12) for
+ *   operand 0 and (2, 0, 4, 14) for operand 1 of a 2-bit word, F =
+ *   (4, 0, 8, 12) for a 4-bit word (one operand).  With
+ *   nw = head_dim * bits / 128, the region holds 64 lanes L = 16 j + m
+ *   (j = 0..3, m = 0..15) of 4 nw words each;
  *   V word at index L * 4nw + kc * 2nw + u   (kc = 0..1, u = 0..2nw-1)
  *     token    32 kc + 8 j + i
  *     channel  16 nt + m,  nt = u * (B / 8) + o
- *
- *   (This is the operand order of the 16x16x32 bf16 matrix instructions the
- *   decode kernel feeds: a lane loads its words with 128-bit loads and
- *   widens two codes per 32-bit operand register.)
+ *   (the operand order of the 16x16x32 fp16 product: a few shifts and one
+ *   mask per operand register move each code near the top of an fp16
+ *   fraction).
  *
  * win_k: bf16 [batch][n_kv_heads][win_slots][head_dim]   (token-major)
  * win_v: bf16 [batch][n_kv_heads][head_dim][win_slots]   (channel-major)

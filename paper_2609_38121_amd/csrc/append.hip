@@ -331,34 +331,32 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
             *reinterpret_cast<uint32_t *>(pg + L::kParamOffset + 4 * r + (is_v ? 4 * kPage : 0)) =
                 s16 | (z16 << 16);
             if (!is_v) {
-                // key words of this token: word (j, w) holds channels
-                // 32 c + 8 j + i with c = w (B/8) + o.
-                uint32_t kw[4][L::kNw];
+                // key words of this token: lane group jj = ch / 32 holds
+                // BITS words per token (see Layout::k_pos)
+                uint32_t kw[D / 32][BITS];
 #pragma unroll
-                for (int jj = 0; jj < 4; ++jj)
+                for (int jj = 0; jj < D / 32; ++jj)
 #pragma unroll
-                    for (int w = 0; w < L::kNw; ++w) kw[jj][w] = 0u;
+                    for (int w = 0; w < BITS; ++w) kw[jj][w] = 0u;
 #pragma unroll
                 for (int c8 = 0; c8 < D / 8; ++c8) {
                     uint4 v = *reinterpret_cast<const uint4 *>(row + 8 * c8);
                     uint32_t wv[4] = {v.x, v.y, v.z, v.w};
-                    const int c = c8 >> 2, jj = c8 & 3;
-                    const int w = c / L::kOpsPerWord, o = c % L::kOpsPerWord;
 #pragma unroll
                     for (int i = 0; i < 8; ++i) {
                         uint32_t hb = (i & 1) ? (wv[i >> 1] >> 16) : (wv[i >> 1] & 0xFFFFu);
                         uint32_t code = code_of(bf16_bits_to_f32(hb), z, inv, (float)kLevels);
-                        kw[jj][w] |= code << L::elem_bit(8 * o + i);
+                        int word, bit;
+                        L::k_pos(r, 8 * c8 + i, word, bit);
+                        kw[(8 * c8 + i) >> 5][((8 * c8 + i) & 31) / (32 / BITS)] |= code << bit;
                     }
                 }
-                const int tau = 2 * (r >> 5) + ((r >> 2) & 1);
-                const int m = 4 * ((r >> 3) & 3) + (r & 3);
                 uint32_t *kreg = reinterpret_cast<uint32_t *>(pg);
 #pragma unroll
-                for (int jj = 0; jj < 4; ++jj)
+                for (int jj = 0; jj < D / 32; ++jj)
 #pragma unroll
-                    for (int w = 0; w < L::kNw; ++w)
-                        kreg[(16 * jj + m) * L::kWordsPerLane + tau * L::kNw + w] = kw[jj][w];
+                    for (int w = 0; w < BITS; ++w)
+                        kreg[(16 * jj + (r >> 2)) * L::kKWordsPerLane + BITS * (r & 3) + w] = kw[jj][w];
             } else {
 #pragma unroll
                 for (int c8 = 0; c8 < D / 8; ++c8) {
@@ -395,7 +393,7 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
                 const int32_t p = blk_lo + t;
                 if (p >= lo && p < hi && quant_now(p)) {
                     const int ch = 16 * (u * L::kOpsPerWord + o) + m;
-                    const int bit = L::elem_bit(e);
+                    const int bit = L::v_bit(o, i);
                     mask |= ((1u << BITS) - 1u) << bit;
                     bits |= (uint32_t)vcodes[t * D + ch] << bit;
                 }

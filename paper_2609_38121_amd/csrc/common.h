@@ -20,8 +20,6 @@ typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
 typedef __attribute__((ext_vector_type(2))) _Float16 f16x2;
 
 constexpr int kPage = WUSHKV_PAGE_TOKENS;  // tokens per page
-constexpr uint32_t kBias2 = 0x43004300u;      // two bf16 128.0: 0x4300 | c == 128 + c
-constexpr uint32_t kBiasF16x2 = 0x64006400u;  // two fp16 1024.0: 0x6400 | c == 1024 + c
 
 // ---------------------------------------------------------------- formats
 
@@ -62,26 +60,39 @@ template <int D, int BITS>
 struct Layout {
     static constexpr int kCodesPerWord = 32 / BITS;            // B
     static constexpr int kOpsPerWord = kCodesPerWord / 8;      // B / 8
-    static constexpr int kNw = D * BITS / 128;                 // words per (lane, tile)
-    static constexpr int kWordsPerLane = 4 * kNw;
+    static constexpr int kNw = D * BITS / 128;                 // V words per (lane, slice)
+    static constexpr int kWordsPerLane = 4 * kNw;              // V words per lane
+    static constexpr int kKLanes = D / 2;                      // lanes holding key codes
+    static constexpr int kKWordsPerLane = 4 * BITS;            // key words per lane (4 tiles)
     static constexpr int kRegionBytes = 8 * D * BITS;          // one code region
     static constexpr int kParamOffset = 2 * kRegionBytes;
     static constexpr int kPageBytes = 2 * kRegionBytes + 8 * kPage;
-    static constexpr int kChunks = D / 32;                     // score K-chunks
+    static constexpr int kChunks = D / 32;                     // 32-channel chunks
     static constexpr int kNTiles = D / 16;                     // PV N-tiles
 
-    // Bit offset of element e inside its word.
-    __host__ __device__ static constexpr int elem_bit(int e) { return 16 * (e & 1) + BITS * (e >> 1); }
+    // Bit of value code (operand o, slot i) inside its word: slot i sits in
+    // half word i % 2 at field v_field(o, i / 2) (see widen_word_f16).
+    __host__ __device__ static constexpr int v_field(int o, int r)
+    {
+        return BITS == 2 ? (o == 0 ? (r == 0 ? 6 : r == 1 ? 10 : r == 2 ? 8 : 12)
+                                   : (r == 0 ? 2 : r == 1 ? 0 : r == 2 ? 4 : 14))
+                         : (r == 0 ? 4 : r == 1 ? 0 : r == 2 ? 8 : 12);
+    }
+    __host__ __device__ static constexpr int v_bit(int o, int i) { return 16 * (i & 1) + v_field(o, i >> 1); }
 
     // K region: (token t of the page, channel ch) -> (word index, bit).
+    // Lane 16 j + n holds tokens 4 n .. 4 n + 3 (tile t % 4) and channels
+    // 32 j .. 32 j + 31, BITS words per tile.  Inside a word the channels
+    // split into two halves of 16 / BITS codes; code i of half h sits at
+    // bit 2 BITS i + BITS h, so that one mask (and one shift for h = 1)
+    // spreads a word into nibbles (2-bit) or bytes (4-bit), one code each.
     __host__ __device__ static inline void k_pos(int t, int ch, int &word, int &bit)
     {
-        int tau = 2 * (t >> 5) + ((t >> 2) & 1);
-        int m = 4 * ((t >> 3) & 3) + (t & 3);
-        int c = ch >> 5, j = (ch >> 3) & 3, i = ch & 7;
-        int w = c / kOpsPerWord, o = c % kOpsPerWord;
-        word = (16 * j + m) * kWordsPerLane + tau * kNw + w;
-        bit = elem_bit(8 * o + i);
+        constexpr int kSpan = 32 / BITS;  // channels per word
+        const int n = t >> 2, tt = t & 3, j = ch >> 5, q = ch & 31;
+        const int w = q / kSpan, r = q % kSpan, h = r / (kSpan / 2), i = r % (kSpan / 2);
+        word = (16 * j + n) * kKWordsPerLane + BITS * tt + w;
+        bit = 2 * BITS * i + BITS * h;
     }
     // V region: (token t of the page, channel ch) -> (word index, bit).
     __host__ __device__ static inline void v_pos(int t, int ch, int &word, int &bit)
@@ -90,114 +101,43 @@ struct Layout {
         int nt = ch >> 4, m = ch & 15;
         int u = nt / kOpsPerWord, o = nt % kOpsPerWord;
         word = (16 * j + m) * kWordsPerLane + kc * 2 * kNw + u;
-        bit = elem_bit(8 * o + i);
+        bit = v_bit(o, i);
     }
 };
 
-// Widen the codes of one word into bf16 operand registers: out[e] holds
-// elements 2e (low half) and 2e+1 (high half) as bf16 values 128 + c * 2^s.
-// For 2-bit codes the shift s depends on the slot pair p = e % 4 as
-// s = {0, 2, 4, 0}[p]; the other matrix operand carries 2^-s for those slots.
-// 4-bit codes use s = 0.
-//
-// Each output is (word & mask) | bias, one v_and_or_b32.  That encoding
-// takes no literal constants, so the masks and the bias arrive as kernel
-// arguments (scalar registers) instead of compile-time constants, which
-// keeps the compiler from splitting the operation in two.
-struct WidenMasks {
-    uint32_t m0, m1, m2;  // field masks (see the widen functions)
-    uint32_t bias;        // two copies of the offset value's bit pattern
-    uint32_t m3;
-};
-
-inline WidenMasks widen_masks(int bits)
-{
-    return bits == 2 ? WidenMasks{0x00030003u, 0x000C000Cu, 0x00300030u, kBias2, 0u}
-                     : WidenMasks{0x000F000Fu, 0x000F000Fu, 0x000F000Fu, kBias2, 0u};
-}
-
+// Widen the value codes of one word into fp16 operand registers: out[4 o +
+// r] is register r (slots 2r, 2r+1, one per half word) of operand o, each
+// code c in the fraction bits of an fp16 subnormal with exponent field zero:
+// the value c 2^T 2^-24, where T is the code's target field.  No offset is
+// added, so nothing has to be removed afterwards.  The matrix instruction
+// multiplies subnormal inputs exactly, but aligns each product by its
+// operands' exponent fields: a code far below the top of the fraction would
+// lose that many bits when summed with other products, so every code is
+// moved within two bits of the top, T = 6 or 8 (2-bit: registers 0-1 and
+// 2-3; the other operand carries 2^-(T - 6)) or T = 4 (4-bit).  The page
+// layout (Layout::v_field) puts the codes where four shifts and one mask per
+// register (2-bit; three shifts for 4-bit) reach those targets.
 template <int BITS>
-__device__ __forceinline__ void widen_word(uint32_t w, uint32_t *out, const WidenMasks &k);
-
-template <>
-__device__ __forceinline__ void widen_word<2>(uint32_t w, uint32_t *out, const WidenMasks &k)
+__device__ __forceinline__ void widen_word_f16(uint32_t w, uint32_t *out)
 {
-    out[0] = (w & k.m0) | k.bias;
-    out[1] = (w & k.m1) | k.bias;
-    out[2] = (w & k.m2) | k.bias;
-    const uint32_t t6 = w >> 6, t8 = w >> 8, t14 = w >> 14;
-    out[3] = (t6 & k.m0) | k.bias;
-    out[4] = (t8 & k.m0) | k.bias;
-    out[5] = (t8 & k.m1) | k.bias;
-    out[6] = (t8 & k.m2) | k.bias;
-    out[7] = (t14 & k.m0) | k.bias;
-}
-
-template <>
-__device__ __forceinline__ void widen_word<4>(uint32_t w, uint32_t *out, const WidenMasks &k)
-{
-    out[0] = (w & k.m0) | k.bias;
-    out[1] = ((w >> 4) & k.m0) | k.bias;
-    out[2] = ((w >> 8) & k.m0) | k.bias;
-    out[3] = ((w >> 12) & k.m0) | k.bias;
-}
-
-// The same widening into fp16 operands, 1024 + c 2^s: fp16 keeps 10
-// fraction bits, so 2-bit fields fit at s = 0, 2, 4, 6 and one shift by 8
-// reaches the upper byte of each half word (s = 2p for slot pair p); 4-bit
-// fields fit at s = 0 and 4 (s = 4 (p % 2)).
-inline WidenMasks widen_masks_f16(int bits)
-{
-    return bits == 2 ? WidenMasks{0x00030003u, 0x000C000Cu, 0x00300030u, kBiasF16x2, 0x00C000C0u}
-                     : WidenMasks{0x000F000Fu, 0x00F000F0u, 0x000F000Fu, kBiasF16x2, 0x00F000F0u};
-}
-
-template <int BITS>
-__device__ __forceinline__ void widen_word_f16(uint32_t w, uint32_t *out, const WidenMasks &k);
-
-template <>
-__device__ __forceinline__ void widen_word_f16<2>(uint32_t w, uint32_t *out, const WidenMasks &k)
-{
-    out[0] = (w & k.m0) | k.bias;
-    out[1] = (w & k.m1) | k.bias;
-    out[2] = (w & k.m2) | k.bias;
-    out[3] = (w & k.m3) | k.bias;
-    const uint32_t t8 = w >> 8;
-    out[4] = (t8 & k.m0) | k.bias;
-    out[5] = (t8 & k.m1) | k.bias;
-    out[6] = (t8 & k.m2) | k.bias;
-    out[7] = (t8 & k.m3) | k.bias;
-}
-
-template <>
-__device__ __forceinline__ void widen_word_f16<4>(uint32_t w, uint32_t *out, const WidenMasks &k)
-{
-    out[0] = (w & k.m0) | k.bias;
-    out[1] = (w & k.m1) | k.bias;
-    const uint32_t t8 = w >> 8;
-    out[2] = (t8 & k.m0) | k.bias;
-    out[3] = (t8 & k.m1) | k.bias;
-}
-
-// 2^-s of operand slot i for the fp16 widening above.
-template <int BITS>
-__host__ __device__ constexpr float slot_scale_f16(int i)
-{
-    return BITS == 2 ? (i >> 1) == 0 ? 1.0f : (i >> 1) == 1 ? 0.25f : (i >> 1) == 2 ? 0.0625f : 0.015625f
-                     : ((i >> 1) & 1) ? 0.0625f : 1.0f;
-}
-
-// 2^-s of operand slot i (0..7) for the widened codes above.
-template <int BITS>
-__host__ __device__ constexpr float slot_scale(int i)
-{
-    return BITS == 2 ? ((i >> 1) == 1 ? 0.25f : ((i >> 1) == 2 ? 0.0625f : 1.0f)) : 1.0f;
-}
-
-__device__ __forceinline__ bf16x8 as_op(const uint32_t *u)
-{
-    u32x4 v = {u[0], u[1], u[2], u[3]};
-    return __builtin_bit_cast(bf16x8, v);
+    if constexpr (BITS == 2) {
+        constexpr uint32_t m6 = 0x00C000C0u, m8 = 0x03000300u;
+        const uint32_t l4 = w << 4, r4 = w >> 4, l6 = w << 6, r6 = w >> 6;
+        out[0] = w & m6;   // field 6
+        out[1] = r4 & m6;  // field 10
+        out[2] = w & m8;   // field 8
+        out[3] = r4 & m8;  // field 12
+        out[4] = l4 & m6;  // field 2
+        out[5] = l6 & m6;  // field 0
+        out[6] = l4 & m8;  // field 4
+        out[7] = r6 & m8;  // field 14
+    } else {
+        constexpr uint32_t m4 = 0x00F000F0u;
+        out[0] = w & m4;          // field 4
+        out[1] = (w << 4) & m4;   // field 0
+        out[2] = (w >> 4) & m4;   // field 8
+        out[3] = (w >> 8) & m4;   // field 12
+    }
 }
 
 __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c)

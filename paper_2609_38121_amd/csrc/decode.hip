@@ -4,40 +4,49 @@
 //
 // Three launches on the caller's stream:
 //   decode_qt_kernel       q~ for every query head, scaled by sm_scale log2(e)
-//                          so that the softmax runs in base 2.
+//                          so that the softmax runs in base 2, plus the form
+//                          the quantised-key product consumes: q~ in 24-bit
+//                          fixed point as six fp8 digit "limbs" with one
+//                          power-of-two scale each, and sum(q~).
 //   decode_main_kernel     grid (splits, kv heads, batch), four waves per
-//                          workgroup.  The "units" of a (sequence, head) are
-//                          the win_slots / 64 window units (bf16 sink + ring)
-//                          followed by the quantised pages.  A split owns a
-//                          run of units and each wave a contiguous part of
-//                          it; while a wave computes one page it has the next
-//                          page's words and parameters in flight.  Per unit
-//                          the wave forms 64 scores with the 16x16x32 bf16
-//                          matrix instruction (codes as the A operand, the G
-//                          query heads as columns), keeps an online softmax
-//                          and accumulates P V with a second matrix product.
-//                          The four waves merge in LDS; the workgroup writes
-//                          one partial (m, l, o) per query head.
+//                          workgroup.  Workgroups 0 .. n_page_splits - 1 scan
+//                          the quantised pages, each wave a contiguous run;
+//                          the last workgroup of a (sequence, head) scans the
+//                          bf16 sink + ring slots, one 64-slot unit per wave.
+//                          Each workgroup writes one partial (m, l, o) per
+//                          query head.
 //   decode_combine_kernel  log-sum-exp merge of the splits.
 //
-// Scores against codes.  A stored key is k = s c + z per token, so
+// Quantised pages.  A stored key is k = s c + z per token, so
 //   q~ . k = s (q~ . c) + z sum(q~).
-// The codes are widened to bf16 as 128 + c 2^sh (see widen_word), hence
-//   q~' . (128 + c 2^sh) = 128 sum(q~') + q~ . c   with q~' = q~ 2^-sh,
-// and the correction 128 sum(q~') is subtracted per query head.  Values
-// likewise: sum_t p_t (s_t c_t + z_t) = sum_t (p_t s_t) c_t + sum_t p_t z_t;
-// value codes are widened to fp16 as 1024 + c 4^p and the weights
-// p_t s_t 4^-p enter the fp16 product as one fp16 operand (11 significant
-// bits, a relative error below 2.5e-4 per weight); the 1024 offset is removed
-// with one more matrix product against a constant-1024 operand, which yields
-// 1024 sum_t A_t per row.  q~' is split into bf16 hi + lo parts (about 16
-// significant bits), so the scores carry fp32-level accuracy.
+// q~ . c comes from one 16x16x128 scaled matrix instruction per 16 tokens:
+// (two of them: limbs 0-3, then limbs 4-5) the rows are (query head, limb)
+// pairs of fp8 limbs with their E8M0 scales,
+// the columns are tokens whose 2-bit codes read as fp4 e2m1 (a code c in the
+// low two bits of a nibble is the value c / 2, exactly) or whose 4-bit codes
+// read as fp8 e4m3 (c in the low nibble of a byte is c 2^-9); a column scale
+// of 2 or 2^9 restores c.  Each lane then owns one query head and four
+// tokens: it adds its four limb rows, forms the logits, and updates the
+// online softmax.  The weights p s, split into fp16 hi + lo parts, go through
+// a small per-wave LDS buffer to become the A operand rows (head, part) of
+// the P V product (16x16x32 fp16), whose B operand is the value codes
+// widened to fp16 subnormals with the code near the top of the fraction (see
+// widen_word_f16); a slot's power-of-two factor is folded into the exponent
+// of p.
+//
+// Window slots.  bf16 keys and values: q~ in bf16 hi + lo parts forms the A
+// rows (head, part) of 16x16x32 bf16 products against the key slots; the
+// probabilities, again split hi + lo, go through LDS into the P V product
+// against the channel-major value slots.
 #include "common.h"
 
 namespace wushkv {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kMaxSplits = 1024;
+constexpr int kLimbs = 6;
+
+typedef __attribute__((ext_vector_type(8))) int i32x8;
 
 struct DecodeArgs {
     const uint8_t *pages;
@@ -47,25 +56,49 @@ struct DecodeArgs {
     const int32_t *seq_len;
     const int32_t *quant_end;
     int32_t n_kv, s_sink, win_slots, max_pages, n_pages;
-    int32_t G, n_q;
-    int32_t units_per_wave, n_splits;
-    WidenMasks wk, wv;  // key codes to bf16, value codes to fp16
-    const float *qt;  // [batch][n_q][D]
-    float *part;      // [batch][n_kv][n_splits][G][D + 2]
+    int32_t n_q;
+    int32_t units_per_wave, n_page_splits, n_splits;
+    const float *qt;       // [batch][n_q][D], scaled q~
+    const uint8_t *qlimb;  // [batch][n_q][6][128] fp8 limbs in operand order
+    const uint32_t *qaux;  // [batch][n_q][4]: limb scales (E8M0 bytes, limbs 0-3 then 4-5),
+                           // sum(q~) (fp32 bits), unused
+    float *part;           // [batch][n_kv][n_splits][G][D + 2]
 };
 
 __device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Byte position, inside a limb's 128 operand bytes, of query channel ch: the
+// A operand lane group j' element i' of the scaled product meets the key
+// operand at the position the key codes' format dictates.  With fp4 keys
+// (2-bit) the fp8 element (j', i') meets fp4 lane group 2 (i' / 16) + j' / 2,
+// element 16 (j' % 2) + i' % 16, and the key codes put channel 32 j + i at
+// fp4 element (j, i); with fp8 keys (4-bit) elements meet one to one.
+template <int BITS>
+__host__ __device__ constexpr int limb_pos(int ch)
+{
+    if (BITS == 4) return ch;
+    const int j = ch >> 5, i = ch & 31;  // key lane group and element
+    // solve 2 (i' / 16) + j' / 2 = j and 16 (j' % 2) + i' % 16 = i
+    const int jp = 2 * (j & 1) + (i >> 4);
+    const int ip = 16 * (j >> 1) + (i & 15);
+    return 32 * jp + ip;
+}
 
 // ------------------------------------------------------------------ q~
 
 // One workgroup per (kv head, sequence).  Thread (ig, jg) multiplies a block
 // of rows i of T^{-1} (kRows of them) by the G queries for 8 output channels
-// j; all of a thread's loads are independent and issued together, and the
-// row blocks are summed in LDS.
-template <int D>
+// j; the row blocks are summed in LDS.  Then one wave per query head writes
+// q~ in fixed point, N = rne(q~ 2^F) with F the largest exponent that keeps
+// |N| <= 7829367, as six balanced base-16 digits d_l in [-8, 7]
+// (N = sum_l d_l 16^(5 - l)).  Each digit is an fp8 integer and limb l
+// carries the E8M0 scale 16^(5 - l) 2^-F, so every product the matrix
+// instruction forms is an integer times a power of two: its block sums,
+// which it does not accumulate at full fp32 precision in general, are exact.
+template <int D, int BITS>
 __global__ void __launch_bounds__(256) decode_qt_kernel(const uint16_t *q, const float *tinv,
-                                                        float *qt, int32_t n_kv, int32_t G,
-                                                        float scale)
+                                                        float *qt, uint8_t *qlimb, uint32_t *qaux,
+                                                        int32_t n_kv, int32_t G, float scale)
 {
     constexpr int kJG = D / 8;        // groups of 8 output channels
     constexpr int kIG = 256 / kJG;    // groups of rows
@@ -104,77 +137,148 @@ __global__ void __launch_bounds__(256) decode_qt_kernel(const uint16_t *q, const
         float s = 0.0f;
 #pragma unroll
         for (int k = 0; k < kIG; ++k) s += red[k][g][jj];
-        qt[((int64_t)b * n_q + h * G + g) * D + jj] = s * scale;
+        s *= scale;
+        qt[((int64_t)b * n_q + h * G + g) * D + jj] = s;
+        red[0][g][jj] = s;
+    }
+    __syncthreads();
+
+    // limbs: wave w handles query heads w, w + 4
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    constexpr int kPer = D / 64;  // channels per lane
+    for (int g = wave; g < G; g += 4) {
+        const int64_t qh = (int64_t)b * n_q + h * G + g;
+        float r[kPer];
+        float zs = 0.0f;
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            r[e] = red[0][g][64 * e + lane];
+            zs += r[e];
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) zs += __shfl_xor(zs, off);
+        uint8_t *out = qlimb + qh * (kLimbs * 128);
+        float mx = 0.0f;
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) mx = fmaxf(mx, fabsf(r[e]));
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+        // fixed point N = rne(q~ 2^F) with |N| <= 7829367 (< 2^23, exact
+        // in fp32), the largest value six balanced base-16 digits reach
+        constexpr float kNMax = 7829367.0f;
+        int F = 0;
+        if (mx > 0.0f) {
+            int ex;
+            (void)frexpf(kNMax / mx, &ex);
+            F = ex - 1;
+            if (ldexpf(mx, F) > kNMax) F -= 1;
+            if (ldexpf(mx, F + 1) <= kNMax) F += 1;
+            F = F < -100 ? -100 : (F > 100 ? 100 : F);
+        }
+        uint32_t scales[2] = {0u, 0u};
+#pragma unroll
+        for (int l = 0; l < kLimbs; ++l)
+            scales[l >> 2] |= (uint32_t)(127 + 4 * (kLimbs - 1 - l) - F) << (8 * (l & 3));
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            const int ch = 64 * e + lane;
+            int N = (int)rintf(ldexpf(r[e], F));
+#pragma unroll
+            for (int l = kLimbs - 1; l >= 0; --l) {
+                const int d = ((N + 8) & 15) - 8;  // balanced digit
+                N = (N - d) >> 4;
+                // fp8 e4m3 of the integer d: exponent and top mantissa bits
+                // of its fp32 form
+                const uint32_t fb = __float_as_uint((float)(d < 0 ? -d : d));
+                const uint32_t code = (d == 0 ? 0u : ((((fb >> 23) - 120u) << 3) | ((fb >> 20) & 7u))) |
+                                      (d < 0 ? 0x80u : 0u);
+                out[l * 128 + limb_pos<BITS>(ch)] = (uint8_t)code;
+            }
+        }
+        if (D == 64) {
+            // operand positions no channel maps to are zero: with fp4 keys
+            // the elements 16 .. 31 of each lane group, with fp8 keys 64 ..
+            for (int l = 0; l < kLimbs; ++l)
+                for (int p = lane; p < 128; p += 64)
+                    if (BITS == 2 ? (p & 16) != 0 : p >= 64) out[l * 128 + p] = 0;
+        }
+        if (lane == 0) {
+            qaux[4 * qh] = scales[0];
+            qaux[4 * qh + 1] = scales[1];
+            qaux[4 * qh + 2] = __float_as_uint(zs);
+            qaux[4 * qh + 3] = 0u;
+        }
     }
 }
 
 // ------------------------------------------------------------------ main
 
-__device__ __forceinline__ float wave_max_xor_16_32(float x)
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x)
 {
-    x = fmaxf(x, __shfl_xor(x, 16));
-    x = fmaxf(x, __shfl_xor(x, 32));
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x),
+                                                                  CTRL, 0xF, 0xF, false));
+}
+// max / sum over the 16 lanes of a row (quad butterflies, then rotations)
+__device__ __forceinline__ float row_max16(float x)
+{
+    x = fmaxf(x, dpp<0xB1>(x));   // quad_perm [1,0,3,2]
+    x = fmaxf(x, dpp<0x4E>(x));   // quad_perm [2,3,0,1]
+    x = fmaxf(x, dpp<0x124>(x));  // row_ror 4
+    x = fmaxf(x, dpp<0x128>(x));  // row_ror 8
     return x;
 }
-__device__ __forceinline__ float wave_sum_xor_16_32(float x)
+__device__ __forceinline__ float row_sum16(float x)
 {
-    x += __shfl_xor(x, 16);
-    x += __shfl_xor(x, 32);
+    x += dpp<0xB1>(x);
+    x += dpp<0x4E>(x);
+    x += dpp<0x124>(x);
+    x += dpp<0x128>(x);
     return x;
-}
-
-__device__ __forceinline__ float bf16_hi_to_f32(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
-
-// hi = bf16(x) (nearest even), lo = bf16(x - hi), for a pair of values.
-__device__ __forceinline__ void split_hi_lo(float x0, float x1, uint32_t &hi, uint32_t &lo)
-{
-    hi = pack_bf16_rne(x0, x1);
-    lo = pack_bf16_rne(x0 - bf16_bits_to_f32(hi & 0xFFFFu), x1 - bf16_hi_to_f32(hi));
-}
-
-// Token of the page (or window unit) whose score lands in accumulator row
-// 4 j + r of score tile tau.
-__device__ __forceinline__ int score_token(int tau, int j, int r)
-{
-    return 32 * (tau >> 1) + 8 * j + 4 * (tau & 1) + r;
 }
 
 __device__ __forceinline__ void __attribute__((address_space(3))) *lds_ptr(void *p)
 {
     return (void __attribute__((address_space(3))) *)p;
 }
+__device__ __forceinline__ uint32_t lds_addr(const void *p)
+{
+    return (uint32_t)(uintptr_t)lds_ptr(const_cast<void *>(p));
+}
 
-// 16-byte LDS read of page data staged by the direct-to-LDS loads.  Written
-// as inline assembly because the compiler, unable to tell the staging slots
-// apart, would otherwise wait for every outstanding load before any LDS read
-// and undo the pipelining.  The caller waits for the data with
-// lds_reads_done() before using it; stage_ready() has already ensured the
-// page itself has arrived.
-__device__ __forceinline__ u32x4 lds_read16(const uint8_t *p)
+// LDS accesses written as inline assembly: the compiler cannot tell the
+// direct-to-LDS staging slots apart from other LDS data and would wait for
+// every outstanding global load before any LDS access.  lds_wait() with the
+// values as read-write operands orders the uses after the reads.
+__device__ __forceinline__ u32x4 lds_read16(uint32_t addr)
 {
     u32x4 r;
-    const uint32_t addr = (uint32_t)(uintptr_t)lds_ptr(const_cast<uint8_t *>(p));
     asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr) : "memory");
     return r;
 }
-
-// Wait for the LDS reads above.  The read results pass through the asm as
-// read-write operands, so nothing that uses them can be scheduled before it.
-template <int NX>
-__device__ __forceinline__ void lds_reads_done(u32x4 (&x)[NX], u32x4 (&y)[2][2])
+__device__ __forceinline__ void lds_write8(uint32_t addr, uint32_t lo, uint32_t hi)
 {
-    static_assert(NX == 1 || NX == 2 || NX == 4, "words per lane");
-    if constexpr (NX == 1)
+    typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+    u32x2 v = {lo, hi};
+    asm volatile("ds_write_b64 %0, %1" ::"v"(addr), "v"(v) : "memory");
+}
+template <int N>
+__device__ __forceinline__ void lds_wait(u32x4 (&x)[N])
+{
+    static_assert(N >= 1 && N <= 8, "operands");
+    if constexpr (N == 1) asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x[0])::"memory");
+    else if constexpr (N == 2) asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x[0]), "+v"(x[1])::"memory");
+    else if constexpr (N == 3)
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x[0]), "+v"(x[1]), "+v"(x[2])::"memory");
+    else if constexpr (N == 4)
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3])::"memory");
+    else if constexpr (N == 6)
         asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(x[0]), "+v"(y[0][0]), "+v"(y[0][1]), "+v"(y[1][0]), "+v"(y[1][1])::"memory");
-    else if constexpr (NX == 2)
-        asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(x[0]), "+v"(x[1]), "+v"(y[0][0]), "+v"(y[0][1]), "+v"(y[1][0]),
-                       "+v"(y[1][1])::"memory");
+                     : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]), "+v"(x[4]), "+v"(x[5])::"memory");
     else
         asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]), "+v"(y[0][0]),
-                       "+v"(y[0][1]), "+v"(y[1][0]), "+v"(y[1][1])::"memory");
+                     : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]), "+v"(x[4]), "+v"(x[5]),
+                       "+v"(x[6]), "+v"(x[7])::"memory");
 }
 
 // Wait until at most `after` direct-to-LDS loads are outstanding.  `after`
@@ -189,201 +293,138 @@ __device__ __forceinline__ void wait_vmcnt_at_most(int after)
     else asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kMaxAhead * kDma) : "memory");
 }
 
-// Packed operands and parameters of one page, as one lane holds them.
-template <int D, int BITS>
-struct PageRegs {
+__device__ __forceinline__ f32x4 mfma_scaled(const i32x8 &a, const i32x8 &b, int fmt_b, int scale_a,
+                                             int scale_b)
+{
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    if (fmt_b == 4)
+        return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, z, 0, 4, 0, scale_a, 0, scale_b);
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, z, 0, 0, 0, scale_a, 0, scale_b);
+}
+
+// LDS per wave: page stages (also the merge buffer) and the weight buffer.
+template <int D, int BITS, int G>
+struct MainLds {
     using L = Layout<D, BITS>;
-    uint32_t kw[L::kWordsPerLane];
-    uint32_t vw[L::kWordsPerLane];
-    uint32_t kp[2][8];  // (scale, zero) of tokens 32 kc + 8 j + i
-    uint32_t vp[2][8];
-
-    __device__ __forceinline__ void load(const uint8_t *pgb, int lane, int j)
-    {
-        constexpr int kQ = L::kWordsPerLane / 4;
-        const u32x4 *kr = reinterpret_cast<const u32x4 *>(pgb) + lane * kQ;
-        const u32x4 *vr = reinterpret_cast<const u32x4 *>(pgb + L::kRegionBytes) + lane * kQ;
-#pragma unroll
-        for (int q4 = 0; q4 < kQ; ++q4) {
-            const u32x4 x = kr[q4], y = vr[q4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                kw[4 * q4 + e] = x[e];
-                vw[4 * q4 + e] = y[e];
-            }
-        }
-        const u32x4 *kpr = reinterpret_cast<const u32x4 *>(pgb + L::kParamOffset);
-        const u32x4 *vpr = reinterpret_cast<const u32x4 *>(pgb + L::kParamOffset + 4 * kPage);
-#pragma unroll
-        for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-            for (int h2 = 0; h2 < 2; ++h2) {
-                const u32x4 x = kpr[(32 * kc + 8 * j) / 4 + h2];
-                const u32x4 y = vpr[(32 * kc + 8 * j) / 4 + h2];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    kp[kc][4 * h2 + e] = x[e];
-                    vp[kc][4 * h2 + e] = y[e];
-                }
-            }
-    }
+    static constexpr int kStages = 2;
+    static constexpr int kDma = (L::kPageBytes + 1023) / 1024;  // direct-to-LDS loads per page
+    static constexpr int kSlot = kDma * 1024;
+    static constexpr int kStageBytes = kStages * kSlot > G * D * 4 ? kStages * kSlot : G * D * 4;
+    // weight buffer: 2G rows of 64 tokens (fp16 or bf16), then a zero row
+    static constexpr int kTRows = 2 * G;
+    static constexpr int kTBytes = kTRows * 128 + 64;
+    static constexpr int kWave = kStageBytes + kTBytes;
 };
 
-// One wave's online softmax and output accumulators.
-template <int D>
-struct WaveState {
-    static constexpr int kNT = D / 16;
-    f32x4 acc[kNT];  // P V accumulators, rows 4 j + r (head g: hi row g, lo row g + G)
-    f32x4 accb;      // 128 sum_t A_t per row (offset of the widened value codes)
-    float m_lane;    // running max of this lane's column
-    float l_lane;    // sum of p over this lane's tokens
-    float z_lane;    // sum of p * value zero over this lane's tokens
-
-    __device__ __forceinline__ void init()
-    {
-#pragma unroll
-        for (int nt = 0; nt < kNT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        accb = f32x4{0.f, 0.f, 0.f, 0.f};
-        m_lane = -INFINITY;
-        l_lane = 0.0f;
-        z_lane = 0.0f;
-    }
-
-    // Fold a unit's column max into the running max; rescale on change.
-    // Accumulator row 4 j + r belongs to head (4 j + r) mod G, whose factor
-    // lane (4 j + r) mod G holds (every lane of a column has the same max).
-    __device__ __forceinline__ void update_max(float mloc, int j, int G)
-    {
-        const float m_new = fmaxf(m_lane, mloc);
-        if (__any(m_new > m_lane)) {
-            const float al = (m_new == -INFINITY) ? 1.0f : fexp2(m_lane - m_new);
-            l_lane *= al;
-            z_lane *= al;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float ar = __shfl(al, (4 * j + r) & (G - 1));
-#pragma unroll
-                for (int nt = 0; nt < kNT; ++nt) acc[nt][r] *= ar;
-                accb[r] *= ar;
-            }
-        }
-        m_lane = m_new;
-    }
-};
-
-template <int D, int BITS>
-__global__ void __launch_bounds__(256, 2) decode_main_kernel(DecodeArgs a)
+template <int D, int BITS, int G>
+__global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
 {
     using L = Layout<D, BITS>;
-    // pages per wave in LDS (kStages - 1 in flight): three for pages up to
-    // 5 KB, two for the 8.5 KB 4-bit pages, keeping two workgroups per CU
-    constexpr int kStages = L::kPageBytes <= 5120 ? 3 : 2;
-    constexpr int kC = L::kChunks;   // D / 32
-    constexpr int kNT = L::kNTiles;  // D / 16
+    using M = MainLds<D, BITS, G>;
+    constexpr int kStages = M::kStages;
+    constexpr int kDma = M::kDma;
+    constexpr int kSlot = M::kSlot;
+    constexpr int kNT = L::kNTiles;   // D / 16
+    constexpr int kC = L::kChunks;    // D / 32
     constexpr int kNw = L::kNw;
     constexpr int kOpw = L::kOpsPerWord;
+    constexpr int kHG = G > 4 ? 2 : 1;          // score products per 16 tokens
+    constexpr int kRowsPerHead = G > 4 ? 2 : 4; // P V rows per head (pages): hi, lo, [zero, zero]
+    constexpr int kFmtB = BITS == 2 ? 4 : 0;    // fp4 or fp8 key codes
+    constexpr int kScaleB = BITS == 2 ? 128 : 136;  // 2^1 or 2^9
 
-    // page stages of the four waves; after its loops a wave reuses its own
-    // stage area for its slice of the merge buffer
-    constexpr int kPB = L::kPageBytes;
-    constexpr int kDma = (kPB + 1023) / 1024;  // direct-to-LDS loads per page
-    constexpr int kSlot = kDma * 1024;
-    constexpr int kWaveLds = kStages * kSlot > 16 * D * 4 ? kStages * kSlot : 16 * D * 4;
-    __shared__ __attribute__((aligned(16))) uint8_t lds[4 * kWaveLds];
-    __shared__ float sM[4][8], sL[4][8], sZ[4][8];
+    __shared__ __attribute__((aligned(16))) uint8_t lds[4 * M::kWave];
+    __shared__ float sM[4][8], sL[4][8];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int j = lane >> 4, n = lane & 15;
     const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-    const int G = a.G;
-    const int g = n & (G - 1);
-    const int cls = n < G ? 0 : (n < 2 * G ? 1 : 2);  // 0: hi column/row, 1: lo, 2: unused
+    uint8_t *stage = lds + wave * M::kWave;
+    uint8_t *tbuf = stage + M::kStageBytes;
+    const uint32_t zero_row = lds_addr(tbuf + M::kTRows * 128);
+    if (lane < 16) reinterpret_cast<uint32_t *>(tbuf + M::kTRows * 128)[lane] = 0u;
 
     const int32_t S = a.seq_len[b];
     int32_t qend = a.quant_end[b];
     qend = qend < S ? qend : S;
     const int32_t q_hi = qend > a.s_sink ? qend : a.s_sink;  // quantised: [s_sink, q_hi)
     const int32_t n_qpages = (q_hi - a.s_sink + kPage - 1) / kPage;
-    const int32_t n_wunits = a.win_slots / kPage;
-    const int32_t n_units = n_qpages + n_wunits;  // pages first, then the window units
-    const int32_t ring = a.win_slots - a.s_sink;
-    // the ring holds positions [q_hi, S); the oldest sits at ring index a0
-    const int32_t a0 = S > q_hi ? (q_hi - a.s_sink) % ring : 0;
-    const int32_t ring_live = S > q_hi ? S - q_hi : 0;
+    const int64_t qhead0 = (int64_t)b * a.n_q + h * G;       // first query head of the group
 
-    // this wave's units
-    const int upw = a.units_per_wave;
-    const int w0 = (split * 4 + wave) * upw;
-    const int w1 = min(w0 + upw, n_units);
+    // per-wave results for the merge: o (unnormalised, relative to m), m, l
+    float(*sC)[D] = reinterpret_cast<float(*)[D]>(stage);
 
-    const float *qrow = a.qt + ((int64_t)b * a.n_q + h * G + g) * D;
-    const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;
+    if (split < a.n_page_splits) {
+        // ================================================ quantised pages
+        const int upw = a.units_per_wave;
+        const int w0 = (split * 4 + wave) * upw;
+        const int w1 = min(w0 + upw, n_qpages);
 
-    WaveState<D> st;
-    st.init();
-
-    // B operands of the score products: hi and lo parts of q~ (2^-sh scaled
-    // for pages); columns n < 2G carry query head g = n mod G.
-    uint32_t bhi[kC][4], blo[kC][4];
-    float zsum = 0.0f, qbias = 0.0f;
-    auto build_b = [&](bool pages) {
-        float part = 0.0f, zs = 0.0f;
+        // score A operands, two per head group: row m = 4 g' + r holds limb
+        // r (first) or limb 4 + r for r < 2 (second; rows r >= 2 zero) of
+        // head hd = g' (G <= 4) or 2 g' + hg (G = 8); heads >= G give zero rows
+        i32x8 qa[kHG][2];
+        int qsc[kHG][2];
+        float zs[kHG];  // sum(q~) of the head this lane's scores belong to
 #pragma unroll
-        for (int c = 0; c < kC; ++c) {
-            float x[8];
-            if (cls < 2) {
-                const f32x4 lo4 = *reinterpret_cast<const f32x4 *>(qrow + 32 * c + 8 * j);
-                const f32x4 hi4 = *reinterpret_cast<const f32x4 *>(qrow + 32 * c + 8 * j + 4);
+        for (int hg = 0; hg < kHG; ++hg) {
+            const int hd = G > 4 ? 2 * (n >> 2) + hg : (n >> 2);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    x[e] = lo4[e];
-                    x[4 + e] = hi4[e];
+            for (int part = 0; part < 2; ++part) {
+                const int limb = 4 * part + (n & 3);
+                u32x4 x0 = {0u, 0u, 0u, 0u}, x1 = x0;
+                qsc[hg][part] = 127;
+                if (hd < G && limb < kLimbs) {
+                    const uint8_t *src = a.qlimb + ((qhead0 + hd) * kLimbs + limb) * 128 + 32 * j;
+                    x0 = *reinterpret_cast<const u32x4 *>(src);
+                    x1 = *reinterpret_cast<const u32x4 *>(src + 16);
+                    qsc[hg][part] = (a.qaux[4 * (qhead0 + hd) + part] >> (8 * (n & 3))) & 0xFFu;
                 }
-            } else {
-#pragma unroll
-                for (int e = 0; e < 8; ++e) x[e] = 0.0f;
+                qa[hg][part] = i32x8{(int)x0[0], (int)x0[1], (int)x0[2], (int)x0[3],
+                                     (int)x1[0], (int)x1[1], (int)x1[2], (int)x1[3]};
             }
-#pragma unroll
-            for (int p = 0; p < 4; ++p) {
-                zs += x[2 * p] + x[2 * p + 1];
-                const float sc = pages ? slot_scale<BITS>(2 * p) : 1.0f;
-                split_hi_lo(x[2 * p] * sc, x[2 * p + 1] * sc, bhi[c][p], blo[c][p]);
-                part += (bf16_bits_to_f32(bhi[c][p] & 0xFFFFu) + bf16_hi_to_f32(bhi[c][p])) +
-                        (bf16_bits_to_f32(blo[c][p] & 0xFFFFu) + bf16_hi_to_f32(blo[c][p]));
-            }
+            const int hs = G > 4 ? 2 * j + hg : j;
+            zs[hg] = hs < G ? __uint_as_float(a.qaux[4 * (qhead0 + hs) + 2]) : 0.0f;
         }
-        zsum = wave_sum_xor_16_32(zs);
-        qbias = pages ? 128.0f * wave_sum_xor_16_32(part) : 0.0f;
-    };
-    auto bop = [](const uint32_t (&v)[4]) {
-        return __builtin_bit_cast(bf16x8, u32x4{v[0], v[1], v[2], v[3]});
-    };
+        // this lane's heads in the score layout, and whether they exist
+        bool hvalid[kHG];
+#pragma unroll
+        for (int hg = 0; hg < kHG; ++hg) hvalid[hg] = (G > 4 ? 2 * j + hg : j) < G;
 
-    // ---------------------------------------------------- quantised pages
-    // Pages are copied whole, global -> LDS, by the direct-to-LDS loads
-    // (64 lanes x 16 B per instruction, lane l's bytes at slot + 16 l), so
-    // a stage holds the page block byte for byte.  A wave keeps kStages - 1
-    // pages in flight while it computes the oldest one; the compiler does not
-    // track these loads, so the waits below are explicit.
-    const int pw1 = min(w1, n_qpages);
-    if (w0 < pw1) {
-        build_b(true);
-        // widening masks in scalar registers and the biases in vector
-        // registers (one v_mov each, opaque to the optimizer), so that
-        // (word & mask) | bias selects v_and_or_b32 with one scalar operand
-        WidenMasks wk = a.wk, wv = a.wv;
-        asm volatile("v_mov_b32 %0, %1" : "=v"(wk.bias) : "s"(a.wk.bias));
-        asm volatile("v_mov_b32 %0, %1" : "=v"(wv.bias) : "s"(a.wv.bias));
-        const f16x8 c1024 = __builtin_bit_cast(f16x8, u32x4{kBiasF16x2, kBiasF16x2, kBiasF16x2, kBiasF16x2});
-        // the wave's page-table entries, one per lane, read once
+        // online-softmax state per head of this lane (l and z in units of
+        // 2^-off, below)
+        f32x4 acc[kNT];
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        float m_run[kHG], lc[kHG], zc[kHG];
+#pragma unroll
+        for (int hg = 0; hg < kHG; ++hg) {
+            m_run[hg] = -INFINITY;
+            lc[hg] = zc[hg] = 0.0f;
+        }
+        // token 4 n + t is slot i = 4 (n % 2) + t of the value operand, in
+        // register i / 2 = 2 (n % 2) + t / 2; the value widening puts 2-bit
+        // codes of registers 2-3 two bits higher (2^8 instead of 2^6), so this
+        // lane's weights carry 2^-off, off = 2 (n % 2); 4-bit codes all sit
+        // at 2^4.  The products are p s c 2^-18 (2-bit) or 2^-20 (4-bit).
+        const float off = BITS == 2 ? 2.0f * (n & 1) : 0.0f;
+        constexpr float kOutScale = BITS == 2 ? 262144.0f : 1048576.0f;
+
+        // P V A operand rows: row m is part m % kRowsPerHead (0: fp16 hi
+        // of the weight, 1: the fp16 rest, others zero) of head
+        // m / kRowsPerHead; weight rows sit at 2 g + part in the buffer
+        const int ahead = n / kRowsPerHead, apart = n % kRowsPerHead;
+        const bool arow_ok = ahead < G && apart < 2;
+        const uint32_t a_addr = arow_ok ? lds_addr(tbuf + (2 * ahead + apart) * 128 + 16 * j) : zero_row;
+        const uint32_t a_step = arow_ok ? 64u : 0u;  // second 32-token chunk
+
         int32_t tbl = -1;
-        if (w0 + lane < pw1 && w0 + lane < a.max_pages)
+        if (w0 + lane < w1 && w0 + lane < a.max_pages)
             tbl = a.page_table[(int64_t)b * a.max_pages + w0 + lane];
-        uint8_t *stage = lds + wave * kWaveLds;
-        // Every page of the run issues exactly kDma loads; a page-table entry
-        // outside the pool loads physical page 0 instead (its data is never
-        // used), which keeps the count of outstanding loads a closed form.
         auto phys_of = [&](int u) -> int32_t { return __builtin_amdgcn_readlane(tbl, u - w0); };
+        // Every page of the run issues exactly kDma loads; an entry outside
+        // the pool loads physical page 0 instead (its data is never used),
+        // which keeps the count of outstanding loads a closed form.
         auto issue = [&](int u, int s) {
             int32_t phys = phys_of(u);
             if (phys < 0 || phys >= a.n_pages) phys = 0;
@@ -395,157 +436,213 @@ __global__ void __launch_bounds__(256, 2) decode_main_kernel(DecodeArgs a)
                     __builtin_amdgcn_global_load_lds(src + 1024 * i, lds_ptr(dst + 1024 * i), 16, 0, 0);
             }
         };
-        if (a.n_pages > 0) {
+        if (a.n_pages > 0 && w0 < w1) {
 #pragma unroll
-        for (int s = 0; s < kStages - 1; ++s)
-            if (w0 + s < pw1) issue(w0 + s, s);
-        for (int u = w0; u < pw1; ++u) {
-            const int s = (u - w0) % kStages;
-            if (u + kStages - 1 < pw1) issue(u + kStages - 1, (u - w0 + kStages - 1) % kStages);
-            // pages issued after page u: min(kStages - 1, pw1 - 1 - u)
-            // stage_ready: page u has landed in LDS once at most the later
-            // pages' loads are outstanding
-            wait_vmcnt_at_most<kStages - 1, kDma>(kDma * min(kStages - 1, pw1 - 1 - u));
-            {
-                const int32_t phys = phys_of(u);
-                if (phys < 0 || phys >= a.n_pages) continue;
-            }
-            const uint8_t *pg = stage + s * kSlot;
-            const int32_t nvalid = min(kPage, q_hi - (a.s_sink + u * kPage));
-            // scores S^T[token][column] - 128 sum q~', four tiles of 16 tokens
-            uint32_t kw[L::kWordsPerLane];
-            uint32_t kp[2][8];
-            {
-                u32x4 x[L::kWordsPerLane / 4], y[2][2];
-#pragma unroll
-                for (int q4 = 0; q4 < L::kWordsPerLane / 4; ++q4)
-                    x[q4] = lds_read16(pg + 16 * (lane * (L::kWordsPerLane / 4) + q4));
-#pragma unroll
-                for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-                    for (int h2 = 0; h2 < 2; ++h2)
-                        y[kc][h2] = lds_read16(pg + L::kParamOffset + 4 * (32 * kc + 8 * j) + 16 * h2);
-                lds_reads_done(x, y);
-#pragma unroll
-                for (int q4 = 0; q4 < L::kWordsPerLane / 4; ++q4)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) kw[4 * q4 + e] = x[q4][e];
-#pragma unroll
-                for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-                    for (int h2 = 0; h2 < 2; ++h2)
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) kp[kc][4 * h2 + e] = y[kc][h2][e];
-            }
-            f32x4 sc[4];
-#pragma unroll
-            for (int tau = 0; tau < 4; ++tau) {
-                sc[tau] = f32x4{-qbias, -qbias, -qbias, -qbias};
-#pragma unroll
-                for (int w = 0; w < kNw; ++w) {
-                    uint32_t op[L::kCodesPerWord / 2];
-                    widen_word<BITS>(kw[tau * kNw + w], op, wk);
-#pragma unroll
-                    for (int o = 0; o < kOpw; ++o) {
-                        const int c = w * kOpw + o;
-                        const bf16x8 A = as_op(op + 4 * o);
-                        sc[tau] = mfma16(A, bop(bhi[c]), sc[tau]);
-                        sc[tau] = mfma16(A, bop(blo[c]), sc[tau]);
-                    }
+            for (int s = 0; s < kStages - 1; ++s)
+                if (w0 + s < w1) issue(w0 + s, s);
+            for (int u = w0; u < w1; ++u) {
+                const int s = (u - w0) % kStages;
+                if (u + kStages - 1 < w1) issue(u + kStages - 1, (u - w0 + kStages - 1) % kStages);
+                wait_vmcnt_at_most<kStages - 1, kDma>(kDma * min(kStages - 1, w1 - 1 - u));
+                {
+                    const int32_t phys = phys_of(u);
+                    if (phys < 0 || phys >= a.n_pages) continue;
                 }
-            }
-            // logits (base 2): s (S - 128 sum q~') + z sum q~
-            float lg[4][4];
-#pragma unroll
-            for (int tau = 0; tau < 4; ++tau)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const uint32_t kprm = kp[tau >> 1][4 * (tau & 1) + r];
-                    lg[tau][r] = fmaf(f16_bits_to_f32(kprm & 0xFFFFu), sc[tau][r],
-                                      f16_bits_to_f32(kprm >> 16) * zsum);
-                }
-            if (nvalid < kPage) {
-#pragma unroll
-                for (int tau = 0; tau < 4; ++tau)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        if (score_token(tau, j, r) >= nvalid) lg[tau][r] = -INFINITY;
-            }
-            float mloc = -INFINITY;
-#pragma unroll
-            for (int tau = 0; tau < 4; ++tau)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) mloc = fmaxf(mloc, lg[tau][r]);
-            st.update_max(wave_max_xor_16_32(mloc), j, G);
-            // weights p s 4^-p as fp16, in the A rows g < G
-            uint32_t vp[2][8];
-            uint32_t vw[L::kWordsPerLane];
-            {
-                u32x4 x[L::kWordsPerLane / 4], y[2][2];
-#pragma unroll
-                for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-                    for (int h2 = 0; h2 < 2; ++h2)
-                        y[kc][h2] = lds_read16(pg + L::kParamOffset + 4 * kPage + 4 * (32 * kc + 8 * j) + 16 * h2);
-#pragma unroll
-                for (int q4 = 0; q4 < L::kWordsPerLane / 4; ++q4)
-                    x[q4] = lds_read16(pg + L::kRegionBytes + 16 * (lane * (L::kWordsPerLane / 4) + q4));
-                lds_reads_done(x, y);
-#pragma unroll
-                for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-                    for (int h2 = 0; h2 < 2; ++h2)
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) vp[kc][4 * h2 + e] = y[kc][h2][e];
-#pragma unroll
-                for (int q4 = 0; q4 < L::kWordsPerLane / 4; ++q4)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) vw[4 * q4 + e] = x[q4][e];
-            }
-            uint32_t aop[2][4];
-#pragma unroll
-            for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-                for (int p = 0; p < 4; ++p) {
-                    float wv2[2];
-#pragma unroll
-                    for (int e = 0; e < 2; ++e) {
-                        const int i = 2 * p + e;  // slot: token 32 kc + 8 j + i
-                        const float pr = fexp2(lg[2 * kc + (i >> 2)][i & 3] - st.m_lane);
-                        const uint32_t vprm = vp[kc][i];
-                        st.l_lane += pr;
-                        st.z_lane = fmaf(pr, f16_bits_to_f32(vprm >> 16), st.z_lane);
-                        wv2[e] = pr * (f16_bits_to_f32(vprm & 0xFFFFu) * slot_scale_f16<BITS>(i));
-                    }
-                    aop[kc][p] = cls == 0 ? pack_f16_rne(wv2[0], wv2[1]) : 0u;
-                }
-            // P V, plus the row sums that remove the 1024 offset
-#pragma unroll
-            for (int kc = 0; kc < 2; ++kc) {
-                const f16x8 A = __builtin_bit_cast(f16x8, u32x4{aop[kc][0], aop[kc][1], aop[kc][2], aop[kc][3]});
-#pragma unroll
-                for (int uu = 0; uu < 2 * kNw; ++uu) {
-                    uint32_t op[L::kCodesPerWord / 2];
-                    widen_word_f16<BITS>(vw[kc * 2 * kNw + uu], op, wv);
-#pragma unroll
-                    for (int o = 0; o < kOpw; ++o) {
-                        const int nt = uu * kOpw + o;
-                        st.acc[nt] = mfma16h(A, as_op_h(op + 4 * o), st.acc[nt]);
-                    }
-                }
-                st.accb = mfma16h(A, c1024, st.accb);
-            }
-        }
-        }
-    }
+                const uint32_t pg = lds_addr(stage + s * kSlot);
+                const int32_t nvalid = min(kPage, q_hi - (a.s_sink + u * kPage));
 
-    // ---------------------------------------------------- window units
-    const int ww0 = max(w0, n_qpages);
-    if (ww0 < w1) {
-        build_b(false);
-        for (int u = ww0; u < w1; ++u) {
-            const int32_t slot0 = (u - n_qpages) * kPage;
-            // slot validity of the unit, one bit per slot
+                // key words of this lane (tokens 4n..4n+3, channels 32j..),
+                // and the parameters of tokens 4n .. 4n+3
+                constexpr int kKX = L::kKWordsPerLane / 4;
+                u32x4 kx[kKX + 2];
+#pragma unroll
+                for (int q4 = 0; q4 < kKX; ++q4)
+                    kx[q4] = lds_read16(pg + 16 * (lane * kKX + q4));
+                kx[kKX] = lds_read16(pg + L::kParamOffset + 16 * n);
+                kx[kKX + 1] = lds_read16(pg + L::kParamOffset + 4 * kPage + 16 * n);
+                lds_wait(kx);
+                const u32x4 kp = kx[kKX], vp = kx[kKX + 1];
+
+                // scores: one product per 16 tokens (and head group)
+                float lg[kHG][4];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    uint32_t w[BITS];
+#pragma unroll
+                    for (int i = 0; i < BITS; ++i) w[i] = kx[(BITS * t + i) / 4][(BITS * t + i) % 4];
+                    i32x8 bop;
+                    if constexpr (BITS == 2) {
+                        bop = i32x8{(int)(w[0] & 0x33333333u), (int)((w[0] >> 2) & 0x33333333u),
+                                    (int)(w[1] & 0x33333333u), (int)((w[1] >> 2) & 0x33333333u),
+                                    0, 0, 0, 0};
+                    } else {
+                        bop = i32x8{(int)(w[0] & 0x0F0F0F0Fu), (int)((w[0] >> 4) & 0x0F0F0F0Fu),
+                                    (int)(w[1] & 0x0F0F0F0Fu), (int)((w[1] >> 4) & 0x0F0F0F0Fu),
+                                    (int)(w[2] & 0x0F0F0F0Fu), (int)((w[2] >> 4) & 0x0F0F0F0Fu),
+                                    (int)(w[3] & 0x0F0F0F0Fu), (int)((w[3] >> 4) & 0x0F0F0F0Fu)};
+                    }
+                    const float ks = f16_bits_to_f32(kp[t] & 0xFFFFu);
+                    const float kz = f16_bits_to_f32(kp[t] >> 16);
+#pragma unroll
+                    for (int hg = 0; hg < kHG; ++hg) {
+                        const f32x4 c0 = mfma_scaled(qa[hg][0], bop, kFmtB, qsc[hg][0], kScaleB);
+                        const f32x4 c1 = mfma_scaled(qa[hg][1], bop, kFmtB, qsc[hg][1], kScaleB);
+                        // the six limbs, most significant first
+                        const float dot = (((c0[0] + c0[1]) + c0[2]) + (c0[3] + c1[0])) + c1[1];
+                        lg[hg][t] = fmaf(ks, dot, kz * zs[hg]);
+                    }
+                }
+                if (nvalid < kPage) {
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        if (4 * n + t >= nvalid)
+#pragma unroll
+                            for (int hg = 0; hg < kHG; ++hg) lg[hg][t] = -INFINITY;
+                }
+                // running max per head (every lane of a row holds its head's)
+                float m_new[kHG];
+                bool grow = false;
+#pragma unroll
+                for (int hg = 0; hg < kHG; ++hg) {
+                    const float mx = row_max16(fmaxf(fmaxf(lg[hg][0], lg[hg][1]), fmaxf(lg[hg][2], lg[hg][3])));
+                    m_new[hg] = fmaxf(m_run[hg], mx);
+                    grow |= hvalid[hg] && m_new[hg] > m_run[hg];
+                }
+                if (__any(grow)) {
+                    // rescale: P V rows of lane (j, n) register r belong to
+                    // head j (G <= 4) or 2 j + r / 2 (G = 8), this lane's own
+                    float al[kHG];
+#pragma unroll
+                    for (int hg = 0; hg < kHG; ++hg) {
+                        al[hg] = m_new[hg] == -INFINITY ? 1.0f : fexp2(m_run[hg] - m_new[hg]);
+                        lc[hg] *= al[hg];
+                        zc[hg] *= al[hg];
+                    }
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const float ar = al[G > 4 ? (r >> 1) : 0];
+#pragma unroll
+                        for (int nt = 0; nt < kNT; ++nt) acc[nt][r] *= ar;
+                    }
+                }
+#pragma unroll
+                for (int hg = 0; hg < kHG; ++hg) m_run[hg] = m_new[hg];
+
+                // weights p s 2^-off as fp16, through LDS into the A operand
+#pragma unroll
+                for (int hg = 0; hg < kHG; ++hg) {
+                    const float mo = m_run[hg] + off;
+                    float wgt[4];
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        const float pw = fexp2(lg[hg][t] - mo);
+                        lc[hg] += pw;
+                        zc[hg] = fmaf(pw, f16_bits_to_f32(vp[t] >> 16), zc[hg]);
+                        wgt[t] = pw * f16_bits_to_f32(vp[t] & 0xFFFFu);
+                    }
+                    const int hs = G > 4 ? 2 * j + hg : j;
+                    if (hs < G) {
+                        // fp16 hi + lo: about 22 significant bits per weight
+                        const uint32_t h01 = pack_f16_rne(wgt[0], wgt[1]);
+                        const uint32_t h23 = pack_f16_rne(wgt[2], wgt[3]);
+                        const uint32_t l01 = pack_f16_rne(wgt[0] - f16_bits_to_f32(h01 & 0xFFFFu),
+                                                          wgt[1] - f16_bits_to_f32(h01 >> 16));
+                        const uint32_t l23 = pack_f16_rne(wgt[2] - f16_bits_to_f32(h23 & 0xFFFFu),
+                                                          wgt[3] - f16_bits_to_f32(h23 >> 16));
+                        lds_write8(lds_addr(tbuf + (2 * hs) * 128 + 8 * n), h01, h23);
+                        lds_write8(lds_addr(tbuf + (2 * hs + 1) * 128 + 8 * n), l01, l23);
+                    }
+                }
+                // A operands (two 32-token chunks) and the value words
+                u32x4 vx[2 + L::kWordsPerLane / 4];
+                vx[0] = lds_read16(a_addr);
+                vx[1] = lds_read16(a_addr + a_step);
+#pragma unroll
+                for (int q4 = 0; q4 < L::kWordsPerLane / 4; ++q4)
+                    vx[2 + q4] = lds_read16(pg + L::kRegionBytes + 16 * (lane * (L::kWordsPerLane / 4) + q4));
+                lds_wait(vx);
+#pragma unroll
+                for (int kc = 0; kc < 2; ++kc) {
+                    const f16x8 A = __builtin_bit_cast(f16x8, vx[kc]);
+#pragma unroll
+                    for (int uu = 0; uu < 2 * kNw; ++uu) {
+                        const int widx = kc * 2 * kNw + uu;
+                        uint32_t op[L::kCodesPerWord / 2];
+                        widen_word_f16<BITS>(vx[2 + widx / 4][widx % 4], op);
+#pragma unroll
+                        for (int o = 0; o < kOpw; ++o) {
+                            const int nt = uu * kOpw + o;
+                            acc[nt] = mfma16h(A, as_op_h(op + 4 * o), acc[nt]);
+                        }
+                    }
+                }
+            }
+        }
+
+        // ---- this wave's result per head: o = acc 2^18 (or 2^20) + z (rows of
+        // lane (j, n) register r: head j, or 2 j + r / 2 for G = 8)
+        float zt[kHG], lt[kHG];
+#pragma unroll
+        for (int hg = 0; hg < kHG; ++hg) {
+            const float f = ldexpf(1.0f, (int)off);
+            zt[hg] = row_sum16(zc[hg] * f);
+            lt[hg] = row_sum16(lc[hg] * f);
+        }
+#pragma unroll
+        for (int hg = 0; hg < kHG; ++hg) {
+            const int hs = G > 4 ? 2 * j + hg : j;
+            const int r = G > 4 ? 2 * hg : 0;  // the hi row; the lo row follows
+            if (hs < G) {
+#pragma unroll
+                for (int nt = 0; nt < kNT; ++nt)
+                    sC[hs][16 * nt + n] = fmaf(acc[nt][r] + acc[nt][r + 1], kOutScale, zt[hg]);
+                if (n == 0) {
+                    sM[wave][hs] = m_run[hg];
+                    sL[wave][hs] = lt[hg];
+                }
+            }
+        }
+    } else {
+        // ================================================ window slots
+        const int32_t n_wunits = a.win_slots / kPage;
+        const int32_t ring = a.win_slots - a.s_sink;
+        // the ring holds positions [q_hi, S); the oldest sits at ring index a0
+        const int32_t a0 = S > q_hi ? (q_hi - a.s_sink) % ring : 0;
+        const int32_t ring_live = S > q_hi ? S - q_hi : 0;
+        const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;
+
+        // A operands: row m = 2 g + part (hi, lo) of q~, chunk c
+        bf16x8 qa[kC];
+        {
+            const int g = n >> 1, part = n & 1;
+#pragma unroll
+            for (int c = 0; c < kC; ++c) {
+                uint32_t u[4] = {0u, 0u, 0u, 0u};
+                if (g < G) {
+                    const float *src = a.qt + (qhead0 + g) * D + 32 * c + 8 * j;
+                    const f32x4 x0 = *reinterpret_cast<const f32x4 *>(src);
+                    const f32x4 x1 = *reinterpret_cast<const f32x4 *>(src + 4);
+                    const float x[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+#pragma unroll
+                    for (int p = 0; p < 4; ++p) {
+                        const uint32_t hi = pack_bf16_rne(x[2 * p], x[2 * p + 1]);
+                        const uint32_t lo = pack_bf16_rne(x[2 * p] - bf16_bits_to_f32(hi & 0xFFFFu),
+                                                          x[2 * p + 1] - bf16_bits_to_f32(hi >> 16));
+                        u[p] = part ? lo : hi;
+                    }
+                }
+                qa[c] = __builtin_bit_cast(bf16x8, u32x4{u[0], u[1], u[2], u[3]});
+            }
+        }
+        f32x4 acc[kNT];
+#pragma unroll
+        for (int nt = 0; nt < kNT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        float m_run[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f};
+        const uint32_t a_addr = n < 2 * G ? lds_addr(tbuf + n * 128 + 16 * j) : zero_row;
+        const uint32_t a_step = n < 2 * G ? 64u : 0u;
+
+        for (int u = wave; u < n_wunits; u += 4) {
+            const int32_t slot0 = u * kPage;
             bool mine;
             {
                 const int32_t sl = slot0 + lane;
@@ -554,109 +651,111 @@ __global__ void __launch_bounds__(256, 2) decode_main_kernel(DecodeArgs a)
             }
             const uint64_t vmask = __ballot(mine);
             if (vmask == 0) continue;
-            auto valid = [&](int t) -> bool { return (vmask >> t) & 1u; };
-            const uint16_t *wk = a.win_k + (head_win + slot0) * D;
-            // All loads stay inside this unit's slots, so they are issued
-            // unconditionally (a branch per load would serialise them);
-            // dead slots are zeroed afterwards, whatever bits they held.
-            u32x4 kx[4][kC];
+            // scores: lane (j, n) gets rows 4 j + r = (head 2 j + r / 2,
+            // part r % 2) of token slot0 + 4 n + t
+            float lg[2][4];
 #pragma unroll
-            for (int tau = 0; tau < 4; ++tau)
+            for (int t = 0; t < 4; ++t) {
+                const uint16_t *krow = a.win_k + (head_win + slot0 + 4 * n + t) * D + 8 * j;
+                u32x4 kx[kC];
 #pragma unroll
-                for (int c = 0; c < kC; ++c)
-                    kx[tau][c] = *reinterpret_cast<const u32x4 *>(
-                        wk + (int64_t)score_token(tau, n >> 2, n & 3) * D + 32 * c + 8 * j);
-            const uint16_t *wvp = a.win_v + head_win * D + slot0;
-            u32x4 vx[2][kNT];
+                for (int c = 0; c < kC; ++c) kx[c] = *reinterpret_cast<const u32x4 *>(krow + 32 * c);
+                f32x4 sc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int kc = 0; kc < 2; ++kc)
+                for (int c = 0; c < kC; ++c) sc = mfma16(qa[c], __builtin_bit_cast(bf16x8, kx[c]), sc);
+                const bool ok = (vmask >> (4 * n + t)) & 1u;
+                lg[0][t] = ok ? sc[0] + sc[1] : -INFINITY;
+                lg[1][t] = ok ? sc[2] + sc[3] : -INFINITY;
+            }
+            float m_new[2];
+            bool grow = false;
 #pragma unroll
-                for (int nt = 0; nt < kNT; ++nt)
-                    vx[kc][nt] = *reinterpret_cast<const u32x4 *>(
-                        wvp + (int64_t)(16 * nt + n) * a.win_slots + 32 * kc + 8 * j);
-            f32x4 sc[4];
+            for (int e = 0; e < 2; ++e) {
+                const float mx = row_max16(fmaxf(fmaxf(lg[e][0], lg[e][1]), fmaxf(lg[e][2], lg[e][3])));
+                m_new[e] = fmaxf(m_run[e], mx);
+                grow |= (2 * j + e < G) && m_new[e] > m_run[e];
+            }
+            if (__any(grow)) {
+                float al[2];
 #pragma unroll
-            for (int tau = 0; tau < 4; ++tau) {
-                // A row n of tile tau is token score_token(tau, n / 4, n % 4)
-                const uint32_t keep = valid(score_token(tau, n >> 2, n & 3)) ? 0xFFFFFFFFu : 0u;
-                sc[tau] = f32x4{0.f, 0.f, 0.f, 0.f};
+                for (int e = 0; e < 2; ++e) {
+                    al[e] = m_new[e] == -INFINITY ? 1.0f : fexp2(m_run[e] - m_new[e]);
+                    lsum[e] *= al[e];
+                }
 #pragma unroll
-                for (int c = 0; c < kC; ++c) {
-                    const u32x4 x = {kx[tau][c][0] & keep, kx[tau][c][1] & keep,
-                                     kx[tau][c][2] & keep, kx[tau][c][3] & keep};
-                    const bf16x8 A = __builtin_bit_cast(bf16x8, x);
-                    sc[tau] = mfma16(A, bop(bhi[c]), sc[tau]);
-                    sc[tau] = mfma16(A, bop(blo[c]), sc[tau]);
+                for (int r = 0; r < 4; ++r)
+#pragma unroll
+                    for (int nt = 0; nt < kNT; ++nt) acc[nt][r] *= al[r >> 1];
+            }
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+                m_run[e] = m_new[e];
+                float p[4];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    p[t] = m_run[e] == -INFINITY ? 0.0f : fexp2(lg[e][t] - m_run[e]);
+                    lsum[e] += p[t];
+                }
+                const int g = 2 * j + e;
+                if (g < G) {
+                    uint32_t hi[2], lo[2];
+#pragma unroll
+                    for (int q = 0; q < 2; ++q) {
+                        hi[q] = pack_bf16_rne(p[2 * q], p[2 * q + 1]);
+                        lo[q] = pack_bf16_rne(p[2 * q] - bf16_bits_to_f32(hi[q] & 0xFFFFu),
+                                              p[2 * q + 1] - bf16_bits_to_f32(hi[q] >> 16));
+                    }
+                    lds_write8(lds_addr(tbuf + (2 * g) * 128 + 8 * n), hi[0], hi[1]);
+                    lds_write8(lds_addr(tbuf + (2 * g + 1) * 128 + 8 * n), lo[0], lo[1]);
                 }
             }
-            float lg[4][4];
-            float mloc = -INFINITY;
-#pragma unroll
-            for (int tau = 0; tau < 4; ++tau)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const float v = valid(score_token(tau, j, r)) ? sc[tau][r] : -INFINITY;
-                    lg[tau][r] = v;
-                    mloc = fmaxf(mloc, v);
-                }
-            st.update_max(wave_max_xor_16_32(mloc), j, G);
-            uint32_t aop[2][4];
-#pragma unroll
-            for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-                for (int p = 0; p < 4; ++p) {
-                    float pr[2];
-#pragma unroll
-                    for (int e = 0; e < 2; ++e) {
-                        const int i = 2 * p + e;
-                        pr[e] = fexp2(lg[2 * kc + (i >> 2)][i & 3] - st.m_lane);
-                    }
-                    st.l_lane += pr[0] + pr[1];
-                    uint32_t hi, lo;
-                    split_hi_lo(pr[0], pr[1], hi, lo);
-                    aop[kc][p] = cls == 0 ? hi : (cls == 1 ? lo : 0u);
-                }
+            u32x4 pa[2];
+            pa[0] = lds_read16(a_addr);
+            pa[1] = lds_read16(a_addr + a_step);
+            lds_wait(pa);
+            // P V against the channel-major value slots; dead slots are
+            // zeroed, whatever bits they hold
+            const uint16_t *wvp = a.win_v + head_win * D + slot0;
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc) {
-                const bf16x8 A = bop(aop[kc]);
+                const bf16x8 A = __builtin_bit_cast(bf16x8, pa[kc]);
                 const uint32_t bits8 = (uint32_t)(vmask >> (32 * kc + 8 * j)) & 0xFFu;
                 uint32_t msk[4];
 #pragma unroll
                 for (int p = 0; p < 4; ++p)
                     msk[p] = (((bits8 >> (2 * p)) & 1u) ? 0x0000FFFFu : 0u) |
                              (((bits8 >> (2 * p + 1)) & 1u) ? 0xFFFF0000u : 0u);
+                u32x4 vv[kNT];
+#pragma unroll
+                for (int nt = 0; nt < kNT; ++nt)
+                    vv[nt] = *reinterpret_cast<const u32x4 *>(wvp + (int64_t)(16 * nt + n) * a.win_slots +
+                                                              32 * kc + 8 * j);
 #pragma unroll
                 for (int nt = 0; nt < kNT; ++nt) {
-                    const u32x4 x = vx[kc][nt];
-                    const u32x4 y = {x[0] & msk[0], x[1] & msk[1], x[2] & msk[2], x[3] & msk[3]};
-                    st.acc[nt] = mfma16(A, __builtin_bit_cast(bf16x8, y), st.acc[nt]);
+                    const u32x4 y = {vv[nt][0] & msk[0], vv[nt][1] & msk[1], vv[nt][2] & msk[2],
+                                     vv[nt][3] & msk[3]};
+                    acc[nt] = mfma16(A, __builtin_bit_cast(bf16x8, y), acc[nt]);
+                }
+            }
+        }
+        // result per head g = 2 j + e: rows 4 j + 2 e (hi) and + 1 (lo)
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int g = 2 * j + e;
+            const float lt = row_sum16(lsum[e]);
+            if (g < G) {
+#pragma unroll
+                for (int nt = 0; nt < kNT; ++nt) sC[g][16 * nt + n] = acc[nt][2 * e] + acc[nt][2 * e + 1];
+                if (n == 0) {
+                    sM[wave][g] = m_run[e];
+                    sL[wave][g] = lt;
                 }
             }
         }
     }
-
-    // ---------------------------------------------------- merge the waves
-    // head g: rows g (pages and window hi parts) and g + G (window lo parts)
-    const float l_col = wave_sum_xor_16_32(st.l_lane);
-    const float z_col = wave_sum_xor_16_32(st.z_lane);
-    // this wave's stage reads are complete: every value read was consumed
-    float(*sC)[16][D] = reinterpret_cast<float(*)[16][D]>(lds);
-    auto sCw = [&](int w) -> float(*)[D] { return reinterpret_cast<float(*)[D]>(lds + w * kWaveLds); };
-    {
-        float(*mine)[D] = sCw(wave);
-#pragma unroll
-        for (int nt = 0; nt < kNT; ++nt)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) mine[4 * j + r][16 * nt + n] = st.acc[nt][r] - st.accb[r];
-    }
-    (void)sC;
-    if (lane < G) {
-        sM[wave][lane] = st.m_lane;
-        sL[wave][lane] = l_col;
-        sZ[wave][lane] = z_col;
-    }
     __syncthreads();
 
+    // ---- merge the four waves
     float *part = a.part + (((int64_t)b * a.n_kv + h) * a.n_splits + split) * G * (D + 2);
     for (int idx = tid; idx < G * D; idx += 256) {
         const int gg = idx / D, ch = idx % D;
@@ -669,7 +768,7 @@ __global__ void __launch_bounds__(256, 2) decode_main_kernel(DecodeArgs a)
             for (int w = 0; w < 4; ++w) {
                 if (sM[w][gg] == -INFINITY) continue;
                 const float f = fexp2(sM[w][gg] - mx);
-                o += f * (sCw(w)[gg][ch] + sCw(w)[gg + G][ch] + sZ[w][gg]);
+                o += f * reinterpret_cast<const float(*)[D]>(lds + w * M::kWave)[gg][ch];
                 l += f * sL[w][gg];
             }
         }
@@ -730,32 +829,52 @@ __global__ void __launch_bounds__(D) decode_combine_kernel(const float *part, fl
 // ------------------------------------------------------------------ host
 
 struct DecodePlan {
-    int32_t units_per_wave, n_splits;
-    size_t qt_bytes, part_bytes;
+    int32_t units_per_wave, n_page_splits, n_splits;
+    size_t qt_bytes, limb_bytes, aux_bytes, part_bytes;
 };
 
 static bool make_plan(const wushkv_cache *c, int32_t n_q, int32_t max_seq_len, DecodePlan &p)
 {
     const int32_t G = n_q / c->n_kv_heads;
     const int64_t qpages = max_seq_len > c->s_sink ? (max_seq_len - c->s_sink + kPage - 1) / kPage : 0;
-    const int64_t units = c->win_slots / kPage + qpages;
     const int64_t heads = (int64_t)c->batch * c->n_kv_heads;
-    // about one full residency round of waves (256 CUs x 8 waves), with at
-    // least 2 and at most 32 units per wave so ragged lengths still balance
-    int64_t upw = (units * heads + 2047) / 2048;
+    // about three waves per SIMD over the chip (256 CUs x 4 SIMDs) for the
+    // page scan, at least 2 and at most 32 pages per wave
+    int64_t upw = (qpages * heads + 3071) / 3072;
     if (upw < 2) upw = 2;
     if (upw > 32) upw = 32;
-    int64_t splits = (units + 4 * upw - 1) / (4 * upw);
-    if (splits > kMaxSplits) {
-        upw = (units + 4 * kMaxSplits - 1) / (4 * kMaxSplits);
-        splits = (units + 4 * upw - 1) / (4 * upw);
+    int64_t psplits = (qpages + 4 * upw - 1) / (4 * upw);
+    if (psplits + 1 > kMaxSplits) {
+        upw = (qpages + 4 * (kMaxSplits - 1) - 1) / (4 * (kMaxSplits - 1));
+        psplits = (qpages + 4 * upw - 1) / (4 * upw);
     }
-    if (splits < 1 || splits > kMaxSplits || upw > 0x7FFFFFFF / 4 / kMaxSplits) return false;
+    const int64_t splits = psplits + 1;  // the window workgroup
+    if (splits > kMaxSplits || upw > 0x7FFFFFFF / 4 / kMaxSplits) return false;
     p.units_per_wave = (int32_t)upw;
+    p.n_page_splits = (int32_t)psplits;
     p.n_splits = (int32_t)splits;
     p.qt_bytes = ((size_t)c->batch * n_q * c->head_dim * 4 + 255) / 256 * 256;
+    p.limb_bytes = (size_t)c->batch * n_q * kLimbs * 128;
+    p.aux_bytes = ((size_t)c->batch * n_q * 16 + 255) / 256 * 256;
     p.part_bytes = (size_t)heads * splits * G * (c->head_dim + 2) * 4;
     return true;
+}
+
+template <int D, int BITS, int G>
+static void launch_main(dim3 grid, hipStream_t s, const DecodeArgs &a)
+{
+    hipLaunchKernelGGL((decode_main_kernel<D, BITS, G>), grid, dim3(256), 0, s, a);
+}
+
+template <int D, int BITS>
+static void launch_main_g(int G, dim3 grid, hipStream_t s, const DecodeArgs &a)
+{
+    switch (G) {
+        case 1: launch_main<D, BITS, 1>(grid, s, a); break;
+        case 2: launch_main<D, BITS, 2>(grid, s, a); break;
+        case 4: launch_main<D, BITS, 4>(grid, s, a); break;
+        default: launch_main<D, BITS, 8>(grid, s, a); break;
+    }
 }
 
 }  // namespace wushkv
@@ -780,7 +899,7 @@ extern "C" size_t wushkv_decode_workspace_bytes(const wushkv_cache *c, int32_t n
     if (check_decode_args(c, n_q_heads, max_seq_len) != WUSHKV_OK) return 0;
     DecodePlan p;
     if (!make_plan(c, n_q_heads, max_seq_len, p)) return 0;
-    return p.qt_bytes + p.part_bytes;
+    return p.qt_bytes + p.limb_bytes + p.aux_bytes + p.part_bytes;
 }
 
 extern "C" int wushkv_decode_attention(const wushkv_cache *c, const uint16_t *q, int32_t n_q_heads,
@@ -796,12 +915,15 @@ extern "C" int wushkv_decode_attention(const wushkv_cache *c, const uint16_t *q,
     if (!(sm_scale > 0.0f) || sm_scale == INFINITY) return WUSHKV_EINVAL;
     DecodePlan p;
     if (!make_plan(c, n_q_heads, max_seq_len, p)) return WUSHKV_EINVAL;
-    if (workspace_bytes < p.qt_bytes + p.part_bytes) return WUSHKV_EWORKSPACE;
+    if (workspace_bytes < p.qt_bytes + p.limb_bytes + p.aux_bytes + p.part_bytes) return WUSHKV_EWORKSPACE;
 
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const int32_t G = n_q_heads / c->n_kv_heads;
-    float *qt = reinterpret_cast<float *>(workspace);
-    float *part = reinterpret_cast<float *>(reinterpret_cast<uint8_t *>(workspace) + p.qt_bytes);
+    uint8_t *ws = reinterpret_cast<uint8_t *>(workspace);
+    float *qt = reinterpret_cast<float *>(ws);
+    uint8_t *qlimb = ws + p.qt_bytes;
+    uint32_t *qaux = reinterpret_cast<uint32_t *>(ws + p.qt_bytes + p.limb_bytes);
+    float *part = reinterpret_cast<float *>(ws + p.qt_bytes + p.limb_bytes + p.aux_bytes);
 
     DecodeArgs a{};
     a.pages = c->pages;
@@ -815,13 +937,13 @@ extern "C" int wushkv_decode_attention(const wushkv_cache *c, const uint16_t *q,
     a.win_slots = c->win_slots;
     a.max_pages = c->max_pages_per_seq;
     a.n_pages = c->n_pages;
-    a.G = G;
     a.n_q = n_q_heads;
     a.units_per_wave = p.units_per_wave;
+    a.n_page_splits = p.n_page_splits;
     a.n_splits = p.n_splits;
-    a.wk = widen_masks(c->bits);
-    a.wv = widen_masks_f16(c->bits);
     a.qt = qt;
+    a.qlimb = qlimb;
+    a.qaux = qaux;
     a.part = part;
 
     const dim3 gq(c->n_kv_heads, c->batch);
@@ -831,16 +953,20 @@ extern "C" int wushkv_decode_attention(const wushkv_cache *c, const uint16_t *q,
     const int key = c->head_dim * 10 + c->bits;
 
     timing_begin("decode_qt_kernel", s);
-    if (c->head_dim == 128) hipLaunchKernelGGL(decode_qt_kernel<128>, gq, dim3(256), 0, s, q, t_k_inv, qt, c->n_kv_heads, G, scale);
-    else hipLaunchKernelGGL(decode_qt_kernel<64>, gq, dim3(256), 0, s, q, t_k_inv, qt, c->n_kv_heads, G, scale);
+    switch (key) {
+        case 1282: hipLaunchKernelGGL((decode_qt_kernel<128, 2>), gq, dim3(256), 0, s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
+        case 1284: hipLaunchKernelGGL((decode_qt_kernel<128, 4>), gq, dim3(256), 0, s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
+        case 642: hipLaunchKernelGGL((decode_qt_kernel<64, 2>), gq, dim3(256), 0, s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
+        case 644: hipLaunchKernelGGL((decode_qt_kernel<64, 4>), gq, dim3(256), 0, s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
+    }
     timing_end(s);
 
     timing_begin("decode_main_kernel", s);
     switch (key) {
-        case 1282: hipLaunchKernelGGL((decode_main_kernel<128, 2>), gm, dim3(256), 0, s, a); break;
-        case 1284: hipLaunchKernelGGL((decode_main_kernel<128, 4>), gm, dim3(256), 0, s, a); break;
-        case 642: hipLaunchKernelGGL((decode_main_kernel<64, 2>), gm, dim3(256), 0, s, a); break;
-        case 644: hipLaunchKernelGGL((decode_main_kernel<64, 4>), gm, dim3(256), 0, s, a); break;
+        case 1282: launch_main_g<128, 2>(G, gm, s, a); break;
+        case 1284: launch_main_g<128, 4>(G, gm, s, a); break;
+        case 642: launch_main_g<64, 2>(G, gm, s, a); break;
+        case 644: launch_main_g<64, 4>(G, gm, s, a); break;
     }
     timing_end(s);
 

@@ -3,11 +3,14 @@ in include/wushkv.h (not from the kernels), so a layout slip on the GPU side
 shows up as a parity failure rather than cancelling out.
 
 One (page, head) block: K code words, V code words, K params, V params.
-A word holds B = 32 / bits elements; element e sits at bit
-16 * (e % 2) + bits * (e // 2) and is slot i = e % 8 of operand o = e // 8.
-Lane L = 16 j + m owns 4 nw consecutive words, nw = d * bits / 128.
-  K word L*4nw + tau*nw + w : token 32(tau//2) + 8(m//4) + 4(tau%2) + m%4,
-                              channel 32 c + 8 j + i, c = w (B/8) + o
+A word holds B = 32 / bits codes.
+K: lane L = 16 j + n (j < d / 32) owns 4 bits consecutive words;
+  K word L*4bits + bits*t + w, code e = h (B/2) + i (h = 0, 1; i < B/2) at
+  bit 2 bits i + bits h : token 4 n + t, channel 32 j + B w + e
+V: element e is slot i = e % 8 of operand o = e // 8 and sits at bit
+  16 * (i % 2) + F(o, i // 2) with F = (6, 10, 8, 12 | 2, 0, 4, 14) for
+  2-bit operands 0 | 1 and (4, 0, 8, 12) for 4-bit.  Lane L = 16 j + m owns
+  4 nw consecutive words, nw = d * bits / 128.
   V word L*4nw + kc*2nw + u : token 32 kc + 8 j + i,
                               channel 16 nt + m, nt = u (B/8) + o
 """
@@ -24,9 +27,17 @@ def page_bytes(d: int, bits: int) -> int:
     return PAGE * (2 * d * bits // 8 + 8)
 
 
+def _v_field(bits: int, o: int, r: int) -> int:
+    """Bit of the low-half code of register r of operand o in a V word."""
+    if bits == 2:
+        return (6, 10, 8, 12)[r] if o == 0 else (2, 0, 4, 14)[r]
+    return (4, 0, 8, 12)[r]
+
+
 @functools.lru_cache(maxsize=None)
 def _maps(d: int, bits: int):
-    """For every (word, element): (token, channel, bit) for K and for V."""
+    """For every (word, element): (token, channel) for K and for V, and the
+    bit of each element (K and V order their elements differently)."""
     B = 32 // bits
     nw = d * bits // 128
     ops = B // 8
@@ -35,17 +46,18 @@ def _maps(d: int, bits: int):
     kc_ = np.empty((n_words, B), np.int64)
     vt = np.empty((n_words, B), np.int64)
     vc_ = np.empty((n_words, B), np.int64)
-    bit = np.array([16 * (e % 2) + bits * (e // 2) for e in range(B)], np.int64)
+    kbit = np.array([2 * bits * (e % (B // 2)) + bits * (e // (B // 2)) for e in range(B)], np.int64)
+    vbit = np.array([16 * (e % 2) + _v_field(bits, e // 8, (e % 8) // 2) for e in range(B)], np.int64)
+    for L in range(d // 2):
+        j, n = divmod(L, 16)
+        for t in range(4):
+            for w in range(bits):
+                widx = L * 4 * bits + bits * t + w
+                for e in range(B):
+                    kt[widx, e] = 4 * n + t
+                    kc_[widx, e] = 32 * j + B * w + e
     for L in range(64):
         j, m = divmod(L, 16)
-        for tau in range(4):
-            for w in range(nw):
-                widx = L * 4 * nw + tau * nw + w
-                for e in range(B):
-                    o, i = divmod(e, 8)
-                    c = w * ops + o
-                    kt[widx, e] = 32 * (tau // 2) + 8 * (m // 4) + 4 * (tau % 2) + m % 4
-                    kc_[widx, e] = 32 * c + 8 * j + i
         for kc in range(2):
             for u in range(2 * nw):
                 widx = L * 4 * nw + kc * 2 * nw + u
@@ -54,7 +66,7 @@ def _maps(d: int, bits: int):
                     nt = u * ops + o
                     vt[widx, e] = 32 * kc + 8 * j + i
                     vc_[widx, e] = 16 * nt + m
-    return kt, kc_, vt, vc_, bit
+    return kt, kc_, vt, vc_, kbit, vbit
 
 
 def decode_block(block: np.ndarray, d: int, bits: int):
@@ -63,14 +75,14 @@ def decode_block(block: np.ndarray, d: int, bits: int):
     (scale, zero)."""
     block = np.ascontiguousarray(block, dtype=np.uint8)
     region = 8 * d * bits
-    kt, kch, vt, vch, bit = _maps(d, bits)
+    kt, kch, vt, vch, kbit, vbit = _maps(d, bits)
     mask = (1 << bits) - 1
     kw = block[:region].view("<u4").astype(np.int64)
     vw = block[region:2 * region].view("<u4").astype(np.int64)
     kcodes = np.full((PAGE, d), -1, np.int64)
     vcodes = np.full((PAGE, d), -1, np.int64)
-    kcodes[kt, kch] = (kw[:, None] >> bit[None, :]) & mask
-    vcodes[vt, vch] = (vw[:, None] >> bit[None, :]) & mask
+    kcodes[kt, kch] = (kw[:, None] >> kbit[None, :]) & mask
+    vcodes[vt, vch] = (vw[:, None] >> vbit[None, :]) & mask
     assert (kcodes >= 0).all() and (vcodes >= 0).all(), "layout map is not a bijection"
     prm = block[2 * region:2 * region + 8 * PAGE].view("<u2").reshape(2, PAGE, 2)
     return kcodes.astype(np.uint8), vcodes.astype(np.uint8), prm[0].copy(), prm[1].copy()
@@ -79,9 +91,9 @@ def decode_block(block: np.ndarray, d: int, bits: int):
 def encode_block(kcodes, vcodes, kparams, vparams, d: int, bits: int) -> np.ndarray:
     """Inverse of decode_block (used to check the maps form a bijection)."""
     region = 8 * d * bits
-    kt, kch, vt, vch, bit = _maps(d, bits)
-    kw = (np.asarray(kcodes, np.int64)[kt, kch] << bit[None, :]).sum(axis=1)
-    vw = (np.asarray(vcodes, np.int64)[vt, vch] << bit[None, :]).sum(axis=1)
+    kt, kch, vt, vch, kbit, vbit = _maps(d, bits)
+    kw = (np.asarray(kcodes, np.int64)[kt, kch] << kbit[None, :]).sum(axis=1)
+    vw = (np.asarray(vcodes, np.int64)[vt, vch] << vbit[None, :]).sum(axis=1)
     out = np.zeros(page_bytes(d, bits), np.uint8)
     out[:region] = kw.astype("<u4").view(np.uint8)
     out[region:2 * region] = vw.astype("<u4").view(np.uint8)

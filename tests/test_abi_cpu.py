@@ -20,7 +20,7 @@ def test_exports_every_declared_function():
     L = _lib.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert wk.wushkv_abi_version() == 1
+    assert wk.wushkv_abi_version() == 2
 
 
 @pytest.mark.parametrize("d,bits", [(64, 2), (64, 4), (128, 2), (128, 4)])
@@ -104,12 +104,14 @@ def test_call_specific_validation():
 def test_workspace_bytes_closed_form():
     L = _lib.lib()
     d = _desc()
-    # q~: batch * n_q * d * 4 rounded up to 256; partials: one (o[d], m, l)
-    # per (sequence, kv head, split, query head of the group).  Units per
-    # (sequence, head): 192/64 window units + ceil((1000 - 4)/64) pages = 19;
-    # 2 units per wave, 8 per four-wave split -> 3 splits.
+    # q~: batch * n_q * d * 4 rounded up to 256; six 128-byte fp8 limbs and
+    # 16 bytes of scales and sum per query head (the latter rounded up to
+    # 256); partials: one (o[d], m, l) per (sequence, kv head, split, query
+    # head of the group).  ceil((1000 - 4)/64) = 16 pages per (sequence,
+    # head), 2 per wave, 8 per four-wave workgroup -> 2 page splits, plus the
+    # window workgroup -> 3 splits.
     ws = L.wushkv_decode_workspace_bytes(ctypes.byref(d), 8, 1000)
-    assert ws == 2 * 8 * 128 * 4 + (2 * 2) * 3 * 4 * (128 + 2) * 4
+    assert ws == 2 * 8 * 128 * 4 + 2 * 8 * 6 * 128 + 256 + (2 * 2) * 3 * 4 * (128 + 2) * 4
 
 
 @pytest.mark.parametrize("d,bits", [(64, 2), (64, 4), (128, 2), (128, 4)])
@@ -126,17 +128,21 @@ def test_layout_maps_are_bijections(d, bits):
 
 
 def test_layout_first_words_as_documented():
-    # K word 0 (lane 0, tile 0): token 0, channels 0..7 then 32..39 (2-bit),
-    # even channels in the low half word.  V word 0: channel 0, tokens 0..7
-    # of the first N-tile and channel 16 for the second operand.
+    # K word 0 (lane 0, tile 0): token 0, channels 0..15 (2-bit); channel
+    # 8 h + i at bit 4 i + 2 h.  Lane 17 = (j 1, n 1) holds tokens 4..7 and
+    # channels 32..63.  V word 0: channel 0, tokens 0..7 of the first N-tile
+    # and channel 16 for the second operand.
     d, bits = 128, 2
     kc = np.zeros((64, d), np.int64)
-    kc[0, 2] = 3   # element e = 2 -> bit 2
-    kc[0, 33] = 1  # channel 33: operand 1, slot 1 -> element 9 -> bit 16 + 8 = 24
+    kc[0, 2] = 3   # i = 2, h = 0 -> bit 8
+    kc[0, 9] = 1   # i = 1, h = 1 -> bit 6
+    kc[4, 40] = 2  # token 4: lane 17, tile 0; channel 40: word 0, i = 0, h = 1 -> bit 2
     vc = np.zeros((64, d), np.int64)
-    vc[5, 16] = 2  # token 5 slot 5, channel 16: operand 1 -> element 13 -> bit 16 + 12
+    vc[5, 16] = 2  # token 5 slot 5, channel 16: operand 1, register 2, high half -> bit 16 + 4
     blk = pagelayout.encode_block(kc, vc, np.zeros((64, 2)), np.zeros((64, 2)), d, bits)
     w = blk[:8 * d * bits].view("<u4")
-    assert w[0] == (3 << 2) | (1 << 24)
+    assert w[0] == (3 << 8) | (1 << 6)
+    assert w[17 * 8] == 2 << 2
+    assert np.count_nonzero(w) == 2
     vw = blk[8 * d * bits:16 * d * bits].view("<u4")
-    assert vw[0] == 2 << 28
+    assert vw[0] == 2 << 20
