@@ -266,7 +266,9 @@ def main():
     step_gbs = (tot_main + tot_other + tot_app) / K / (ms_graph * 1e-3) / 1e9
     log("graph step: %.2f us, %.1f GB/s" % (ms_graph * 1e3, step_gbs))
 
-    # ---- eager steps with per-launch kernel timing (roofline of the decode kernel)
+    # ---- eager steps with per-launch kernel timing (roofline of the decode
+    # kernel): the library launches each kernel with a start/stop event pair
+    # that the runtime stamps at that kernel's start and end
     wk.wushkv_timing_enable(8 * 64)
     KT = 64
     e0.record()
@@ -277,7 +279,7 @@ def main():
     ms_eager = e0.elapsed_time(e1) / KT
     kernels = {}
     for name in ("decode_main_kernel", "decode_qt_kernel", "decode_combine_kernel",
-                 "append_kernel", "append_commit_kernel"):
+                 "append_step_kernel", "append_kernel", "append_commit_kernel"):
         n, tot = wk.wushkv_timing_read(name)
         kernels[name] = (tot / n) if n else None
     wk.wushkv_timing_enable(0)
@@ -354,7 +356,8 @@ def main():
                      "traffic": profiled_traffic("decode_main_kernel_llama8b_2bit.md",
                                                  os.path.join(ROOT, "paper_2609_38121_amd", "csrc")),
                      "avg_us": round(t_main * 1e3, 3),
-                     "bytes_per_launch": int(main_per_launch)},
+                     "bytes_per_launch": int(main_per_launch),
+                     "timing": "HIP start/stop events of each launch (hipExtLaunchKernelGGL)"},
         "cpu_baseline": cpu,
         "decode_call_gbps": round(dec_gbs, 2),
         "decode_call_us": round(ms_dec * 1e3, 3),

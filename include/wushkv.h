@@ -86,13 +86,16 @@ enum {
  *   Reconstruction of a stored entry: x = scale * code + zero (fp32 fma).
  *
  *   Code words.  Both code regions are arrays of little-endian 32-bit
- *   words; a word holds B = 32 / bits codes.
+ *   words; a word holds B = 32 / bits codes.  Each region is a sequence of
+ *   16-byte chunks: chunk q holds words 4q .. 4q+3 of every "lane" in lane
+ *   order, so the k-th word of lane L is word (k / 4) * 4 * lanes + 4 L +
+ *   k % 4 of the region (lanes = 16 * head_dim / 32 for K, 64 for V).
  *
- *   K region: 16 * head_dim / 32 "lanes" L = 16 j + n (j < head_dim / 32,
- *   n = 0..15) of 4 * bits words each.  K word L * 4 bits + bits * t + w
- *   (t = 0..3, w = 0..bits-1) holds token 4 n + t, channels
- *   32 j + B w + e for e = 0..B-1; code e = h * B/2 + i (h = 0, 1) sits at
- *   bit 2 * bits * i + bits * h.  A mask then spreads a word, or the word
+ *   K region: lanes L = 16 j + n (j < head_dim / 32, n = 0..15) of
+ *   4 * bits words each.  Word k = bits * t + w of lane L (t = 0..3,
+ *   w = 0..bits-1) holds token 4 n + t, channels 32 j + B w + e for
+ *   e = 0..B-1; code e = h * B/2 + i (h = 0, 1) sits at bit
+ *   2 * bits * i + bits * h.  A mask then spreads a word, or the word
  *   shifted right by bits, into one code per nibble (2-bit) or per byte
  *   (4-bit): the fp4 / fp8 operands of the decode kernel's scaled matrix
  *   instruction.
@@ -103,8 +106,8 @@ enum {
  *   operand 0 and (2, 0, 4, 14) for operand 1 of a 2-bit word, F =
  *   (4, 0, 8, 12) for a 4-bit word (one operand).  With
  *   nw = head_dim * bits / 128, the region holds 64 lanes L = 16 j + m
- *   (j = 0..3, m = 0..15) of 4 nw words each;
- *   V word at index L * 4nw + kc * 2nw + u   (kc = 0..1, u = 0..2nw-1)
+ *   (j = 0..3, m = 0..15) of 4 nw words each; word k = kc * 2nw + u of
+ *   lane L (kc = 0..1, u = 0..2nw-1) holds
  *     token    32 kc + 8 j + i
  *     channel  16 nt + m,  nt = u * (B / 8) + o
  *   (the operand order of the 16x16x32 fp16 product: a few shifts and one
@@ -226,9 +229,10 @@ const char *wushkv_status_string(int status);
 int wushkv_abi_version(void);
 
 /*
- * Kernel timing for measurement.  While enabled (slots > 0), every launch
- * the library makes is bracketed by a pair of HIP events on its stream, for
- * up to `slots` launches; disabling (slots = 0) releases the events.  This
+ * Kernel timing for measurement.  While enabled (slots > 0), each of the
+ * next `slots` launches the library makes records a pair of HIP events on
+ * its stream that the runtime stamps when that kernel starts and when it
+ * ends (hipExtLaunchKernelGGL); disabling (slots = 0) releases them.  This
  * is the only library state and it is not thread-safe; leave it off in
  * production.  wushkv_timing_read synchronises on the recorded events and
  * returns, for launches whose kernel name contains `name_substr` (all

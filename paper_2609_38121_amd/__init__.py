@@ -59,8 +59,9 @@ def wushkv_timing_enable(slots: int) -> None:
 
 
 def wushkv_timing_read(name_substr: str = ""):
-    """(launch count, summed milliseconds) of recorded launches whose kernel
-    name contains name_substr; clears the record."""
+    """(launch count, summed milliseconds per launch) of recorded launches
+    whose kernel name contains name_substr; reading does not clear the
+    record (re-enabling does)."""
     cnt = ctypes.c_int32()
     ms = ctypes.c_double()
     check(_lib.lib().wushkv_timing_read(name_substr.encode(), ctypes.byref(cnt),

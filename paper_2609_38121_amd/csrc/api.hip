@@ -15,27 +15,19 @@ struct Timing {
     std::vector<const char *> names;   // per slot
     int slots = 0;
     int used = 0;
-    bool open = false;                 // a begin without its end
 };
 Timing g_timing;
 
 }  // namespace
 
-void timing_begin(const char *name, hipStream_t s)
+TimedLaunch timing_slot(const char *name)
 {
     Timing &t = g_timing;
-    if (t.slots == 0 || t.used >= t.slots) return;
-    if (hipEventRecord(t.ev[2 * t.used], s) != hipSuccess) return;
+    if (t.slots == 0 || t.used >= t.slots) return TimedLaunch{};
     t.names[t.used] = name;
-    t.open = true;
-}
-
-void timing_end(hipStream_t s)
-{
-    Timing &t = g_timing;
-    if (!t.open) return;
-    t.open = false;
-    if (hipEventRecord(t.ev[2 * t.used + 1], s) == hipSuccess) t.used += 1;
+    const TimedLaunch r{t.ev[2 * t.used], t.ev[2 * t.used + 1]};
+    t.used += 1;
+    return r;
 }
 
 }  // namespace wushkv
@@ -101,7 +93,6 @@ extern "C" int wushkv_timing_enable(int32_t slots)
     t.names.clear();
     t.slots = 0;
     t.used = 0;
-    t.open = false;
     if (slots <= 0) return WUSHKV_OK;
     if (slots > (1 << 20)) return WUSHKV_EINVAL;
     t.ev.resize(2 * (size_t)slots);

@@ -173,6 +173,112 @@ __device__ void order_stats(const uint16_t *row, int lo, float &a_lo, float &a_h
     else order_stats_rank<D>(row, lo, a_lo, a_hi, mn, mx);
 }
 
+// Phases B and C of a tile of up to 64 positions starting at blk_lo, all in
+// one page (pg, or null when the page is outside the pool): quantise every
+// position p with quant(p) from its bf16 rows in kt / vt (row p - blk_lo),
+// write its parameters and key words, then assemble the value words, merging
+// words only partly covered with what the page holds.  Every thread of the
+// workgroup must call it (it synchronises).
+template <int D, int BITS, typename Pred>
+__device__ void quantise_tile(const AppendArgs &a, const uint16_t *kt, const uint16_t *vt,
+                              uint8_t *vcodes, int32_t blk_lo, Pred quant, uint8_t *pg, int tid)
+{
+    using L = Layout<D, BITS>;
+    constexpr int kPitch = D + 8;
+    // ---- phase B: quantise (threads 0-63 keys, 64-127 values)
+    if (tid < 2 * kPage) {
+        const bool is_v = tid >= kPage;
+        const int r = tid & (kPage - 1);
+        const int32_t p = blk_lo + r;
+        if (quant(p) && pg != nullptr) {
+            const uint16_t *row = (is_v ? vt : kt) + r * kPitch;
+            const int qlo = is_v ? a.lo_v : a.lo_k;
+            const float qt = is_v ? a.t_v : a.t_k;
+            float a_lo, a_hi, mn, mx;
+            order_stats<D, BITS>(row, qlo, a_lo, a_hi, mn, mx);
+            uint32_t s16, z16;
+            float z, inv;
+            constexpr int kLevels = (1 << BITS) - 1;
+            quant_params(a_lo, a_hi, qt, qlo + 1 < D, mn, mx, kLevels, s16, z16, z, inv);
+            *reinterpret_cast<uint32_t *>(pg + L::kParamOffset + 4 * r + (is_v ? 4 * kPage : 0)) =
+                s16 | (z16 << 16);
+            if (!is_v) {
+                // key words of this token: lane group jj = ch / 32 holds
+                // BITS words per token (see Layout::k_pos)
+                uint32_t kw[D / 32][BITS];
+#pragma unroll
+                for (int jj = 0; jj < D / 32; ++jj)
+#pragma unroll
+                    for (int w = 0; w < BITS; ++w) kw[jj][w] = 0u;
+#pragma unroll
+                for (int c8 = 0; c8 < D / 8; ++c8) {
+                    uint4 v = *reinterpret_cast<const uint4 *>(row + 8 * c8);
+                    uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        uint32_t hb = (i & 1) ? (wv[i >> 1] >> 16) : (wv[i >> 1] & 0xFFFFu);
+                        uint32_t code = code_of(bf16_bits_to_f32(hb), z, inv, (float)kLevels);
+                        int word, bit;
+                        L::k_pos(r, 8 * c8 + i, word, bit);
+                        kw[(8 * c8 + i) >> 5][((8 * c8 + i) & 31) / (32 / BITS)] |= code << bit;
+                    }
+                }
+                uint32_t *kreg = reinterpret_cast<uint32_t *>(pg);
+#pragma unroll
+                for (int jj = 0; jj < D / 32; ++jj)
+#pragma unroll
+                    for (int w = 0; w < BITS; ++w)
+                        kreg[L::k_word(16 * jj + (r >> 2), BITS * (r & 3) + w)] = kw[jj][w];
+            } else {
+#pragma unroll
+                for (int c8 = 0; c8 < D / 8; ++c8) {
+                    uint4 v = *reinterpret_cast<const uint4 *>(row + 8 * c8);
+                    uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+                    uint32_t lo4 = 0, hi4 = 0;
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        uint32_t hb = (i & 1) ? (wv[i >> 1] >> 16) : (wv[i >> 1] & 0xFFFFu);
+                        uint32_t code = code_of(bf16_bits_to_f32(hb), z, inv, (float)kLevels);
+                        if (i < 4) lo4 |= code << (8 * i);
+                        else hi4 |= code << (8 * (i - 4));
+                    }
+                    *reinterpret_cast<uint2 *>(vcodes + r * D + 8 * c8) = make_uint2(lo4, hi4);
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    // ---- phase C: value-code words
+    if (pg != nullptr) {
+        uint32_t *vreg = reinterpret_cast<uint32_t *>(pg + L::kRegionBytes);
+        constexpr int kWords = 64 * L::kWordsPerLane;
+        for (int idx = tid; idx < kWords; idx += 256) {
+            const int Ln = idx / L::kWordsPerLane, rem = idx % L::kWordsPerLane;
+            const int kc = rem / (2 * L::kNw), u = rem % (2 * L::kNw);
+            const int widx = L::v_word(Ln, rem);
+            const int j = Ln >> 4, m = Ln & 15;
+            uint32_t mask = 0, bits = 0;
+#pragma unroll
+            for (int e = 0; e < L::kCodesPerWord; ++e) {
+                const int o = e >> 3, i = e & 7;
+                const int t = 32 * kc + 8 * j + i;
+                const int32_t p = blk_lo + t;
+                if (quant(p)) {
+                    const int ch = 16 * (u * L::kOpsPerWord + o) + m;
+                    const int bit = L::v_bit(o, i);
+                    mask |= ((1u << BITS) - 1u) << bit;
+                    bits |= (uint32_t)vcodes[t * D + ch] << bit;
+                }
+            }
+            if (mask == 0u) continue;
+            if (mask != 0xFFFFFFFFu) bits |= vreg[widx] & ~mask;
+            vreg[widx] = bits;
+        }
+    }
+
+}
+
 template <int D, int BITS>
 __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
 {
@@ -313,96 +419,9 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
     const int32_t page = sh_page;
     uint8_t *pg = page >= 0 ? a.pages + ((int64_t)page * a.n_kv + h) * L::kPageBytes : nullptr;
 
-    // ---- phase B: quantise (threads 0-63 keys, 64-127 values)
-    if (tid < 2 * kPage) {
-        const bool is_v = tid >= kPage;
-        const int r = tid & (kPage - 1);
-        const int32_t p = blk_lo + r;
-        if (p >= lo && p < hi && quant_now(p) && pg != nullptr) {
-            const uint16_t *row = (is_v ? vt : kt) + r * kPitch;
-            const int qlo = is_v ? a.lo_v : a.lo_k;
-            const float qt = is_v ? a.t_v : a.t_k;
-            float a_lo, a_hi, mn, mx;
-            order_stats<D, BITS>(row, qlo, a_lo, a_hi, mn, mx);
-            uint32_t s16, z16;
-            float z, inv;
-            constexpr int kLevels = (1 << BITS) - 1;
-            quant_params(a_lo, a_hi, qt, qlo + 1 < D, mn, mx, kLevels, s16, z16, z, inv);
-            *reinterpret_cast<uint32_t *>(pg + L::kParamOffset + 4 * r + (is_v ? 4 * kPage : 0)) =
-                s16 | (z16 << 16);
-            if (!is_v) {
-                // key words of this token: lane group jj = ch / 32 holds
-                // BITS words per token (see Layout::k_pos)
-                uint32_t kw[D / 32][BITS];
-#pragma unroll
-                for (int jj = 0; jj < D / 32; ++jj)
-#pragma unroll
-                    for (int w = 0; w < BITS; ++w) kw[jj][w] = 0u;
-#pragma unroll
-                for (int c8 = 0; c8 < D / 8; ++c8) {
-                    uint4 v = *reinterpret_cast<const uint4 *>(row + 8 * c8);
-                    uint32_t wv[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-                    for (int i = 0; i < 8; ++i) {
-                        uint32_t hb = (i & 1) ? (wv[i >> 1] >> 16) : (wv[i >> 1] & 0xFFFFu);
-                        uint32_t code = code_of(bf16_bits_to_f32(hb), z, inv, (float)kLevels);
-                        int word, bit;
-                        L::k_pos(r, 8 * c8 + i, word, bit);
-                        kw[(8 * c8 + i) >> 5][((8 * c8 + i) & 31) / (32 / BITS)] |= code << bit;
-                    }
-                }
-                uint32_t *kreg = reinterpret_cast<uint32_t *>(pg);
-#pragma unroll
-                for (int jj = 0; jj < D / 32; ++jj)
-#pragma unroll
-                    for (int w = 0; w < BITS; ++w)
-                        kreg[(16 * jj + (r >> 2)) * L::kKWordsPerLane + BITS * (r & 3) + w] = kw[jj][w];
-            } else {
-#pragma unroll
-                for (int c8 = 0; c8 < D / 8; ++c8) {
-                    uint4 v = *reinterpret_cast<const uint4 *>(row + 8 * c8);
-                    uint32_t wv[4] = {v.x, v.y, v.z, v.w};
-                    uint32_t lo4 = 0, hi4 = 0;
-#pragma unroll
-                    for (int i = 0; i < 8; ++i) {
-                        uint32_t hb = (i & 1) ? (wv[i >> 1] >> 16) : (wv[i >> 1] & 0xFFFFu);
-                        uint32_t code = code_of(bf16_bits_to_f32(hb), z, inv, (float)kLevels);
-                        if (i < 4) lo4 |= code << (8 * i);
-                        else hi4 |= code << (8 * (i - 4));
-                    }
-                    *reinterpret_cast<uint2 *>(vcodes + r * D + 8 * c8) = make_uint2(lo4, hi4);
-                }
-            }
-        }
-    }
-    __syncthreads();
-
-    // ---- phase C: value-code words
-    if (pg != nullptr) {
-        uint32_t *vreg = reinterpret_cast<uint32_t *>(pg + L::kRegionBytes);
-        constexpr int kWords = 64 * L::kWordsPerLane;
-        for (int widx = tid; widx < kWords; widx += 256) {
-            const int Ln = widx / L::kWordsPerLane, rem = widx % L::kWordsPerLane;
-            const int kc = rem / (2 * L::kNw), u = rem % (2 * L::kNw);
-            const int j = Ln >> 4, m = Ln & 15;
-            uint32_t mask = 0, bits = 0;
-#pragma unroll
-            for (int e = 0; e < L::kCodesPerWord; ++e) {
-                const int o = e >> 3, i = e & 7;
-                const int t = 32 * kc + 8 * j + i;
-                const int32_t p = blk_lo + t;
-                if (p >= lo && p < hi && quant_now(p)) {
-                    const int ch = 16 * (u * L::kOpsPerWord + o) + m;
-                    const int bit = L::v_bit(o, i);
-                    mask |= ((1u << BITS) - 1u) << bit;
-                    bits |= (uint32_t)vcodes[t * D + ch] << bit;
-                }
-            }
-            if (mask == 0u) continue;
-            if (mask != 0xFFFFFFFFu) bits |= vreg[widx] & ~mask;
-            vreg[widx] = bits;
-        }
-    }
+    // ---- phases B and C
+    quantise_tile<D, BITS>(a, kt, vt, vcodes, blk_lo, [&](int32_t p) { return p >= lo && p < hi && quant_now(p); },
+                           pg, tid);
 
     // ---- phase D: bf16 windows and the optional k~ output
     {
@@ -431,6 +450,137 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
     }
 }
 
+// Appends of at most kStepMax tokens per sequence (decode steps): one
+// workgroup per (kv head, sequence).  The new keys are transformed as
+// matrix-vector products (each thread one output channel over D / kParts
+// inputs, the parts summed across neighbouring lanes, fp32, rounded once to
+// bf16) into LDS; then the newly eligible positions are quantised page by
+// page from the ring or from those new rows (quantise_tile); last, the new
+// tokens that stay bf16 are written to the windows.  Reading the flushed
+// ring slots before writing the new ones makes the order independent of the
+// ring's length.
+constexpr int kStepMax = 16;
+
+template <int D, int BITS>
+__global__ void __launch_bounds__(256) append_step_kernel(AppendArgs a)
+{
+    using L = Layout<D, BITS>;
+    constexpr int kPitch = D + 8;
+    constexpr int kParts = 256 / D;   // threads per output channel
+    constexpr int kIn = D / kParts;   // inputs per thread
+    __shared__ __attribute__((aligned(16))) uint16_t kn[kStepMax * kPitch];
+    __shared__ __attribute__((aligned(16))) uint16_t kt[kPage * kPitch];
+    __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * kPitch];
+    __shared__ __attribute__((aligned(16))) uint8_t vcodes[kPage * D];
+    __shared__ float kin[D];
+    __shared__ int32_t sh_page;
+
+    const int tid = threadIdx.x;
+    const int h = blockIdx.x, b = blockIdx.y;
+    const int32_t s_old = a.seq_len[b];
+    const int32_t q_old = a.quant_end[b];
+    int32_t nn = a.n_new[b];
+    nn = nn < 0 ? 0 : (nn > a.max_new ? a.max_new : nn);
+    const int32_t s_new = s_old + nn;
+    const int32_t q_new = next_quant_end(s_new, q_old, a.s_sink, a.s_keep, a.s_flush);
+    const int32_t start_old = q_old > a.s_sink ? q_old : a.s_sink;
+    const int32_t ring = a.win_slots - a.s_sink;
+    const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;
+    auto new_row = [&](auto *base, int32_t p) {
+        return base + (((int64_t)b * a.max_new + (p - s_old)) * a.n_kv + h) * D;
+    };
+
+    // ---- transformed new keys -> kn
+    const int o = tid / kParts, part = tid % kParts;
+    uint32_t trow[kIn / 2];
+    {
+        const uint16_t *src = a.tk + ((int64_t)h * D + o) * D + part * kIn;
+#pragma unroll
+        for (int q = 0; q < kIn / 8; ++q) {
+            const uint4 v = *reinterpret_cast<const uint4 *>(src + 8 * q);
+            trow[4 * q + 0] = v.x;
+            trow[4 * q + 1] = v.y;
+            trow[4 * q + 2] = v.z;
+            trow[4 * q + 3] = v.w;
+        }
+    }
+    for (int t = 0; t < nn; ++t) {
+        if (tid < D) kin[tid] = bf16_bits_to_f32(new_row(a.k_new, s_old + t)[tid]);
+        __syncthreads();
+        float acc = 0.0f;
+#pragma unroll
+        for (int i = 0; i < kIn / 2; ++i) {
+            acc = fmaf(bf16_bits_to_f32(trow[i] & 0xFFFFu), kin[part * kIn + 2 * i], acc);
+            acc = fmaf(bf16_bits_to_f32(trow[i] >> 16), kin[part * kIn + 2 * i + 1], acc);
+        }
+#pragma unroll
+        for (int off = 1; off < kParts; off <<= 1) acc += __shfl_xor(acc, off);
+        if (part == 0) {
+            const uint16_t kb = (uint16_t)(pack_bf16_rne(acc, 0.0f) & 0xFFFFu);
+            kn[t * kPitch + o] = kb;
+            if (a.k_tilde_out != nullptr) new_row(a.k_tilde_out, s_old + t)[o] = kb;
+        }
+        __syncthreads();
+    }
+
+    // ---- quantise [start_old, q_new), one page at a time
+    if (start_old < q_new) {
+        for (int32_t blk = a.s_sink + (start_old - a.s_sink) / kPage * kPage; blk < q_new; blk += kPage) {
+            const int32_t lo = max(blk, start_old), hi = min(blk + kPage, q_new);
+            constexpr int kVec = D / 8;
+            for (int idx = tid; idx < kPage * kVec; idx += 256) {
+                const int r = idx / kVec, cv = idx % kVec;
+                const int32_t p = blk + r;
+                if (p < lo || p >= hi) continue;
+                uint4 kv, vv;
+                if (p >= s_old) {
+                    kv = *reinterpret_cast<const uint4 *>(kn + (p - s_old) * kPitch + 8 * cv);
+                    vv = *reinterpret_cast<const uint4 *>(new_row(a.v_new, p) + 8 * cv);
+                } else {
+                    const int32_t slot = ring_slot(p, a.s_sink, ring);
+                    kv = *reinterpret_cast<const uint4 *>(a.win_k + (head_win + slot) * D + 8 * cv);
+                    const uint16_t *vsrc = a.win_v + (head_win * D) + slot;  // channel-major
+                    uint16_t e[8];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) e[q] = vsrc[(int64_t)(8 * cv + q) * a.win_slots];
+                    vv.x = e[0] | ((uint32_t)e[1] << 16);
+                    vv.y = e[2] | ((uint32_t)e[3] << 16);
+                    vv.z = e[4] | ((uint32_t)e[5] << 16);
+                    vv.w = e[6] | ((uint32_t)e[7] << 16);
+                }
+                *reinterpret_cast<uint4 *>(kt + r * kPitch + 8 * cv) = kv;
+                *reinterpret_cast<uint4 *>(vt + r * kPitch + 8 * cv) = vv;
+            }
+            if (tid == 0) {
+                const int32_t lp = (blk - a.s_sink) / kPage;
+                int32_t phys = -1;
+                if (lp < a.max_pages) {
+                    phys = a.page_table[(int64_t)b * a.max_pages + lp];
+                    if (phys < 0 || phys >= a.n_pages) phys = -1;
+                }
+                sh_page = phys;
+            }
+            __syncthreads();
+            const int32_t page = sh_page;
+            uint8_t *pg = page >= 0 ? a.pages + ((int64_t)page * a.n_kv + h) * L::kPageBytes : nullptr;
+            quantise_tile<D, BITS>(a, kt, vt, vcodes, blk, [&](int32_t p) { return p >= lo && p < hi; },
+                                   pg, tid);
+            __syncthreads();
+        }
+    }
+
+    // ---- new tokens that stay bf16: sink, or the ring at or after q_new
+    for (int t = 0; t < nn; ++t) {
+        const int32_t p = s_old + t;
+        if (!(p < a.s_sink || p >= q_new)) continue;
+        const int32_t slot = p < a.s_sink ? p : ring_slot(p, a.s_sink, ring);
+        if (tid < D / 8)
+            *reinterpret_cast<uint4 *>(a.win_k + (head_win + slot) * D + 8 * tid) =
+                *reinterpret_cast<const uint4 *>(kn + t * kPitch + 8 * tid);
+        if (tid < D) a.win_v[(head_win * D) + (int64_t)tid * a.win_slots + slot] = new_row(a.v_new, p)[tid];
+    }
+}
+
 // Advance seq_len / quant_end after the append kernels have read them.
 __global__ void append_commit_kernel(int32_t *seq_len, int32_t *quant_end, const int32_t *n_new,
                                      int32_t batch, int32_t max_new, int32_t s_sink,
@@ -448,9 +598,14 @@ __global__ void append_commit_kernel(int32_t *seq_len, int32_t *quant_end, const
 template <int D, int BITS>
 static hipError_t launch_append(const AppendArgs &a, dim3 grid, hipStream_t s)
 {
-    timing_begin("append_kernel", s);
-    hipLaunchKernelGGL((append_kernel<D, BITS>), grid, dim3(256), 0, s, a);
-    timing_end(s);
+    launch("append_kernel", append_kernel<D, BITS>, grid, dim3(256), s, a);
+    return hipGetLastError();
+}
+
+template <int D, int BITS>
+static hipError_t launch_append_step(const AppendArgs &a, dim3 grid, hipStream_t s)
+{
+    launch("append_step_kernel", append_step_kernel<D, BITS>, grid, dim3(256), s, a);
     return hipGetLastError();
 }
 
@@ -532,18 +687,24 @@ extern "C" int wushkv_append(const wushkv_cache *c, const uint16_t *k_new, const
         return hipErrorInvalidValue;
     };
     hipError_t e;
-    if (fused) {
+    if (max_new <= kStepMax) {
+        const dim3 sgrid((unsigned)c->n_kv_heads, (unsigned)c->batch);
+        const int key = c->head_dim * 10 + c->bits;
+        switch (key) {
+            case 1282: e = launch_append_step<128, 2>(a, sgrid, s); break;
+            case 1284: e = launch_append_step<128, 4>(a, sgrid, s); break;
+            case 642: e = launch_append_step<64, 2>(a, sgrid, s); break;
+            default: e = launch_append_step<64, 4>(a, sgrid, s); break;
+        }
+    } else if (fused) {
         e = go(kModeFlush | kModeNew);
     } else {
         e = go(kModeFlush);
         if (e == hipSuccess) e = go(kModeNew);
     }
     if (e != hipSuccess) return WUSHKV_ELAUNCH;
-    timing_begin("append_commit_kernel", s);
-    hipLaunchKernelGGL(append_commit_kernel, dim3((c->batch + 255) / 256), dim3(256), 0, s,
-                       c->seq_len, c->quant_end, n_new, c->batch, max_new, c->s_sink, c->s_keep,
-                       c->s_flush);
-    timing_end(s);
+    launch("append_commit_kernel", append_commit_kernel, dim3((c->batch + 255) / 256), dim3(256), s,
+           c->seq_len, c->quant_end, n_new, c->batch, max_new, c->s_sink, c->s_keep, c->s_flush);
     if (hipGetLastError() != hipSuccess) return WUSHKV_ELAUNCH;
     return WUSHKV_OK;
 }

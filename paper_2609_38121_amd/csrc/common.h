@@ -5,6 +5,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stdint.h>
 
 #include "wushkv.h"
@@ -82,25 +83,32 @@ struct Layout {
 
     // K region: (token t of the page, channel ch) -> (word index, bit).
     // Lane 16 j + n holds tokens 4 n .. 4 n + 3 (tile t % 4) and channels
-    // 32 j .. 32 j + 31, BITS words per tile.  Inside a word the channels
-    // split into two halves of 16 / BITS codes; code i of half h sits at
-    // bit 2 BITS i + BITS h, so that one mask (and one shift for h = 1)
-    // spreads a word into nibbles (2-bit) or bytes (4-bit), one code each.
+    // 32 j .. 32 j + 31, BITS words per tile, 4 BITS words in all; its k-th
+    // word is word 4 of 16-byte chunk k / 4, and chunk q holds every lane's
+    // 16 bytes in lane order (one 128-bit LDS read per chunk touches
+    // consecutive addresses).  Inside a word the channels split into two
+    // halves of 16 / BITS codes; code i of half h sits at bit
+    // 2 BITS i + BITS h, so that one mask (and one shift for h = 1) spreads
+    // a word into nibbles (2-bit) or bytes (4-bit), one code each.
+    __host__ __device__ static constexpr int k_word(int lane, int k) { return (k >> 2) * (4 * kKLanes) + 4 * lane + (k & 3); }
     __host__ __device__ static inline void k_pos(int t, int ch, int &word, int &bit)
     {
         constexpr int kSpan = 32 / BITS;  // channels per word
         const int n = t >> 2, tt = t & 3, j = ch >> 5, q = ch & 31;
         const int w = q / kSpan, r = q % kSpan, h = r / (kSpan / 2), i = r % (kSpan / 2);
-        word = (16 * j + n) * kKWordsPerLane + BITS * tt + w;
+        word = k_word(16 * j + n, BITS * tt + w);
         bit = 2 * BITS * i + BITS * h;
     }
     // V region: (token t of the page, channel ch) -> (word index, bit).
+    // Lane 16 j + m's k-th word (k = kc 2nw + u) is word k % 4 of chunk
+    // k / 4, chunks again holding every lane's 16 bytes in lane order.
+    __host__ __device__ static constexpr int v_word(int lane, int k) { return (k >> 2) * 256 + 4 * lane + (k & 3); }
     __host__ __device__ static inline void v_pos(int t, int ch, int &word, int &bit)
     {
         int kc = t >> 5, j = (t >> 3) & 3, i = t & 7;
         int nt = ch >> 4, m = ch & 15;
         int u = nt / kOpsPerWord, o = nt % kOpsPerWord;
-        word = (16 * j + m) * kWordsPerLane + kc * 2 * kNw + u;
+        word = v_word(16 * j + m, kc * 2 * kNw + u);
         bit = v_bit(o, i);
     }
 };
@@ -182,8 +190,23 @@ __host__ __device__ __forceinline__ int32_t ring_slot(int32_t p, int32_t s_sink,
 
 // ------------------------------------------------------- host-side plumbing
 
-// Launch bookkeeping for wushkv_timing_*; defined in api.hip.
-void timing_begin(const char *name, hipStream_t s);
-void timing_end(hipStream_t s);
+// Launch bookkeeping for wushkv_timing_*; defined in api.hip.  While timing
+// is on, each launch takes the next pair of events, which the runtime
+// records at the start and the end of that kernel's execution.
+struct TimedLaunch {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+TimedLaunch timing_slot(const char *name);
+
+template <typename Kernel, typename... Args>
+inline void launch(const char *name, Kernel kernel, dim3 grid, dim3 block, hipStream_t s,
+                   Args... args)
+{
+    const TimedLaunch t = timing_slot(name);
+    if (t.start != nullptr)
+        hipExtLaunchKernelGGL(kernel, grid, block, 0, s, t.start, t.stop, 0, args...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
+}
 
 }  // namespace wushkv

@@ -310,9 +310,12 @@ struct MainLds {
     static constexpr int kDma = (L::kPageBytes + 1023) / 1024;  // direct-to-LDS loads per page
     static constexpr int kSlot = kDma * 1024;
     static constexpr int kStageBytes = kStages * kSlot > G * D * 4 ? kStages * kSlot : G * D * 4;
-    // weight buffer: 2G rows of 64 tokens (fp16 or bf16), then a zero row
+    // weight buffer: 2G rows of 64 tokens (fp16 or bf16; row part G + g
+    // holds part `part` of head g), then a zero row.  The 144-byte pitch
+    // spreads the rows one reads together over distinct LDS banks.
     static constexpr int kTRows = 2 * G;
-    static constexpr int kTBytes = kTRows * 128 + 64;
+    static constexpr int kTPitch = 144;
+    static constexpr int kTBytes = kTRows * kTPitch + 64;
     static constexpr int kWave = kStageBytes + kTBytes;
 };
 
@@ -341,8 +344,9 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
     const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
     uint8_t *stage = lds + wave * M::kWave;
     uint8_t *tbuf = stage + M::kStageBytes;
-    const uint32_t zero_row = lds_addr(tbuf + M::kTRows * 128);
-    if (lane < 16) reinterpret_cast<uint32_t *>(tbuf + M::kTRows * 128)[lane] = 0u;
+    constexpr int kTP = M::kTPitch;
+    const uint32_t zero_row = lds_addr(tbuf + M::kTRows * kTP);
+    if (lane < 16) reinterpret_cast<uint32_t *>(tbuf + M::kTRows * kTP)[lane] = 0u;
 
     const int32_t S = a.seq_len[b];
     int32_t qend = a.quant_end[b];
@@ -415,7 +419,7 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
         // m / kRowsPerHead; weight rows sit at 2 g + part in the buffer
         const int ahead = n / kRowsPerHead, apart = n % kRowsPerHead;
         const bool arow_ok = ahead < G && apart < 2;
-        const uint32_t a_addr = arow_ok ? lds_addr(tbuf + (2 * ahead + apart) * 128 + 16 * j) : zero_row;
+        const uint32_t a_addr = arow_ok ? lds_addr(tbuf + (apart * G + ahead) * kTP + 16 * j) : zero_row;
         const uint32_t a_step = arow_ok ? 64u : 0u;  // second 32-token chunk
 
         int32_t tbl = -1;
@@ -457,7 +461,7 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
                 u32x4 kx[kKX + 2];
 #pragma unroll
                 for (int q4 = 0; q4 < kKX; ++q4)
-                    kx[q4] = lds_read16(pg + 16 * (lane * kKX + q4));
+                    kx[q4] = lds_read16(pg + 4 * L::k_word(lane, 4 * q4));
                 kx[kKX] = lds_read16(pg + L::kParamOffset + 16 * n);
                 kx[kKX + 1] = lds_read16(pg + L::kParamOffset + 4 * kPage + 16 * n);
                 lds_wait(kx);
@@ -549,8 +553,8 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
                                                           wgt[1] - f16_bits_to_f32(h01 >> 16));
                         const uint32_t l23 = pack_f16_rne(wgt[2] - f16_bits_to_f32(h23 & 0xFFFFu),
                                                           wgt[3] - f16_bits_to_f32(h23 >> 16));
-                        lds_write8(lds_addr(tbuf + (2 * hs) * 128 + 8 * n), h01, h23);
-                        lds_write8(lds_addr(tbuf + (2 * hs + 1) * 128 + 8 * n), l01, l23);
+                        lds_write8(lds_addr(tbuf + hs * kTP + 8 * n), h01, h23);
+                        lds_write8(lds_addr(tbuf + (G + hs) * kTP + 8 * n), l01, l23);
                     }
                 }
                 // A operands (two 32-token chunks) and the value words
@@ -559,7 +563,7 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
                 vx[1] = lds_read16(a_addr + a_step);
 #pragma unroll
                 for (int q4 = 0; q4 < L::kWordsPerLane / 4; ++q4)
-                    vx[2 + q4] = lds_read16(pg + L::kRegionBytes + 16 * (lane * (L::kWordsPerLane / 4) + q4));
+                    vx[2 + q4] = lds_read16(pg + L::kRegionBytes + 4 * L::v_word(lane, 4 * q4));
                 lds_wait(vx);
 #pragma unroll
                 for (int kc = 0; kc < 2; ++kc) {
@@ -638,7 +642,7 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
         float m_run[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f};
-        const uint32_t a_addr = n < 2 * G ? lds_addr(tbuf + n * 128 + 16 * j) : zero_row;
+        const uint32_t a_addr = n < 2 * G ? lds_addr(tbuf + ((n & 1) * G + (n >> 1)) * kTP + 16 * j) : zero_row;
         const uint32_t a_step = n < 2 * G ? 64u : 0u;
 
         for (int u = wave; u < n_wunits; u += 4) {
@@ -705,8 +709,8 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
                         lo[q] = pack_bf16_rne(p[2 * q] - bf16_bits_to_f32(hi[q] & 0xFFFFu),
                                               p[2 * q + 1] - bf16_bits_to_f32(hi[q] >> 16));
                     }
-                    lds_write8(lds_addr(tbuf + (2 * g) * 128 + 8 * n), hi[0], hi[1]);
-                    lds_write8(lds_addr(tbuf + (2 * g + 1) * 128 + 8 * n), lo[0], lo[1]);
+                    lds_write8(lds_addr(tbuf + g * kTP + 8 * n), hi[0], hi[1]);
+                    lds_write8(lds_addr(tbuf + (G + g) * kTP + 8 * n), lo[0], lo[1]);
                 }
             }
             u32x4 pa[2];
@@ -863,7 +867,7 @@ static bool make_plan(const wushkv_cache *c, int32_t n_q, int32_t max_seq_len, D
 template <int D, int BITS, int G>
 static void launch_main(dim3 grid, hipStream_t s, const DecodeArgs &a)
 {
-    hipLaunchKernelGGL((decode_main_kernel<D, BITS, G>), grid, dim3(256), 0, s, a);
+    launch("decode_main_kernel", decode_main_kernel<D, BITS, G>, grid, dim3(256), s, a);
 }
 
 template <int D, int BITS>
@@ -952,28 +956,20 @@ extern "C" int wushkv_decode_attention(const wushkv_cache *c, const uint16_t *q,
     const float scale = sm_scale * kLog2e;
     const int key = c->head_dim * 10 + c->bits;
 
-    timing_begin("decode_qt_kernel", s);
     switch (key) {
-        case 1282: hipLaunchKernelGGL((decode_qt_kernel<128, 2>), gq, dim3(256), 0, s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
-        case 1284: hipLaunchKernelGGL((decode_qt_kernel<128, 4>), gq, dim3(256), 0, s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
-        case 642: hipLaunchKernelGGL((decode_qt_kernel<64, 2>), gq, dim3(256), 0, s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
-        case 644: hipLaunchKernelGGL((decode_qt_kernel<64, 4>), gq, dim3(256), 0, s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
+        case 1282: launch("decode_qt_kernel", decode_qt_kernel<128, 2>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
+        case 1284: launch("decode_qt_kernel", decode_qt_kernel<128, 4>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
+        case 642: launch("decode_qt_kernel", decode_qt_kernel<64, 2>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
+        case 644: launch("decode_qt_kernel", decode_qt_kernel<64, 4>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
     }
-    timing_end(s);
-
-    timing_begin("decode_main_kernel", s);
     switch (key) {
         case 1282: launch_main_g<128, 2>(G, gm, s, a); break;
         case 1284: launch_main_g<128, 4>(G, gm, s, a); break;
         case 642: launch_main_g<64, 2>(G, gm, s, a); break;
         case 644: launch_main_g<64, 4>(G, gm, s, a); break;
     }
-    timing_end(s);
-
-    timing_begin("decode_combine_kernel", s);
-    if (c->head_dim == 128) hipLaunchKernelGGL(decode_combine_kernel<128>, gc, dim3(128), 0, s, part, out, c->n_kv_heads, G, p.n_splits);
-    else hipLaunchKernelGGL(decode_combine_kernel<64>, gc, dim3(64), 0, s, part, out, c->n_kv_heads, G, p.n_splits);
-    timing_end(s);
+    if (c->head_dim == 128) launch("decode_combine_kernel", decode_combine_kernel<128>, gc, dim3(128), s, (const float *)part, out, c->n_kv_heads, G, p.n_splits);
+    else launch("decode_combine_kernel", decode_combine_kernel<64>, gc, dim3(64), s, (const float *)part, out, c->n_kv_heads, G, p.n_splits);
     if (hipGetLastError() != hipSuccess) return WUSHKV_ELAUNCH;
     return WUSHKV_OK;
 }

@@ -66,11 +66,10 @@ extern "C" int wushkv_dequant(const wushkv_cache *c, int32_t b, int32_t start, i
     if ((n + 255) / 256 > 0x7FFFFFFF) return WUSHKV_EINVAL;
     dim3 grid((unsigned)((n + 255) / 256), (unsigned)c->n_kv_heads);
     const int key = c->head_dim * 10 + c->bits;
-    timing_begin("dequant_kernel", s);
-#define WUSHKV_DQ(D_, B_)                                                                        \
-    hipLaunchKernelGGL((dequant_kernel<D_, B_>), grid, dim3(256), 0, s, c->pages, c->page_table, \
-                       c->n_kv_heads, c->s_sink, c->max_pages_per_seq, c->n_pages, b, start,     \
-                       count, k_out, v_out)
+#define WUSHKV_DQ(D_, B_)                                                                     \
+    launch("dequant_kernel", dequant_kernel<D_, B_>, grid, dim3(256), s, c->pages, c->page_table, \
+           c->n_kv_heads, c->s_sink, c->max_pages_per_seq, c->n_pages, b, start, count, k_out,   \
+           v_out)
     switch (key) {
         case 1282: WUSHKV_DQ(128, 2); break;
         case 1284: WUSHKV_DQ(128, 4); break;
@@ -78,7 +77,6 @@ extern "C" int wushkv_dequant(const wushkv_cache *c, int32_t b, int32_t start, i
         case 644: WUSHKV_DQ(64, 4); break;
     }
 #undef WUSHKV_DQ
-    timing_end(s);
     if (hipGetLastError() != hipSuccess) return WUSHKV_ELAUNCH;
     return WUSHKV_OK;
 }

@@ -4,15 +4,17 @@ shows up as a parity failure rather than cancelling out.
 
 One (page, head) block: K code words, V code words, K params, V params.
 A word holds B = 32 / bits codes.
-K: lane L = 16 j + n (j < d / 32) owns 4 bits consecutive words;
-  K word L*4bits + bits*t + w, code e = h (B/2) + i (h = 0, 1; i < B/2) at
+Both regions are sequences of 16-byte chunks; chunk q holds word q*4 .. q*4+3
+of every lane in lane order, so a lane's k-th word is word
+(k // 4) * 4 * lanes + 4 L + k % 4 of the region.
+K: lane L = 16 j + n (j < d / 32; d / 2 lanes) owns 4 bits words; its word
+  k = bits*t + w holds code e = h (B/2) + i (h = 0, 1; i < B/2) at
   bit 2 bits i + bits h : token 4 n + t, channel 32 j + B w + e
 V: element e is slot i = e % 8 of operand o = e // 8 and sits at bit
   16 * (i % 2) + F(o, i // 2) with F = (6, 10, 8, 12 | 2, 0, 4, 14) for
-  2-bit operands 0 | 1 and (4, 0, 8, 12) for 4-bit.  Lane L = 16 j + m owns
-  4 nw consecutive words, nw = d * bits / 128.
-  V word L*4nw + kc*2nw + u : token 32 kc + 8 j + i,
-                              channel 16 nt + m, nt = u (B/8) + o
+  2-bit operands 0 | 1 and (4, 0, 8, 12) for 4-bit.  Lane L = 16 j + m (64
+  lanes) owns 4 nw words, nw = d * bits / 128; its word k = kc*2nw + u holds
+  token 32 kc + 8 j + i, channel 16 nt + m, nt = u (B/8) + o
 """
 from __future__ import annotations
 
@@ -52,7 +54,8 @@ def _maps(d: int, bits: int):
         j, n = divmod(L, 16)
         for t in range(4):
             for w in range(bits):
-                widx = L * 4 * bits + bits * t + w
+                k = bits * t + w  # the lane's k-th word: word k % 4 of chunk k // 4
+                widx = (k // 4) * 4 * (d // 2) + 4 * L + k % 4
                 for e in range(B):
                     kt[widx, e] = 4 * n + t
                     kc_[widx, e] = 32 * j + B * w + e
@@ -60,7 +63,8 @@ def _maps(d: int, bits: int):
         j, m = divmod(L, 16)
         for kc in range(2):
             for u in range(2 * nw):
-                widx = L * 4 * nw + kc * 2 * nw + u
+                k = kc * 2 * nw + u
+                widx = (k // 4) * 256 + 4 * L + k % 4
                 for e in range(B):
                     o, i = divmod(e, 8)
                     nt = u * ops + o

@@ -130,8 +130,9 @@ def test_layout_maps_are_bijections(d, bits):
 def test_layout_first_words_as_documented():
     # K word 0 (lane 0, tile 0): token 0, channels 0..15 (2-bit); channel
     # 8 h + i at bit 4 i + 2 h.  Lane 17 = (j 1, n 1) holds tokens 4..7 and
-    # channels 32..63.  V word 0: channel 0, tokens 0..7 of the first N-tile
-    # and channel 16 for the second operand.
+    # channels 32..63; its first word is word 4 * 17 of the first chunk.
+    # V word 0: channel 0, tokens 0..7 of the first N-tile and channel 16
+    # for the second operand.
     d, bits = 128, 2
     kc = np.zeros((64, d), np.int64)
     kc[0, 2] = 3   # i = 2, h = 0 -> bit 8
@@ -142,7 +143,7 @@ def test_layout_first_words_as_documented():
     blk = pagelayout.encode_block(kc, vc, np.zeros((64, 2)), np.zeros((64, 2)), d, bits)
     w = blk[:8 * d * bits].view("<u4")
     assert w[0] == (3 << 8) | (1 << 6)
-    assert w[17 * 8] == 2 << 2
+    assert w[4 * 17] == 2 << 2
     assert np.count_nonzero(w) == 2
     vw = blk[8 * d * bits:16 * d * bits].view("<u4")
     assert vw[0] == 2 << 20
