@@ -11,8 +11,8 @@
 //   decode_main_kernel     grid (splits, kv heads, batch), four waves per
 //                          workgroup.  Workgroups 0 .. n_page_splits - 1 scan
 //                          the quantised pages, each wave a contiguous run;
-//                          the last workgroup of a (sequence, head) scans the
-//                          bf16 sink + ring slots, one 64-slot unit per wave.
+//                          the others scan the bf16 sink + ring slots, one
+//                          64-slot unit per workgroup, 16 slots per wave.
 //                          Each workgroup writes one partial (m, l, o) per
 //                          query head.
 //   decode_combine_kernel  log-sum-exp merge of the splits.
@@ -36,8 +36,8 @@
 //
 // Window slots.  bf16 keys and values: q~ in bf16 hi + lo parts forms the A
 // rows (head, part) of 16x16x32 bf16 products against the key slots; the
-// probabilities, again split hi + lo, go through LDS into the P V product
-// against the channel-major value slots.
+// probabilities, again split hi + lo, go through LDS into a 16x16x16 bf16
+// P V product against the channel-major value slots.
 #include "common.h"
 
 namespace wushkv {
@@ -219,14 +219,25 @@ __device__ __forceinline__ float dpp(float x)
     return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x),
                                                                   CTRL, 0xF, 0xF, false));
 }
-// max / sum over the 16 lanes of a row (quad butterflies, then rotations)
+// max / sum over the 16 lanes of a row (quad butterflies, then rotations).
+// The max is four DPP-operand maxima in one assembly block; each is preceded
+// by the two wait states a DPP read of a just-written register needs.  The
+// inputs are finite or -inf.
 __device__ __forceinline__ float row_max16(float x)
 {
-    x = fmaxf(x, dpp<0xB1>(x));   // quad_perm [1,0,3,2]
-    x = fmaxf(x, dpp<0x4E>(x));   // quad_perm [2,3,0,1]
-    x = fmaxf(x, dpp<0x124>(x));  // row_ror 4
-    x = fmaxf(x, dpp<0x128>(x));  // row_ror 8
-    return x;
+    float y;
+    asm volatile(
+        "s_nop 1\n\t"
+        "v_max_f32_dpp %0, %1, %1 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_max_f32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_max_f32_dpp %0, %0, %0 row_ror:4 row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_max_f32_dpp %0, %0, %0 row_ror:8 row_mask:0xf bank_mask:0xf"
+        : "=&v"(y)
+        : "v"(x));
+    return y;
 }
 __device__ __forceinline__ float row_sum16(float x)
 {
@@ -262,6 +273,22 @@ __device__ __forceinline__ void lds_write8(uint32_t addr, uint32_t lo, uint32_t 
     u32x2 v = {lo, hi};
     asm volatile("ds_write_b64 %0, %1" ::"v"(addr), "v"(v) : "memory");
 }
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+__device__ __forceinline__ void lds_write2(uint32_t addr, uint32_t v)
+{
+    asm volatile("ds_write_b16 %0, %1" ::"v"(addr), "v"(v) : "memory");
+}
+__device__ __forceinline__ u32x2 lds_read8(uint32_t addr)
+{
+    u32x2 r;
+    asm volatile("ds_read_b64 %0, %1" : "=v"(r) : "v"(addr) : "memory");
+    return r;
+}
+__device__ __forceinline__ void lds_wait2(u32x2 &x)
+{
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x)::"memory");
+}
+
 template <int N>
 __device__ __forceinline__ void lds_wait(u32x4 (&x)[N])
 {
@@ -279,6 +306,21 @@ __device__ __forceinline__ void lds_wait(u32x4 (&x)[N])
         asm volatile("s_waitcnt lgkmcnt(0)"
                      : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]), "+v"(x[4]), "+v"(x[5]),
                        "+v"(x[6]), "+v"(x[7])::"memory");
+}
+
+// Wait for all but the last KEEP LDS accesses issued; the values in x (from
+// earlier reads) are then complete.
+template <int KEEP, int N>
+__device__ __forceinline__ void lds_wait_keep(u32x4 (&x)[N])
+{
+    static_assert(N == 4 || N == 6, "operands");
+    if constexpr (N == 4)
+        asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]) : "n"(KEEP) : "memory");
+    else
+        asm volatile("s_waitcnt lgkmcnt(%6)"
+                     : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]), "+v"(x[4]), "+v"(x[5])
+                     : "n"(KEEP)
+                     : "memory");
 }
 
 // Wait until at most `after` direct-to-LDS loads are outstanding.  `after`
@@ -440,57 +482,75 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
                     __builtin_amdgcn_global_load_lds(src + 1024 * i, lds_ptr(dst + 1024 * i), 16, 0, 0);
             }
         };
+        // Per page: the value words are read at the top (they are needed only
+        // by the P V products at the end); the key words and parameters of
+        // page u were read at the end of iteration u - 1, while its P V
+        // products ran.  A page's stage is refilled (page u + 2) as soon as
+        // its last LDS read has completed, before the P V products.
+        constexpr int kKX = L::kKWordsPerLane / 4;  // key chunks per lane
+        constexpr int kVX = L::kWordsPerLane / 4;   // value chunks per lane
+        auto read_keys = [&](uint32_t pg, u32x4 (&kx)[kKX + 2]) {
+#pragma unroll
+            for (int q4 = 0; q4 < kKX; ++q4) kx[q4] = lds_read16(pg + 4 * L::k_word(lane, 4 * q4));
+            kx[kKX] = lds_read16(pg + L::kParamOffset + 16 * n);
+            kx[kKX + 1] = lds_read16(pg + L::kParamOffset + 4 * kPage + 16 * n);
+        };
         if (a.n_pages > 0 && w0 < w1) {
-#pragma unroll
-            for (int s = 0; s < kStages - 1; ++s)
-                if (w0 + s < w1) issue(w0 + s, s);
+            static_assert(kStages == 2, "two stages per wave");
+            issue(w0, 0);
+            if (w0 + 1 < w1) issue(w0 + 1, 1);
+            wait_vmcnt_at_most<1, kDma>(w0 + 1 < w1 ? kDma : 0);
+            u32x4 kx[kKX + 2];
+            read_keys(lds_addr(stage), kx);
             for (int u = w0; u < w1; ++u) {
-                const int s = (u - w0) % kStages;
-                if (u + kStages - 1 < w1) issue(u + kStages - 1, (u - w0 + kStages - 1) % kStages);
-                wait_vmcnt_at_most<kStages - 1, kDma>(kDma * min(kStages - 1, w1 - 1 - u));
-                {
-                    const int32_t phys = phys_of(u);
-                    if (phys < 0 || phys >= a.n_pages) continue;
-                }
+                const int s = (u - w0) & 1;
                 const uint32_t pg = lds_addr(stage + s * kSlot);
-                const int32_t nvalid = min(kPage, q_hi - (a.s_sink + u * kPage));
-
-                // key words of this lane (tokens 4n..4n+3, channels 32j..),
-                // and the parameters of tokens 4n .. 4n+3
-                constexpr int kKX = L::kKWordsPerLane / 4;
-                u32x4 kx[kKX + 2];
+                u32x4 vv[kVX];
 #pragma unroll
-                for (int q4 = 0; q4 < kKX; ++q4)
-                    kx[q4] = lds_read16(pg + 4 * L::k_word(lane, 4 * q4));
-                kx[kKX] = lds_read16(pg + L::kParamOffset + 16 * n);
-                kx[kKX + 1] = lds_read16(pg + L::kParamOffset + 4 * kPage + 16 * n);
-                lds_wait(kx);
+                for (int q4 = 0; q4 < kVX; ++q4)
+                    vv[q4] = lds_read16(pg + L::kRegionBytes + 4 * L::v_word(lane, 4 * q4));
+                lds_wait_keep<kVX>(kx);  // the key reads are done, the value reads may run
+                const int32_t phys = phys_of(u);
+                // a page outside the pool contributes nothing (its stage holds page 0)
+                const int32_t nvalid = (phys < 0 || phys >= a.n_pages)
+                                           ? 0 : min(kPage, q_hi - (a.s_sink + u * kPage));
                 const u32x4 kp = kx[kKX], vp = kx[kKX + 1];
 
-                // scores: one product per 16 tokens (and head group)
-                float lg[kHG][4];
+                // scores: one product per 16 tokens, head group and limb group;
+                // all issued before any result is used
+                i32x8 bop[4];
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
                     uint32_t w[BITS];
 #pragma unroll
                     for (int i = 0; i < BITS; ++i) w[i] = kx[(BITS * t + i) / 4][(BITS * t + i) % 4];
-                    i32x8 bop;
                     if constexpr (BITS == 2) {
-                        bop = i32x8{(int)(w[0] & 0x33333333u), (int)((w[0] >> 2) & 0x33333333u),
-                                    (int)(w[1] & 0x33333333u), (int)((w[1] >> 2) & 0x33333333u),
-                                    0, 0, 0, 0};
+                        bop[t] = i32x8{(int)(w[0] & 0x33333333u), (int)((w[0] >> 2) & 0x33333333u),
+                                       (int)(w[1] & 0x33333333u), (int)((w[1] >> 2) & 0x33333333u),
+                                       0, 0, 0, 0};
                     } else {
-                        bop = i32x8{(int)(w[0] & 0x0F0F0F0Fu), (int)((w[0] >> 4) & 0x0F0F0F0Fu),
-                                    (int)(w[1] & 0x0F0F0F0Fu), (int)((w[1] >> 4) & 0x0F0F0F0Fu),
-                                    (int)(w[2] & 0x0F0F0F0Fu), (int)((w[2] >> 4) & 0x0F0F0F0Fu),
-                                    (int)(w[3] & 0x0F0F0F0Fu), (int)((w[3] >> 4) & 0x0F0F0F0Fu)};
+                        bop[t] = i32x8{(int)(w[0] & 0x0F0F0F0Fu), (int)((w[0] >> 4) & 0x0F0F0F0Fu),
+                                       (int)(w[1] & 0x0F0F0F0Fu), (int)((w[1] >> 4) & 0x0F0F0F0Fu),
+                                       (int)(w[2] & 0x0F0F0F0Fu), (int)((w[2] >> 4) & 0x0F0F0F0Fu),
+                                       (int)(w[3] & 0x0F0F0F0Fu), (int)((w[3] >> 4) & 0x0F0F0F0Fu)};
                     }
+                }
+                f32x4 c[kHG][4][2];
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+#pragma unroll
+                    for (int hg = 0; hg < kHG; ++hg)
+#pragma unroll
+                        for (int part = 0; part < 2; ++part)
+                            c[hg][t][part] = mfma_scaled(qa[hg][part], bop[t], kFmtB, qsc[hg][part], kScaleB);
+                float lg[kHG][4];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
                     const float ks = f16_bits_to_f32(kp[t] & 0xFFFFu);
                     const float kz = f16_bits_to_f32(kp[t] >> 16);
 #pragma unroll
                     for (int hg = 0; hg < kHG; ++hg) {
-                        const f32x4 c0 = mfma_scaled(qa[hg][0], bop, kFmtB, qsc[hg][0], kScaleB);
-                        const f32x4 c1 = mfma_scaled(qa[hg][1], bop, kFmtB, qsc[hg][1], kScaleB);
+                        const f32x4 &c0 = c[hg][t][0], &c1 = c[hg][t][1];
                         // the six limbs, most significant first
                         const float dot = (((c0[0] + c0[1]) + c0[2]) + (c0[3] + c1[0])) + c1[1];
                         lg[hg][t] = fmaf(ks, dot, kz * zs[hg]);
@@ -532,10 +592,12 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
 #pragma unroll
                 for (int hg = 0; hg < kHG; ++hg) m_run[hg] = m_new[hg];
 
-                // weights p s 2^-off as fp16, through LDS into the A operand
+                // weights p s 2^-off as fp16 hi + lo (about 22 significant
+                // bits), through LDS into the A operand rows
 #pragma unroll
                 for (int hg = 0; hg < kHG; ++hg) {
-                    const float mo = m_run[hg] + off;
+                    // (no valid token yet: every weight is exp2(-inf) = 0)
+                    const float mo = m_run[hg] == -INFINITY ? 0.0f : m_run[hg] + off;
                     float wgt[4];
 #pragma unroll
                     for (int t = 0; t < 4; ++t) {
@@ -546,7 +608,6 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
                     }
                     const int hs = G > 4 ? 2 * j + hg : j;
                     if (hs < G) {
-                        // fp16 hi + lo: about 22 significant bits per weight
                         const uint32_t h01 = pack_f16_rne(wgt[0], wgt[1]);
                         const uint32_t h23 = pack_f16_rne(wgt[2], wgt[3]);
                         const uint32_t l01 = pack_f16_rne(wgt[0] - f16_bits_to_f32(h01 & 0xFFFFu),
@@ -557,22 +618,28 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
                         lds_write8(lds_addr(tbuf + (G + hs) * kTP + 8 * n), l01, l23);
                     }
                 }
-                // A operands (two 32-token chunks) and the value words
-                u32x4 vx[2 + L::kWordsPerLane / 4];
-                vx[0] = lds_read16(a_addr);
-                vx[1] = lds_read16(a_addr + a_step);
+                // A operands (two 32-token chunks); with them every read of
+                // this page's stage has completed
+                u32x4 ax[2 + kVX];
+                ax[0] = lds_read16(a_addr);
+                ax[1] = lds_read16(a_addr + a_step);
 #pragma unroll
-                for (int q4 = 0; q4 < L::kWordsPerLane / 4; ++q4)
-                    vx[2 + q4] = lds_read16(pg + L::kRegionBytes + 4 * L::v_word(lane, 4 * q4));
-                lds_wait(vx);
+                for (int q4 = 0; q4 < kVX; ++q4) ax[2 + q4] = vv[q4];
+                lds_wait(ax);
+                if (u + 2 < w1) issue(u + 2, s);
+                if (u + 1 < w1) {
+                    // page u + 1 has landed once at most page u + 2's loads remain
+                    wait_vmcnt_at_most<1, kDma>(u + 2 < w1 ? kDma : 0);
+                    read_keys(lds_addr(stage + (s ^ 1) * kSlot), kx);
+                }
 #pragma unroll
                 for (int kc = 0; kc < 2; ++kc) {
-                    const f16x8 A = __builtin_bit_cast(f16x8, vx[kc]);
+                    const f16x8 A = __builtin_bit_cast(f16x8, ax[kc]);
 #pragma unroll
                     for (int uu = 0; uu < 2 * kNw; ++uu) {
                         const int widx = kc * 2 * kNw + uu;
                         uint32_t op[L::kCodesPerWord / 2];
-                        widen_word_f16<BITS>(vx[2 + widx / 4][widx % 4], op);
+                        widen_word_f16<BITS>(ax[2 + widx / 4][widx % 4], op);
 #pragma unroll
                         for (int o = 0; o < kOpw; ++o) {
                             const int nt = uu * kOpw + o;
@@ -608,138 +675,103 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
         }
     } else {
         // ================================================ window slots
-        const int32_t n_wunits = a.win_slots / kPage;
+        // Workgroup n_page_splits + u owns window unit u (slots 64 u ..
+        // 64 u + 63), wave w its 16 slots 64 u + 16 w .. + 15.  All of a
+        // tile's loads are issued together.
         const int32_t ring = a.win_slots - a.s_sink;
         // the ring holds positions [q_hi, S); the oldest sits at ring index a0
         const int32_t a0 = S > q_hi ? (q_hi - a.s_sink) % ring : 0;
         const int32_t ring_live = S > q_hi ? S - q_hi : 0;
         const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;
+        const int32_t slot0 = (split - a.n_page_splits) * kPage + 16 * wave;
 
-        // A operands: row m = 2 g + part (hi, lo) of q~, chunk c
-        bf16x8 qa[kC];
+        // this tile's live slots, one bit per slot (lanes 0..15)
+        bool mine;
         {
-            const int g = n >> 1, part = n & 1;
-#pragma unroll
-            for (int c = 0; c < kC; ++c) {
-                uint32_t u[4] = {0u, 0u, 0u, 0u};
-                if (g < G) {
-                    const float *src = a.qt + (qhead0 + g) * D + 32 * c + 8 * j;
-                    const f32x4 x0 = *reinterpret_cast<const f32x4 *>(src);
-                    const f32x4 x1 = *reinterpret_cast<const f32x4 *>(src + 4);
-                    const float x[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-#pragma unroll
-                    for (int p = 0; p < 4; ++p) {
-                        const uint32_t hi = pack_bf16_rne(x[2 * p], x[2 * p + 1]);
-                        const uint32_t lo = pack_bf16_rne(x[2 * p] - bf16_bits_to_f32(hi & 0xFFFFu),
-                                                          x[2 * p + 1] - bf16_bits_to_f32(hi >> 16));
-                        u[p] = part ? lo : hi;
-                    }
-                }
-                qa[c] = __builtin_bit_cast(bf16x8, u32x4{u[0], u[1], u[2], u[3]});
-            }
+            const int32_t sl = slot0 + n;
+            if (sl < a.s_sink) mine = sl < S;
+            else mine = ((sl - a.s_sink - a0 + ring) % ring) < ring_live;
         }
+        const uint32_t vmask = (uint32_t)(__ballot(mine) & 0xFFFFu);
         f32x4 acc[kNT];
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
         float m_run[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f};
-        const uint32_t a_addr = n < 2 * G ? lds_addr(tbuf + ((n & 1) * G + (n >> 1)) * kTP + 16 * j) : zero_row;
-        const uint32_t a_step = n < 2 * G ? 64u : 0u;
+        if (vmask != 0) {
+            // key slots (token slot0 + n, channels 32 c + 8 j ..) and value
+            // slots (channel 16 nt + n, tokens slot0 + 4 j .. + 3)
+            const uint16_t *krow = a.win_k + (head_win + slot0 + n) * D + 8 * j;
+            u32x4 kx[kC];
+#pragma unroll
+            for (int c = 0; c < kC; ++c) kx[c] = *reinterpret_cast<const u32x4 *>(krow + 32 * c);
+            typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+            const uint16_t *vrow = a.win_v + head_win * D + slot0 + 4 * j;
+            u32x2 vx[kNT];
+#pragma unroll
+            for (int nt = 0; nt < kNT; ++nt)
+                vx[nt] = *reinterpret_cast<const u32x2 *>(vrow + (int64_t)(16 * nt + n) * a.win_slots);
 
-        for (int u = wave; u < n_wunits; u += 4) {
-            const int32_t slot0 = u * kPage;
-            bool mine;
+            // A operands: row m = 2 g + part (hi, lo) of q~, chunk c
+            bf16x8 qa[kC];
             {
-                const int32_t sl = slot0 + lane;
-                if (sl < a.s_sink) mine = sl < S;
-                else mine = ((sl - a.s_sink - a0 + ring) % ring) < ring_live;
+                const int g = n >> 1, part = n & 1;
+#pragma unroll
+                for (int c = 0; c < kC; ++c) {
+                    uint32_t u[4] = {0u, 0u, 0u, 0u};
+                    if (g < G) {
+                        const float *src = a.qt + (qhead0 + g) * D + 32 * c + 8 * j;
+                        const f32x4 x0 = *reinterpret_cast<const f32x4 *>(src);
+                        const f32x4 x1 = *reinterpret_cast<const f32x4 *>(src + 4);
+                        const float x[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+#pragma unroll
+                        for (int pp = 0; pp < 4; ++pp) {
+                            const uint32_t hi = pack_bf16_rne(x[2 * pp], x[2 * pp + 1]);
+                            const uint32_t lo = pack_bf16_rne(x[2 * pp] - bf16_bits_to_f32(hi & 0xFFFFu),
+                                                              x[2 * pp + 1] - bf16_bits_to_f32(hi >> 16));
+                            u[pp] = part ? lo : hi;
+                        }
+                    }
+                    qa[c] = __builtin_bit_cast(bf16x8, u32x4{u[0], u[1], u[2], u[3]});
+                }
             }
-            const uint64_t vmask = __ballot(mine);
-            if (vmask == 0) continue;
             // scores: lane (j, n) gets rows 4 j + r = (head 2 j + r / 2,
-            // part r % 2) of token slot0 + 4 n + t
-            float lg[2][4];
+            // part r % 2) of token slot0 + n
+            f32x4 sc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const uint16_t *krow = a.win_k + (head_win + slot0 + 4 * n + t) * D + 8 * j;
-                u32x4 kx[kC];
-#pragma unroll
-                for (int c = 0; c < kC; ++c) kx[c] = *reinterpret_cast<const u32x4 *>(krow + 32 * c);
-                f32x4 sc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int c = 0; c < kC; ++c) sc = mfma16(qa[c], __builtin_bit_cast(bf16x8, kx[c]), sc);
-                const bool ok = (vmask >> (4 * n + t)) & 1u;
-                lg[0][t] = ok ? sc[0] + sc[1] : -INFINITY;
-                lg[1][t] = ok ? sc[2] + sc[3] : -INFINITY;
-            }
-            float m_new[2];
-            bool grow = false;
+            for (int c = 0; c < kC; ++c) sc = mfma16(qa[c], __builtin_bit_cast(bf16x8, kx[c]), sc);
+            const bool ok = (vmask >> n) & 1u;
+            float lg[2];
+            lg[0] = ok ? sc[0] + sc[1] : -INFINITY;
+            lg[1] = ok ? sc[2] + sc[3] : -INFINITY;
+            float pr[2];
 #pragma unroll
             for (int e = 0; e < 2; ++e) {
-                const float mx = row_max16(fmaxf(fmaxf(lg[e][0], lg[e][1]), fmaxf(lg[e][2], lg[e][3])));
-                m_new[e] = fmaxf(m_run[e], mx);
-                grow |= (2 * j + e < G) && m_new[e] > m_run[e];
-            }
-            if (__any(grow)) {
-                float al[2];
-#pragma unroll
-                for (int e = 0; e < 2; ++e) {
-                    al[e] = m_new[e] == -INFINITY ? 1.0f : fexp2(m_run[e] - m_new[e]);
-                    lsum[e] *= al[e];
-                }
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-#pragma unroll
-                    for (int nt = 0; nt < kNT; ++nt) acc[nt][r] *= al[r >> 1];
-            }
-#pragma unroll
-            for (int e = 0; e < 2; ++e) {
-                m_run[e] = m_new[e];
-                float p[4];
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    p[t] = m_run[e] == -INFINITY ? 0.0f : fexp2(lg[e][t] - m_run[e]);
-                    lsum[e] += p[t];
-                }
+                m_run[e] = row_max16(lg[e]);
+                pr[e] = m_run[e] == -INFINITY ? 0.0f : fexp2(lg[e] - m_run[e]);
+                lsum[e] = pr[e];
                 const int g = 2 * j + e;
                 if (g < G) {
-                    uint32_t hi[2], lo[2];
-#pragma unroll
-                    for (int q = 0; q < 2; ++q) {
-                        hi[q] = pack_bf16_rne(p[2 * q], p[2 * q + 1]);
-                        lo[q] = pack_bf16_rne(p[2 * q] - bf16_bits_to_f32(hi[q] & 0xFFFFu),
-                                              p[2 * q + 1] - bf16_bits_to_f32(hi[q] >> 16));
-                    }
-                    lds_write8(lds_addr(tbuf + g * kTP + 8 * n), hi[0], hi[1]);
-                    lds_write8(lds_addr(tbuf + (G + g) * kTP + 8 * n), lo[0], lo[1]);
+                    const uint32_t hl = pack_bf16_rne(pr[e], 0.0f) & 0xFFFFu;
+                    const uint32_t ll = pack_bf16_rne(pr[e] - bf16_bits_to_f32(hl), 0.0f) & 0xFFFFu;
+                    lds_write2(lds_addr(tbuf + g * kTP + 2 * n), hl);
+                    lds_write2(lds_addr(tbuf + (G + g) * kTP + 2 * n), ll);
                 }
             }
-            u32x4 pa[2];
-            pa[0] = lds_read16(a_addr);
-            pa[1] = lds_read16(a_addr + a_step);
-            lds_wait(pa);
-            // P V against the channel-major value slots; dead slots are
-            // zeroed, whatever bits they hold
-            const uint16_t *wvp = a.win_v + head_win * D + slot0;
+            // A operand of the 16x16x16 product: row m = 2 g + part, tokens
+            // 4 j .. 4 j + 3
+            const uint32_t pa_addr = n < 2 * G ? lds_addr(tbuf + ((n & 1) * G + (n >> 1)) * kTP + 8 * j) : zero_row;
+            u32x2 pa = lds_read8(pa_addr);
+            lds_wait2(pa);
+            // dead slots' values are zeroed, whatever bits they hold
+            const uint32_t bits4 = (vmask >> (4 * j)) & 0xFu;
+            const uint32_t msk0 = ((bits4 & 1u) ? 0x0000FFFFu : 0u) | ((bits4 & 2u) ? 0xFFFF0000u : 0u);
+            const uint32_t msk1 = ((bits4 & 4u) ? 0x0000FFFFu : 0u) | ((bits4 & 8u) ? 0xFFFF0000u : 0u);
+            typedef __attribute__((ext_vector_type(4))) short s16x4;
+            const s16x4 A = __builtin_bit_cast(s16x4, pa);
 #pragma unroll
-            for (int kc = 0; kc < 2; ++kc) {
-                const bf16x8 A = __builtin_bit_cast(bf16x8, pa[kc]);
-                const uint32_t bits8 = (uint32_t)(vmask >> (32 * kc + 8 * j)) & 0xFFu;
-                uint32_t msk[4];
-#pragma unroll
-                for (int p = 0; p < 4; ++p)
-                    msk[p] = (((bits8 >> (2 * p)) & 1u) ? 0x0000FFFFu : 0u) |
-                             (((bits8 >> (2 * p + 1)) & 1u) ? 0xFFFF0000u : 0u);
-                u32x4 vv[kNT];
-#pragma unroll
-                for (int nt = 0; nt < kNT; ++nt)
-                    vv[nt] = *reinterpret_cast<const u32x4 *>(wvp + (int64_t)(16 * nt + n) * a.win_slots +
-                                                              32 * kc + 8 * j);
-#pragma unroll
-                for (int nt = 0; nt < kNT; ++nt) {
-                    const u32x4 y = {vv[nt][0] & msk[0], vv[nt][1] & msk[1], vv[nt][2] & msk[2],
-                                     vv[nt][3] & msk[3]};
-                    acc[nt] = mfma16(A, __builtin_bit_cast(bf16x8, y), acc[nt]);
-                }
+            for (int nt = 0; nt < kNT; ++nt) {
+                const u32x2 y = {vx[nt][0] & msk0, vx[nt][1] & msk1};
+                acc[nt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(A, __builtin_bit_cast(s16x4, y), acc[nt], 0, 0, 0);
             }
         }
         // result per head g = 2 j + e: rows 4 j + 2 e (hi) and + 1 (lo)
@@ -837,22 +869,74 @@ struct DecodePlan {
     size_t qt_bytes, limb_bytes, aux_bytes, part_bytes;
 };
 
+template <int D, int BITS, int G>
+static void main_kernel_ptr(const void *&f)
+{
+    f = reinterpret_cast<const void *>(&decode_main_kernel<D, BITS, G>);
+}
+
+// Waves of decode_main_kernel the device keeps resident at once (its
+// occupancy from registers and LDS, times the compute units), cached per
+// variant; 256 compute units at three workgroups each when no device answers.
+static int64_t resident_waves(int D, int bits, int G)
+{
+    static int64_t cache[2][2][4] = {};
+    const int di = D == 128, bi = bits == 4, gi = G == 1 ? 0 : G == 2 ? 1 : G == 4 ? 2 : 3;
+    int64_t &slot = cache[di][bi][gi];
+    if (slot > 0) return slot;
+    const void *f = nullptr;
+    const int key = D * 100 + bits * 10 + gi;
+    switch (key) {
+        case 12820: main_kernel_ptr<128, 2, 1>(f); break;
+        case 12821: main_kernel_ptr<128, 2, 2>(f); break;
+        case 12822: main_kernel_ptr<128, 2, 4>(f); break;
+        case 12823: main_kernel_ptr<128, 2, 8>(f); break;
+        case 12840: main_kernel_ptr<128, 4, 1>(f); break;
+        case 12841: main_kernel_ptr<128, 4, 2>(f); break;
+        case 12842: main_kernel_ptr<128, 4, 4>(f); break;
+        case 12843: main_kernel_ptr<128, 4, 8>(f); break;
+        case 6420: main_kernel_ptr<64, 2, 1>(f); break;
+        case 6421: main_kernel_ptr<64, 2, 2>(f); break;
+        case 6422: main_kernel_ptr<64, 2, 4>(f); break;
+        case 6423: main_kernel_ptr<64, 2, 8>(f); break;
+        case 6440: main_kernel_ptr<64, 4, 1>(f); break;
+        case 6441: main_kernel_ptr<64, 4, 2>(f); break;
+        case 6442: main_kernel_ptr<64, 4, 4>(f); break;
+        default: main_kernel_ptr<64, 4, 8>(f); break;
+    }
+    int dev = 0, ncu = 0, blocks = 0;
+    int64_t waves = 256 * 3 * 4;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, f, 256, 0) == hipSuccess && ncu > 0 &&
+        blocks > 0)
+        waves = (int64_t)ncu * blocks * 4;
+    else
+        (void)hipGetLastError();
+    slot = waves;
+    return waves;
+}
+
 static bool make_plan(const wushkv_cache *c, int32_t n_q, int32_t max_seq_len, DecodePlan &p)
 {
     const int32_t G = n_q / c->n_kv_heads;
     const int64_t qpages = max_seq_len > c->s_sink ? (max_seq_len - c->s_sink + kPage - 1) / kPage : 0;
     const int64_t heads = (int64_t)c->batch * c->n_kv_heads;
-    // about three waves per SIMD over the chip (256 CUs x 4 SIMDs) for the
-    // page scan, at least 2 and at most 32 pages per wave
-    int64_t upw = (qpages * heads + 3071) / 3072;
-    if (upw < 2) upw = 2;
-    if (upw > 32) upw = 32;
+    // One residency round if it can be had: the page waves get what the
+    // window workgroups leave of the resident waves; at least 2 and at most
+    // 32 pages per wave.
+    const int64_t wunits = c->win_slots / kPage;
+    const int64_t budget = resident_waves(c->head_dim, c->bits, G) - 4 * heads * wunits;
+    int64_t upw = 2;
+    while (upw < 32 && heads * ((qpages + 4 * upw - 1) / (4 * upw)) * 4 > budget) ++upw;
     int64_t psplits = (qpages + 4 * upw - 1) / (4 * upw);
-    if (psplits + 1 > kMaxSplits) {
-        upw = (qpages + 4 * (kMaxSplits - 1) - 1) / (4 * (kMaxSplits - 1));
+    if (psplits + wunits > kMaxSplits) {
+        const int64_t room = kMaxSplits - wunits;
+        if (room < 1) return false;
+        upw = (qpages + 4 * room - 1) / (4 * room);
         psplits = (qpages + 4 * upw - 1) / (4 * upw);
     }
-    const int64_t splits = psplits + 1;  // the window workgroup
+    const int64_t splits = psplits + wunits;  // and one workgroup per window unit
     if (splits > kMaxSplits || upw > 0x7FFFFFFF / 4 / kMaxSplits) return false;
     p.units_per_wave = (int32_t)upw;
     p.n_page_splits = (int32_t)psplits;

@@ -108,10 +108,10 @@ def test_workspace_bytes_closed_form():
     # 16 bytes of scales and sum per query head (the latter rounded up to
     # 256); partials: one (o[d], m, l) per (sequence, kv head, split, query
     # head of the group).  ceil((1000 - 4)/64) = 16 pages per (sequence,
-    # head), 2 per wave, 8 per four-wave workgroup -> 2 page splits, plus the
-    # window workgroup -> 3 splits.
+    # head), 2 per wave, 8 per four-wave workgroup -> 2 page splits, plus one
+    # workgroup per 64 window slots (192 / 64 = 3) -> 5 splits.
     ws = L.wushkv_decode_workspace_bytes(ctypes.byref(d), 8, 1000)
-    assert ws == 2 * 8 * 128 * 4 + 2 * 8 * 6 * 128 + 256 + (2 * 2) * 3 * 4 * (128 + 2) * 4
+    assert ws == 2 * 8 * 128 * 4 + 2 * 8 * 6 * 128 + 256 + (2 * 2) * 5 * 4 * (128 + 2) * 4
 
 
 @pytest.mark.parametrize("d,bits", [(64, 2), (64, 4), (128, 2), (128, 4)])
