@@ -257,75 +257,68 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p)
     return (uint32_t)(uintptr_t)lds_ptr(const_cast<void *>(p));
 }
 
-// LDS accesses written as inline assembly: the compiler cannot tell the
-// direct-to-LDS staging slots apart from other LDS data and would wait for
-// every outstanding global load before any LDS access.  lds_wait() with the
-// values as read-write operands orders the uses after the reads.
+// LDS reads and writes are ordinary loads and stores, so the compiler tracks
+// their completion (and any register copies of their results) itself.  The
+// direct-to-LDS page loads are not visible to it (dma16 below): it would
+// otherwise wait for every one of them before any LDS access, since it
+// cannot tell the staging slots apart from the rest of LDS.  Ordering
+// against those loads is explicit: wait_vmcnt_at_most before a slot is read,
+// lds_drain before a slot is refilled; both are compiler barriers.
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
+typedef __attribute__((address_space(3))) u32x2 lds_u32x2;
+typedef __attribute__((address_space(3))) uint16_t lds_u16;
+
 __device__ __forceinline__ u32x4 lds_read16(uint32_t addr)
 {
-    u32x4 r;
-    asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr) : "memory");
-    return r;
-}
-__device__ __forceinline__ void lds_write8(uint32_t addr, uint32_t lo, uint32_t hi)
-{
-    typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
-    u32x2 v = {lo, hi};
-    asm volatile("ds_write_b64 %0, %1" ::"v"(addr), "v"(v) : "memory");
-}
-typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
-__device__ __forceinline__ void lds_write2(uint32_t addr, uint32_t v)
-{
-    asm volatile("ds_write_b16 %0, %1" ::"v"(addr), "v"(v) : "memory");
+    return *(const lds_u32x4 *)(uintptr_t)addr;
 }
 __device__ __forceinline__ u32x2 lds_read8(uint32_t addr)
 {
-    u32x2 r;
-    asm volatile("ds_read_b64 %0, %1" : "=v"(r) : "v"(addr) : "memory");
-    return r;
+    return *(const lds_u32x2 *)(uintptr_t)addr;
 }
-__device__ __forceinline__ void lds_wait2(u32x2 &x)
+__device__ __forceinline__ void lds_write8(uint32_t addr, uint32_t lo, uint32_t hi)
 {
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x)::"memory");
+    *(lds_u32x2 *)(uintptr_t)addr = u32x2{lo, hi};
 }
-
-template <int N>
-__device__ __forceinline__ void lds_wait(u32x4 (&x)[N])
+__device__ __forceinline__ void lds_write2(uint32_t addr, uint32_t v)
 {
-    static_assert(N >= 1 && N <= 8, "operands");
-    if constexpr (N == 1) asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x[0])::"memory");
-    else if constexpr (N == 2) asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x[0]), "+v"(x[1])::"memory");
-    else if constexpr (N == 3)
-        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x[0]), "+v"(x[1]), "+v"(x[2])::"memory");
-    else if constexpr (N == 4)
-        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3])::"memory");
-    else if constexpr (N == 6)
-        asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]), "+v"(x[4]), "+v"(x[5])::"memory");
-    else
-        asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]), "+v"(x[4]), "+v"(x[5]),
-                       "+v"(x[6]), "+v"(x[7])::"memory");
+    *(lds_u16 *)(uintptr_t)addr = (uint16_t)v;
+}
+// Every LDS access issued so far has completed.  The assembly form is the
+// compiler barrier (no memory access moves across it); the builtin form
+// tells the compiler's wait bookkeeping that nothing is outstanding, so it
+// adds no waits of its own for those accesses later.  (Encoding: vmcnt 63,
+// expcnt 7, lgkmcnt 0.)
+__device__ __forceinline__ void lds_drain()
+{
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xC07F);
 }
 
-// Wait for all but the last KEEP LDS accesses issued; the values in x (from
-// earlier reads) are then complete.
-template <int KEEP, int N>
-__device__ __forceinline__ void lds_wait_keep(u32x4 (&x)[N])
+// One 16-byte direct-to-LDS load per lane: lane L's bytes src .. src + 15
+// land at LDS byte lds_base + 16 L.  lds_base must be wave-uniform.  M0
+// carries the LDS base; its previous value is restored, so code the
+// compiler generates around this block sees M0 unchanged.  Not tracked by
+// the compiler: completion is waited for with wait_vmcnt_at_most.
+__device__ __forceinline__ void dma16(const void *src, uint32_t lds_base)
 {
-    static_assert(N == 4 || N == 6, "operands");
-    if constexpr (N == 4)
-        asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]) : "n"(KEEP) : "memory");
-    else
-        asm volatile("s_waitcnt lgkmcnt(%6)"
-                     : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]), "+v"(x[4]), "+v"(x[5])
-                     : "n"(KEEP)
-                     : "memory");
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\t"
+                 "s_mov_b32 m0, %2\n\t"
+                 "s_nop 0\n\t"
+                 "global_load_lds_dwordx4 %1, off\n\t"
+                 "s_mov_b32 m0, %0"
+                 : "=&s"(saved)
+                 : "v"(src), "s"(lds_base)
+                 : "memory");
 }
 
 // Wait until at most `after` direct-to-LDS loads are outstanding.  `after`
 // is a multiple of kDma between 0 and kMaxAhead * kDma; the count must be an
 // immediate, hence the cases.  The memory clobber keeps LDS reads below it.
+// The compiler's own vector-memory loads, if any are in flight, only make
+// the wait stricter (loads complete in issue order).
 template <int kMaxAhead, int kDma>
 __device__ __forceinline__ void wait_vmcnt_at_most(int after)
 {
@@ -475,11 +468,11 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
             int32_t phys = phys_of(u);
             if (phys < 0 || phys >= a.n_pages) phys = 0;
             const uint8_t *src = a.pages + ((int64_t)phys * a.n_kv + h) * L::kPageBytes + 16 * lane;
-            uint8_t *dst = stage + s * kSlot;
+            const uint32_t dst = __builtin_amdgcn_readfirstlane(lds_addr(stage + s * kSlot));
 #pragma unroll
             for (int i = 0; i < kDma; ++i) {
                 if (i + 1 < kDma || 1024 * i + 16 * lane < L::kPageBytes)
-                    __builtin_amdgcn_global_load_lds(src + 1024 * i, lds_ptr(dst + 1024 * i), 16, 0, 0);
+                    dma16(src + 1024 * i, dst + 1024 * i);
             }
         };
         // Per page: the value words are read at the top (they are needed only
@@ -509,7 +502,6 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
 #pragma unroll
                 for (int q4 = 0; q4 < kVX; ++q4)
                     vv[q4] = lds_read16(pg + L::kRegionBytes + 4 * L::v_word(lane, 4 * q4));
-                lds_wait_keep<kVX>(kx);  // the key reads are done, the value reads may run
                 const int32_t phys = phys_of(u);
                 // a page outside the pool contributes nothing (its stage holds page 0)
                 const int32_t nvalid = (phys < 0 || phys >= a.n_pages)
@@ -618,14 +610,12 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
                         lds_write8(lds_addr(tbuf + (G + hs) * kTP + 8 * n), l01, l23);
                     }
                 }
-                // A operands (two 32-token chunks); with them every read of
-                // this page's stage has completed
-                u32x4 ax[2 + kVX];
+                // A operands (two 32-token chunks); once they have arrived
+                // every read of this page's stage has completed
+                u32x4 ax[2];
                 ax[0] = lds_read16(a_addr);
                 ax[1] = lds_read16(a_addr + a_step);
-#pragma unroll
-                for (int q4 = 0; q4 < kVX; ++q4) ax[2 + q4] = vv[q4];
-                lds_wait(ax);
+                lds_drain();
                 if (u + 2 < w1) issue(u + 2, s);
                 if (u + 1 < w1) {
                     // page u + 1 has landed once at most page u + 2's loads remain
@@ -639,7 +629,7 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
                     for (int uu = 0; uu < 2 * kNw; ++uu) {
                         const int widx = kc * 2 * kNw + uu;
                         uint32_t op[L::kCodesPerWord / 2];
-                        widen_word_f16<BITS>(ax[2 + widx / 4][widx % 4], op);
+                        widen_word_f16<BITS>(vv[widx / 4][widx % 4], op);
 #pragma unroll
                         for (int o = 0; o < kOpw; ++o) {
                             const int nt = uu * kOpw + o;
@@ -704,7 +694,6 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
             u32x4 kx[kC];
 #pragma unroll
             for (int c = 0; c < kC; ++c) kx[c] = *reinterpret_cast<const u32x4 *>(krow + 32 * c);
-            typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
             const uint16_t *vrow = a.win_v + head_win * D + slot0 + 4 * j;
             u32x2 vx[kNT];
 #pragma unroll
@@ -760,8 +749,7 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
             // A operand of the 16x16x16 product: row m = 2 g + part, tokens
             // 4 j .. 4 j + 3
             const uint32_t pa_addr = n < 2 * G ? lds_addr(tbuf + ((n & 1) * G + (n >> 1)) * kTP + 8 * j) : zero_row;
-            u32x2 pa = lds_read8(pa_addr);
-            lds_wait2(pa);
+            const u32x2 pa = lds_read8(pa_addr);
             // dead slots' values are zeroed, whatever bits they hold
             const uint32_t bits4 = (vmask >> (4 * j)) & 0xFu;
             const uint32_t msk0 = ((bits4 & 1u) ? 0x0000FFFFu : 0u) | ((bits4 & 2u) ? 0xFFFF0000u : 0u);
