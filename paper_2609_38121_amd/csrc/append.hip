@@ -12,10 +12,11 @@
 //            fp32 accumulate, rounded once to bf16 -> LDS.  Keys that are
 //            flushed from the recent ring are copied from it instead.
 //            Values (new or ring) -> LDS.
-//   phase B  one thread per (token, K|V) group: exact top-k of |x| with a
-//            median-of-three insertion network, the type-7 quantile, fp16
-//            scale/zero and the codes.  Key codes go straight to their words;
-//            value codes go to LDS.
+//   phase B  two lanes per (token, K|V) group, half the channels each:
+//            exact top-k of |x| with a median-of-three insertion network
+//            (each lane over its half, then its partner's list merged in),
+//            the type-7 quantile, fp16 scale/zero and the codes.  Key codes
+//            go straight to their words; value codes go to LDS.
 //   phase C  value-code words (each spans 8 tokens) are assembled from LDS;
 //            words only partly covered by this call are merged with what the
 //            page already holds.
@@ -72,19 +73,31 @@ struct TopK {
     }
 };
 
+// The value of the partner lane (lane ^ 1): the two lanes of a pair share
+// one quantisation group, half of its elements each.
+__device__ __forceinline__ float pair_swap(float x)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0xB1, 0xF,
+                                                              0xF, false));
+}
+
 // a_lo and a_{lo+1} of the ascending sort of |x| over a bf16 row in LDS,
-// for lo >= D - KMAX.
+// for lo >= D - KMAX, with the row's min and max.  The lane pair (2 r,
+// 2 r + 1) shares row r: each lane keeps the top KMAX of |x| over its half of
+// the row, then inserts its partner's list, so that both hold the top KMAX
+// of the whole row (the same multiset, hence the same sorted list).
 template <int D, int KMAX>
-__device__ __forceinline__ void order_stats_topk(const uint16_t *row, int lo, float &a_lo,
+__device__ __forceinline__ void order_stats_topk(const uint16_t *row, int hf, int lo, float &a_lo,
                                                  float &a_hi, float &mn, float &mx)
 {
     TopK<KMAX> tk;
     tk.init();
     mn = INFINITY;
     mx = -INFINITY;
+    const uint16_t *half = row + hf * (D / 2);
 #pragma unroll 4
-    for (int c8 = 0; c8 < D / 8; ++c8) {
-        uint4 v = *reinterpret_cast<const uint4 *>(row + 8 * c8);
+    for (int c8 = 0; c8 < D / 16; ++c8) {
+        uint4 v = *reinterpret_cast<const uint4 *>(half + 8 * c8);
         uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -97,6 +110,13 @@ __device__ __forceinline__ void order_stats_topk(const uint16_t *row, int lo, fl
             }
         }
     }
+    float other[KMAX];
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) other[i] = pair_swap(tk.t[i]);
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) tk.push(other[i]);
+    mn = fminf(mn, pair_swap(mn));
+    mx = fmaxf(mx, pair_swap(mx));
     const int K = D - lo;  // a_lo is the K-th largest
     a_lo = tk.get(K - 1);
     a_hi = (K >= 2) ? tk.get(K - 2) : a_lo;
@@ -104,15 +124,18 @@ __device__ __forceinline__ void order_stats_topk(const uint16_t *row, int lo, fl
 
 // Same order statistics by counting ranks: any lo, O(D^2) work.  Used when
 // kappa is small enough that the top-k list would not fit in registers.
+// Each lane of the pair ranks the elements of its half against the whole
+// row; an order statistic is found in the half (or halves, for equal values)
+// that holds it.
 template <int D>
-__device__ __noinline__ void order_stats_rank(const uint16_t *row, int lo, float &a_lo,
+__device__ __forceinline__ void order_stats_rank(const uint16_t *row, int hf, int lo, float &a_lo,
                                               float &a_hi, float &mn, float &mx)
 {
     mn = INFINITY;
     mx = -INFINITY;
-    a_lo = 0.0f;
-    a_hi = 0.0f;
-    for (int e = 0; e < D; ++e) {
+    a_lo = -1.0f;
+    a_hi = -1.0f;
+    for (int e = hf * (D / 2); e < (hf + 1) * (D / 2); ++e) {
         float xe = bf16_bits_to_f32(row[e]);
         mn = fminf(mn, xe);
         mx = fmaxf(mx, xe);
@@ -127,6 +150,10 @@ __device__ __noinline__ void order_stats_rank(const uint16_t *row, int lo, float
         if (less <= lo && lo < le) a_lo = ae;
         if (less <= lo + 1 && lo + 1 < le) a_hi = ae;
     }
+    a_lo = fmaxf(a_lo, pair_swap(a_lo));
+    a_hi = fmaxf(a_hi, pair_swap(a_hi));
+    mn = fminf(mn, pair_swap(mn));
+    mx = fmaxf(mx, pair_swap(mx));
     if (lo + 1 >= D) a_hi = a_lo;
 }
 
@@ -161,16 +188,26 @@ __device__ __forceinline__ uint32_t code_of(float x, float z, float inv, float l
 }
 
 template <int D, int BITS>
-__device__ void order_stats(const uint16_t *row, int lo, float &a_lo, float &a_hi, float &mn,
-                            float &mx)
+__device__ void order_stats(const uint16_t *row, int hf, int lo, float &a_lo, float &a_hi,
+                            float &mn, float &mx)
 {
     const int K = D - lo;
-    if (K <= 2) order_stats_topk<D, 2>(row, lo, a_lo, a_hi, mn, mx);
-    else if (K <= 4) order_stats_topk<D, 4>(row, lo, a_lo, a_hi, mn, mx);
-    else if (K <= 8) order_stats_topk<D, 8>(row, lo, a_lo, a_hi, mn, mx);
-    else if (K <= 12) order_stats_topk<D, 12>(row, lo, a_lo, a_hi, mn, mx);
-    else if (K <= 16) order_stats_topk<D, 16>(row, lo, a_lo, a_hi, mn, mx);
-    else order_stats_rank<D>(row, lo, a_lo, a_hi, mn, mx);
+    if (K <= 2) order_stats_topk<D, 2>(row, hf, lo, a_lo, a_hi, mn, mx);
+    else if (K <= 4) order_stats_topk<D, 4>(row, hf, lo, a_lo, a_hi, mn, mx);
+    else if (K <= 8) order_stats_topk<D, 8>(row, hf, lo, a_lo, a_hi, mn, mx);
+    else if (K <= 12) order_stats_topk<D, 12>(row, hf, lo, a_lo, a_hi, mn, mx);
+    else if (K <= 16) order_stats_topk<D, 16>(row, hf, lo, a_lo, a_hi, mn, mx);
+    else order_stats_rank<D>(row, hf, lo, a_lo, a_hi, mn, mx);
+}
+
+// Value codes (one byte each) are written over the value row they come
+// from: the lane holding channels [h D / 2, (h + 1) D / 2) of row t writes
+// their codes at bytes h D .. h D + D / 2 - 1 of that row, inside the bytes
+// it has already read.
+template <int D>
+__device__ __forceinline__ uint8_t *vcode_row(uint16_t *vt, int t)
+{
+    return reinterpret_cast<uint8_t *>(vt + t * (D + 8));
 }
 
 // Phases B and C of a tile of up to 64 positions starting at blk_lo, all in
@@ -180,59 +217,67 @@ __device__ void order_stats(const uint16_t *row, int lo, float &a_lo, float &a_h
 // words only partly covered with what the page holds.  Every thread of the
 // workgroup must call it (it synchronises).
 template <int D, int BITS, typename Pred>
-__device__ void quantise_tile(const AppendArgs &a, const uint16_t *kt, const uint16_t *vt,
-                              uint8_t *vcodes, int32_t blk_lo, Pred quant, uint8_t *pg, int tid)
+__device__ void quantise_tile(const AppendArgs &a, const uint16_t *kt, uint16_t *vt,
+                              int32_t blk_lo, Pred quant, uint8_t *pg, int tid)
 {
     using L = Layout<D, BITS>;
     constexpr int kPitch = D + 8;
-    // ---- phase B: quantise (threads 0-63 keys, 64-127 values)
-    if (tid < 2 * kPage) {
-        const bool is_v = tid >= kPage;
-        const int r = tid & (kPage - 1);
+    // ---- phase B: quantise.  Lanes 2 r and 2 r + 1 share group r (rows
+    // 0-63 keys, 64-127 values), one half of its channels each, so that all
+    // four waves take part.
+    {
+        const int grp = tid >> 1, hf = tid & 1;
+        const bool is_v = grp >= kPage;
+        const int r = grp & (kPage - 1);
         const int32_t p = blk_lo + r;
-        if (quant(p) && pg != nullptr) {
+        if (quant(p) && pg != nullptr) {  // the same for both lanes of the pair
             const uint16_t *row = (is_v ? vt : kt) + r * kPitch;
             const int qlo = is_v ? a.lo_v : a.lo_k;
             const float qt = is_v ? a.t_v : a.t_k;
             float a_lo, a_hi, mn, mx;
-            order_stats<D, BITS>(row, qlo, a_lo, a_hi, mn, mx);
+            order_stats<D, BITS>(row, hf, qlo, a_lo, a_hi, mn, mx);
             uint32_t s16, z16;
             float z, inv;
             constexpr int kLevels = (1 << BITS) - 1;
             quant_params(a_lo, a_hi, qt, qlo + 1 < D, mn, mx, kLevels, s16, z16, z, inv);
-            *reinterpret_cast<uint32_t *>(pg + L::kParamOffset + 4 * r + (is_v ? 4 * kPage : 0)) =
-                s16 | (z16 << 16);
+            if (hf == 0)
+                *reinterpret_cast<uint32_t *>(pg + L::kParamOffset + 4 * r + (is_v ? 4 * kPage : 0)) =
+                    s16 | (z16 << 16);
+            constexpr int kHalf = D / 2;
+            const int c0 = hf * kHalf;  // first channel of this lane's half
             if (!is_v) {
                 // key words of this token: lane group jj = ch / 32 holds
-                // BITS words per token (see Layout::k_pos)
-                uint32_t kw[D / 32][BITS];
+                // BITS words per token (see Layout::k_pos); this half covers
+                // groups hf D / 64 .. (hf + 1) D / 64 - 1
+                uint32_t kw[D / 64][BITS];
 #pragma unroll
-                for (int jj = 0; jj < D / 32; ++jj)
+                for (int jl = 0; jl < D / 64; ++jl)
 #pragma unroll
-                    for (int w = 0; w < BITS; ++w) kw[jj][w] = 0u;
+                    for (int w = 0; w < BITS; ++w) kw[jl][w] = 0u;
 #pragma unroll
-                for (int c8 = 0; c8 < D / 8; ++c8) {
-                    uint4 v = *reinterpret_cast<const uint4 *>(row + 8 * c8);
+                for (int c8 = 0; c8 < kHalf / 8; ++c8) {
+                    uint4 v = *reinterpret_cast<const uint4 *>(row + c0 + 8 * c8);
                     uint32_t wv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
                     for (int i = 0; i < 8; ++i) {
                         uint32_t hb = (i & 1) ? (wv[i >> 1] >> 16) : (wv[i >> 1] & 0xFFFFu);
                         uint32_t code = code_of(bf16_bits_to_f32(hb), z, inv, (float)kLevels);
+                        const int cl = 8 * c8 + i;  // channel c0 + cl
                         int word, bit;
-                        L::k_pos(r, 8 * c8 + i, word, bit);
-                        kw[(8 * c8 + i) >> 5][((8 * c8 + i) & 31) / (32 / BITS)] |= code << bit;
+                        L::k_pos(r, c0 + cl, word, bit);
+                        kw[cl >> 5][(cl & 31) / (32 / BITS)] |= code << bit;
                     }
                 }
                 uint32_t *kreg = reinterpret_cast<uint32_t *>(pg);
 #pragma unroll
-                for (int jj = 0; jj < D / 32; ++jj)
+                for (int jl = 0; jl < D / 64; ++jl)
 #pragma unroll
                     for (int w = 0; w < BITS; ++w)
-                        kreg[L::k_word(16 * jj + (r >> 2), BITS * (r & 3) + w)] = kw[jj][w];
+                        kreg[L::k_word(16 * (hf * (D / 64) + jl) + (r >> 2), BITS * (r & 3) + w)] = kw[jl][w];
             } else {
 #pragma unroll
-                for (int c8 = 0; c8 < D / 8; ++c8) {
-                    uint4 v = *reinterpret_cast<const uint4 *>(row + 8 * c8);
+                for (int c8 = 0; c8 < kHalf / 8; ++c8) {
+                    uint4 v = *reinterpret_cast<const uint4 *>(row + c0 + 8 * c8);
                     uint32_t wv[4] = {v.x, v.y, v.z, v.w};
                     uint32_t lo4 = 0, hi4 = 0;
 #pragma unroll
@@ -242,7 +287,8 @@ __device__ void quantise_tile(const AppendArgs &a, const uint16_t *kt, const uin
                         if (i < 4) lo4 |= code << (8 * i);
                         else hi4 |= code << (8 * (i - 4));
                     }
-                    *reinterpret_cast<uint2 *>(vcodes + r * D + 8 * c8) = make_uint2(lo4, hi4);
+                    // over bytes of this lane's half of the row that it has read
+                    *reinterpret_cast<uint2 *>(vcode_row<D>(vt, r) + hf * D + 8 * c8) = make_uint2(lo4, hi4);
                 }
             }
         }
@@ -268,7 +314,7 @@ __device__ void quantise_tile(const AppendArgs &a, const uint16_t *kt, const uin
                     const int ch = 16 * (u * L::kOpsPerWord + o) + m;
                     const int bit = L::v_bit(o, i);
                     mask |= ((1u << BITS) - 1u) << bit;
-                    bits |= (uint32_t)vcodes[t * D + ch] << bit;
+                    bits |= (uint32_t)vcode_row<D>(vt, t)[ch + (ch >= D / 2 ? D / 2 : 0)] << bit;
                 }
             }
             if (mask == 0u) continue;
@@ -286,7 +332,6 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
     constexpr int kPitch = D + 8;  // bf16 elements per LDS row (16 B pad)
     __shared__ __attribute__((aligned(16))) uint16_t kt[kPage * kPitch];
     __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * kPitch];
-    __shared__ __attribute__((aligned(16))) uint8_t vcodes[kPage * D];
     __shared__ int32_t sh_page;
 
     const int tid = threadIdx.x;
@@ -341,6 +386,21 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
     const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;  // win_k row base (slots)
     const uint16_t *tk_h = a.tk + (int64_t)h * D * D;
 
+    // new values of this tile: loaded first, so that their latency overlaps
+    // the key transform (idx = tid + 256 q is row idx / kVec, 16-byte chunk
+    // idx % kVec)
+    constexpr int kVec = D / 8;                   // uint4 per row
+    constexpr int kVPer = kPage * kVec / 256;     // uint4 per thread
+    uint4 vpre[kVPer];
+#pragma unroll
+    for (int q = 0; q < kVPer; ++q) {
+        const int idx = tid + 256 * q, r = idx / kVec, cv = idx % kVec;
+        const int32_t p = blk_lo + r;
+        if (p >= lo && p < hi && do_new && is_new(p))
+            vpre[q] = *reinterpret_cast<const uint4 *>(
+                a.v_new + (((int64_t)b * a.max_new + (p - s_old)) * a.n_kv + h) * D + 8 * cv);
+    }
+
     // ---- phase A: transformed keys -> kt, values -> vt
     bool any_new = false;
     for (int32_t p = lo; p < hi; ++p) any_new |= (do_new && is_new(p));
@@ -388,23 +448,22 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
     }
     // ring-sourced keys (flush) and all values, 16 B per thread-step
     {
-        constexpr int kVec = D / 8;  // uint4 per row
-        for (int idx = tid; idx < kPage * kVec; idx += 256) {
-            const int r = idx / kVec, cv = idx % kVec;
+#pragma unroll
+        for (int q = 0; q < kVPer; ++q) {
+            const int idx = tid + 256 * q, r = idx / kVec, cv = idx % kVec;
             const int32_t p = blk_lo + r;
             if (p < lo || p >= hi) continue;
             const bool nw = is_new(p);
             if (nw ? !do_new : !quant_now(p)) continue;
             uint4 vv;
             if (nw) {
-                vv = *reinterpret_cast<const uint4 *>(
-                    a.v_new + (((int64_t)b * a.max_new + (p - s_old)) * a.n_kv + h) * D + 8 * cv);
+                vv = vpre[q];
             } else {
                 const int32_t slot = ring_slot(p, a.s_sink, ring);
                 const uint16_t *vsrc = a.win_v + (head_win * D) + slot;  // channel-major
                 uint16_t e[8];
 #pragma unroll
-                for (int q = 0; q < 8; ++q) e[q] = vsrc[(int64_t)(8 * cv + q) * a.win_slots];
+                for (int qq = 0; qq < 8; ++qq) e[qq] = vsrc[(int64_t)(8 * cv + qq) * a.win_slots];
                 vv.x = e[0] | ((uint32_t)e[1] << 16);
                 vv.y = e[2] | ((uint32_t)e[3] << 16);
                 vv.z = e[4] | ((uint32_t)e[5] << 16);
@@ -420,7 +479,7 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
     uint8_t *pg = page >= 0 ? a.pages + ((int64_t)page * a.n_kv + h) * L::kPageBytes : nullptr;
 
     // ---- phases B and C
-    quantise_tile<D, BITS>(a, kt, vt, vcodes, blk_lo, [&](int32_t p) { return p >= lo && p < hi && quant_now(p); },
+    quantise_tile<D, BITS>(a, kt, vt, blk_lo, [&](int32_t p) { return p >= lo && p < hi && quant_now(p); },
                            pg, tid);
 
     // ---- phase D: bf16 windows and the optional k~ output
@@ -471,7 +530,6 @@ __global__ void __launch_bounds__(256) append_step_kernel(AppendArgs a)
     __shared__ __attribute__((aligned(16))) uint16_t kn[kStepMax * kPitch];
     __shared__ __attribute__((aligned(16))) uint16_t kt[kPage * kPitch];
     __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * kPitch];
-    __shared__ __attribute__((aligned(16))) uint8_t vcodes[kPage * D];
     __shared__ float kin[D];
     __shared__ int32_t sh_page;
 
@@ -563,7 +621,7 @@ __global__ void __launch_bounds__(256) append_step_kernel(AppendArgs a)
             __syncthreads();
             const int32_t page = sh_page;
             uint8_t *pg = page >= 0 ? a.pages + ((int64_t)page * a.n_kv + h) * L::kPageBytes : nullptr;
-            quantise_tile<D, BITS>(a, kt, vt, vcodes, blk, [&](int32_t p) { return p >= lo && p < hi; },
+            quantise_tile<D, BITS>(a, kt, vt, blk, [&](int32_t p) { return p >= lo && p < hi; },
                                    pg, tid);
             __syncthreads();
         }
@@ -596,9 +654,9 @@ __global__ void append_commit_kernel(int32_t *seq_len, int32_t *quant_end, const
 }
 
 template <int D, int BITS>
-static hipError_t launch_append(const AppendArgs &a, dim3 grid, hipStream_t s)
+static hipError_t launch_append(const char *name, const AppendArgs &a, dim3 grid, hipStream_t s)
 {
-    launch("append_kernel", append_kernel<D, BITS>, grid, dim3(256), s, a);
+    launch(name, append_kernel<D, BITS>, grid, dim3(256), s, a);
     return hipGetLastError();
 }
 
@@ -672,17 +730,23 @@ extern "C" int wushkv_append(const wushkv_cache *c, const uint16_t *k_new, const
 
     // Flushed ring slots may be reused by new tokens of the same call only if
     // the ring is shorter than the span; then flush first, in its own launch.
+    // That launch only touches positions already in the ring, which span at
+    // most the ring's length from the first unflushed one.
     const int64_t ring = (int64_t)c->win_slots - c->s_sink;
     const bool fused = ring >= span;
+    const dim3 flush_grid((unsigned)std::min<int64_t>(tiles, a.sink_tiles + (ring + kPage - 1) / kPage + 1),
+                          grid.y, grid.z);
 
     auto go = [&](int mode) -> hipError_t {
         a.mode = mode;
+        const char *name = mode == kModeFlush ? "append_flush" : "append_kernel";
+        const dim3 g = mode == kModeFlush ? flush_grid : grid;
         const int key = c->head_dim * 10 + c->bits;
         switch (key) {
-            case 1282: return launch_append<128, 2>(a, grid, s);
-            case 1284: return launch_append<128, 4>(a, grid, s);
-            case 642: return launch_append<64, 2>(a, grid, s);
-            case 644: return launch_append<64, 4>(a, grid, s);
+            case 1282: return launch_append<128, 2>(name, a, g, s);
+            case 1284: return launch_append<128, 4>(name, a, g, s);
+            case 642: return launch_append<64, 2>(name, a, g, s);
+            case 644: return launch_append<64, 4>(name, a, g, s);
         }
         return hipErrorInvalidValue;
     };
