@@ -52,6 +52,10 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline leg")
     ap.add_argument("--prefill-only", action="store_true",
                     help="only run the append-throughput leg and print its JSON object")
+    ap.add_argument("--no-scale", action="store_true",
+                    help="skip the decode legs at the long-context and large-batch sizes")
+    ap.add_argument("--scale-only", action="store_true",
+                    help="only run the long-context / large-batch decode legs")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 512 MiB device-to-device copy five times (a known-size "
@@ -165,6 +169,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.prefill_only:
         print(json.dumps(bench_prefill(torch, wk, synth, dev, args)), flush=True)
+        return
+    if args.scale_only:
+        print(json.dumps(bench_decode_scale(torch, wk, synth, dev, args)), flush=True)
         return
     cfg = synth.CONFIGS["llama8b"]
     w = synth.Workload(cfg, seed=args.seed)
@@ -331,6 +338,11 @@ def main():
     if not args.no_prefill:
         prefill = bench_prefill(torch, wk, synth, dev, args)
 
+    # ---- decode alone at the long-context and large-batch sizes
+    scale = None
+    if not args.no_scale:
+        scale = bench_decode_scale(torch, wk, synth, dev, args)
+
     # ---- oracle baseline on the host
     cpu = None
     if not args.no_cpu:
@@ -369,6 +381,7 @@ def main():
         "eager_step_us": round(ms_eager * 1e3, 3),
         "kernel_avg_us": {k_: (round(v_ * 1e3, 3) if v_ else None) for k_, v_ in kernels.items()},
         "append": prefill,
+        "decode_at_scale": scale,
     }
     print(json.dumps(line), flush=True)
 
@@ -427,6 +440,84 @@ def bench_prefill(torch, wk, synth, dev, args):
                          "traffic": None, "avg_us": round(t_kernel * 1e3, 3)},
             "flush_launch_us": round(t_flush * 1e3, 3),
             "roofline_tokens_per_s": round(tokens / (byts / (PEAK_HBM_GBS * 1e9)), 1)}
+
+
+def bench_decode_scale(torch, wk, synth, dev, args, calls=24):
+    """Decode calls alone on the long-context (131072 tokens, 2 and 4 bits,
+    random page order) and large-batch (64 ragged sequences of 16384-32768
+    tokens) caches.  The caches are filled by the library's own append from
+    seeded device-side Gaussian keys and values (throughput does not depend
+    on the values); lengths are the workloads' own.  Replicas are cycled so
+    that the calls touch more than twice the 256 MB Infinity Cache."""
+    out = {}
+    for name in ("long2", "long4", "bigbatch"):
+        cfg = synth.CONFIGS[name]
+        w = synth.Workload(cfg, seed=args.seed)
+        B, H, NQ, D, BITS = cfg["batch"], cfg["n_kv"], cfg["n_q"], cfg["d"], cfg["bits"]
+        lengths = w.lengths.astype(np.int64)
+        cap = int(lengths.max()) + 64
+        cache = wk.WushKVCache(B, H, D, BITS, cfg["s_sink"], cfg["s_keep"], cfg["s_flush"],
+                               cfg["kappa_k"], cfg["kappa_v"], max_seq_len=cap,
+                               page_order=cfg.get("page_order", "linear"),
+                               pool_factor=cfg.get("pool_factor", 1.0), seed=args.seed, device=dev)
+        gen = torch.Generator(device=dev).manual_seed(1000 + args.seed)
+        tk = torch.eye(D, device=dev).expand(H, D, D).to(torch.bfloat16).contiguous()
+        chunk = 4096
+        done = np.zeros(B, np.int64)
+        while (done < lengths).any():
+            n = np.minimum(chunk, lengths - done)
+            m = int(n.max())
+            k = torch.randn(B, m, H, D, generator=gen, device=dev).to(torch.bfloat16)
+            v = torch.randn(B, m, H, D, generator=gen, device=dev).to(torch.bfloat16)
+            wk.wushkv_append(cache, k, v, torch.from_numpy(n.astype(np.int32)).to(dev), tk)
+            done += n
+        torch.cuda.synchronize()
+        del k, v
+        seq = cache.seq_len.cpu().numpy()
+        qe = cache.quant_end.cpu().numpy()
+        main_b, other_b = decode_bytes(seq, qe, cfg["s_sink"], H, NQ, D, BITS)
+        cache_bytes = cache.pages.numel() + 2 * cache.win_k.numel() * 2
+        reps = max(1, math.ceil(2 * MALL_BYTES / cache_bytes))
+        caches = [cache] + [cache.clone() for _ in range(reps - 1)]
+        q = torch.randn(B, NQ, D, generator=gen, device=dev).to(torch.bfloat16)
+        tinv = torch.eye(D, device=dev).expand(H, D, D).contiguous()
+        ws = [torch.empty(wk.wushkv_decode_workspace_bytes(cache, NQ, cap), dtype=torch.uint8,
+                          device=dev) for _ in range(reps)]
+        outs = [torch.empty(B, NQ, D, dtype=torch.float32, device=dev) for _ in range(reps)]
+        call = lambda i: wk.wushkv_decode_attention(caches[i % reps], q, tinv, max_seq_len=cap,
+                                                    out=outs[i % reps], workspace=ws[i % reps])
+        for i in range(2 * reps):
+            call(i)
+        torch.cuda.synchronize()
+        n_calls = max(calls, reps) // reps * reps
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(n_calls):
+            call(i)
+        e1.record()
+        torch.cuda.synchronize()
+        t_call = e0.elapsed_time(e1) / n_calls * 1e-3
+        wk.wushkv_timing_enable(8 * n_calls)
+        for i in range(n_calls):
+            call(i)
+        torch.cuda.synchronize()
+        cnt, tot = wk.wushkv_timing_read("decode_main_kernel")
+        wk.wushkv_timing_enable(0)
+        t_main = tot / cnt * 1e-3
+        ach = main_b / t_main / 1e9
+        log("%s decode: call %.1f us (%.1f GB/s), decode_main_kernel %.1f us, %.1f GB/s (%.1f%% of "
+            "8 TB/s), %d replicas" % (name, t_call * 1e6, (main_b + other_b) / t_call / 1e9,
+                                      t_main * 1e6, ach, 100 * ach / PEAK_HBM_GBS, reps))
+        out[name] = {"batch": B, "ctx_max": int(lengths.max()), "bits": BITS,
+                     "tokens": int(seq.sum()), "bytes_per_call": int(main_b + other_b),
+                     "call_us": round(t_call * 1e6, 2),
+                     "call_gbps": round((main_b + other_b) / t_call / 1e9, 1),
+                     "main_kernel_us": round(t_main * 1e6, 2),
+                     "main_kernel_gbps": round(ach, 1),
+                     "main_kernel_frac": round(ach / PEAK_HBM_GBS, 4), "replicas": reps}
+        del caches, cache, ws, outs
+        torch.cuda.empty_cache()
+    return out
 
 
 def bench_oracle(cfg, w, tk_bits, tinv, budget_s):

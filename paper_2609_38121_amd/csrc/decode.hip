@@ -329,12 +329,11 @@ __device__ __forceinline__ void wait_vmcnt_at_most(int after)
 }
 
 __device__ __forceinline__ f32x4 mfma_scaled(const i32x8 &a, const i32x8 &b, int fmt_b, int scale_a,
-                                             int scale_b)
+                                             int scale_b, f32x4 c)
 {
-    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
     if (fmt_b == 4)
-        return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, z, 0, 4, 0, scale_a, 0, scale_b);
-    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, z, 0, 0, 0, scale_a, 0, scale_b);
+        return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 4, 0, scale_a, 0, scale_b);
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, scale_a, 0, scale_b);
 }
 
 // LDS per wave: page stages (also the merge buffer) and the weight buffer.
@@ -374,7 +373,9 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
     __shared__ __attribute__((aligned(16))) uint8_t lds[4 * M::kWave];
     __shared__ float sM[4][8], sL[4][8];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // the wave index is uniform across the wave: keep it (and the page range
+    // derived from it) in scalar registers
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int j = lane >> 4, n = lane & 15;
     const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
     uint8_t *stage = lds + wave * M::kWave;
@@ -479,7 +480,8 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
         // by the P V products at the end); the key words and parameters of
         // page u were read at the end of iteration u - 1, while its P V
         // products ran.  A page's stage is refilled (page u + 2) as soon as
-        // its last LDS read has completed, before the P V products.
+        // its value reads have completed, right after the score products are
+        // issued.
         constexpr int kKX = L::kKWordsPerLane / 4;  // key chunks per lane
         constexpr int kVX = L::kWordsPerLane / 4;   // value chunks per lane
         auto read_keys = [&](uint32_t pg, u32x4 (&kx)[kKX + 2]) {
@@ -488,20 +490,26 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
             kx[kKX] = lds_read16(pg + L::kParamOffset + 16 * n);
             kx[kKX + 1] = lds_read16(pg + L::kParamOffset + 4 * kPage + 16 * n);
         };
+        auto read_values = [&](uint32_t pg, u32x4 (&vx)[kVX]) {
+#pragma unroll
+            for (int q4 = 0; q4 < kVX; ++q4) vx[q4] = lds_read16(pg + L::kRegionBytes + 4 * L::v_word(lane, 4 * q4));
+        };
         if (a.n_pages > 0 && w0 < w1) {
-            static_assert(kStages == 2, "two stages per wave");
+            // Three stages: page u in registers, pages u + 1 and u + 2 in
+            // flight to the two LDS slots.  A slot is emptied into registers
+            // as soon as its page has landed and refilled right away, so both
+            // slots stay in flight while a page is computed.
+            static_assert(kStages == 2, "two slots per wave");
             issue(w0, 0);
             if (w0 + 1 < w1) issue(w0 + 1, 1);
             wait_vmcnt_at_most<1, kDma>(w0 + 1 < w1 ? kDma : 0);
-            u32x4 kx[kKX + 2];
+            u32x4 kx[kKX + 2], vv[kVX];
             read_keys(lds_addr(stage), kx);
+            read_values(lds_addr(stage), vv);
+            lds_drain();
+            if (w0 + 2 < w1) issue(w0 + 2, 0);
             for (int u = w0; u < w1; ++u) {
                 const int s = (u - w0) & 1;
-                const uint32_t pg = lds_addr(stage + s * kSlot);
-                u32x4 vv[kVX];
-#pragma unroll
-                for (int q4 = 0; q4 < kVX; ++q4)
-                    vv[q4] = lds_read16(pg + L::kRegionBytes + 4 * L::v_word(lane, 4 * q4));
                 const int32_t phys = phys_of(u);
                 // a page outside the pool contributes nothing (its stage holds page 0)
                 const int32_t nvalid = (phys < 0 || phys >= a.n_pages)
@@ -527,14 +535,20 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
                                        (int)(w[3] & 0x0F0F0F0Fu), (int)((w[3] >> 4) & 0x0F0F0F0Fu)};
                     }
                 }
-                f32x4 c[kHG][4][2];
+                // limbs 4-5 (rows 4 g' + 0, 1 of the second product) are
+                // accumulated onto limbs 0-1 of the first, so each head's six
+                // limbs end up in its four rows
+                f32x4 c[kHG][4];
 #pragma unroll
                 for (int t = 0; t < 4; ++t)
 #pragma unroll
                     for (int hg = 0; hg < kHG; ++hg)
+                        c[hg][t] = mfma_scaled(qa[hg][0], bop[t], kFmtB, qsc[hg][0], kScaleB, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
-                        for (int part = 0; part < 2; ++part)
-                            c[hg][t][part] = mfma_scaled(qa[hg][part], bop[t], kFmtB, qsc[hg][part], kScaleB);
+                for (int t = 0; t < 4; ++t)
+#pragma unroll
+                    for (int hg = 0; hg < kHG; ++hg)
+                        c[hg][t] = mfma_scaled(qa[hg][1], bop[t], kFmtB, qsc[hg][1], kScaleB, c[hg][t]);
                 float lg[kHG][4];
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
@@ -542,9 +556,8 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
                     const float kz = f16_bits_to_f32(kp[t] >> 16);
 #pragma unroll
                     for (int hg = 0; hg < kHG; ++hg) {
-                        const f32x4 &c0 = c[hg][t][0], &c1 = c[hg][t][1];
-                        // the six limbs, most significant first
-                        const float dot = (((c0[0] + c0[1]) + c0[2]) + (c0[3] + c1[0])) + c1[1];
+                        const f32x4 &c0 = c[hg][t];
+                        const float dot = (c0[0] + c0[1]) + (c0[2] + c0[3]);
                         lg[hg][t] = fmaf(ks, dot, kz * zs[hg]);
                     }
                 }
@@ -596,31 +609,33 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
                         const float pw = fexp2(lg[hg][t] - mo);
                         lc[hg] += pw;
                         zc[hg] = fmaf(pw, f16_bits_to_f32(vp[t] >> 16), zc[hg]);
-                        wgt[t] = pw * f16_bits_to_f32(vp[t] & 0xFFFFu);
+                        // one mixed-precision product, rounded once like pw * s
+                        wgt[t] = fmaf(pw, f16_bits_to_f32(vp[t] & 0xFFFFu), 0.0f);
                     }
                     const int hs = G > 4 ? 2 * j + hg : j;
                     if (hs < G) {
                         const uint32_t h01 = pack_f16_rne(wgt[0], wgt[1]);
                         const uint32_t h23 = pack_f16_rne(wgt[2], wgt[3]);
-                        const uint32_t l01 = pack_f16_rne(wgt[0] - f16_bits_to_f32(h01 & 0xFFFFu),
-                                                          wgt[1] - f16_bits_to_f32(h01 >> 16));
-                        const uint32_t l23 = pack_f16_rne(wgt[2] - f16_bits_to_f32(h23 & 0xFFFFu),
-                                                          wgt[3] - f16_bits_to_f32(h23 >> 16));
+                        // the rest w - hi is exact in fp32 (one fused step each)
+                        const uint32_t l01 = pack_f16_rne(fmaf(-1.0f, f16_bits_to_f32(h01 & 0xFFFFu), wgt[0]),
+                                                          fmaf(-1.0f, f16_bits_to_f32(h01 >> 16), wgt[1]));
+                        const uint32_t l23 = pack_f16_rne(fmaf(-1.0f, f16_bits_to_f32(h23 & 0xFFFFu), wgt[2]),
+                                                          fmaf(-1.0f, f16_bits_to_f32(h23 >> 16), wgt[3]));
                         lds_write8(lds_addr(tbuf + hs * kTP + 8 * n), h01, h23);
                         lds_write8(lds_addr(tbuf + (G + hs) * kTP + 8 * n), l01, l23);
                     }
                 }
-                // A operands (two 32-token chunks); once they have arrived
-                // every read of this page's stage has completed
+                // A operands (two 32-token chunks)
                 u32x4 ax[2];
                 ax[0] = lds_read16(a_addr);
                 ax[1] = lds_read16(a_addr + a_step);
-                lds_drain();
-                if (u + 2 < w1) issue(u + 2, s);
+                // page u + 1 (slot s ^ 1) into registers: it has landed once at
+                // most page u + 2's loads remain
+                u32x4 vn[kVX];
                 if (u + 1 < w1) {
-                    // page u + 1 has landed once at most page u + 2's loads remain
                     wait_vmcnt_at_most<1, kDma>(u + 2 < w1 ? kDma : 0);
                     read_keys(lds_addr(stage + (s ^ 1) * kSlot), kx);
+                    read_values(lds_addr(stage + (s ^ 1) * kSlot), vn);
                 }
 #pragma unroll
                 for (int kc = 0; kc < 2; ++kc) {
@@ -636,6 +651,13 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
                             acc[nt] = mfma16h(A, as_op_h(op + 4 * o), acc[nt]);
                         }
                     }
+                }
+                if (u + 1 < w1) {
+                    // slot s ^ 1 has been read out: refill it with page u + 3
+                    lds_drain();
+                    if (u + 3 < w1) issue(u + 3, s ^ 1);
+#pragma unroll
+                    for (int q4 = 0; q4 < kVX; ++q4) vv[q4] = vn[q4];
                 }
             }
         }
@@ -912,11 +934,12 @@ static bool make_plan(const wushkv_cache *c, int32_t n_q, int32_t max_seq_len, D
     const int64_t heads = (int64_t)c->batch * c->n_kv_heads;
     // One residency round if it can be had: the page waves get what the
     // window workgroups leave of the resident waves; at least 2 and at most
-    // 32 pages per wave.
+    // 16 pages per wave (when the work cannot fit one round, shorter waves
+    // balance the last round better).
     const int64_t wunits = c->win_slots / kPage;
     const int64_t budget = resident_waves(c->head_dim, c->bits, G) - 4 * heads * wunits;
     int64_t upw = 2;
-    while (upw < 32 && heads * ((qpages + 4 * upw - 1) / (4 * upw)) * 4 > budget) ++upw;
+    while (upw < 16 && heads * ((qpages + 4 * upw - 1) / (4 * upw)) * 4 > budget) ++upw;
     int64_t psplits = (qpages + 4 * upw - 1) / (4 * upw);
     if (psplits + wunits > kMaxSplits) {
         const int64_t room = kMaxSplits - wunits;
