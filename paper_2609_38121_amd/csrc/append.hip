@@ -64,11 +64,17 @@ struct TopK {
         for (int i = KMAX - 1; i >= 1; --i) t[i] = __builtin_amdgcn_fmed3f(t[i - 1], t[i], a);
         t[0] = fmaxf(t[0], a);
     }
+    // t[k] for a runtime k, as a chain of selects.  The empty assembly step
+    // keeps the chain in registers: without it the compiler turns the chain
+    // into an indexed load from a private (scratch) copy of the list.
     __device__ __forceinline__ float get(int k) const
     {
         float r = t[0];
 #pragma unroll
-        for (int i = 1; i < KMAX; ++i) r = (k == i) ? t[i] : r;
+        for (int i = 1; i < KMAX; ++i) {
+            r = (k == i) ? t[i] : r;
+            asm volatile("" : "+v"(r));
+        }
         return r;
     }
 };
