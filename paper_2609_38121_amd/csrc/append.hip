@@ -185,12 +185,15 @@ __device__ __forceinline__ void quant_params(float a_lo, float a_hi, float t, bo
     inv = (s > 0.0f) ? 1.0f / s : 0.0f;
 }
 
+// clamp(rne((x - z) inv), 0, levels).  Clamping to [0, levels] before the
+// rounding gives the same integer (levels is an integer), and adding 2^23 to
+// a value in [0, 2^23) rounds it to an integer in the default
+// nearest-even mode, leaving that integer in the low bits of the sum.
 __device__ __forceinline__ uint32_t code_of(float x, float z, float inv, float levels)
 {
-    float y = (x - z) * inv;
-    float r = rintf(y);
-    r = fminf(fmaxf(r, 0.0f), levels);
-    return (uint32_t)r;
+    const float y = (x - z) * inv;
+    const float c = __builtin_amdgcn_fmed3f(y, 0.0f, levels);
+    return __float_as_uint(c + 8388608.0f) - 0x4B000000u;
 }
 
 template <int D, int BITS>
@@ -228,6 +231,10 @@ __device__ void quantise_tile(const AppendArgs &a, const uint16_t *kt, uint16_t 
 {
     using L = Layout<D, BITS>;
     constexpr int kPitch = D + 8;
+    // every position of the tile quantised now (the common case of a
+    // prefill): the value words are then assembled without per-code checks
+    // or merges
+    const bool full = __syncthreads_and(quant(blk_lo + ((tid >> 1) & (kPage - 1))) && pg != nullptr);
     // ---- phase B: quantise.  Lanes 2 r and 2 r + 1 share group r (rows
     // 0-63 keys, 64-127 values), one half of its channels each, so that all
     // four waves take part.
@@ -302,7 +309,25 @@ __device__ void quantise_tile(const AppendArgs &a, const uint16_t *kt, uint16_t 
     __syncthreads();
 
     // ---- phase C: value-code words
-    if (pg != nullptr) {
+    if (full) {
+        uint32_t *vreg = reinterpret_cast<uint32_t *>(pg + L::kRegionBytes);
+        constexpr int kWords = 64 * L::kWordsPerLane;
+        constexpr int kRowBytes = 2 * kPitch;
+        for (int idx = tid; idx < kWords; idx += 256) {
+            const int Ln = idx / L::kWordsPerLane, rem = idx % L::kWordsPerLane;
+            const int kc = rem / (2 * L::kNw), u = rem % (2 * L::kNw);
+            const int j = Ln >> 4, m = Ln & 15;
+            const uint8_t *base = vcode_row<D>(vt, 32 * kc + 8 * j);  // token i at + i kRowBytes
+            uint32_t bits = 0;
+#pragma unroll
+            for (int e = 0; e < L::kCodesPerWord; ++e) {
+                const int o = e >> 3, i = e & 7;
+                const int ch = 16 * (u * L::kOpsPerWord + o) + m;
+                bits |= (uint32_t)base[i * kRowBytes + ch + (ch >= D / 2 ? D / 2 : 0)] << L::v_bit(o, i);
+            }
+            vreg[L::v_word(Ln, rem)] = bits;
+        }
+    } else if (pg != nullptr) {
         uint32_t *vreg = reinterpret_cast<uint32_t *>(pg + L::kRegionBytes);
         constexpr int kWords = 64 * L::kWordsPerLane;
         for (int idx = tid; idx < kWords; idx += 256) {
