@@ -273,3 +273,38 @@ def attend(q, K, V, scale: float) -> np.ndarray:
     out = np.empty(d, np.float64)
     lib().orc_attend(d, K.shape[0], _ptr(q), _ptr(K), _ptr(V), float(scale), _ptr(out))
     return out
+
+
+# --------------------------------------------------------------------------
+# Headwise normalisation and rotary embedding of new keys (Eq. (2), Alg. 2
+# step 1; the RMS form of Norm and the pairwise rotations R_s of RoPE are
+# those written in the appendix on RoPE-commuting transforms)
+# --------------------------------------------------------------------------
+
+def rope_frequencies(theta: float, d: int) -> np.ndarray:
+    """omega_j = theta^(-2j/d) for the d/2 rotary pairs, fp64."""
+    return float(theta) ** (-2.0 * np.arange(d // 2, dtype=np.float64) / d)
+
+
+def norm_rope(k_bits, positions, theta: float, gain=None, eps: float = 0.0) -> np.ndarray:
+    """bf16 patterns of RoPE(Norm(k)) for keys k (bf16 patterns [..., n, d])
+    at integer positions [n], evaluated in fp64 and rounded once to bf16.
+
+    Norm(x) = diag(gain) x / sqrt(mean_i x_i^2 + eps): the RMS normalisation
+    d^(1/2) ||x||^-1 diag(gain) x, with eps inside the root (eps = 0 is the
+    form written in the paper).  RoPE rotates coordinate pair (j, j + d/2)
+    by the angle s omega_j of position s: the 2x2 rotation
+    [[cos, -sin], [sin, cos]] applied to (x_j, x_{j+d/2})."""
+    x = bf16_to_f32(np.asarray(k_bits, np.uint16)).astype(np.float64)
+    d = x.shape[-1]
+    half = d // 2
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    g = np.ones(d) if gain is None else np.asarray(gain, np.float64)
+    y = x / np.sqrt(ms + float(eps)) * g
+    ang = np.asarray(positions, np.float64)[:, None] * rope_frequencies(theta, d)[None, :]
+    shape = (1,) * (x.ndim - 2) + ang.shape
+    c = np.cos(ang).reshape(shape)
+    s = np.sin(ang).reshape(shape)
+    y1, y2 = y[..., :half], y[..., half:]
+    out = np.concatenate([y1 * c - y2 * s, y2 * c + y1 * s], axis=-1)
+    return f64_to_bf16(out)

@@ -135,6 +135,22 @@ class Workload:
             x = rope(x, pos, c["rope_theta"])
         return to_bf16_bits(x)
 
+    def raw_keys(self, b: int, start: int, n: int) -> np.ndarray:
+        """bf16 bits [n][n_kv][d] of keys before headwise normalisation and
+        RoPE (the input of the fused norm + RoPE append): the Student-t or
+        Gaussian draw of keys() without its normalisation and rotation."""
+        c = self.cfg
+        rng = make_rng(self.seed * 1000003 + b, "raw_keys@%d" % start)
+        if c["k_dist"] == "gauss":
+            x = rng.standard_normal((n, self.n_kv, self.d), dtype=np.float32)
+            if len(self.k_outlier_ch):
+                x[..., self.k_outlier_ch] *= np.float32(c["outlier_scale"])
+        elif c["k_dist"] == "student_t3_rmsnorm":
+            x = rng.standard_t(3.0, size=(n, self.n_kv, self.d)).astype(np.float32)
+        else:
+            raise ValueError(c["k_dist"])
+        return to_bf16_bits(x)
+
     def values(self, b: int, start: int, n: int) -> np.ndarray:
         c = self.cfg
         rng = make_rng(self.seed * 1000003 + b, "values@%d" % start)
@@ -155,6 +171,16 @@ class Workload:
                 out[b] = rope(x[b][None], pos, c["rope_theta"])[0]
             x = out
         return to_bf16_bits(x)
+
+
+def rope_table(theta: float, d: int, max_pos: int) -> np.ndarray:
+    """The model's rotary table, fp32 [max_pos][d]: cos(s w_j) in columns
+    j < d/2 and sin(s w_j) in columns d/2 + j, w_j = theta^(-2j/d), evaluated
+    in fp64 and rounded once."""
+    half = d // 2
+    w = float(theta) ** (-np.arange(half, dtype=np.float64) * 2.0 / d)
+    ang = np.arange(max_pos, dtype=np.float64)[:, None] * w[None, :]
+    return np.concatenate([np.cos(ang), np.sin(ang)], axis=1).astype(np.float32)
 
 
 def rope(x: np.ndarray, positions: np.ndarray, theta: float) -> np.ndarray:
