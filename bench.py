@@ -387,59 +387,83 @@ def main():
 
 
 def bench_prefill(torch, wk, synth, dev, args):
+    """Append throughput on the prefill workload: 4 x 16384 new tokens, 8 kv
+    heads, d 128, 2-bit.  The keys are given as projected: the append applies
+    the headwise RMS normalisation and RoPE (theta 1e6) itself, then the key
+    transform, the quantisation and the packing (the whole prefill path of
+    that workload).  The same append on keys normalised and rotated by the
+    input generator is reported beside it."""
     cfg = synth.CONFIGS["prefill"]
     w = synth.Workload(cfg, seed=args.seed)
     B, H, D, BITS, n = cfg["batch"], cfg["n_kv"], cfg["d"], cfg["bits"], cfg["ctx"]
     log("prefill append: generating %d x %d tokens" % (B, n))
     as_dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+    k_raw = as_dev(np.stack([w.raw_keys(b, 0, n) for b in range(B)]))
     k = as_dev(np.stack([w.keys(b, 0, n) for b in range(B)]))
     v = as_dev(np.stack([w.values(b, 0, n) for b in range(B)]))
     tk_bits, _ = w.transform()
     tk = as_dev(tk_bits)
     cache = wk.WushKVCache(B, H, D, BITS, cfg["s_sink"], cfg["s_keep"], cfg["s_flush"],
                            cfg["kappa_k"], cfg["kappa_v"], max_seq_len=n)
+    table = torch.from_numpy(synth.rope_table(cfg["rope_theta"], D, cache.max_pages * 64 + cfg["s_sink"])).to(dev)
     nn = torch.full((B,), n, dtype=torch.int32, device=dev)
     reps = 10
-    times = []
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    for r in range(reps + 2):
-        cache.seq_len.zero_()
-        cache.quant_end.zero_()
+    calls = {
+        "norm_rope": lambda: wk.wushkv_append_norm_rope(cache, k_raw, v, nn, tk, table, norm_eps=1e-6),
+        "prenormed": lambda: wk.wushkv_append(cache, k, v, nn, tk),
+    }
+    res = {}
+    for name, call in calls.items():
+        times = []
+        for r in range(reps + 2):
+            cache.seq_len.zero_()
+            cache.quant_end.zero_()
+            torch.cuda.synchronize()
+            e0.record()
+            call()
+            e1.record()
+            torch.cuda.synchronize()
+            if r >= 2:
+                times.append(e0.elapsed_time(e1))
+        # the same calls again, each kernel stamped by the library
+        wk.wushkv_timing_enable(16 * reps)
+        for r in range(reps):
+            cache.seq_len.zero_()
+            cache.quant_end.zero_()
+            call()
         torch.cuda.synchronize()
-        e0.record()
-        wk.wushkv_append(cache, k, v, nn, tk)
-        e1.record()
-        torch.cuda.synchronize()
-        if r >= 2:
-            times.append(e0.elapsed_time(e1))
-    # the same calls again, each kernel stamped by the library
-    wk.wushkv_timing_enable(16 * reps)
-    for r in range(reps):
-        cache.seq_len.zero_()
-        cache.quant_end.zero_()
-        wk.wushkv_append(cache, k, v, nn, tk)
-    torch.cuda.synchronize()
-    cnt, tot = wk.wushkv_timing_read("append_kernel")
-    fcnt, ftot = wk.wushkv_timing_read("append_flush")
-    wk.wushkv_timing_enable(0)
-    ms = float(np.median(times))
-    t_kernel = tot / cnt
-    t_flush = ftot / fcnt if fcnt else 0.0
+        cnt, tot = wk.wushkv_timing_read("append_kernel")
+        fcnt, ftot = wk.wushkv_timing_read("append_flush")
+        wk.wushkv_timing_enable(0)
+        res[name] = (float(np.median(times)), tot / cnt, ftot / fcnt if fcnt else 0.0)
     tokens = B * n
     Q = int(cache.quant_end[0].item())
     n_quant = Q - cfg["s_sink"]
     byts = prefill_bytes(B, H, D, BITS, n, n_quant)
-    ach = byts / (t_kernel * 1e-3) / 1e9
-    log("prefill append: %.1f us/call, %.3g tokens/s, append_kernel %.1f us, %.1f GB/s "
-        "(flush-only launch %.1f us)" % (ms * 1e3, tokens / (ms * 1e-3), t_kernel * 1e3, ach,
-                                         t_flush * 1e3))
-    return {"workload": "prefill-append-4x16384-2bit", "tokens_per_s": round(tokens / (ms * 1e-3), 1),
-            "ms_per_call": round(ms, 4), "bytes_per_call": int(byts),
-            "roofline": {"bound": "hbm", "kernel": "append_kernel", "achieved": round(ach, 2),
-                         "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
-                         "traffic": None, "avg_us": round(t_kernel * 1e3, 3)},
-            "flush_launch_us": round(t_flush * 1e3, 3),
-            "roofline_tokens_per_s": round(tokens / (byts / (PEAK_HBM_GBS * 1e9)), 1)}
+    table_bytes = n * D * 4  # the rotary table rows of the positions written
+    out = None
+    for name in ("norm_rope", "prenormed"):
+        ms, t_kernel, t_flush = res[name]
+        b_ = byts + (table_bytes if name == "norm_rope" else 0)
+        ach = b_ / (t_kernel * 1e-3) / 1e9
+        log("prefill append (%s): %.1f us/call, %.3g tokens/s, append_kernel %.1f us, %.1f GB/s "
+            "(flush-only launch %.1f us)" % (name, ms * 1e3, tokens / (ms * 1e-3), t_kernel * 1e3,
+                                             ach, t_flush * 1e3))
+        entry = {"tokens_per_s": round(tokens / (ms * 1e-3), 1), "ms_per_call": round(ms, 4),
+                 "bytes_per_call": int(b_),
+                 "roofline": {"bound": "hbm", "kernel": "append_kernel", "achieved": round(ach, 2),
+                              "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                              "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+                              "avg_us": round(t_kernel * 1e3, 3)},
+                 "flush_launch_us": round(t_flush * 1e3, 3),
+                 "roofline_tokens_per_s": round(tokens / (b_ / (PEAK_HBM_GBS * 1e9)), 1)}
+        if out is None:
+            out = dict(entry, workload="prefill-append-4x16384-2bit, RMS norm + RoPE fused",
+                       keys="projected (Student-t), normalised and rotated by the append")
+        else:
+            out["prenormed_keys"] = entry
+    return out
 
 
 def bench_decode_scale(torch, wk, synth, dev, args, calls=24):

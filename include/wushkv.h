@@ -177,6 +177,42 @@ int wushkv_append(const wushkv_cache *c,
                   wushkv_stream_t stream);
 
 /*
+ * wushkv_append_norm_rope -- wushkv_append with Alg. 2 step 1 fused in
+ * front of it: the keys arrive as projected, BEFORE the headwise
+ * normalisation and the rotary embedding of Eq. (2), K = RoPE(Norm(W_K^T X)).
+ *
+ *   k_raw   bf16 [batch][max_new][n_kv_heads][head_dim]: projected keys.
+ *           Row t of sequence b is position s = seq_len[b] + t.
+ *   norm_gain  fp32 [head_dim] device, or NULL for a gain of one.
+ *   norm_eps   (host) >= 0, added to the mean square inside the root.
+ *   rope_table fp32 [rope_positions][head_dim] device: for position s,
+ *              column j < head_dim/2 holds cos(s w_j) and column
+ *              head_dim/2 + j holds sin(s w_j) (the model's own rotary table).
+ *   rope_positions (host) rows of rope_table; must be at least the cache's
+ *              capacity, max_pages_per_seq * 64 + s_sink.
+ *   The other arguments are wushkv_append's.
+ *
+ * Per key row x (fp32 from bf16), each step rounded to nearest-even fp32:
+ *   r = 1 / sqrt(sum_i x_i^2 / head_dim + norm_eps)   (sum in any order);
+ *   y_i = (x_i * r) * gain_i;
+ *   for j < h = head_dim/2, with c, s the table's cos and sin at (s, j):
+ *     k'_j = y_j c - y_{j+h} s,   k'_{j+h} = y_{j+h} c + y_j s;
+ * k' is rounded once to bf16 and then appended exactly as wushkv_append
+ * appends k_new (k~ = T_K k', windows, quantisation).  This is the RMS form
+ * of Norm and the pairwise rotation R(s w_j) of the coordinate pairs
+ * (j, j + h) written in the paper's appendix on RoPE-commuting transforms.
+ * Returns WUSHKV_EINVAL for a null table, a negative or non-finite eps or a
+ * table shorter than the capacity, besides wushkv_append's checks.
+ */
+int wushkv_append_norm_rope(const wushkv_cache *c,
+                            const uint16_t *k_raw, const uint16_t *v_new,
+                            const int32_t *n_new, int32_t max_new,
+                            const uint16_t *t_k,
+                            const float *norm_gain, float norm_eps,
+                            const float *rope_table, int32_t rope_positions,
+                            uint16_t *k_tilde_out, wushkv_stream_t stream);
+
+/*
  * wushkv_decode_attention -- one decode query per query head (Eq. (2)).
  *
  *   q          bf16 [batch][n_q_heads][head_dim]: queries after norm and RoPE.

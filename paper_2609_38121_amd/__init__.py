@@ -162,6 +162,26 @@ def wushkv_append(cache: WushKVCache, k_new, v_new, n_new, t_k, k_tilde_out=None
     check(st, "wushkv_append")
 
 
+def wushkv_append_norm_rope(cache: WushKVCache, k_raw, v_new, n_new, t_k, rope_table,
+                            norm_gain=None, norm_eps=0.0, k_tilde_out=None, max_new=None,
+                            stream=None) -> None:
+    """wushkv_append with the headwise RMS normalisation and the rotary
+    embedding of the new keys fused in front (Alg. 2 step 1).  k_raw: bf16
+    [batch][max_new][n_kv][d] projected keys; rope_table: fp32 [positions][d]
+    (cos | sin); norm_gain: fp32 [d] or None."""
+    for t, nm in ((k_raw, "k_raw"), (v_new, "v_new"), (t_k, "t_k"), (k_tilde_out, "k_tilde_out")):
+        _check_2byte(t, nm)
+    if rope_table.element_size() != 4 or not rope_table.is_contiguous():
+        raise ValueError("rope_table must be a contiguous fp32 tensor")
+    if max_new is None:
+        max_new = k_raw.shape[1]
+    st = _lib.lib().wushkv_append_norm_rope(
+        ctypes.byref(cache.desc), _ptr(k_raw), _ptr(v_new), _ptr(n_new), int(max_new), _ptr(t_k),
+        _ptr(norm_gain), float(norm_eps), _ptr(rope_table), int(rope_table.shape[0]),
+        _ptr(k_tilde_out), _stream_handle(stream))
+    check(st, "wushkv_append_norm_rope")
+
+
 def wushkv_decode_workspace_bytes(cache: WushKVCache, n_q_heads: int, max_seq_len: int) -> int:
     return _lib.lib().wushkv_decode_workspace_bytes(ctypes.byref(cache.desc), n_q_heads,
                                                     max_seq_len)

@@ -71,6 +71,8 @@ def _declare(L):
     L.wushkv_page_bytes.restype = SZ
     L.wushkv_append.argtypes = [D, P, P, P, I32, P, P, P]
     L.wushkv_append.restype = ctypes.c_int
+    L.wushkv_append_norm_rope.argtypes = [D, P, P, P, I32, P, P, F32, P, I32, P, P]
+    L.wushkv_append_norm_rope.restype = ctypes.c_int
     L.wushkv_decode_attention.argtypes = [D, P, I32, I32, P, F32, P, P, SZ, P]
     L.wushkv_decode_attention.restype = ctypes.c_int
     L.wushkv_decode_workspace_bytes.argtypes = [D, I32, I32]

@@ -45,7 +45,64 @@ struct AppendArgs {
     uint16_t *k_tilde_out;
     int32_t mode;
     int32_t sink_tiles;  // ceil(s_sink / 64)
+    // headwise RMS normalisation + rotary embedding of the new keys (Alg. 2
+    // step 1), applied when rope is not null
+    const float *gain;   // [D] or null (one)
+    float eps;
+    const float *rope;   // [positions][D]: cos(s w_j) | sin(s w_j)
 };
+
+// RoPE(Norm(x)) of one key row held by four lanes (the lanes n + 16 j,
+// j = 0..3 of a 16-lane column group): lane j holds channels 32 c + 8 j + e
+// (c = 0..3, e = 0..7) in x[c][e].  The rotary partner of channel i < D/2
+// is i + D/2, chunk c + D/64 of the same lane, so the rotation is local.
+// Each step is a separately rounded fp32 operation.
+template <int D>
+__device__ __forceinline__ void norm_rope_row(float (&x)[D / 32][8], int j, int32_t pos,
+                                              const AppendArgs &a)
+{
+    constexpr int kC = D / 32;
+    float ss = 0.0f;
+#pragma unroll
+    for (int c = 0; c < kC; ++c)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ss = fmaf(x[c][e], x[c][e], ss);
+    ss += __shfl_xor(ss, 16);
+    ss += __shfl_xor(ss, 32);
+    const float r = 1.0f / sqrtf(ss / (float)D + a.eps);
+#pragma unroll
+    for (int c = 0; c < kC; ++c) {
+        float g[8];
+        if (a.gain != nullptr) {
+            const float4 g0 = *reinterpret_cast<const float4 *>(a.gain + 32 * c + 8 * j);
+            const float4 g1 = *reinterpret_cast<const float4 *>(a.gain + 32 * c + 8 * j + 4);
+            g[0] = g0.x; g[1] = g0.y; g[2] = g0.z; g[3] = g0.w;
+            g[4] = g1.x; g[5] = g1.y; g[6] = g1.z; g[7] = g1.w;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) g[e] = 1.0f;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[c][e] = (x[c][e] * r) * g[e];
+    }
+    const float *row = a.rope + (int64_t)pos * D;
+#pragma unroll
+    for (int c = 0; c < kC / 2; ++c) {
+        const float *cs = row + 32 * c + 8 * j;
+        const float4 c0 = *reinterpret_cast<const float4 *>(cs);
+        const float4 c1 = *reinterpret_cast<const float4 *>(cs + 4);
+        const float4 s0 = *reinterpret_cast<const float4 *>(cs + D / 2);
+        const float4 s1 = *reinterpret_cast<const float4 *>(cs + D / 2 + 4);
+        const float co[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+        const float si[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const float lo = x[c][e], hi = x[c + kC / 2][e];
+            x[c][e] = lo * co[e] - hi * si[e];
+            x[c + kC / 2][e] = hi * co[e] + lo * si[e];
+        }
+    }
+}
 
 // Descending top-KMAX of the values pushed so far; t[0] is the largest.
 // Inserting a into a sorted list is one median-of-three per slot:
@@ -356,7 +413,7 @@ __device__ void quantise_tile(const AppendArgs &a, const uint16_t *kt, uint16_t 
 
 }
 
-template <int D, int BITS>
+template <int D, int BITS, bool ROPE>
 __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
 {
     using L = Layout<D, BITS>;
@@ -439,6 +496,34 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
         // Wave w produces output channels [w D/4, (w+1) D/4) for all 64 rows.
         constexpr int kNtW = D / 64;  // N-tiles per wave
         const int j = lane >> 4, n = lane & 15;
+        constexpr bool fused = ROPE;
+        if constexpr (fused) {
+            // phase A0: RoPE(Norm(k)) of each new row once (wave w rows
+            // 16 w .. 16 w + 15), rounded to bf16 into the value rows, which
+            // serve as the key operand's staging until the values arrive
+            const int r = 16 * wave + n;
+            const int32_t p = blk_lo + r;
+            const bool ld = (p >= lo && p < hi && is_new(p) && do_new);
+            const uint16_t *krow = a.k_new + (((int64_t)b * a.max_new + (p - s_old)) * a.n_kv + h) * D;
+            float x[L::kChunks][8];
+#pragma unroll
+            for (int c = 0; c < L::kChunks; ++c) {
+                u32x4 av = {0u, 0u, 0u, 0u};
+                if (ld) av = *reinterpret_cast<const u32x4 *>(krow + 32 * c + 8 * j);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[c][e] = bf16_bits_to_f32((av[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
+            }
+            // (a row not loaded is zero: its result is discarded below)
+            norm_rope_row<D>(x, j, ld ? p : 0, a);
+#pragma unroll
+            for (int c = 0; c < L::kChunks; ++c) {
+                u32x4 pk;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) pk[q] = ld ? pack_bf16_rne(x[c][2 * q], x[c][2 * q + 1]) : 0u;
+                *reinterpret_cast<u32x4 *>(vt + r * kPitch + 32 * c + 8 * j) = pk;
+            }
+            __syncthreads();
+        }
         bf16x8 bop[kNtW][L::kChunks];
 #pragma unroll
         for (int nt = 0; nt < kNtW; ++nt) {
@@ -459,7 +544,8 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
 #pragma unroll
             for (int c = 0; c < L::kChunks; ++c) {
                 u32x4 av = {0u, 0u, 0u, 0u};
-                if (ld) av = *reinterpret_cast<const u32x4 *>(krow + 32 * c + 8 * j);
+                if constexpr (fused) av = *reinterpret_cast<const u32x4 *>(vt + r * kPitch + 32 * c + 8 * j);
+                else if (ld) av = *reinterpret_cast<const u32x4 *>(krow + 32 * c + 8 * j);
                 bf16x8 aop = __builtin_bit_cast(bf16x8, av);
 #pragma unroll
                 for (int nt = 0; nt < kNtW; ++nt) acc[nt] = mfma16(aop, bop[nt][c], acc[nt]);
@@ -476,6 +562,9 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
                 }
             }
         }
+        // the value rows are about to be overwritten: every wave must have
+        // read its key operands from them
+        if constexpr (fused) __syncthreads();
     }
     // ring-sourced keys (flush) and all values, 16 B per thread-step
     {
@@ -562,6 +651,8 @@ __global__ void __launch_bounds__(256) append_step_kernel(AppendArgs a)
     __shared__ __attribute__((aligned(16))) uint16_t kt[kPage * kPitch];
     __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * kPitch];
     __shared__ float kin[D];
+    __shared__ float kin2[D];
+    __shared__ float red4[4];
     __shared__ int32_t sh_page;
 
     const int tid = threadIdx.x;
@@ -596,6 +687,32 @@ __global__ void __launch_bounds__(256) append_step_kernel(AppendArgs a)
     for (int t = 0; t < nn; ++t) {
         if (tid < D) kin[tid] = bf16_bits_to_f32(new_row(a.k_new, s_old + t)[tid]);
         __syncthreads();
+        if (a.rope != nullptr) {
+            // RoPE(Norm(k)) of this key (same fp32 steps as norm_rope_row):
+            // the mean square over D channels, then each thread j < D/2
+            // rotates the pair (j, j + D/2) and rounds it to bf16
+            float sq = tid < D ? kin[tid] * kin[tid] : 0.0f;
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) sq += __shfl_xor(sq, off);
+            if ((tid & 63) == 0) red4[tid >> 6] = sq;
+            __syncthreads();
+            float ss = 0.0f;
+#pragma unroll
+            for (int w = 0; w < 4; ++w) ss += red4[w];
+            const float r = 1.0f / sqrtf(ss / (float)D + a.eps);
+            if (tid < D / 2) {
+                const float g0 = a.gain ? a.gain[tid] : 1.0f, g1 = a.gain ? a.gain[tid + D / 2] : 1.0f;
+                const float lo = (kin[tid] * r) * g0, hi = (kin[tid + D / 2] * r) * g1;
+                const float *row = a.rope + (int64_t)(s_old + t) * D;
+                const float co = row[tid], si = row[tid + D / 2];
+                const uint32_t pk = pack_bf16_rne(lo * co - hi * si, hi * co + lo * si);
+                kin2[tid] = bf16_bits_to_f32(pk & 0xFFFFu);
+                kin2[tid + D / 2] = bf16_bits_to_f32(pk >> 16);
+            }
+            __syncthreads();
+            if (tid < D) kin[tid] = kin2[tid];
+            __syncthreads();
+        }
         float acc = 0.0f;
 #pragma unroll
         for (int i = 0; i < kIn / 2; ++i) {
@@ -687,7 +804,8 @@ __global__ void append_commit_kernel(int32_t *seq_len, int32_t *quant_end, const
 template <int D, int BITS>
 static hipError_t launch_append(const char *name, const AppendArgs &a, dim3 grid, hipStream_t s)
 {
-    launch(name, append_kernel<D, BITS>, grid, dim3(256), s, a);
+    if (a.rope != nullptr) launch(name, append_kernel<D, BITS, true>, grid, dim3(256), s, a);
+    else launch(name, append_kernel<D, BITS, false>, grid, dim3(256), s, a);
     return hipGetLastError();
 }
 
@@ -716,9 +834,12 @@ static void kappa_position(float kappa, int d, int32_t &lo, float &t)
 
 int wushkv_validate_cache(const wushkv_cache *c);  // api.hip
 
-extern "C" int wushkv_append(const wushkv_cache *c, const uint16_t *k_new, const uint16_t *v_new,
-                             const int32_t *n_new, int32_t max_new, const uint16_t *t_k,
-                             uint16_t *k_tilde_out, wushkv_stream_t stream)
+// Both entry points: rope == nullptr appends keys as given; otherwise the
+// keys are normalised and rotated first (the caller checked the table).
+static int append_impl(const wushkv_cache *c, const uint16_t *k_new, const uint16_t *v_new,
+                       const int32_t *n_new, int32_t max_new, const uint16_t *t_k,
+                       const float *gain, float eps, const float *rope,
+                       uint16_t *k_tilde_out, wushkv_stream_t stream)
 {
     int st = wushkv_validate_cache(c);
     if (st != WUSHKV_OK) return st;
@@ -750,6 +871,9 @@ extern "C" int wushkv_append(const wushkv_cache *c, const uint16_t *k_new, const
     a.tk = t_k;
     a.k_tilde_out = k_tilde_out;
     a.sink_tiles = (c->s_sink + kPage - 1) / kPage;
+    a.gain = gain;
+    a.eps = eps;
+    a.rope = rope;
 
     // Tiles a sequence can touch: the sink tiles, plus the span from the
     // oldest unflushed position (at most s_keep + s_flush - 1 back) to the
@@ -802,4 +926,28 @@ extern "C" int wushkv_append(const wushkv_cache *c, const uint16_t *k_new, const
            c->seq_len, c->quant_end, n_new, c->batch, max_new, c->s_sink, c->s_keep, c->s_flush);
     if (hipGetLastError() != hipSuccess) return WUSHKV_ELAUNCH;
     return WUSHKV_OK;
+}
+
+extern "C" int wushkv_append(const wushkv_cache *c, const uint16_t *k_new, const uint16_t *v_new,
+                             const int32_t *n_new, int32_t max_new, const uint16_t *t_k,
+                             uint16_t *k_tilde_out, wushkv_stream_t stream)
+{
+    return append_impl(c, k_new, v_new, n_new, max_new, t_k, nullptr, 0.0f, nullptr, k_tilde_out,
+                       stream);
+}
+
+extern "C" int wushkv_append_norm_rope(const wushkv_cache *c, const uint16_t *k_raw,
+                                       const uint16_t *v_new, const int32_t *n_new,
+                                       int32_t max_new, const uint16_t *t_k,
+                                       const float *norm_gain, float norm_eps,
+                                       const float *rope_table, int32_t rope_positions,
+                                       uint16_t *k_tilde_out, wushkv_stream_t stream)
+{
+    int st = wushkv_validate_cache(c);
+    if (st != WUSHKV_OK) return st;
+    if (rope_table == nullptr || !(norm_eps >= 0.0f) || norm_eps == INFINITY) return WUSHKV_EINVAL;
+    if ((int64_t)rope_positions < (int64_t)c->max_pages_per_seq * kPage + c->s_sink) return WUSHKV_EINVAL;
+    if (((uintptr_t)rope_table | (uintptr_t)norm_gain) & 15u) return WUSHKV_EINVAL;
+    return append_impl(c, k_raw, v_new, n_new, max_new, t_k, norm_gain, norm_eps, rope_table,
+                       k_tilde_out, stream);
 }

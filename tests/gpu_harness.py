@@ -84,6 +84,37 @@ class Pair:
         self.k_tilde_log.append((k, kt_np, n_new))
         return kt_np
 
+    def append_norm_rope(self, k_raw: np.ndarray, v: np.ndarray, n_new, theta: float,
+                         gain=None, eps: float = 1e-6) -> np.ndarray:
+        """The fused append: raw keys are normalised and rotated on the GPU
+        (rotary table built by the input generator); the reference oracle
+        gets RoPE(Norm(k)) from the oracle's own fp64 evaluation, the mirror
+        gets the GPU's k~."""
+        n_new = np.asarray(n_new, np.int32)
+        cap = self.gpu.max_pages * 64 + self.s_sink
+        table = torch.from_numpy(synth.rope_table(theta, self.d, cap)).to(self.dev)
+        g = None if gain is None else torch.from_numpy(np.asarray(gain, np.float32)).to(self.dev)
+        kd, vd = to_dev_bf16(k_raw, self.dev), to_dev_bf16(v, self.dev)
+        nd = torch.from_numpy(n_new).to(self.dev)
+        kt = torch.full_like(kd, float("nan"))
+        wk.wushkv_append_norm_rope(self.gpu, kd, vd, nd, self.tk_dev, table, norm_gain=g,
+                                   norm_eps=eps, k_tilde_out=kt)
+        torch.cuda.synchronize()
+        kt_np = to_np_bits(kt)
+        k_rot = np.zeros_like(k_raw)
+        for b in range(self.batch):
+            n = int(n_new[b])
+            if n == 0:
+                continue
+            pos = int(self.mirror.seq_len[b]) + np.arange(n)
+            rows = np.transpose(k_raw[b, :n], (1, 0, 2))               # [H][n][d]
+            k_rot[b, :n] = np.transpose(oracle.norm_rope(rows, pos, theta, gain, eps), (1, 0, 2))
+        if self.ref is not None:
+            self.ref.append(k_rot, v, n_new, self.tk)
+        self.mirror.append(kt_np, v, n_new, self.eye)
+        self.k_tilde_log.append((k_rot, kt_np, n_new))
+        return kt_np
+
     def k_tilde_vs_ref(self):
         """Check the GPU's bf16 k~ = T_K k against the exact product.  The GPU
         accumulates in fp32 and rounds once to bf16, so each element must lie

@@ -85,6 +85,16 @@ def test_call_specific_validation():
     assert L.wushkv_append(by, None, FAKE, FAKE, 1, FAKE, None, None) == -1
     assert L.wushkv_append(by, FAKE, FAKE, FAKE, -1, FAKE, None, None) == -1
     assert L.wushkv_append(by, FAKE, FAKE, FAKE, 0, FAKE, None, None) == 0
+    # fused norm + RoPE append: the table must exist and cover the capacity
+    # (4 pages * 64 + 4 sink = 260 positions); eps must be finite and >= 0
+    nr = L.wushkv_append_norm_rope
+    assert nr(by, FAKE, FAKE, FAKE, 1, FAKE, None, 0.0, None, 260, None, None) == -1
+    assert nr(by, FAKE, FAKE, FAKE, 1, FAKE, None, 0.0, FAKE, 259, None, None) == -1
+    assert nr(by, FAKE, FAKE, FAKE, 1, FAKE, None, -1.0, FAKE, 260, None, None) == -1
+    assert nr(by, FAKE, FAKE, FAKE, 1, FAKE, None, float("inf"), FAKE, 260, None, None) == -1
+    assert nr(by, FAKE, FAKE, FAKE, 1, FAKE, FAKE + 4, 0.0, FAKE, 260, None, None) == -1
+    assert nr(by, None, FAKE, FAKE, 1, FAKE, None, 0.0, FAKE, 260, None, None) == -1
+    assert nr(by, FAKE, FAKE, FAKE, 0, FAKE, None, 0.0, FAKE, 260, None, None) == 0
     # decode: n_q not a multiple of n_kv, G too large or not a power of two,
     # bad scale, small workspace
     assert L.wushkv_decode_attention(by, FAKE, 7, 100, FAKE, 0.1, FAKE, FAKE, 1 << 30, None) == -1

@@ -37,8 +37,10 @@ SPLIT_TOL = 1e-5  # two split plans of the same cache
 class SampledCache:
     """Full-size GPU cache plus oracle caches for sampled (b, h) pairs."""
 
-    def __init__(self, dev, cfg, w, pairs, cap, seed=0):
+    def __init__(self, dev, cfg, w, pairs, cap, seed=0, norm_rope=False):
         self.dev, self.cfg, self.w, self.pairs = dev, cfg, w, list(pairs)
+        # keys given before normalisation and RoPE, fused into the append
+        self.norm_rope = norm_rope
         c = cfg
         self.B, self.H, self.d, self.bits = c["batch"], c["n_kv"], c["d"], c["bits"]
         self.G = c["n_q"] // c["n_kv"]
@@ -57,6 +59,10 @@ class SampledCache:
         self.eye = eye_bits(1, self.d)
         self.sm = 1.0 / np.sqrt(self.d)
         self.pos = np.zeros(self.B, np.int64)  # tokens generated so far per sequence
+        if norm_rope:
+            self.theta = c["rope_theta"]
+            self.table = torch.from_numpy(
+                synth.rope_table(self.theta, self.d, self.gpu.max_pages * 64 + self.s_sink)).to(dev)
 
     def append(self, n_new, max_new=None):
         """Append the workload's next n_new[b] tokens of every sequence."""
@@ -64,19 +70,27 @@ class SampledCache:
         n_max = int(n_new.max())
         k = np.zeros((self.B, n_max, self.H, self.d), np.uint16)
         v = np.zeros_like(k)
+        keys = self.w.raw_keys if self.norm_rope else self.w.keys
         for b in range(self.B):
             if n_new[b]:
-                k[b, :n_new[b]] = self.w.keys(b, int(self.pos[b]), int(n_new[b]))
+                k[b, :n_new[b]] = keys(b, int(self.pos[b]), int(n_new[b]))
                 v[b, :n_new[b]] = self.w.values(b, int(self.pos[b]), int(n_new[b]))
         kd, vd = to_dev_bf16(k, self.dev), to_dev_bf16(v, self.dev)
         kt = torch.empty_like(kd)
         nd = torch.from_numpy(n_new.astype(np.int32)).to(self.dev)
-        wk.wushkv_append(self.gpu, kd, vd, nd, self.tk_dev, k_tilde_out=kt, max_new=max_new)
+        if self.norm_rope:
+            wk.wushkv_append_norm_rope(self.gpu, kd, vd, nd, self.tk_dev, self.table,
+                                       norm_eps=1e-6, k_tilde_out=kt, max_new=max_new)
+        else:
+            wk.wushkv_append(self.gpu, kd, vd, nd, self.tk_dev, k_tilde_out=kt, max_new=max_new)
         torch.cuda.synchronize()
         for (b, h) in self.pairs:
             n = int(n_new[b])
             kth = to_np_bits(kt[b, :n, h])[None, :, None]
             kh = np.ascontiguousarray(k[b:b + 1, :n, h:h + 1])
+            if self.norm_rope:
+                pos = int(self.pos[b]) + np.arange(n)
+                kh = oracle.norm_rope(kh[0, :, 0][None], pos, self.theta, None, 1e-6)[0][None, :, None]
             vh = np.ascontiguousarray(v[b:b + 1, :n, h:h + 1])
             self.mirror[(b, h)].append(kth, vh, [n], self.eye)
             self.ref[(b, h)].append(kh, vh, [n], self.tk[h:h + 1])
@@ -156,10 +170,10 @@ class SampledCache:
         return out, worst
 
 
-def _run(gpu, name, pairs, cap, decode_len, steps, chunk=None, split_len=None):
+def _run(gpu, name, pairs, cap, decode_len, steps, chunk=None, split_len=None, norm_rope=False):
     cfg = synth.CONFIGS[name]
     w = synth.Workload(cfg)
-    sc = SampledCache(gpu, cfg, w, pairs, cap)
+    sc = SampledCache(gpu, cfg, w, pairs, cap, norm_rope=norm_rope)
     lengths = w.lengths.astype(np.int64)
     say("%s: prefill %s tokens, pairs %s" % (name, lengths.tolist() if len(lengths) <= 8 else
                                               "%d..%d" % (lengths.min(), lengths.max()), pairs))
@@ -229,3 +243,12 @@ def test_prefill_append_workload(gpu):
     cfg = synth.CONFIGS["prefill"]
     cap = cfg["ctx"] + 64
     _run(gpu, "prefill", [(0, 0), (1, 7), (3, 4)], cap=cap, decode_len=cap, steps=1)
+
+
+@pytest.mark.timeout(600)
+def test_prefill_workload_with_fused_norm_rope(gpu):
+    """The same prefill with the keys given before the headwise RMS
+    normalisation and RoPE (theta 1e6), which the append applies itself."""
+    cfg = synth.CONFIGS["prefill"]
+    cap = cfg["ctx"] + 64
+    _run(gpu, "prefill", [(0, 2), (2, 5)], cap=cap, decode_len=cap, steps=2, norm_rope=True)
