@@ -253,6 +253,32 @@ class OracleCache:
         return out
 
 
+def chunk_attention(cache: "OracleCache", q, n_tok, tinv, sm_scale):
+    """Attention of a chunk of new tokens (Alg. 2 step 5 with S' > 1; the
+    causal mask of Eq. (2)): q bf16 patterns [batch][S'][n_q][d]; sequence b's
+    chunk is its last n_tok[b] positions, token t at position
+    p = seq_len[b] - n_tok[b] + t, which attends to positions [0, p].  Rows
+    t >= n_tok[b] are left NaN.  Returns fp64 [batch][S'][n_q][d]."""
+    q = np.ascontiguousarray(q, dtype=np.uint16)
+    tinv = np.ascontiguousarray(tinv, dtype=np.float32)
+    B, T, nq, d = q.shape
+    G = nq // cache.n_kv
+    out = np.full((B, T, nq, d), np.nan, np.float64)
+    for b in range(B):
+        S, Q = int(cache.seq_len[b]), int(cache.quant_end[b])
+        n = int(n_tok[b])
+        for t in range(n):
+            visible = S - n + t + 1  # positions [0, visible)
+            for h in range(cache.n_kv):
+                o = np.empty((G, d), np.float64)
+                qg = np.ascontiguousarray(q[b, t, h * G:(h + 1) * G])
+                decode_head(d, G, cache.s_sink, visible, min(Q, visible), cache.kbits[b, h],
+                            cache.vbits[b, h], cache.kc[b, h], cache.kp[b, h], cache.vc[b, h],
+                            cache.vp[b, h], qg, tinv[h], sm_scale, o)
+                out[b, t, h * G:(h + 1) * G] = o
+    return out
+
+
 def decode_head(d, G, s_sink, S, q_end, kbits, vbits, kc, kp, vc, vp, q, tinv, sm_scale, out):
     """Thin wrapper over orc_decode_head; arrays are per (sequence, head):
     kbits/vbits [cap][d] uint16, kc/vc [cap][d] uint8, kp/vp [cap][2] uint16,

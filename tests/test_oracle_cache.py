@@ -205,3 +205,56 @@ def test_decode_head_brute_force_tiny():
         w = [np.exp(x - m) for x in logits]
         ref = [sum(w[p] * rows[p][i] for p in range(S)) / sum(w) for i in range(d)]
         assert np.max(np.abs(out[0, g] - np.array(ref))) < 1e-12
+
+
+def test_chunk_attention_brute_force_causal():
+    """Chunk attention (Alg. 2 step 5 with S' > 1): token t of the chunk sees
+    positions up to its own and no later one.  Checked against an explicit
+    causal softmax over the reconstructed rows, built element by element, and
+    the chunk's last token against decode."""
+    rng = np.random.default_rng(8)
+    B, H, G, d, n0, T = 2, 1, 2, 64, 70, 5
+    tk = oracle.f32_to_bf16(np.eye(d, dtype=np.float32))[None]
+    tinv = np.eye(d, dtype=np.float32)[None]
+    cache = oracle.OracleCache(B, H, d, 2, 4, 16, 8, 0.96, 0.92, n0 + T)
+    k = _rand_bits(rng, (B, n0, H, d))
+    v = _rand_bits(rng, (B, n0, H, d))
+    cache.append(k, v, np.array([n0, n0 - 9]), tk)
+    k = _rand_bits(rng, (B, T, H, d))
+    v = _rand_bits(rng, (B, T, H, d))
+    n_tok = np.array([T, 3])
+    cache.append(k, v, n_tok, tk)
+    q = _rand_bits(rng, (B, T, G * H, d))
+    out = oracle.chunk_attention(cache, q, n_tok, tinv, 0.125)
+    for b in range(B):
+        S, Q = int(cache.seq_len[b]), int(cache.quant_end[b])
+        assert Q > 4
+        n = int(n_tok[b])
+        assert np.all(np.isnan(out[b, n:]))
+        for t in range(n):
+            last = S - n + t  # the position of this token
+            for g in range(G):
+                qq = [float(oracle.bf16_to_f32(q[b, t, g, i])) for i in range(d)]
+                logits, rows = [], []
+                for p in range(last + 1):
+                    if 4 <= p < Q:
+                        s = float(oracle.f16_to_f32(cache.kp[b, 0, p, 0]))
+                        z = float(oracle.f16_to_f32(cache.kp[b, 0, p, 1]))
+                        kr = [s * int(cache.kc[b, 0, p, i]) + z for i in range(d)]
+                        s = float(oracle.f16_to_f32(cache.vp[b, 0, p, 0]))
+                        z = float(oracle.f16_to_f32(cache.vp[b, 0, p, 1]))
+                        vr = [s * int(cache.vc[b, 0, p, i]) + z for i in range(d)]
+                    else:
+                        kr = [float(oracle.bf16_to_f32(cache.kbits[b, 0, p, i])) for i in range(d)]
+                        vr = [float(oracle.bf16_to_f32(cache.vbits[b, 0, p, i])) for i in range(d)]
+                    logits.append(0.125 * sum(a * c for a, c in zip(qq, kr)))
+                    rows.append(vr)
+                m = max(logits)
+                w = [np.exp(x - m) for x in logits]
+                ref = [sum(w[p] * rows[p][i] for p in range(last + 1)) / sum(w) for i in range(d)]
+                assert np.max(np.abs(out[b, t, g] - np.array(ref))) < 1e-12
+    # the last token of each chunk attends to everything: that is decode
+    q_last = np.stack([q[b, int(n_tok[b]) - 1] for b in range(B)])
+    dec = cache.decode(q_last, tinv, 0.125)
+    for b in range(B):
+        assert np.array_equal(dec[b], out[b, int(n_tok[b]) - 1])
