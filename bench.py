@@ -338,6 +338,10 @@ def main():
     if not args.no_prefill:
         prefill = bench_prefill(torch, wk, synth, dev, args)
 
+    # ---- chunk attention: 16 new tokens per sequence on the same cache
+    chunk = bench_chunk(torch, wk, caches, reps, k1, tk, tinv_d, B, NQ, D, max_seq, sm, cfg,
+                        lengths_at, done) if not args.no_scale else None
+
     # ---- decode alone at the long-context and large-batch sizes
     scale = None
     if not args.no_scale:
@@ -382,6 +386,7 @@ def main():
         "kernel_avg_us": {k_: (round(v_ * 1e3, 3) if v_ else None) for k_, v_ in kernels.items()},
         "append": prefill,
         "decode_at_scale": scale,
+        "chunk_attention": chunk,
     }
     print(json.dumps(line), flush=True)
 
@@ -464,6 +469,52 @@ def bench_prefill(torch, wk, synth, dev, args):
         else:
             out["prenormed_keys"] = entry
     return out
+
+
+def bench_chunk(torch, wk, caches, reps, k1, tk, tinv, B, NQ, D, max_seq, sm, cfg, lengths_at,
+                done, T=16, calls=24):
+    """Chunk attention (Alg. 2 step 5 with S' = 16, causal inside the chunk)
+    on the Llama-shaped caches: each replica first takes a 16-token chunk
+    per sequence (one append), then the timed calls attend all 16 x 32
+    query rows per sequence.  Reported: query tokens per second and the
+    algorithmic bytes (the cache once, the queries and outputs) per second."""
+    dev = k1.device
+    gen = torch.Generator(device=dev).manual_seed(7)
+    kc = torch.randn(B, T, k1.shape[2], D, generator=gen, device=dev).to(torch.bfloat16)
+    vc = torch.randn(B, T, k1.shape[2], D, generator=gen, device=dev).to(torch.bfloat16)
+    q = torch.randn(B, T, NQ, D, generator=gen, device=dev).to(torch.bfloat16)
+    n = torch.full((B,), T, dtype=torch.int32, device=dev)
+    for c in caches:
+        wk.wushkv_append(c, kc, vc, n, tk)
+    torch.cuda.synchronize()
+    need = wk.wushkv_chunk_workspace_bytes(caches[0], NQ, T, max_seq)
+    ws = [torch.empty(need, dtype=torch.uint8, device=dev) for _ in range(reps)]
+    outs = [torch.empty(B, T, NQ, D, dtype=torch.float32, device=dev) for _ in range(reps)]
+    call = lambda i: wk.wushkv_chunk_attention(caches[i % reps], q, tinv, n_tok=n, sm_scale=sm,
+                                               max_seq_len=max_seq, out=outs[i % reps],
+                                               workspace=ws[i % reps])
+    for i in range(2 * reps):
+        call(i)
+    torch.cuda.synchronize()
+    n_calls = max(calls, reps) // reps * reps
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(n_calls):
+        call(i)
+    e1.record()
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) / n_calls * 1e-3
+    S = int(caches[0].seq_len[0].item())
+    Q = int(caches[0].quant_end[0].item())
+    main_b, other_b = decode_bytes([S] * B, [Q] * B, cfg["s_sink"], k1.shape[2], NQ, D, cfg["bits"])
+    byts = main_b + other_b + (T - 1) * B * NQ * D * (2 + 4)  # the other 15 tokens' q and out
+    log("chunk attention (16 tokens x %d sequences): %.1f us per call, %.3g query tokens/s, "
+        "%.1f GB/s algorithmic" % (B, t * 1e6, B * T / t, byts / t / 1e9))
+    return {"tokens_per_call": B * T, "call_us": round(t * 1e6, 2),
+            "query_tokens_per_s": round(B * T / t, 1), "bytes_per_call": int(byts),
+            "gbps_algorithmic": round(byts / t / 1e9, 1),
+            "note": "16-token chunks on the 8192-token Llama-shaped cache; the cache is read "
+                    "once per group of two chunk tokens (8 virtual query heads per kv head)"}
 
 
 def bench_decode_scale(torch, wk, synth, dev, args, calls=24):

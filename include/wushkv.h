@@ -246,6 +246,34 @@ size_t wushkv_decode_workspace_bytes(const wushkv_cache *c,
                                      int32_t n_q_heads, int32_t max_seq_len);
 
 /*
+ * wushkv_chunk_attention -- attention of a chunk of new tokens per sequence
+ * (Alg. 2 step 5 with S' > 1): Eq. (2) with its causal mask, over the cache
+ * as stored after the append that brought the chunk.
+ *
+ *   q          bf16 [batch][max_tok][n_q_heads][head_dim]: queries after norm
+ *              and RoPE; row t of sequence b is its chunk token t.
+ *   n_tok      int32 [batch] device, or NULL for max_tok everywhere: the
+ *              chunk of sequence b is its last n_tok[b] positions (clamped to
+ *              [0, min(max_tok, seq_len[b])]); token t sits at position
+ *              p = seq_len[b] - n_tok[b] + t and attends to positions [0, p].
+ *   max_tok    (host) 1 <= max_tok <= s_keep: the chunk lies inside the
+ *              recent window, so every quantised position precedes it.
+ *   out        fp32 [batch][max_tok][n_q_heads][head_dim]; rows beyond a
+ *              sequence's chunk are zero.
+ *   The other arguments are wushkv_decode_attention's; the workspace needs
+ *   wushkv_chunk_workspace_bytes().  Decode is the case max_tok = 1.
+ */
+int wushkv_chunk_attention(const wushkv_cache *c, const uint16_t *q,
+                           const int32_t *n_tok, int32_t max_tok, int32_t n_q_heads,
+                           int32_t max_seq_len, const float *t_k_inv, float sm_scale,
+                           float *out, void *workspace, size_t workspace_bytes,
+                           wushkv_stream_t stream);
+
+/* Workspace of wushkv_chunk_attention, or 0 for invalid arguments. */
+size_t wushkv_chunk_workspace_bytes(const wushkv_cache *c, int32_t n_q_heads,
+                                    int32_t max_tok, int32_t max_seq_len);
+
+/*
  * wushkv_dequant -- reconstruct stored entries x = scale * code + zero
  * (Eq. (7), last term) of sequence b, positions [start, start + count).
  *   k_out, v_out  fp32 [n_kv_heads][count][head_dim] (either may be null).

@@ -213,6 +213,40 @@ def wushkv_decode_attention(cache: WushKVCache, q, t_k_inv, sm_scale=None, max_s
     return out
 
 
+def wushkv_chunk_workspace_bytes(cache: WushKVCache, n_q_heads: int, max_tok: int,
+                                 max_seq_len: int) -> int:
+    return _lib.lib().wushkv_chunk_workspace_bytes(ctypes.byref(cache.desc), n_q_heads, max_tok,
+                                                   max_seq_len)
+
+
+def wushkv_chunk_attention(cache: WushKVCache, q, t_k_inv, n_tok=None, sm_scale=None,
+                           max_seq_len=None, out=None, workspace=None, stream=None):
+    """Attention of each sequence's chunk of new tokens, causal inside the
+    chunk.  q: bf16 [batch][max_tok][n_q][d]; n_tok: int32 [batch] on the
+    device or None (max_tok for all).  Returns fp32 [batch][max_tok][n_q][d]."""
+    torch = _torch()
+    _check_2byte(q, "q")
+    max_tok, n_q = q.shape[1], q.shape[2]
+    if max_seq_len is None:
+        max_seq_len = cache.max_seq_len
+    if sm_scale is None:
+        sm_scale = 1.0 / math.sqrt(cache.head_dim)
+    if out is None:
+        out = torch.empty(cache.batch, max_tok, n_q, cache.head_dim, dtype=torch.float32,
+                          device=q.device)
+    need = wushkv_chunk_workspace_bytes(cache, n_q, max_tok, max_seq_len)
+    if need == 0:
+        raise WushKVError(_lib.EINVAL, "wushkv_chunk_workspace_bytes")
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    st = _lib.lib().wushkv_chunk_attention(
+        ctypes.byref(cache.desc), _ptr(q), _ptr(n_tok), int(max_tok), n_q, int(max_seq_len),
+        _ptr(t_k_inv), float(sm_scale), _ptr(out), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream_handle(stream))
+    check(st, "wushkv_chunk_attention")
+    return out
+
+
 def wushkv_dequant(cache: WushKVCache, b: int, start: int, count: int, k_out=None, v_out=None,
                    stream=None):
     """fp32 [n_kv][count][d] reconstructions of stored positions

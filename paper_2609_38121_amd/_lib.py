@@ -77,6 +77,10 @@ def _declare(L):
     L.wushkv_decode_attention.restype = ctypes.c_int
     L.wushkv_decode_workspace_bytes.argtypes = [D, I32, I32]
     L.wushkv_decode_workspace_bytes.restype = SZ
+    L.wushkv_chunk_attention.argtypes = [D, P, P, I32, I32, I32, P, F32, P, P, SZ, P]
+    L.wushkv_chunk_attention.restype = ctypes.c_int
+    L.wushkv_chunk_workspace_bytes.argtypes = [D, I32, I32, I32]
+    L.wushkv_chunk_workspace_bytes.restype = SZ
     L.wushkv_dequant.argtypes = [D, I32, I32, I32, P, P, P]
     L.wushkv_dequant.restype = ctypes.c_int
     L.wushkv_status_string.argtypes = [ctypes.c_int]

@@ -63,7 +63,25 @@ struct DecodeArgs {
     const uint32_t *qaux;  // [batch][n_q][4]: limb scales (E8M0 bytes, limbs 0-3 then 4-5),
                            // sum(q~) (fp32 bits), unused
     float *part;           // [batch][n_kv][n_splits][G][D + 2]
+    // query rows: G is the number of virtual query heads per kv head, each
+    // a (chunk token, query head) pair; grid z runs over (sequence, token
+    // group) pairs bz = b n_groups + tg, token group tg holding chunk tokens
+    // tg tpg .. tg tpg + tpg - 1 (virtual head v: token tg tpg + v / g_real,
+    // head v % g_real).  Decode is the case max_tok = tpg = n_groups = 1.
+    int32_t n_groups, tpg, g_real, max_tok;
+    const int32_t *n_tok;  // [batch] chunk tokens per sequence, or null (max_tok)
 };
+
+// Tokens of sequence b's chunk: n_tok[b] (or max_tok), at most max_tok and
+// at most seq_len; the chunk is the last that many positions.
+__device__ __forceinline__ int32_t chunk_tokens(const int32_t *n_tok, int32_t max_tok, int32_t b,
+                                                int32_t S)
+{
+    int32_t n = n_tok != nullptr ? n_tok[b] : max_tok;
+    n = n < max_tok ? n : max_tok;
+    n = n < S ? n : S;
+    return n < 0 ? 0 : n;
+}
 
 __device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -98,17 +116,34 @@ __host__ __device__ constexpr int limb_pos(int ch)
 template <int D, int BITS>
 __global__ void __launch_bounds__(256) decode_qt_kernel(const uint16_t *q, const float *tinv,
                                                         float *qt, uint8_t *qlimb, uint32_t *qaux,
-                                                        int32_t n_kv, int32_t G, float scale)
+                                                        int32_t n_kv, int32_t G, float scale,
+                                                        DecodeArgs a)
 {
     constexpr int kJG = D / 8;        // groups of 8 output channels
     constexpr int kIG = 256 / kJG;    // groups of rows
     constexpr int kRows = D / kIG;    // rows per group
     __shared__ float qs[8 * D];
     __shared__ float red[kIG][8][D];
-    const int h = blockIdx.x, b = blockIdx.y;
-    const int n_q = n_kv * G;
-    const uint16_t *qb = q + ((int64_t)b * n_q + h * G) * D;
-    for (int i = threadIdx.x; i < G * D; i += 256) qs[i] = bf16_bits_to_f32(qb[i]);
+    // G virtual heads per kv head (see DecodeArgs); rows of tokens beyond the
+    // chunk are zero
+    const int h = blockIdx.x, bz = blockIdx.y;
+    const int b = bz / a.n_groups, tg = bz % a.n_groups;
+    // (decode: one token per sequence, always a valid row; an empty
+    // sequence's output is zero anyway)
+    const bool decode = a.max_tok == 1 && a.n_tok == nullptr;
+    const int32_t nb = decode ? 1 : chunk_tokens(a.n_tok, a.max_tok, b, a.seq_len[b]);
+    if (decode) {
+        const uint16_t *qb = q + ((int64_t)b * n_kv * G + h * G) * D;
+        for (int i = threadIdx.x; i < G * D; i += 256) qs[i] = bf16_bits_to_f32(qb[i]);
+    } else {
+        for (int i = threadIdx.x; i < G * D; i += 256) {
+            const int v = i / D, c = i % D;
+            const int t = tg * a.tpg + v / a.g_real, g = v % a.g_real;
+            qs[i] = t < nb ? bf16_bits_to_f32(q[(((int64_t)b * a.max_tok + t) * n_kv * a.g_real + h * a.g_real + g) * D + c])
+                           : 0.0f;
+        }
+    }
+    const int64_t qrow0 = ((int64_t)bz * n_kv + h) * G;  // first virtual head's row
     const int jg = threadIdx.x % kJG, ig = threadIdx.x / kJG;
     const float *T = tinv + (int64_t)h * D * D + (int64_t)ig * kRows * D + 8 * jg;
     f32x4 t[kRows][2];
@@ -138,7 +173,7 @@ __global__ void __launch_bounds__(256) decode_qt_kernel(const uint16_t *q, const
 #pragma unroll
         for (int k = 0; k < kIG; ++k) s += red[k][g][jj];
         s *= scale;
-        qt[((int64_t)b * n_q + h * G + g) * D + jj] = s;
+        qt[(qrow0 + g) * D + jj] = s;
         red[0][g][jj] = s;
     }
     __syncthreads();
@@ -147,7 +182,7 @@ __global__ void __launch_bounds__(256) decode_qt_kernel(const uint16_t *q, const
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     constexpr int kPer = D / 64;  // channels per lane
     for (int g = wave; g < G; g += 4) {
-        const int64_t qh = (int64_t)b * n_q + h * G + g;
+        const int64_t qh = qrow0 + g;
         float r[kPer];
         float zs = 0.0f;
 #pragma unroll
@@ -377,7 +412,9 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
     // derived from it) in scalar registers
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int j = lane >> 4, n = lane & 15;
-    const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+    // grid z: (sequence, token group) pairs; see DecodeArgs
+    const int split = blockIdx.x, h = blockIdx.y, bz = blockIdx.z;
+    const int b = bz / a.n_groups, tg = bz % a.n_groups;
     uint8_t *stage = lds + wave * M::kWave;
     uint8_t *tbuf = stage + M::kStageBytes;
     constexpr int kTP = M::kTPitch;
@@ -389,7 +426,7 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
     qend = qend < S ? qend : S;
     const int32_t q_hi = qend > a.s_sink ? qend : a.s_sink;  // quantised: [s_sink, q_hi)
     const int32_t n_qpages = (q_hi - a.s_sink + kPage - 1) / kPage;
-    const int64_t qhead0 = (int64_t)b * a.n_q + h * G;       // first query head of the group
+    const int64_t qhead0 = ((int64_t)bz * a.n_kv + h) * G;   // first (virtual) query head
 
     // per-wave results for the merge: o (unnormalised, relative to m), m, l
     float(*sC)[D] = reinterpret_cast<float(*)[D]>(stage);
@@ -751,9 +788,24 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
 #pragma unroll
             for (int c = 0; c < kC; ++c) sc = mfma16(qa[c], __builtin_bit_cast(bf16x8, kx[c]), sc);
             const bool ok = (vmask >> n) & 1u;
+            // causal visibility of this slot's position to the query rows
+            // 2 j and 2 j + 1: a chunk token at position p sees [0, p] (the
+            // quantised pages all lie before the chunk, so only the windows
+            // need this)
+            bool vis[2] = {ok, ok};  // decode: the query sees every live slot
+            if (a.max_tok > 1 || a.n_tok != nullptr) {
+                const int32_t sl = slot0 + n;
+                const int32_t pos = sl < a.s_sink ? sl : q_hi + ((sl - a.s_sink - a0 + ring) % ring);
+                const int32_t nb = chunk_tokens(a.n_tok, a.max_tok, b, S);
+#pragma unroll
+                for (int e = 0; e < 2; ++e) {
+                    const int32_t t = tg * a.tpg + (2 * j + e) / a.g_real;  // chunk token of the row
+                    vis[e] = ok && t < nb && pos <= S - nb + t;
+                }
+            }
             float lg[2];
-            lg[0] = ok ? sc[0] + sc[1] : -INFINITY;
-            lg[1] = ok ? sc[2] + sc[3] : -INFINITY;
+            lg[0] = vis[0] ? sc[0] + sc[1] : -INFINITY;
+            lg[1] = vis[1] ? sc[2] + sc[3] : -INFINITY;
             float pr[2];
 #pragma unroll
             for (int e = 0; e < 2; ++e) {
@@ -802,7 +854,7 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
     __syncthreads();
 
     // ---- merge the four waves
-    float *part = a.part + (((int64_t)b * a.n_kv + h) * a.n_splits + split) * G * (D + 2);
+    float *part = a.part + (((int64_t)bz * a.n_kv + h) * a.n_splits + split) * G * (D + 2);
     for (int idx = tid; idx < G * D; idx += 256) {
         const int gg = idx / D, ch = idx % D;
         float mx = -INFINITY;
@@ -834,16 +886,30 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
 template <int D>
 __global__ void __launch_bounds__(D) decode_combine_kernel(const float *part, float *out,
                                                            int32_t n_kv, int32_t G,
-                                                           int32_t n_splits)
+                                                           int32_t n_splits, DecodeArgs a)
 {
     __shared__ float fw[kMaxSplits];
     __shared__ float red[D];
-    const int qh = blockIdx.x, b = blockIdx.y;
+    // virtual head qh = (h, v) of grid row bz = (b, token group tg): chunk
+    // token tg tpg + v / g_real, query head h g_real + v % g_real
+    const int qh = blockIdx.x, bz = blockIdx.y;
     const int h = qh / G, g = qh % G;
     const int ch = threadIdx.x;
-    const int n_q = n_kv * G;
+    float *dst;
+    if (a.max_tok == 1 && a.n_tok == nullptr) {
+        dst = out + ((int64_t)bz * n_kv * G + qh) * D;  // decode: row bz = b, head qh
+    } else {
+        const int b = bz / a.n_groups, tg = bz % a.n_groups;
+        const int t = tg * a.tpg + g / a.g_real;
+        if (t >= a.max_tok) return;
+        dst = out + (((int64_t)b * a.max_tok + t) * n_kv * a.g_real + h * a.g_real + g % a.g_real) * D;
+        if (t >= chunk_tokens(a.n_tok, a.max_tok, b, a.seq_len[b])) {
+            dst[ch] = 0.0f;  // beyond this sequence's chunk
+            return;
+        }
+    }
     const int64_t stride = (int64_t)G * (D + 2);
-    const float *pp = part + (((int64_t)b * n_kv + h) * n_splits) * stride + g * (D + 2);
+    const float *pp = part + (((int64_t)bz * n_kv + h) * n_splits) * stride + g * (D + 2);
     float mx = -INFINITY;
     for (int s = ch; s < n_splits; s += D) {
         const float m = pp[s * stride + D];
@@ -869,7 +935,7 @@ __global__ void __launch_bounds__(D) decode_combine_kernel(const float *part, fl
             l = fmaf(f, pp[s * stride + D + 1], l);
         }
     }
-    out[((int64_t)b * n_q + qh) * D + ch] = (l > 0.0f) ? o / l : 0.0f;
+    dst[ch] = (l > 0.0f) ? o / l : 0.0f;
 }
 
 // ------------------------------------------------------------------ host
@@ -927,11 +993,31 @@ static int64_t resident_waves(int D, int bits, int G)
     return waves;
 }
 
-static bool make_plan(const wushkv_cache *c, int32_t n_q, int32_t max_seq_len, DecodePlan &p)
+// Query rows of a call: G virtual heads per kv head, each a (chunk token,
+// query head) pair, and n_groups token groups per sequence (see DecodeArgs).
+struct RowShape {
+    int32_t g_real, tpg, G, n_groups, max_tok;
+};
+
+static RowShape row_shape(const wushkv_cache *c, int32_t n_q, int32_t max_tok)
 {
-    const int32_t G = n_q / c->n_kv_heads;
+    RowShape r;
+    r.g_real = n_q / c->n_kv_heads;
+    r.max_tok = max_tok;
+    r.tpg = 1;
+    while (r.g_real * r.tpg * 2 <= 8 && r.tpg < max_tok) r.tpg *= 2;
+    r.G = r.g_real * r.tpg;
+    r.n_groups = (max_tok + r.tpg - 1) / r.tpg;
+    return r;
+}
+
+static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq_len, DecodePlan &p)
+{
+    const int32_t G = rs.G;
     const int64_t qpages = max_seq_len > c->s_sink ? (max_seq_len - c->s_sink + kPage - 1) / kPage : 0;
-    const int64_t heads = (int64_t)c->batch * c->n_kv_heads;
+    const int64_t rows_z = (int64_t)c->batch * rs.n_groups;  // grid z
+    const int64_t heads = rows_z * c->n_kv_heads;
+    const int64_t n_q = (int64_t)c->n_kv_heads * G;          // virtual query heads per row
     // One residency round if it can be had: the page waves get what the
     // window workgroups leave of the resident waves; at least 2 and at most
     // 16 pages per wave (when the work cannot fit one round, shorter waves
@@ -952,9 +1038,9 @@ static bool make_plan(const wushkv_cache *c, int32_t n_q, int32_t max_seq_len, D
     p.units_per_wave = (int32_t)upw;
     p.n_page_splits = (int32_t)psplits;
     p.n_splits = (int32_t)splits;
-    p.qt_bytes = ((size_t)c->batch * n_q * c->head_dim * 4 + 255) / 256 * 256;
-    p.limb_bytes = (size_t)c->batch * n_q * kLimbs * 128;
-    p.aux_bytes = ((size_t)c->batch * n_q * 16 + 255) / 256 * 256;
+    p.qt_bytes = ((size_t)rows_z * n_q * c->head_dim * 4 + 255) / 256 * 256;
+    p.limb_bytes = (size_t)rows_z * n_q * kLimbs * 128;
+    p.aux_bytes = ((size_t)rows_z * n_q * 16 + 255) / 256 * 256;
     p.part_bytes = (size_t)heads * splits * G * (c->head_dim + 2) * 4;
     return true;
 }
@@ -992,19 +1078,25 @@ static int check_decode_args(const wushkv_cache *c, int32_t n_q, int32_t max_seq
     return WUSHKV_OK;
 }
 
-extern "C" size_t wushkv_decode_workspace_bytes(const wushkv_cache *c, int32_t n_q_heads,
-                                                int32_t max_seq_len)
+// A chunk must lie inside the recent window (at most s_keep tokens): every
+// quantised position then precedes it.
+static int check_chunk(const wushkv_cache *c, int32_t max_tok)
 {
-    if (check_decode_args(c, n_q_heads, max_seq_len) != WUSHKV_OK) return 0;
+    if (max_tok < 1 || max_tok > c->s_keep) return WUSHKV_EINVAL;
+    return WUSHKV_OK;
+}
+
+static size_t workspace_bytes(const wushkv_cache *c, int32_t n_q, int32_t max_tok, int32_t max_seq_len)
+{
+    if (check_decode_args(c, n_q, max_seq_len) != WUSHKV_OK) return 0;
     DecodePlan p;
-    if (!make_plan(c, n_q_heads, max_seq_len, p)) return 0;
+    if (!make_plan(c, row_shape(c, n_q, max_tok), max_seq_len, p)) return 0;
     return p.qt_bytes + p.limb_bytes + p.aux_bytes + p.part_bytes;
 }
 
-extern "C" int wushkv_decode_attention(const wushkv_cache *c, const uint16_t *q, int32_t n_q_heads,
-                                       int32_t max_seq_len, const float *t_k_inv, float sm_scale,
-                                       float *out, void *workspace, size_t workspace_bytes,
-                                       wushkv_stream_t stream)
+static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok, int32_t max_tok,
+                  int32_t n_q_heads, int32_t max_seq_len, const float *t_k_inv, float sm_scale,
+                  float *out, void *workspace, size_t workspace_bytes, wushkv_stream_t stream)
 {
     int st = check_decode_args(c, n_q_heads, max_seq_len);
     if (st != WUSHKV_OK) return st;
@@ -1012,12 +1104,13 @@ extern "C" int wushkv_decode_attention(const wushkv_cache *c, const uint16_t *q,
     if (((uintptr_t)q | (uintptr_t)t_k_inv | (uintptr_t)out | (uintptr_t)workspace) & 15u)
         return WUSHKV_EINVAL;
     if (!(sm_scale > 0.0f) || sm_scale == INFINITY) return WUSHKV_EINVAL;
+    const RowShape rs = row_shape(c, n_q_heads, max_tok);
     DecodePlan p;
-    if (!make_plan(c, n_q_heads, max_seq_len, p)) return WUSHKV_EINVAL;
+    if (!make_plan(c, rs, max_seq_len, p)) return WUSHKV_EINVAL;
     if (workspace_bytes < p.qt_bytes + p.limb_bytes + p.aux_bytes + p.part_bytes) return WUSHKV_EWORKSPACE;
 
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const int32_t G = n_q_heads / c->n_kv_heads;
+    const int32_t G = rs.G;
     uint8_t *ws = reinterpret_cast<uint8_t *>(workspace);
     float *qt = reinterpret_cast<float *>(ws);
     uint8_t *qlimb = ws + p.qt_bytes;
@@ -1036,7 +1129,7 @@ extern "C" int wushkv_decode_attention(const wushkv_cache *c, const uint16_t *q,
     a.win_slots = c->win_slots;
     a.max_pages = c->max_pages_per_seq;
     a.n_pages = c->n_pages;
-    a.n_q = n_q_heads;
+    a.n_q = c->n_kv_heads * G;
     a.units_per_wave = p.units_per_wave;
     a.n_page_splits = p.n_page_splits;
     a.n_splits = p.n_splits;
@@ -1044,18 +1137,24 @@ extern "C" int wushkv_decode_attention(const wushkv_cache *c, const uint16_t *q,
     a.qlimb = qlimb;
     a.qaux = qaux;
     a.part = part;
+    a.n_groups = rs.n_groups;
+    a.tpg = rs.tpg;
+    a.g_real = rs.g_real;
+    a.max_tok = rs.max_tok;
+    a.n_tok = n_tok;
 
-    const dim3 gq(c->n_kv_heads, c->batch);
-    const dim3 gm(p.n_splits, c->n_kv_heads, c->batch);
-    const dim3 gc(n_q_heads, c->batch);
+    const unsigned rows_z = (unsigned)(c->batch * rs.n_groups);
+    const dim3 gq(c->n_kv_heads, rows_z);
+    const dim3 gm(p.n_splits, c->n_kv_heads, rows_z);
+    const dim3 gc(c->n_kv_heads * G, rows_z);
     const float scale = sm_scale * kLog2e;
     const int key = c->head_dim * 10 + c->bits;
 
     switch (key) {
-        case 1282: launch("decode_qt_kernel", decode_qt_kernel<128, 2>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
-        case 1284: launch("decode_qt_kernel", decode_qt_kernel<128, 4>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
-        case 642: launch("decode_qt_kernel", decode_qt_kernel<64, 2>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
-        case 644: launch("decode_qt_kernel", decode_qt_kernel<64, 4>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale); break;
+        case 1282: launch("decode_qt_kernel", decode_qt_kernel<128, 2>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale, a); break;
+        case 1284: launch("decode_qt_kernel", decode_qt_kernel<128, 4>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale, a); break;
+        case 642: launch("decode_qt_kernel", decode_qt_kernel<64, 2>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale, a); break;
+        case 644: launch("decode_qt_kernel", decode_qt_kernel<64, 4>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale, a); break;
     }
     switch (key) {
         case 1282: launch_main_g<128, 2>(G, gm, s, a); break;
@@ -1063,8 +1162,44 @@ extern "C" int wushkv_decode_attention(const wushkv_cache *c, const uint16_t *q,
         case 642: launch_main_g<64, 2>(G, gm, s, a); break;
         case 644: launch_main_g<64, 4>(G, gm, s, a); break;
     }
-    if (c->head_dim == 128) launch("decode_combine_kernel", decode_combine_kernel<128>, gc, dim3(128), s, (const float *)part, out, c->n_kv_heads, G, p.n_splits);
-    else launch("decode_combine_kernel", decode_combine_kernel<64>, gc, dim3(64), s, (const float *)part, out, c->n_kv_heads, G, p.n_splits);
+    if (c->head_dim == 128) launch("decode_combine_kernel", decode_combine_kernel<128>, gc, dim3(128), s, (const float *)part, out, c->n_kv_heads, G, p.n_splits, a);
+    else launch("decode_combine_kernel", decode_combine_kernel<64>, gc, dim3(64), s, (const float *)part, out, c->n_kv_heads, G, p.n_splits, a);
     if (hipGetLastError() != hipSuccess) return WUSHKV_ELAUNCH;
     return WUSHKV_OK;
+}
+
+extern "C" size_t wushkv_decode_workspace_bytes(const wushkv_cache *c, int32_t n_q_heads,
+                                                int32_t max_seq_len)
+{
+    return workspace_bytes(c, n_q_heads, 1, max_seq_len);
+}
+
+extern "C" int wushkv_decode_attention(const wushkv_cache *c, const uint16_t *q, int32_t n_q_heads,
+                                       int32_t max_seq_len, const float *t_k_inv, float sm_scale,
+                                       float *out, void *workspace, size_t workspace_bytes,
+                                       wushkv_stream_t stream)
+{
+    return attend(c, q, nullptr, 1, n_q_heads, max_seq_len, t_k_inv, sm_scale, out, workspace,
+                  workspace_bytes, stream);
+}
+
+extern "C" size_t wushkv_chunk_workspace_bytes(const wushkv_cache *c, int32_t n_q_heads,
+                                               int32_t max_tok, int32_t max_seq_len)
+{
+    if (wushkv_validate_cache(c) != WUSHKV_OK || check_chunk(c, max_tok) != WUSHKV_OK) return 0;
+    return workspace_bytes(c, n_q_heads, max_tok, max_seq_len);
+}
+
+extern "C" int wushkv_chunk_attention(const wushkv_cache *c, const uint16_t *q,
+                                      const int32_t *n_tok, int32_t max_tok, int32_t n_q_heads,
+                                      int32_t max_seq_len, const float *t_k_inv, float sm_scale,
+                                      float *out, void *workspace, size_t workspace_bytes,
+                                      wushkv_stream_t stream)
+{
+    int st = wushkv_validate_cache(c);
+    if (st != WUSHKV_OK) return st;
+    st = check_chunk(c, max_tok);
+    if (st != WUSHKV_OK) return st;
+    return attend(c, q, n_tok, max_tok, n_q_heads, max_seq_len, t_k_inv, sm_scale, out, workspace,
+                  workspace_bytes, stream);
 }

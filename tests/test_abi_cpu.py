@@ -95,6 +95,14 @@ def test_call_specific_validation():
     assert nr(by, FAKE, FAKE, FAKE, 1, FAKE, FAKE + 4, 0.0, FAKE, 260, None, None) == -1
     assert nr(by, None, FAKE, FAKE, 1, FAKE, None, 0.0, FAKE, 260, None, None) == -1
     assert nr(by, FAKE, FAKE, FAKE, 0, FAKE, None, 0.0, FAKE, 260, None, None) == 0
+    # chunk attention: 1 <= max_tok <= s_keep (128 here)
+    ca = L.wushkv_chunk_attention
+    assert ca(by, FAKE, None, 0, 8, 100, FAKE, 0.1, FAKE, FAKE, 1 << 30, None) == -1
+    assert ca(by, FAKE, None, 129, 8, 100, FAKE, 0.1, FAKE, FAKE, 1 << 30, None) == -1
+    assert L.wushkv_chunk_workspace_bytes(by, 8, 129, 100) == 0
+    assert L.wushkv_chunk_workspace_bytes(by, 8, 16, 100) > L.wushkv_decode_workspace_bytes(by, 8, 100)
+    need = L.wushkv_chunk_workspace_bytes(by, 8, 16, 100)
+    assert ca(by, FAKE, None, 16, 8, 100, FAKE, 0.1, FAKE, FAKE, need - 1, None) == -3
     # decode: n_q not a multiple of n_kv, G too large or not a power of two,
     # bad scale, small workspace
     assert L.wushkv_decode_attention(by, FAKE, 7, 100, FAKE, 0.1, FAKE, FAKE, 1 << 30, None) == -1
