@@ -10,7 +10,7 @@ bf16 value of every position plus the codes and fp16 (scale, zero) of the
 quantised positions.  It knows nothing of pages, rings or kernel layouts.
 
 Paper references: Eq. (2) attention, Eq. (3) transform insertion, Eq. (7)
-quantiser, Sec. 4.4 windows, Alg. 2 cache management.
+and Eq. (5) quantisers, Sec. 4.4 windows, Alg. 2 cache management.
 """
 from __future__ import annotations
 
@@ -80,7 +80,9 @@ def _declare(L):
     L.orc_dequant.restype = _F32
     L.orc_next_quant_end.argtypes = [_I32] * 5
     L.orc_next_quant_end.restype = _I32
-    L.orc_append_head.argtypes = [ctypes.c_int] * 5 + [_F32, _F32, _I32, _I32, _I32,
+    L.orc_quest_quantize_groups.argtypes = [_P, _I64, ctypes.c_int, ctypes.c_int, _F32, _P, _P]
+    L.orc_quest_quantize_groups.restype = None
+    L.orc_append_head.argtypes = [ctypes.c_int] * 6 + [_F32, _F32, _F32, _I32, _I32, _I32,
                                                        _P, _I64, _P, _I64, _P,
                                                        _P, _P, _P, _P, _P, _P]
     L.orc_append_head.restype = _I32
@@ -160,6 +162,52 @@ def quantize_groups(x, bits: int, kappa: float):
     return codes, params[..., 0].copy(), params[..., 1].copy()
 
 
+# --------------------------------------------------------------------------
+# QuEST quantiser, Eq. (5)
+# --------------------------------------------------------------------------
+
+def quest_grid_mse(alpha: float, bits: int) -> float:
+    """Mean squared error of rounding a standard Gaussian to the nearest of
+    the 2^bits levels spaced evenly from -alpha to +alpha (Sec. 4.3, and the
+    fixed-scale grid of the clipping lemma in App. B).  Sum over the levels
+    of the integral of (x - level)^2 over its nearest-level cell, with the
+    Gaussian moments int phi = Phi, int x phi = -phi, int x^2 phi = Phi - x phi."""
+    from scipy.special import ndtr
+    n = 1 << bits
+    lv = -alpha + 2.0 * alpha / (n - 1) * np.arange(n, dtype=np.float64)
+    edges = np.concatenate([[-np.inf], 0.5 * (lv[1:] + lv[:-1]), [np.inf]])
+    a, b = edges[:-1], edges[1:]
+    phi = lambda t: np.where(np.isfinite(t), np.exp(-0.5 * np.where(np.isfinite(t), t, 0.0) ** 2)
+                             / np.sqrt(2.0 * np.pi), 0.0)
+    tphi = lambda t: np.where(np.isfinite(t), np.where(np.isfinite(t), t, 0.0) * phi(t), 0.0)
+    m0 = ndtr(b) - ndtr(a)
+    m1 = phi(a) - phi(b)
+    m2 = m0 - (tphi(b) - tphi(a))
+    return float(np.sum(m2 - 2.0 * lv * m1 + lv * lv * m0))
+
+
+def quest_alpha(bits: int) -> float:
+    """alpha_b of Eq. (5): the endpoint that minimises quest_grid_mse (Sec. 4.3),
+    found by bounded scalar minimisation of the error itself."""
+    from scipy.optimize import minimize_scalar
+    r = minimize_scalar(lambda a: quest_grid_mse(a, bits), bounds=(1e-3, 16.0), method="bounded",
+                        options={"xatol": 1e-12, "maxiter": 500})
+    return float(r.x)
+
+
+def quest_quantize_groups(x, bits: int, alpha: float):
+    """x [..., d] fp32 -> (codes uint8 [..., d] in [0, 2^bits - 1],
+    scale16, zero16 uint16 [...]) of Eq. (5); reconstruction is
+    dequant(codes, scale16, zero16)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    d = x.shape[-1]
+    n = x.size // d
+    codes = np.empty(x.shape, dtype=np.uint8)
+    params = np.empty(x.shape[:-1] + (2,), dtype=np.uint16)
+    lib().orc_quest_quantize_groups(_ptr(x), n, d, bits, alpha, _ptr(codes), _ptr(params))
+    return codes, params[..., 0].copy(), params[..., 1].copy()
+
+
 def dequant(codes, s16, z16) -> np.ndarray:
     """fp32 reconstruction scale * code + zero (one rounding)."""
     codes = np.asarray(codes, dtype=np.uint8)
@@ -188,10 +236,12 @@ class OracleCache:
     """
 
     def __init__(self, batch, n_kv, d, bits, s_sink, s_keep, s_flush,
-                 kappa_k, kappa_v, capacity):
+                 kappa_k, kappa_v, capacity, codec="pclip", quest_alpha=0.0):
         self.batch, self.n_kv, self.d, self.bits = batch, n_kv, d, bits
         self.s_sink, self.s_keep, self.s_flush = s_sink, s_keep, s_flush
         self.kappa_k, self.kappa_v = float(kappa_k), float(kappa_v)
+        assert codec in ("pclip", "quest")
+        self.codec, self.quest_alpha = codec, float(quest_alpha)
         self.cap = capacity
         shp = (batch, n_kv, capacity, d)
         self.kbits = np.zeros(shp, np.uint16)
@@ -223,7 +273,8 @@ class OracleCache:
                 vptr = ctypes.c_void_p(v_new.ctypes.data + (b * v_new.shape[1] * nkv + h) * d * 2)
                 q_new = L.orc_append_head(
                     d, self.bits, self.s_sink, self.s_keep, self.s_flush,
-                    self.kappa_k, self.kappa_v, s_old, q_old, n,
+                    1 if self.codec == "quest" else 0, self.kappa_k, self.kappa_v,
+                    self.quest_alpha, s_old, q_old, n,
                     kptr, row_stride, vptr, row_stride,
                     _ptr(tk[h]),
                     _ptr(self.kbits[b, h]), _ptr(self.vbits[b, h]),

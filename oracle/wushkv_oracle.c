@@ -14,6 +14,9 @@
  *   orc_next_quant_end  the S_quant update of Alg. 2 (0-based, exclusive).
  *   orc_quantize_group  Eq. (7): the OSCAR-style percentile-clipped affine
  *                    quantiser used for the end-to-end runs (Sec. 5.3).
+ *   orc_quest_quantize_group  Eq. (5): the QuEST projection of Sec. 4.3, the
+ *                    quantiser of the paper's analysis (App. B) and of its
+ *                    reconstruction-error and perplexity runs (Sec. 5.1-5.2).
  *   orc_dequant      the reconstruction term of Eq. (7).
  *   orc_decode_head  Eq. (2) GQA attention for one query per query head,
  *                    with the query compensation of Eq. (3) (q -> T_K^{-T} q,
@@ -213,6 +216,51 @@ void orc_quantize_groups(const float *x, int64_t n, int d, int bits, float kappa
                            params + 2 * g, params + 2 * g + 1);
 }
 
+/* Eq. (5), the QuEST projection (Sec. 4.3), for one group x of d values:
+ * the step is 2 alpha (2^b - 1)^-1 d^-1/2 ||x||, the code is the floor of
+ * x / step clamped to [-2^(b-1), 2^(b-1) - 1], and the reconstruction is the
+ * bin centre step (code + 1/2), so the 2^b levels run evenly from -alpha to
+ * +alpha times the group's RMS.  Precision (the paper does not fix it):
+ *   - ||x||^2 is summed in fp64 over the exact squares; the step is formed
+ *     in fp64 as (2 alpha / (2^b - 1)) * sqrt(||x||^2 / d) and rounded once
+ *     to fp32, then to the fp16 scale s;
+ *   - the code is chosen on the stored grid, from the fp32 product x * (1/s);
+ *   - the stored code is u = code + 2^(b-1) in [0, 2^b - 1] and the stored
+ *     zero is fp16(s (1/2 - 2^(b-1))) (exact in fp32), so that the common
+ *     reconstruction s u + zero is the bin centre s (code + 1/2), up to the
+ *     fp16 rounding of the zero;
+ *   - the zero group (or a step that underflows fp16) has s = 0: every code
+ *     is 2^(b-1) and the reconstruction is 0, matching Q(0) = 0. */
+void orc_quest_quantize_group(const float *x, int d, int bits, float alpha,
+                              uint8_t *codes, uint16_t *s16_out, uint16_t *z16_out)
+{
+    double ss = 0.0;
+    for (int i = 0; i < d; ++i) ss += (double)x[i] * (double)x[i];
+    int h = 1 << (bits - 1);
+    double coef = 2.0 * (double)alpha / (double)((1 << bits) - 1);
+    float step = (float)(coef * sqrt(ss / (double)d));
+    uint16_t s16 = orc_f32_to_f16(step);
+    float s = orc_f16_to_f32(s16);
+    uint16_t z16 = orc_f32_to_f16(s * (0.5f - (float)h));
+    float inv = (s > 0.0f) ? 1.0f / s : 0.0f;
+    for (int i = 0; i < d; ++i) {
+        float c = floorf(x[i] * inv);
+        if (c < (float)-h) c = (float)-h;
+        if (c > (float)(h - 1)) c = (float)(h - 1);
+        codes[i] = (uint8_t)(int)(c + (float)h);
+    }
+    *s16_out = s16;
+    *z16_out = z16;
+}
+
+void orc_quest_quantize_groups(const float *x, int64_t n, int d, int bits, float alpha,
+                               uint8_t *codes, uint16_t *params)
+{
+    for (int64_t g = 0; g < n; ++g)
+        orc_quest_quantize_group(x + g * d, d, bits, alpha, codes + g * d,
+                                 params + 2 * g, params + 2 * g + 1);
+}
+
 /* Reconstruction: scale * code + zero, one rounding to fp32. */
 float orc_dequant(uint8_t code, uint16_t s16, uint16_t z16)
 {
@@ -256,7 +304,7 @@ int32_t orc_next_quant_end(int32_t s_new, int32_t s_quant, int32_t s_sink,
  * do not depend on whether it is quantised in the call that appends it or in
  * a later one.  Returns the new S_quant. */
 int32_t orc_append_head(int d, int bits, int s_sink, int s_keep, int s_flush,
-                        float kappa_k, float kappa_v,
+                        int codec, float kappa_k, float kappa_v, float alpha,
                         int32_t s_old, int32_t q_old, int32_t n_new,
                         const uint16_t *k_new, int64_t k_row_stride,
                         const uint16_t *v_new, int64_t v_row_stride,
@@ -285,9 +333,15 @@ int32_t orc_append_head(int d, int bits, int s_sink, int s_keep, int s_flush,
     float x[512];
     for (int64_t p = start; p < q_new; ++p) {
         for (int i = 0; i < d; ++i) x[i] = orc_bf16_to_f32(kbits[p * d + i]);
-        orc_quantize_group(x, d, bits, lok, tkf, kc + p * d, kp + 2 * p, kp + 2 * p + 1);
+        if (codec == 1)
+            orc_quest_quantize_group(x, d, bits, alpha, kc + p * d, kp + 2 * p, kp + 2 * p + 1);
+        else
+            orc_quantize_group(x, d, bits, lok, tkf, kc + p * d, kp + 2 * p, kp + 2 * p + 1);
         for (int i = 0; i < d; ++i) x[i] = orc_bf16_to_f32(vbits[p * d + i]);
-        orc_quantize_group(x, d, bits, lov, tvf, vc + p * d, vp + 2 * p, vp + 2 * p + 1);
+        if (codec == 1)
+            orc_quest_quantize_group(x, d, bits, alpha, vc + p * d, vp + 2 * p, vp + 2 * p + 1);
+        else
+            orc_quantize_group(x, d, bits, lov, tvf, vc + p * d, vp + 2 * p, vp + 2 * p + 1);
     }
     return q_new;
 }
