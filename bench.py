@@ -397,7 +397,8 @@ def bench_prefill(torch, wk, synth, dev, args):
     the headwise RMS normalisation and RoPE (theta 1e6) itself, then the key
     transform, the quantisation and the packing (the whole prefill path of
     that workload).  The same append on keys normalised and rotated by the
-    input generator is reported beside it."""
+    input generator is reported beside it, and so is the fused append into a
+    cache that uses the QuEST codec (Eq. (5)) instead of Eq. (7)."""
     cfg = synth.CONFIGS["prefill"]
     w = synth.Workload(cfg, seed=args.seed)
     B, H, D, BITS, n = cfg["batch"], cfg["n_kv"], cfg["d"], cfg["bits"], cfg["ctx"]
@@ -410,20 +411,25 @@ def bench_prefill(torch, wk, synth, dev, args):
     tk = as_dev(tk_bits)
     cache = wk.WushKVCache(B, H, D, BITS, cfg["s_sink"], cfg["s_keep"], cfg["s_flush"],
                            cfg["kappa_k"], cfg["kappa_v"], max_seq_len=n)
+    qcache = wk.WushKVCache(B, H, D, BITS, cfg["s_sink"], cfg["s_keep"], cfg["s_flush"],
+                            cfg["kappa_k"], cfg["kappa_v"], max_seq_len=n, codec="quest")
     table = torch.from_numpy(synth.rope_table(cfg["rope_theta"], D, cache.max_pages * 64 + cfg["s_sink"])).to(dev)
     nn = torch.full((B,), n, dtype=torch.int32, device=dev)
     reps = 10
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     calls = {
-        "norm_rope": lambda: wk.wushkv_append_norm_rope(cache, k_raw, v, nn, tk, table, norm_eps=1e-6),
-        "prenormed": lambda: wk.wushkv_append(cache, k, v, nn, tk),
+        "norm_rope": (cache, lambda: wk.wushkv_append_norm_rope(cache, k_raw, v, nn, tk, table,
+                                                                norm_eps=1e-6)),
+        "prenormed": (cache, lambda: wk.wushkv_append(cache, k, v, nn, tk)),
+        "quest": (qcache, lambda: wk.wushkv_append_norm_rope(qcache, k_raw, v, nn, tk, table,
+                                                             norm_eps=1e-6)),
     }
     res = {}
-    for name, call in calls.items():
+    for name, (cc, call) in calls.items():
         times = []
         for r in range(reps + 2):
-            cache.seq_len.zero_()
-            cache.quant_end.zero_()
+            cc.seq_len.zero_()
+            cc.quant_end.zero_()
             torch.cuda.synchronize()
             e0.record()
             call()
@@ -434,8 +440,8 @@ def bench_prefill(torch, wk, synth, dev, args):
         # the same calls again, each kernel stamped by the library
         wk.wushkv_timing_enable(16 * reps)
         for r in range(reps):
-            cache.seq_len.zero_()
-            cache.quant_end.zero_()
+            cc.seq_len.zero_()
+            cc.quant_end.zero_()
             call()
         torch.cuda.synchronize()
         cnt, tot = wk.wushkv_timing_read("append_kernel")
@@ -448,9 +454,9 @@ def bench_prefill(torch, wk, synth, dev, args):
     byts = prefill_bytes(B, H, D, BITS, n, n_quant)
     table_bytes = n * D * 4  # the rotary table rows of the positions written
     out = None
-    for name in ("norm_rope", "prenormed"):
+    for name in ("norm_rope", "prenormed", "quest"):
         ms, t_kernel, t_flush = res[name]
-        b_ = byts + (table_bytes if name == "norm_rope" else 0)
+        b_ = byts + (table_bytes if name != "prenormed" else 0)
         ach = b_ / (t_kernel * 1e-3) / 1e9
         log("prefill append (%s): %.1f us/call, %.3g tokens/s, append_kernel %.1f us, %.1f GB/s "
             "(flush-only launch %.1f us)" % (name, ms * 1e3, tokens / (ms * 1e-3), t_kernel * 1e3,
@@ -466,8 +472,10 @@ def bench_prefill(torch, wk, synth, dev, args):
         if out is None:
             out = dict(entry, workload="prefill-append-4x16384-2bit, RMS norm + RoPE fused",
                        keys="projected (Student-t), normalised and rotated by the append")
-        else:
+        elif name == "prenormed":
             out["prenormed_keys"] = entry
+        else:
+            out["quest_codec"] = dict(entry, codec="QuEST, Eq. (5), alpha_2 = %.6f" % qcache.quest_alpha)
     return out
 
 

@@ -9,7 +9,9 @@
  * here already transformed; the key transform is applied online after norm
  * and RoPE.  Queries are compensated with T_K^{-T} (Alg. 2, step 3).  The
  * quantiser is the per-token percentile-clipped affine quantiser of Eq. (7)
- * and the cache keeps two bf16 windows, a sink and a recent window, with
+ * or, per cache, the RMS-scaled symmetric QuEST quantiser of Eq. (5) (the
+ * one the paper's analysis and reconstruction-error experiments use), and
+ * the cache keeps two bf16 windows, a sink and a recent window, with
  * quantisation in multiples of S_flush (Sec. 4.4, Alg. 2).
  *
  * Entry points:
@@ -58,7 +60,13 @@ enum {
 };
 
 #define WUSHKV_PAGE_TOKENS 64
-#define WUSHKV_ABI_VERSION 2
+#define WUSHKV_ABI_VERSION 3
+
+/* Per-token quantisers (wushkv_cache.codec). */
+enum {
+    WUSHKV_CODEC_PCLIP = 0, /* Eq. (7): percentile-clipped affine */
+    WUSHKV_CODEC_QUEST = 1  /* Eq. (5): RMS-scaled, symmetric, bin centres */
+};
 
 /*
  * Cache descriptor.  Sizes are host values; the arrays are device memory.
@@ -83,7 +91,9 @@ enum {
  *     V codes   8 * head_dim * bits bytes
  *     K params  64 tokens x 4 bytes: fp16 scale, fp16 zero (token t at 4 t)
  *     V params  64 tokens x 4 bytes, same form
- *   Reconstruction of a stored entry: x = scale * code + zero (fp32 fma).
+ *   Reconstruction of a stored entry: x = scale * code + zero (fp32 fma),
+ *   for both codecs (the QuEST codec stores its bin-centre offset as the
+ *   zero, see wushkv_append).
  *
  *   Code words.  Both code regions are arrays of little-endian 32-bit
  *   words; a word holds B = 32 / bits codes.  Each region is a sequence of
@@ -131,8 +141,11 @@ typedef struct wushkv_cache {
     int32_t win_slots;         /* multiple of 64, >= s_sink + max(1, s_keep + s_flush - 1) */
     int32_t max_pages_per_seq; /* row length of page_table, >= 0 */
     int32_t n_pages;           /* pages in the pool, >= 0 */
-    float kappa_k;             /* Eq. (7) clipping quantile for keys, (0, 1] */
+    float kappa_k;             /* Eq. (7) clipping quantile for keys, (0, 1] (PCLIP) */
     float kappa_v;             /* same for values */
+    int32_t codec;             /* WUSHKV_CODEC_PCLIP or WUSHKV_CODEC_QUEST */
+    float quest_alpha;         /* Eq. (5) clip multiplier alpha_b > 0, finite (QUEST);
+                                  wushkv_quest_alpha(bits) is the paper's choice */
     uint8_t *pages;
     int32_t *page_table;       /* [batch][max_pages_per_seq] */
     uint16_t *win_k;
@@ -163,10 +176,25 @@ size_t wushkv_page_bytes(int32_t head_dim, int32_t bits);
  *   S_new = S + S'; S_start = max(S_quant, s_sink);
  *   S_quant_new = max(S_quant, S_start + floor((S_new - s_keep - S_start)
  *                 / s_flush) * s_flush)          (floor toward -infinity);
- *   positions [S_start, S_quant_new) are quantised with Eq. (7) from their
- *   bf16 values (kappa_k for keys, kappa_v for values); new positions below
- *   s_sink go to the sink, new positions at or after S_quant_new go to the
- *   recent ring; seq_len[b] = S_new; quant_end[b] = S_quant_new.
+ *   positions [S_start, S_quant_new) are quantised from their bf16 values
+ *   with the cache's codec; new positions below s_sink go to the sink, new
+ *   positions at or after S_quant_new go to the recent ring;
+ *   seq_len[b] = S_new; quant_end[b] = S_quant_new.
+ *
+ * Codecs, per group x (one token-head of keys or values, fp32 from bf16,
+ * every step one correctly rounded operation):
+ *   PCLIP (Eq. (7)): q = type-7 quantile of |x| at kappa_k / kappa_v;
+ *     x_min = max(min x, -q), x_max = min(max x, q);
+ *     scale = fp16(fp32((x_max - x_min) / (2^bits - 1))), zero = fp16(x_min);
+ *     code = clamp(rne((x - zero) / scale), 0, 2^bits - 1), with the
+ *     division as a product by 1 / scale (codes 0 when scale is 0).
+ *   QUEST (Eq. (5)): with h = 2^(bits-1),
+ *     step = fp32(2 quest_alpha / (2^bits - 1) * sqrt(sum_i x_i^2 / head_dim))
+ *     evaluated in fp64 (the sum in any order), scale = fp16(step),
+ *     zero = fp16(scale * (1/2 - h));
+ *     code = clamp(floor(x * (1 / scale)) + h, 0, 2^bits - 1)  (code h when
+ *     scale is 0), so that scale * code + zero is the bin centre
+ *     scale (floor(x / scale) + 1/2) up to the fp16 rounding of the zero.
  * Capacity (caller's contract): page_table holds valid pages for every
  *   logical page the new S_quant reaches.
  */
@@ -288,6 +316,14 @@ int wushkv_dequant(const wushkv_cache *c, int32_t b, int32_t start,
 
 /* Name of a status code. */
 const char *wushkv_status_string(int status);
+
+/*
+ * wushkv_quest_alpha -- the clip multiplier alpha_b of Eq. (5): the endpoint
+ * of the 2^bits evenly spaced levels that minimises the mean squared error of
+ * rounding a standard Gaussian to the nearest level (Sec. 4.3).  Host only;
+ * returns NaN for bits outside 1..8.
+ */
+double wushkv_quest_alpha(int32_t bits);
 
 /* WUSHKV_ABI_VERSION of the loaded library. */
 int wushkv_abi_version(void);

@@ -23,7 +23,7 @@ __all__ = [
     "WushKVCache", "WushKVError", "wushkv_append", "wushkv_decode_attention",
     "wushkv_decode_workspace_bytes", "wushkv_dequant", "wushkv_page_bytes",
     "wushkv_status_string", "wushkv_abi_version", "wushkv_timing_enable",
-    "wushkv_timing_read", "PAGE_TOKENS", "header_functions",
+    "wushkv_timing_read", "wushkv_quest_alpha", "PAGE_TOKENS", "header_functions",
 ]
 
 
@@ -54,6 +54,11 @@ def wushkv_abi_version() -> int:
     return _lib.lib().wushkv_abi_version()
 
 
+def wushkv_quest_alpha(bits: int) -> float:
+    """The Gaussian-MSE-optimal clip multiplier alpha_b of Eq. (5)."""
+    return _lib.lib().wushkv_quest_alpha(bits)
+
+
 def wushkv_timing_enable(slots: int) -> None:
     check(_lib.lib().wushkv_timing_enable(slots), "wushkv_timing_enable")
 
@@ -77,16 +82,25 @@ class WushKVCache:
     windows, which may hold anything (they are only read where live).
     ``page_order`` "linear" maps logical page i of sequence b to physical
     page b * max_pages + i; "random" draws a seeded permutation of a pool
-    ``pool_factor`` times the needed size.
+    ``pool_factor`` times the needed size.  ``codec`` is "pclip" (Eq. (7),
+    clip quantiles kappa_k / kappa_v) or "quest" (Eq. (5), clip multiplier
+    ``quest_alpha``, by default the library's wushkv_quest_alpha(bits)).
     """
 
     def __init__(self, batch, n_kv_heads, head_dim, bits, s_sink, s_keep, s_flush,
                  kappa_k, kappa_v, max_seq_len, win_slots=None, page_order="linear",
-                 pool_factor=1.0, seed=0, device="cuda"):
+                 pool_factor=1.0, seed=0, device="cuda", codec="pclip", quest_alpha=None):
         torch = _torch()
         self.batch, self.n_kv_heads, self.head_dim, self.bits = batch, n_kv_heads, head_dim, bits
         self.s_sink, self.s_keep, self.s_flush = s_sink, s_keep, s_flush
         self.kappa_k, self.kappa_v = float(kappa_k), float(kappa_v)
+        codes = {"pclip": _lib.CODEC_PCLIP, "quest": _lib.CODEC_QUEST}
+        if codec not in codes:
+            raise ValueError(codec)
+        self.codec = codec
+        if quest_alpha is None:
+            quest_alpha = wushkv_quest_alpha(bits) if codec == "quest" else 0.0
+        self.quest_alpha = float(ctypes.c_float(quest_alpha).value)  # as the descriptor holds it
         self.max_seq_len = max_seq_len
         if win_slots is None:
             need = s_sink + max(1, s_keep + s_flush - 1)
@@ -122,7 +136,8 @@ class WushKVCache:
         return CacheDesc(
             self.batch, self.n_kv_heads, self.head_dim, self.bits, self.s_sink, self.s_keep,
             self.s_flush, self.win_slots, self.max_pages, self.n_pages, self.kappa_k,
-            self.kappa_v, self.pages.data_ptr(), self.page_table.data_ptr(),
+            self.kappa_v, {"pclip": _lib.CODEC_PCLIP, "quest": _lib.CODEC_QUEST}[self.codec],
+            self.quest_alpha, self.pages.data_ptr(), self.page_table.data_ptr(),
             self.win_k.data_ptr(), self.win_v.data_ptr(), self.seq_len.data_ptr(),
             self.quant_end.data_ptr())
 

@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(_HERE, "_build", "libwushkv.so")
 HEADER = os.path.join(os.path.dirname(_HERE), "include", "wushkv.h")
 
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, ELAUNCH, ENODEVICE = 0, -1, -2, -3, -4, -5
+CODEC_PCLIP, CODEC_QUEST = 0, 1
 PAGE_TOKENS = 64
 
 
@@ -33,6 +34,8 @@ class CacheDesc(ctypes.Structure):
         ("n_pages", ctypes.c_int32),
         ("kappa_k", ctypes.c_float),
         ("kappa_v", ctypes.c_float),
+        ("codec", ctypes.c_int32),
+        ("quest_alpha", ctypes.c_float),
         ("pages", ctypes.c_void_p),
         ("page_table", ctypes.c_void_p),
         ("win_k", ctypes.c_void_p),
@@ -87,6 +90,8 @@ def _declare(L):
     L.wushkv_status_string.restype = ctypes.c_char_p
     L.wushkv_abi_version.argtypes = []
     L.wushkv_abi_version.restype = ctypes.c_int
+    L.wushkv_quest_alpha.argtypes = [I32]
+    L.wushkv_quest_alpha.restype = ctypes.c_double
     L.wushkv_timing_enable.argtypes = [I32]
     L.wushkv_timing_enable.restype = ctypes.c_int
     L.wushkv_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(I32),

@@ -48,8 +48,14 @@ int wushkv_validate_cache(const wushkv_cache *c)
     const int64_t ring = (int64_t)c->win_slots - c->s_sink;
     if (ring < 1 || ring < need) return WUSHKV_EINVAL;
     if (c->max_pages_per_seq < 0 || c->n_pages < 0) return WUSHKV_EINVAL;
-    if (!(c->kappa_k > 0.0f && c->kappa_k <= 1.0f)) return WUSHKV_EINVAL;
-    if (!(c->kappa_v > 0.0f && c->kappa_v <= 1.0f)) return WUSHKV_EINVAL;
+    if (c->codec == WUSHKV_CODEC_PCLIP) {
+        if (!(c->kappa_k > 0.0f && c->kappa_k <= 1.0f)) return WUSHKV_EINVAL;
+        if (!(c->kappa_v > 0.0f && c->kappa_v <= 1.0f)) return WUSHKV_EINVAL;
+    } else if (c->codec == WUSHKV_CODEC_QUEST) {
+        if (!(c->quest_alpha > 0.0f && c->quest_alpha < INFINITY)) return WUSHKV_EINVAL;
+    } else {
+        return WUSHKV_EINVAL;
+    }
     if (!c->win_k || !c->win_v || !c->seq_len || !c->quant_end) return WUSHKV_EINVAL;
     const bool paged = c->n_pages > 0 && c->max_pages_per_seq > 0;
     if (paged && (!c->pages || !c->page_table)) return WUSHKV_EINVAL;
@@ -84,6 +90,48 @@ extern "C" const char *wushkv_status_string(int status)
 }
 
 extern "C" int wushkv_abi_version(void) { return WUSHKV_ABI_VERSION; }
+
+namespace {
+
+// Standard normal density and the probability of [a, b), 0 <= a <= b <= inf.
+double npdf(double x) { return std::isinf(x) ? 0.0 : 0.3989422804014327 * std::exp(-0.5 * x * x); }
+double nprob(double a, double b) { return 0.5 * (std::erfc(a * M_SQRT1_2) - std::erfc(b * M_SQRT1_2)); }
+
+// E[zh^2] - E[z zh] for zh the level nearest to a standard Gaussian z on the
+// grid of n = 2^bits levels from -alpha to alpha (levels (k + 1/2) step, step
+// 2 alpha / (n - 1), bin [k step, (k + 1) step), outer bins unbounded).
+// Every level scales with alpha and the bins are the nearest-level cells, so
+// the derivative of the mean squared error in alpha is 2 / alpha times this
+// value: the optimum is its root.  By symmetry only the bins above zero are
+// summed (and doubled).
+double quest_gradient(int bits, double alpha)
+{
+    const int half = 1 << (bits - 1);
+    const double step = 2.0 * alpha / (2.0 * half - 1.0);
+    double g = 0.0;
+    for (int k = 0; k < half; ++k) {
+        const double a = k * step;
+        const double b = (k == half - 1) ? INFINITY : (k + 1) * step;
+        const double lvl = (k + 0.5) * step;
+        g += lvl * lvl * nprob(a, b) - lvl * (npdf(a) - npdf(b));
+    }
+    return 2.0 * g;
+}
+
+}  // namespace
+
+extern "C" double wushkv_quest_alpha(int32_t bits)
+{
+    if (bits < 1 || bits > 8) return NAN;
+    // the gradient is negative below the optimum and positive above it
+    double lo = 1e-3, hi = 16.0;
+    for (int it = 0; it < 200 && hi - lo > 1e-15 * hi; ++it) {
+        const double mid = 0.5 * (lo + hi);
+        if (quest_gradient(bits, mid) < 0.0) lo = mid;
+        else hi = mid;
+    }
+    return 0.5 * (lo + hi);
+}
 
 extern "C" int wushkv_timing_enable(int32_t slots)
 {

@@ -37,6 +37,8 @@ struct AppendArgs {
     int32_t n_kv, s_sink, s_keep, s_flush, win_slots, max_pages, n_pages;
     int32_t lo_k, lo_v;  // quantile positions: lo = floor(kappa (d-1))
     float t_k, t_v;      // and t = kappa (d-1) - lo
+    int32_t codec;       // WUSHKV_CODEC_PCLIP (Eq. (7)) or WUSHKV_CODEC_QUEST (Eq. (5))
+    double quest_coef;   // QuEST: 2 alpha_b / (2^bits - 1)
     const uint16_t *k_new;
     const uint16_t *v_new;
     const int32_t *n_new;
@@ -253,6 +255,50 @@ __device__ __forceinline__ uint32_t code_of(float x, float z, float inv, float l
     return __float_as_uint(c + 8388608.0f) - 0x4B000000u;
 }
 
+// Eq. (5) (QuEST) parameters of a group held by a lane pair (this lane's
+// half of the channels from hf): the step is 2 alpha_b / (2^bits - 1) times
+// the group's RMS, with the sum of squares in fp64 (each square exact, the
+// two halves added last; the order does not change the result beyond fp64
+// rounding) and the step rounded once to fp32 and then to the fp16 scale.
+// The zero is the offset of the lowest bin centre, scale (1/2 - 2^(bits-1)),
+// exact in fp32 and rounded to fp16.
+template <int D, int BITS>
+__device__ __forceinline__ void quest_params(const uint16_t *row, int hf, double coef,
+                                             uint32_t &s16, uint32_t &z16, float &z, float &inv)
+{
+    const uint16_t *half = row + hf * (D / 2);
+    double ss = 0.0;
+#pragma unroll 4
+    for (int c8 = 0; c8 < D / 16; ++c8) {
+        uint4 v = *reinterpret_cast<const uint4 *>(half + 8 * c8);
+        uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const double lo = (double)bf16_bits_to_f32(w[q] & 0xFFFFu);
+            const double hi = (double)bf16_bits_to_f32(w[q] >> 16);
+            ss = fma(lo, lo, ss);
+            ss = fma(hi, hi, ss);
+        }
+    }
+    const uint64_t u = __builtin_bit_cast(uint64_t, ss);
+    const uint32_t plo = __builtin_bit_cast(uint32_t, pair_swap(__builtin_bit_cast(float, (uint32_t)u)));
+    const uint32_t phi = __builtin_bit_cast(uint32_t, pair_swap(__builtin_bit_cast(float, (uint32_t)(u >> 32))));
+    ss += __builtin_bit_cast(double, ((uint64_t)phi << 32) | plo);
+    const float step = (float)(coef * sqrt(ss / (double)D));
+    s16 = f32_to_f16_bits(step);
+    const float s = f16_bits_to_f32(s16);
+    z16 = f32_to_f16_bits(s * (0.5f - (float)(1 << (BITS - 1))));
+    z = f16_bits_to_f32(z16);
+    inv = (s > 0.0f) ? 1.0f / s : 0.0f;
+}
+
+// clamp(floor(x inv) + 2^(bits-1), 0, levels) of Eq. (5), as code_of.
+__device__ __forceinline__ uint32_t quest_code_of(float x, float inv, float h, float levels)
+{
+    const float c = __builtin_amdgcn_fmed3f(floorf(x * inv) + h, 0.0f, levels);
+    return __float_as_uint(c + 8388608.0f) - 0x4B000000u;
+}
+
 template <int D, int BITS>
 __device__ void order_stats(const uint16_t *row, int hf, int lo, float &a_lo, float &a_hi,
                             float &mn, float &mx)
@@ -302,64 +348,80 @@ __device__ void quantise_tile(const AppendArgs &a, const uint16_t *kt, uint16_t 
         const int32_t p = blk_lo + r;
         if (quant(p) && pg != nullptr) {  // the same for both lanes of the pair
             const uint16_t *row = (is_v ? vt : kt) + r * kPitch;
-            const int qlo = is_v ? a.lo_v : a.lo_k;
-            const float qt = is_v ? a.t_v : a.t_k;
-            float a_lo, a_hi, mn, mx;
-            order_stats<D, BITS>(row, hf, qlo, a_lo, a_hi, mn, mx);
             uint32_t s16, z16;
             float z, inv;
             constexpr int kLevels = (1 << BITS) - 1;
-            quant_params(a_lo, a_hi, qt, qlo + 1 < D, mn, mx, kLevels, s16, z16, z, inv);
+            const bool quest = a.codec == WUSHKV_CODEC_QUEST;
+            if (quest) {
+                quest_params<D, BITS>(row, hf, a.quest_coef, s16, z16, z, inv);
+            } else {
+                const int qlo = is_v ? a.lo_v : a.lo_k;
+                const float qt = is_v ? a.t_v : a.t_k;
+                float a_lo, a_hi, mn, mx;
+                order_stats<D, BITS>(row, hf, qlo, a_lo, a_hi, mn, mx);
+                quant_params(a_lo, a_hi, qt, qlo + 1 < D, mn, mx, kLevels, s16, z16, z, inv);
+            }
             if (hf == 0)
                 *reinterpret_cast<uint32_t *>(pg + L::kParamOffset + 4 * r + (is_v ? 4 * kPage : 0)) =
                     s16 | (z16 << 16);
             constexpr int kHalf = D / 2;
             const int c0 = hf * kHalf;  // first channel of this lane's half
-            if (!is_v) {
-                // key words of this token: lane group jj = ch / 32 holds
-                // BITS words per token (see Layout::k_pos); this half covers
-                // groups hf D / 64 .. (hf + 1) D / 64 - 1
-                uint32_t kw[D / 64][BITS];
+            // the code loops, instantiated once per codec's code formula
+            auto write_codes = [&](auto code_fn) {
+                if (!is_v) {
+                    // key words of this token: lane group jj = ch / 32 holds
+                    // BITS words per token (see Layout::k_pos); this half covers
+                    // groups hf D / 64 .. (hf + 1) D / 64 - 1
+                    uint32_t kw[D / 64][BITS];
 #pragma unroll
-                for (int jl = 0; jl < D / 64; ++jl)
+                    for (int jl = 0; jl < D / 64; ++jl)
 #pragma unroll
-                    for (int w = 0; w < BITS; ++w) kw[jl][w] = 0u;
+                        for (int w = 0; w < BITS; ++w) kw[jl][w] = 0u;
 #pragma unroll
-                for (int c8 = 0; c8 < kHalf / 8; ++c8) {
-                    uint4 v = *reinterpret_cast<const uint4 *>(row + c0 + 8 * c8);
-                    uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+                    for (int c8 = 0; c8 < kHalf / 8; ++c8) {
+                        uint4 v = *reinterpret_cast<const uint4 *>(row + c0 + 8 * c8);
+                        uint32_t wv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-                    for (int i = 0; i < 8; ++i) {
-                        uint32_t hb = (i & 1) ? (wv[i >> 1] >> 16) : (wv[i >> 1] & 0xFFFFu);
-                        uint32_t code = code_of(bf16_bits_to_f32(hb), z, inv, (float)kLevels);
-                        const int cl = 8 * c8 + i;  // channel c0 + cl
-                        int word, bit;
-                        L::k_pos(r, c0 + cl, word, bit);
-                        kw[cl >> 5][(cl & 31) / (32 / BITS)] |= code << bit;
+                        for (int i = 0; i < 8; ++i) {
+                            uint32_t hb = (i & 1) ? (wv[i >> 1] >> 16) : (wv[i >> 1] & 0xFFFFu);
+                            uint32_t code = code_fn(bf16_bits_to_f32(hb));
+                            const int cl = 8 * c8 + i;  // channel c0 + cl
+                            int word, bit;
+                            L::k_pos(r, c0 + cl, word, bit);
+                            kw[cl >> 5][(cl & 31) / (32 / BITS)] |= code << bit;
+                        }
+                    }
+                    uint32_t *kreg = reinterpret_cast<uint32_t *>(pg);
+#pragma unroll
+                    for (int jl = 0; jl < D / 64; ++jl)
+#pragma unroll
+                        for (int w = 0; w < BITS; ++w)
+                            kreg[L::k_word(16 * (hf * (D / 64) + jl) + (r >> 2), BITS * (r & 3) + w)] = kw[jl][w];
+                } else {
+#pragma unroll
+                    for (int c8 = 0; c8 < kHalf / 8; ++c8) {
+                        uint4 v = *reinterpret_cast<const uint4 *>(row + c0 + 8 * c8);
+                        uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+                        uint32_t lo4 = 0, hi4 = 0;
+#pragma unroll
+                        for (int i = 0; i < 8; ++i) {
+                            uint32_t hb = (i & 1) ? (wv[i >> 1] >> 16) : (wv[i >> 1] & 0xFFFFu);
+                            uint32_t code = code_fn(bf16_bits_to_f32(hb));
+                            if (i < 4) lo4 |= code << (8 * i);
+                            else hi4 |= code << (8 * (i - 4));
+                        }
+                        // over bytes of this lane's half of the row that it has read
+                        *reinterpret_cast<uint2 *>(vcode_row<D>(vt, r) + hf * D + 8 * c8) = make_uint2(lo4, hi4);
                     }
                 }
-                uint32_t *kreg = reinterpret_cast<uint32_t *>(pg);
-#pragma unroll
-                for (int jl = 0; jl < D / 64; ++jl)
-#pragma unroll
-                    for (int w = 0; w < BITS; ++w)
-                        kreg[L::k_word(16 * (hf * (D / 64) + jl) + (r >> 2), BITS * (r & 3) + w)] = kw[jl][w];
+            };
+            constexpr float kLv = (float)kLevels;
+            if (quest) {
+                // Eq. (5): clamp(floor(x inv) + 2^(bits-1))
+                write_codes([&](float x) { return quest_code_of(x, inv, (float)(1 << (BITS - 1)), kLv); });
             } else {
-#pragma unroll
-                for (int c8 = 0; c8 < kHalf / 8; ++c8) {
-                    uint4 v = *reinterpret_cast<const uint4 *>(row + c0 + 8 * c8);
-                    uint32_t wv[4] = {v.x, v.y, v.z, v.w};
-                    uint32_t lo4 = 0, hi4 = 0;
-#pragma unroll
-                    for (int i = 0; i < 8; ++i) {
-                        uint32_t hb = (i & 1) ? (wv[i >> 1] >> 16) : (wv[i >> 1] & 0xFFFFu);
-                        uint32_t code = code_of(bf16_bits_to_f32(hb), z, inv, (float)kLevels);
-                        if (i < 4) lo4 |= code << (8 * i);
-                        else hi4 |= code << (8 * (i - 4));
-                    }
-                    // over bytes of this lane's half of the row that it has read
-                    *reinterpret_cast<uint2 *>(vcode_row<D>(vt, r) + hf * D + 8 * c8) = make_uint2(lo4, hi4);
-                }
+                // Eq. (7): clamp(rne((x - z) inv))
+                write_codes([&](float x) { return code_of(x, z, inv, kLv); });
             }
         }
     }
@@ -862,8 +924,13 @@ static int append_impl(const wushkv_cache *c, const uint16_t *k_new, const uint1
     a.win_slots = c->win_slots;
     a.max_pages = c->max_pages_per_seq;
     a.n_pages = c->n_pages;
-    kappa_position(c->kappa_k, c->head_dim, a.lo_k, a.t_k);
-    kappa_position(c->kappa_v, c->head_dim, a.lo_v, a.t_v);
+    a.codec = c->codec;
+    if (c->codec == WUSHKV_CODEC_PCLIP) {
+        kappa_position(c->kappa_k, c->head_dim, a.lo_k, a.t_k);
+        kappa_position(c->kappa_v, c->head_dim, a.lo_v, a.t_v);
+    } else {
+        a.quest_coef = 2.0 * (double)c->quest_alpha / (double)((1 << c->bits) - 1);
+    }
     a.k_new = k_new;
     a.v_new = v_new;
     a.n_new = n_new;

@@ -51,17 +51,20 @@ def eye_bits(n_kv: int, d: int) -> np.ndarray:
 class Pair:
     def __init__(self, dev, batch, n_kv, G, d, bits, s_sink, s_keep, s_flush, kappa_k, kappa_v,
                  cap, win_slots=None, page_order="linear", pool_factor=1.0, symmetric=True,
-                 seed=0, oracle_ref=True):
+                 seed=0, oracle_ref=True, codec="pclip"):
         self.dev = dev
         self.batch, self.n_kv, self.G, self.d, self.bits = batch, n_kv, G, d, bits
         self.s_sink = s_sink
         self.gpu = wk.WushKVCache(batch, n_kv, d, bits, s_sink, s_keep, s_flush, kappa_k,
                                   kappa_v, max_seq_len=cap, win_slots=win_slots,
                                   page_order=page_order, pool_factor=pool_factor, seed=seed,
-                                  device=dev)
+                                  device=dev, codec=codec,
+                                  quest_alpha=oracle.quest_alpha(bits) if codec == "quest" else None)
         args = (batch, n_kv, d, bits, s_sink, s_keep, s_flush, kappa_k, kappa_v, cap)
-        self.ref = oracle.OracleCache(*args) if oracle_ref else None
-        self.mirror = oracle.OracleCache(*args)
+        # the oracle gets the clip multiplier exactly as the descriptor holds it
+        kw = dict(codec=codec, quest_alpha=self.gpu.quest_alpha)
+        self.ref = oracle.OracleCache(*args, **kw) if oracle_ref else None
+        self.mirror = oracle.OracleCache(*args, **kw)
         self.tk, self.tinv = synth.make_transform(n_kv, d, seed, symmetric)
         self.eye = eye_bits(n_kv, d)
         self.tk_dev = to_dev_bf16(self.tk, dev)

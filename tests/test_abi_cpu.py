@@ -20,7 +20,7 @@ def test_exports_every_declared_function():
     L = _lib.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert wk.wushkv_abi_version() == 2
+    assert wk.wushkv_abi_version() == 3
 
 
 @pytest.mark.parametrize("d,bits", [(64, 2), (64, 4), (128, 2), (128, 4)])
@@ -59,6 +59,12 @@ BAD = [
     (dict(kappa_k=0.0), -1), (dict(kappa_v=1.5), -1), (dict(kappa_k=float("nan")), -1),
     (dict(win_k=None), -1), (dict(seq_len=None), -1), (dict(pages=None), -1),
     (dict(win_v=FAKE + 4), -1), (dict(max_pages_per_seq=-1), -1),
+    (dict(codec=2), -1), (dict(codec=-1), -1),
+    (dict(codec=1, quest_alpha=0.0), -1), (dict(codec=1, quest_alpha=float("inf")), -1),
+    (dict(codec=1, quest_alpha=float("nan")), -1),
+    # a QuEST cache does not use (so does not check) the quantiles, but every
+    # other field still is
+    (dict(codec=1, quest_alpha=1.5, kappa_k=0.0, batch=0), -1),
 ]
 
 
