@@ -2,16 +2,17 @@
 // bf16 / packed-code cache (Alg. 2 step 5, Eq. (2)), with the query-side
 // compensation q~ = q^T T_K^{-1} of Eq. (3).
 //
-// Three launches on the caller's stream:
-//   decode_qt_kernel       q~ for every query head, scaled by sm_scale log2(e)
-//                          so that the softmax runs in base 2, plus the form
-//                          the quantised-key product consumes: q~ in 24-bit
-//                          fixed point as six fp8 digit "limbs" with one
-//                          power-of-two scale each, and sum(q~).
+// Two launches on the caller's stream:
 //   decode_main_kernel     grid (splits, kv heads, batch), four waves per
-//                          workgroup.  Workgroups 0 .. n_page_splits - 1 scan
-//                          the quantised pages, each wave a contiguous run;
-//                          the others scan the bf16 sink + ring slots, one
+//                          workgroup.  Each workgroup first forms q~ for its
+//                          query heads in LDS, scaled by sm_scale log2(e) so
+//                          that the softmax runs in base 2, together with the
+//                          form the quantised-key product consumes: q~ in
+//                          24-bit fixed point as six fp8 digit "limbs" with
+//                          one power-of-two scale each, and sum(q~).
+//                          Workgroups 0 .. n_page_splits - 1 then scan the
+//                          quantised pages, each wave a contiguous run; the
+//                          others scan the bf16 sink + ring slots, one
 //                          64-slot unit per workgroup, 16 slots per wave.
 //                          Each workgroup writes one partial (m, l, o) per
 //                          query head.
@@ -58,11 +59,16 @@ struct DecodeArgs {
     int32_t n_kv, s_sink, win_slots, max_pages, n_pages;
     int32_t n_q;
     int32_t units_per_wave, n_page_splits, n_splits;
-    const float *qt;       // [batch][n_q][D], scaled q~
-    const uint8_t *qlimb;  // [batch][n_q][6][128] fp8 limbs in operand order
-    const uint32_t *qaux;  // [batch][n_q][4]: limb scales (E8M0 bytes, limbs 0-3 then 4-5),
-                           // sum(q~) (fp32 bits), unused
+    const uint16_t *q;     // bf16 queries (decode [batch][n_q][D]; chunks [batch][max_tok][n_q][D])
+    const float *tinv;     // [n_kv][D][D] T_K^{-1}, row-major
+    float scale;           // sm_scale log2(e)
     float *part;           // [batch][n_kv][n_splits][G][D + 2]
+    // formed by decode_qt_kernel when the main kernel does not form q~
+    // itself (rows (grid row, kv head, query head of the group)):
+    float *qt;             // [rows][D], scaled q~
+    uint8_t *qlimb;        // [rows][6][128] fp8 limbs in operand order
+    uint32_t *qaux;        // [rows][4]: limb scales (E8M0 bytes, limbs 0-3 then 4-5),
+                           // sum(q~) (fp32 bits), unused
     // query rows: G is the number of virtual query heads per kv head, each
     // a (chunk token, query head) pair; grid z runs over (sequence, token
     // group) pairs bz = b n_groups + tg, token group tg holding chunk tokens
@@ -104,98 +110,173 @@ __host__ __device__ constexpr int limb_pos(int ch)
 
 // ------------------------------------------------------------------ q~
 
-// One workgroup per (kv head, sequence).  Thread (ig, jg) multiplies a block
-// of rows i of T^{-1} (kRows of them) by the G queries for 8 output channels
-// j; the row blocks are summed in LDS.  Then one wave per query head writes
-// q~ in fixed point, N = rne(q~ 2^F) with F the largest exponent that keeps
-// |N| <= 7829367, as six balanced base-16 digits d_l in [-8, 7]
-// (N = sum_l d_l 16^(5 - l)).  Each digit is an fp8 integer and limb l
-// carries the E8M0 scale 16^(5 - l) 2^-F, so every product the matrix
-// instruction forms is an integer times a power of two: its block sums,
-// which it does not accumulate at full fp32 precision in general, are exact.
-template <int D, int BITS>
-__global__ void __launch_bounds__(256) decode_qt_kernel(const uint16_t *q, const float *tinv,
-                                                        float *qt, uint8_t *qlimb, uint32_t *qaux,
-                                                        int32_t n_kv, int32_t G, float scale,
-                                                        DecodeArgs a)
-{
-    constexpr int kJG = D / 8;        // groups of 8 output channels
-    constexpr int kIG = 256 / kJG;    // groups of rows
-    constexpr int kRows = D / kIG;    // rows per group
-    __shared__ float qs[8 * D];
-    __shared__ float red[kIG][8][D];
-    // G virtual heads per kv head (see DecodeArgs); rows of tokens beyond the
-    // chunk are zero
-    const int h = blockIdx.x, bz = blockIdx.y;
-    const int b = bz / a.n_groups, tg = bz % a.n_groups;
-    // (decode: one token per sequence, always a valid row; an empty
-    // sequence's output is zero anyway)
-    const bool decode = a.max_tok == 1 && a.n_tok == nullptr;
-    const int32_t nb = decode ? 1 : chunk_tokens(a.n_tok, a.max_tok, b, a.seq_len[b]);
-    if (decode) {
-        const uint16_t *qb = q + ((int64_t)b * n_kv * G + h * G) * D;
-        for (int i = threadIdx.x; i < G * D; i += 256) qs[i] = bf16_bits_to_f32(qb[i]);
-    } else {
-        for (int i = threadIdx.x; i < G * D; i += 256) {
-            const int v = i / D, c = i % D;
-            const int t = tg * a.tpg + v / a.g_real, g = v % a.g_real;
-            qs[i] = t < nb ? bf16_bits_to_f32(q[(((int64_t)b * a.max_tok + t) * n_kv * a.g_real + h * a.g_real + g) * D + c])
-                           : 0.0f;
-        }
-    }
-    const int64_t qrow0 = ((int64_t)bz * n_kv + h) * G;  // first virtual head's row
-    const int jg = threadIdx.x % kJG, ig = threadIdx.x / kJG;
-    const float *T = tinv + (int64_t)h * D * D + (int64_t)ig * kRows * D + 8 * jg;
-    f32x4 t[kRows][2];
-#pragma unroll
-    for (int r = 0; r < kRows; ++r) {
-        t[r][0] = *reinterpret_cast<const f32x4 *>(T + (int64_t)r * D);
-        t[r][1] = *reinterpret_cast<const f32x4 *>(T + (int64_t)r * D + 4);
-    }
-    __syncthreads();
-    for (int g = 0; g < G; ++g) {
-        float acc[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
-#pragma unroll
-        for (int r = 0; r < kRows; ++r) {
-            const float qi = qs[g * D + ig * kRows + r];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) acc[e] = fmaf(qi, t[r][e >> 2][e & 3], acc[e]);
-        }
-#pragma unroll
-        for (int e = 0; e < 8; ++e) red[ig][g][8 * jg + e] = acc[e];
-    }
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < G * D; idx += 256) {
-        const int g = idx / D, jj = idx % D;
-        float s = 0.0f;
-#pragma unroll
-        for (int k = 0; k < kIG; ++k) s += red[k][g][jj];
-        s *= scale;
-        qt[(qrow0 + g) * D + jj] = s;
-        red[0][g][jj] = s;
-    }
-    __syncthreads();
+// LDS of a workgroup's query rows.  One region holds, in turn, the raw bf16
+// queries, q~ (fp32, scaled) and the digit limbs in operand order; the limb
+// scale bytes and sum(q~) of each head follow it.
+template <int D, int G>
+struct QueryLds {
+    static constexpr int kRegion = G * D * 4 > G * kLimbs * 128 ? G * D * 4 : G * kLimbs * 128;
+    static constexpr int kAux = kRegion;  // uint32 [G][4]: limb scales (E8M0 bytes, limbs
+                                          // 0-3 then 4-5), sum(q~) (fp32 bits), unused
+    static constexpr int kBytes = kRegion + G * 16;
+};
 
-    // limbs: wave w handles query heads w, w + 4
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+// What a thread loads for query_rows, requested before any page so that
+// the pages' in-order completion cannot hold it back: its T^{-1} entries
+// (wave w covers columns D/4 w .. D/4 w + D/4 - 1 as kQuads groups of four;
+// lane (cq, part), cq = lane % kQuads, reads columns D/4 w + 4 cq .. + 3 of
+// rows part kRr .. part kRr + kRr - 1, one 16-byte load per row) and its
+// share of the raw queries (elements tid + 256 k of the G x D rows; rows of
+// tokens beyond a sequence's chunk are zero).
+template <int D, int G>
+struct QueryIn {
+    static constexpr int kQuads = D / 16;       // column quads per wave: 8 or 4
+    static constexpr int kParts = 64 / kQuads;  // row parts per wave: 8 or 16
+    static constexpr int kRr = D / kParts;      // rows per part: 16 or 4
+    static constexpr int kPer = (G * D + 255) / 256;
+    f32x4 t[kRr];
+    uint16_t q[kPer];
+    __device__ __forceinline__ void load(const DecodeArgs &a, int b, int tg, int h, int32_t S, int tid)
+    {
+        const int lane = tid & 63, wave = tid >> 6;
+        const float *T = a.tinv + (int64_t)h * D * D + (int64_t)(lane / kQuads) * kRr * D +
+                         (D / 4) * wave + 4 * (lane % kQuads);
+#pragma unroll
+        for (int r = 0; r < kRr; ++r) t[r] = *reinterpret_cast<const f32x4 *>(T + (int64_t)r * D);
+        // one load per element, its address chosen first (a load in each of
+        // two branches would leave the compiler waiting on both)
+        const bool decode = a.max_tok == 1 && a.n_tok == nullptr;
+        const int32_t nb = decode ? 1 : chunk_tokens(a.n_tok, a.max_tok, b, S);
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int i = tid + 256 * k;
+            int64_t at = -1;
+            if (i < G * D) {
+                if (decode) {
+                    // one token per sequence, always a valid row (an empty
+                    // sequence's output is zero anyway)
+                    at = ((int64_t)b * a.n_kv * G + h * G) * D + i;
+                } else {
+                    const int v = i / D, c = i % D;
+                    const int t = tg * a.tpg + v / a.g_real, g = v % a.g_real;
+                    if (t < nb)
+                        at = (((int64_t)b * a.max_tok + t) * a.n_kv * a.g_real + h * a.g_real + g) * D + c;
+                }
+            }
+            q[k] = at >= 0 ? a.q[at] : (uint16_t)0;
+        }
+    }
+};
+
+// The raw queries into the region R (no barrier).
+template <int D, int G>
+__device__ __forceinline__ void stage_queries(const QueryIn<D, G> &in, uint8_t *R, int tid)
+{
+    uint16_t *qs = reinterpret_cast<uint16_t *>(R);  // bf16 [G][D]
+#pragma unroll
+    for (int k = 0; k < QueryIn<D, G>::kPer; ++k)
+        if (tid + 256 * k < G * D) qs[tid + 256 * k] = in.q[k];
+}
+
+// q~ = q^T T^{-1} for the workgroup's G query rows (Alg. 2 step 3, Eq. (3)),
+// scaled by sm_scale log2(e), over the staged queries in R (QueryLds).  Each
+// lane forms its columns' partial products over its rows from the T^{-1}
+// entries it loaded (in); the row parts of a column are summed by lane
+// exchanges in a fixed order, so every workgroup of a (sequence, kv head)
+// forms the same q~.  Every thread of the workgroup calls it after
+// stage_queries; it starts and ends with a barrier.
+template <int D, int G>
+__device__ void form_qt(const DecodeArgs &a, const QueryIn<D, G> &in, uint8_t *R, int tid)
+{
+    using C = QueryIn<D, G>;
+    const uint16_t *qs = reinterpret_cast<const uint16_t *>(R);
+    __syncthreads();
+    const int lane = tid & 63, wave = tid >> 6;
+    const int part = lane / C::kQuads;
+    float acc[G][4];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[g][e] = 0.0f;
+    constexpr int kRv = C::kRr < 8 ? C::kRr : 8;  // rows per LDS read of the queries
+#pragma unroll
+    for (int r0 = 0; r0 < C::kRr; r0 += kRv)
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            uint32_t ww[4];
+            if constexpr (kRv == 8) {
+                const uint4 w = *reinterpret_cast<const uint4 *>(qs + g * D + part * C::kRr + r0);
+                ww[0] = w.x; ww[1] = w.y; ww[2] = w.z; ww[3] = w.w;
+            } else {
+                const uint2 w = *reinterpret_cast<const uint2 *>(qs + g * D + part * C::kRr + r0);
+                ww[0] = w.x; ww[1] = w.y;
+            }
+#pragma unroll
+            for (int e = 0; e < kRv; ++e) {
+                const float qi = bf16_bits_to_f32((e & 1) ? (ww[e >> 1] >> 16) : (ww[e >> 1] & 0xFFFFu));
+#pragma unroll
+                for (int c = 0; c < 4; ++c) acc[g][c] = fmaf(qi, in.t[r0 + e][c], acc[g][c]);
+            }
+        }
+    // the row parts of the wave's columns: lanes cq + kQuads m
+#pragma unroll
+    for (int off = C::kQuads; off < 64; off <<= 1)
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) acc[g][c] += __shfl_xor(acc[g][c], off);
+    __syncthreads();  // the raw queries are read
+    float *qt = reinterpret_cast<float *>(R);
+    if (lane < C::kQuads) {
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+            *reinterpret_cast<f32x4 *>(qt + g * D + (D / 4) * wave + 4 * lane) =
+                f32x4{acc[g][0] * a.scale, acc[g][1] * a.scale, acc[g][2] * a.scale, acc[g][3] * a.scale};
+    }
+    __syncthreads();
+}
+
+// Rewrites q~ in R (form_qt) as the operands of the quantised-key product:
+// one wave per query head writes q~ in fixed point, N = rne(q~ 2^F) with F
+// the largest exponent that keeps |N| <= 7829367, as six balanced base-16
+// digits d_l in [-8, 7] (N = sum_l d_l 16^(5 - l)).  Each digit is an fp8
+// integer and limb l carries the E8M0 scale 16^(5 - l) 2^-F, so every
+// product the matrix instruction forms is an integer times a power of two:
+// its block sums, which it does not accumulate at full fp32 precision in
+// general, are exact.  Also sum(q~) per head.  Every thread of the
+// workgroup calls it; it ends with a barrier.
+template <int D, int BITS, int G>
+__device__ void form_limbs(uint8_t *R, int tid)
+{
+    using Q = QueryLds<D, G>;
+    const int lane = tid & 63, wave = tid >> 6;
+    const float *qt = reinterpret_cast<const float *>(R);
+    // wave w handles query heads w, w + 4; the rows are read before the
+    // region is rewritten
     constexpr int kPer = D / 64;  // channels per lane
-    for (int g = wave; g < G; g += 4) {
-        const int64_t qh = qrow0 + g;
-        float r[kPer];
+    constexpr int kMine = (G + 3) / 4;
+    float r[kMine][kPer];
+#pragma unroll
+    for (int k = 0; k < kMine; ++k)
+#pragma unroll
+        for (int e = 0; e < kPer; ++e)
+            r[k][e] = (wave + 4 * k < G) ? qt[(wave + 4 * k) * D + 64 * e + lane] : 0.0f;
+    __syncthreads();
+    uint8_t *qlimb = R;
+    uint32_t *qaux = reinterpret_cast<uint32_t *>(R + Q::kAux);
+#pragma unroll
+    for (int k = 0; k < kMine; ++k) {
+        const int g = wave + 4 * k;
+        if (g >= G) break;
         float zs = 0.0f;
 #pragma unroll
-        for (int e = 0; e < kPer; ++e) {
-            r[e] = red[0][g][64 * e + lane];
-            zs += r[e];
-        }
+        for (int e = 0; e < kPer; ++e) zs += r[k][e];
 #pragma unroll
         for (int off = 32; off > 0; off >>= 1) zs += __shfl_xor(zs, off);
-        uint8_t *out = qlimb + qh * (kLimbs * 128);
+        uint8_t *out = qlimb + g * (kLimbs * 128);
         float mx = 0.0f;
 #pragma unroll
-        for (int e = 0; e < kPer; ++e) mx = fmaxf(mx, fabsf(r[e]));
+        for (int e = 0; e < kPer; ++e) mx = fmaxf(mx, fabsf(r[k][e]));
 #pragma unroll
         for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
         // fixed point N = rne(q~ 2^F) with |N| <= 7829367 (< 2^23, exact
@@ -217,7 +298,7 @@ __global__ void __launch_bounds__(256) decode_qt_kernel(const uint16_t *q, const
 #pragma unroll
         for (int e = 0; e < kPer; ++e) {
             const int ch = 64 * e + lane;
-            int N = (int)rintf(ldexpf(r[e], F));
+            int N = (int)rintf(ldexpf(r[k][e], F));
 #pragma unroll
             for (int l = kLimbs - 1; l >= 0; --l) {
                 const int d = ((N + 8) & 15) - 8;  // balanced digit
@@ -238,12 +319,40 @@ __global__ void __launch_bounds__(256) decode_qt_kernel(const uint16_t *q, const
                     if (BITS == 2 ? (p & 16) != 0 : p >= 64) out[l * 128 + p] = 0;
         }
         if (lane == 0) {
-            qaux[4 * qh] = scales[0];
-            qaux[4 * qh + 1] = scales[1];
-            qaux[4 * qh + 2] = __float_as_uint(zs);
-            qaux[4 * qh + 3] = 0u;
+            qaux[4 * g] = scales[0];
+            qaux[4 * g + 1] = scales[1];
+            qaux[4 * g + 2] = __float_as_uint(zs);
+            qaux[4 * g + 3] = 0u;
         }
     }
+    __syncthreads();
+}
+
+// One workgroup per (kv head, grid row): q~ and its limbs for that kv
+// head's G query rows, written to the workspace for the main kernel.  Used
+// when the main grid does not fit on the device at once: its workgroups
+// then run in several rounds, and each forming q~ itself would read T^{-1}
+// from L2 once per workgroup.
+template <int D, int BITS, int G>
+__global__ void __launch_bounds__(256) decode_qt_kernel(DecodeArgs a)
+{
+    using Q = QueryLds<D, G>;
+    __shared__ __attribute__((aligned(16))) uint8_t R[Q::kBytes];
+    const int tid = threadIdx.x;
+    const int h = blockIdx.x, bz = blockIdx.y;
+    const int b = bz / a.n_groups, tg = bz % a.n_groups;
+    const int32_t S = (a.max_tok == 1 && a.n_tok == nullptr) ? 0 : a.seq_len[b];
+    QueryIn<D, G> in;
+    in.load(a, b, tg, h, S, tid);
+    stage_queries<D, G>(in, R, tid);
+    form_qt<D, G>(a, in, R, tid);
+    const int64_t row0 = ((int64_t)bz * a.n_kv + h) * G;  // first (virtual) query head
+    for (int i = tid; i < G * D / 4; i += 256)
+        reinterpret_cast<f32x4 *>(a.qt + row0 * D)[i] = reinterpret_cast<const f32x4 *>(R)[i];
+    form_limbs<D, BITS, G>(R, tid);
+    for (int i = tid; i < G * kLimbs * 128 / 16; i += 256)
+        reinterpret_cast<u32x4 *>(a.qlimb + row0 * kLimbs * 128)[i] = reinterpret_cast<const u32x4 *>(R)[i];
+    if (tid < G * 4) a.qaux[row0 * 4 + tid] = reinterpret_cast<const uint32_t *>(R + Q::kAux)[tid];
 }
 
 // ------------------------------------------------------------------ main
@@ -386,13 +495,29 @@ struct MainLds {
     static constexpr int kTPitch = 144;
     static constexpr int kTBytes = kTRows * kTPitch + 64;
     static constexpr int kWave = kStageBytes + kTBytes;
+    // Workgroups a compute unit keeps resident, as the variants' register
+    // counts allow (three waves per SIMD at most; fewer for the 4-bit and
+    // the eight-head ones); it only decides the query rows' placement.
+    static constexpr int kResident = D == 128 ? (BITS == 2 ? 3 : (G == 8 ? 1 : 2))
+                                              : (BITS == 2 ? (G == 8 ? 3 : 4) : 3);
+    // The query rows get LDS of their own when that keeps the residency:
+    // the pages can then be in flight while the rows are formed.  Otherwise
+    // they borrow the start of the page stages, and the pages wait for them.
+    static constexpr int kOwnBytes = 4 * kWave + QueryLds<D, G>::kBytes + 2 * 4 * G * 4;
+    static constexpr bool kEarly = kOwnBytes <= 163840 / kResident;
+    static constexpr int kRowsAt = kEarly ? 4 * kWave : 0;
+    static constexpr int kBytes = kEarly ? 4 * kWave + QueryLds<D, G>::kBytes : 4 * kWave;
+    static_assert(QueryLds<D, G>::kBytes <= 4 * kWave, "the query rows fit the page stages");
 };
 
-template <int D, int BITS, int G>
+// FORM: the workgroup forms q~ and its limbs itself (the grid fits on the
+// device at once); otherwise decode_qt_kernel has written them.
+template <int D, int BITS, int G, bool FORM>
 __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
 {
     using L = Layout<D, BITS>;
     using M = MainLds<D, BITS, G>;
+    constexpr bool kEarly = FORM && M::kEarly;
     constexpr int kStages = M::kStages;
     constexpr int kDma = M::kDma;
     constexpr int kSlot = M::kSlot;
@@ -405,8 +530,8 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
     constexpr int kFmtB = BITS == 2 ? 4 : 0;    // fp4 or fp8 key codes
     constexpr int kScaleB = BITS == 2 ? 128 : 136;  // 2^1 or 2^9
 
-    __shared__ __attribute__((aligned(16))) uint8_t lds[4 * M::kWave];
-    __shared__ float sM[4][8], sL[4][8];
+    __shared__ __attribute__((aligned(16))) uint8_t lds[FORM ? M::kBytes : 4 * M::kWave];
+    __shared__ float sM[4][G], sL[4][G];
 
     // the wave index is uniform across the wave: keep it (and the page range
     // derived from it) in scalar registers
@@ -419,23 +544,74 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
     uint8_t *tbuf = stage + M::kStageBytes;
     constexpr int kTP = M::kTPitch;
     const uint32_t zero_row = lds_addr(tbuf + M::kTRows * kTP);
-    if (lane < 16) reinterpret_cast<uint32_t *>(tbuf + M::kTRows * kTP)[lane] = 0u;
 
     const int32_t S = a.seq_len[b];
     int32_t qend = a.quant_end[b];
     qend = qend < S ? qend : S;
     const int32_t q_hi = qend > a.s_sink ? qend : a.s_sink;  // quantised: [s_sink, q_hi)
     const int32_t n_qpages = (q_hi - a.s_sink + kPage - 1) / kPage;
-    const int64_t qhead0 = ((int64_t)bz * a.n_kv + h) * G;   // first (virtual) query head
 
     // per-wave results for the merge: o (unnormalised, relative to m), m, l
     float(*sC)[D] = reinterpret_cast<float(*)[D]>(stage);
 
-    if (split < a.n_page_splits) {
+    // the page run of this wave and its page-table entries, then the T^{-1}
+    // entries of q~, all requested before any page
+    const bool page_wg = split < a.n_page_splits;
+    const int upw = a.units_per_wave;
+    const int w0 = page_wg ? (split * 4 + wave) * upw : 0;
+    const int w1 = page_wg ? min(w0 + upw, n_qpages) : 0;
+    int32_t tbl = -1;
+    if (w0 + lane < w1 && w0 + lane < a.max_pages)
+        tbl = a.page_table[(int64_t)b * a.max_pages + w0 + lane];
+    QueryIn<D, G> qin;
+    if constexpr (FORM) qin.load(a, b, tg, h, S, tid);
+    using Q = QueryLds<D, G>;
+    uint8_t *qrows = lds + M::kRowsAt;
+    const int64_t row0 = ((int64_t)bz * a.n_kv + h) * G;  // first (virtual) query head
+
+    if (page_wg) {
         // ================================================ quantised pages
-        const int upw = a.units_per_wave;
-        const int w0 = (split * 4 + wave) * upw;
-        const int w1 = min(w0 + upw, n_qpages);
+        auto phys_of = [&](int u) -> int32_t { return __builtin_amdgcn_readlane(tbl, u - w0); };
+        // Every page of the run issues exactly kDma loads; an entry outside
+        // the pool loads physical page 0 instead (its data is never used),
+        // which keeps the count of outstanding loads a closed form.
+        auto issue = [&](int u, int s) {
+            int32_t phys = phys_of(u);
+            if (phys < 0 || phys >= a.n_pages) phys = 0;
+            const uint8_t *src = a.pages + ((int64_t)phys * a.n_kv + h) * L::kPageBytes + 16 * lane;
+            const uint32_t dst = __builtin_amdgcn_readfirstlane(lds_addr(stage + s * kSlot));
+#pragma unroll
+            for (int i = 0; i < kDma; ++i) {
+                if (i + 1 < kDma || 1024 * i + 16 * lane < L::kPageBytes)
+                    dma16(src + 1024 * i, dst + 1024 * i);
+            }
+        };
+        const bool run = a.n_pages > 0 && w0 < w1;
+        const uint8_t *qlimb;
+        const uint32_t *qaux;
+        if constexpr (FORM) {
+            // When the rows have LDS of their own, the first two pages of the
+            // run go in flight while q~ is formed.  Every load made so far
+            // completes first, so that no later wait of the rows' arithmetic
+            // can be held up by the pages (loads complete in issue order).
+            stage_queries<D, G>(qin, qrows, tid);
+            if (kEarly) {
+                // vmcnt(0) as the compiler's own wait: it then counts the
+                // rows' loads complete and sets no wait on them behind the pages
+                __builtin_amdgcn_s_waitcnt(0x0F70);
+                if (run) {
+                    issue(w0, 0);
+                    if (w0 + 1 < w1) issue(w0 + 1, 1);
+                }
+            }
+            form_qt<D, G>(a, qin, qrows, tid);
+            form_limbs<D, BITS, G>(qrows, tid);
+            qlimb = qrows;
+            qaux = reinterpret_cast<const uint32_t *>(qrows + Q::kAux);
+        } else {
+            qlimb = a.qlimb + row0 * kLimbs * 128;
+            qaux = a.qaux + row0 * 4;
+        }
 
         // score A operands, two per head group: row m = 4 g' + r holds limb
         // r (first) or limb 4 + r for r < 2 (second; rows r >= 2 zero) of
@@ -452,17 +628,29 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
                 u32x4 x0 = {0u, 0u, 0u, 0u}, x1 = x0;
                 qsc[hg][part] = 127;
                 if (hd < G && limb < kLimbs) {
-                    const uint8_t *src = a.qlimb + ((qhead0 + hd) * kLimbs + limb) * 128 + 32 * j;
+                    const uint8_t *src = qlimb + (hd * kLimbs + limb) * 128 + 32 * j;
                     x0 = *reinterpret_cast<const u32x4 *>(src);
                     x1 = *reinterpret_cast<const u32x4 *>(src + 16);
-                    qsc[hg][part] = (a.qaux[4 * (qhead0 + hd) + part] >> (8 * (n & 3))) & 0xFFu;
+                    qsc[hg][part] = (qaux[4 * hd + part] >> (8 * (n & 3))) & 0xFFu;
                 }
                 qa[hg][part] = i32x8{(int)x0[0], (int)x0[1], (int)x0[2], (int)x0[3],
                                      (int)x1[0], (int)x1[1], (int)x1[2], (int)x1[3]};
             }
             const int hs = G > 4 ? 2 * j + hg : j;
-            zs[hg] = hs < G ? __uint_as_float(a.qaux[4 * (qhead0 + hs) + 2]) : 0.0f;
+            zs[hg] = hs < G ? __uint_as_float(qaux[4 * hs + 2]) : 0.0f;
         }
+        if constexpr (!kEarly) {
+            // every wave has its operands: the pages may now land over the
+            // rows (LDS), or (memory) the operands have arrived, so that the
+            // compiler's wait for them cannot include the pages
+            if constexpr (FORM) __syncthreads();
+            else __builtin_amdgcn_s_waitcnt(0x0F70);
+            if (run) {
+                issue(w0, 0);
+                if (w0 + 1 < w1) issue(w0 + 1, 1);
+            }
+        }
+        if (lane < 16) reinterpret_cast<uint32_t *>(tbuf + M::kTRows * kTP)[lane] = 0u;
         // this lane's heads in the score layout, and whether they exist
         bool hvalid[kHG];
 #pragma unroll
@@ -495,24 +683,6 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
         const uint32_t a_addr = arow_ok ? lds_addr(tbuf + (apart * G + ahead) * kTP + 16 * j) : zero_row;
         const uint32_t a_step = arow_ok ? 64u : 0u;  // second 32-token chunk
 
-        int32_t tbl = -1;
-        if (w0 + lane < w1 && w0 + lane < a.max_pages)
-            tbl = a.page_table[(int64_t)b * a.max_pages + w0 + lane];
-        auto phys_of = [&](int u) -> int32_t { return __builtin_amdgcn_readlane(tbl, u - w0); };
-        // Every page of the run issues exactly kDma loads; an entry outside
-        // the pool loads physical page 0 instead (its data is never used),
-        // which keeps the count of outstanding loads a closed form.
-        auto issue = [&](int u, int s) {
-            int32_t phys = phys_of(u);
-            if (phys < 0 || phys >= a.n_pages) phys = 0;
-            const uint8_t *src = a.pages + ((int64_t)phys * a.n_kv + h) * L::kPageBytes + 16 * lane;
-            const uint32_t dst = __builtin_amdgcn_readfirstlane(lds_addr(stage + s * kSlot));
-#pragma unroll
-            for (int i = 0; i < kDma; ++i) {
-                if (i + 1 < kDma || 1024 * i + 16 * lane < L::kPageBytes)
-                    dma16(src + 1024 * i, dst + 1024 * i);
-            }
-        };
         // Per page: the value words are read at the top (they are needed only
         // by the P V products at the end); the key words and parameters of
         // page u were read at the end of iteration u - 1, while its P V
@@ -531,14 +701,13 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
 #pragma unroll
             for (int q4 = 0; q4 < kVX; ++q4) vx[q4] = lds_read16(pg + L::kRegionBytes + 4 * L::v_word(lane, 4 * q4));
         };
-        if (a.n_pages > 0 && w0 < w1) {
+        if (run) {
             // Three stages: page u in registers, pages u + 1 and u + 2 in
-            // flight to the two LDS slots.  A slot is emptied into registers
-            // as soon as its page has landed and refilled right away, so both
-            // slots stay in flight while a page is computed.
+            // flight to the two LDS slots (the first two issued above).  A
+            // slot is emptied into registers as soon as its page has landed
+            // and refilled right away, so both slots stay in flight while a
+            // page is computed.
             static_assert(kStages == 2, "two slots per wave");
-            issue(w0, 0);
-            if (w0 + 1 < w1) issue(w0 + 1, 1);
             wait_vmcnt_at_most<1, kDma>(w0 + 1 < w1 ? kDma : 0);
             u32x4 kx[kKX + 2], vv[kVX];
             read_keys(lds_addr(stage), kx);
@@ -734,6 +903,43 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
         const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;
         const int32_t slot0 = (split - a.n_page_splits) * kPage + 16 * wave;
 
+        const float *qtl;
+        if constexpr (FORM) {
+            stage_queries<D, G>(qin, qrows, tid);
+            form_qt<D, G>(a, qin, qrows, tid);
+            qtl = reinterpret_cast<const float *>(qrows);
+        } else {
+            qtl = a.qt + row0 * D;
+        }
+        // A operands: row m = 2 g + part (hi, lo) of q~, chunk c.  From LDS
+        // they are formed at once; from memory only after the slot loads are
+        // issued, so that the latencies overlap.
+        bf16x8 qa[kC];
+        auto form_qa = [&]() {
+            const int g = n >> 1, part = n & 1;
+#pragma unroll
+            for (int c = 0; c < kC; ++c) {
+                uint32_t u[4] = {0u, 0u, 0u, 0u};
+                if (g < G) {
+                    const float *src = qtl + g * D + 32 * c + 8 * j;
+                    const f32x4 x0 = *reinterpret_cast<const f32x4 *>(src);
+                    const f32x4 x1 = *reinterpret_cast<const f32x4 *>(src + 4);
+                    const float x[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+#pragma unroll
+                    for (int pp = 0; pp < 4; ++pp) {
+                        const uint32_t hi = pack_bf16_rne(x[2 * pp], x[2 * pp + 1]);
+                        const uint32_t lo = pack_bf16_rne(x[2 * pp] - bf16_bits_to_f32(hi & 0xFFFFu),
+                                                          x[2 * pp + 1] - bf16_bits_to_f32(hi >> 16));
+                        u[pp] = part ? lo : hi;
+                    }
+                }
+                qa[c] = __builtin_bit_cast(bf16x8, u32x4{u[0], u[1], u[2], u[3]});
+            }
+        };
+        if constexpr (FORM) form_qa();
+        if constexpr (FORM && !kEarly) __syncthreads();  // the rows may now be overwritten
+        if (lane < 16) reinterpret_cast<uint32_t *>(tbuf + M::kTRows * kTP)[lane] = 0u;
+
         // this tile's live slots, one bit per slot (lanes 0..15)
         bool mine;
         {
@@ -758,30 +964,8 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
 #pragma unroll
             for (int nt = 0; nt < kNT; ++nt)
                 vx[nt] = *reinterpret_cast<const u32x2 *>(vrow + (int64_t)(16 * nt + n) * a.win_slots);
+            if constexpr (!FORM) form_qa();
 
-            // A operands: row m = 2 g + part (hi, lo) of q~, chunk c
-            bf16x8 qa[kC];
-            {
-                const int g = n >> 1, part = n & 1;
-#pragma unroll
-                for (int c = 0; c < kC; ++c) {
-                    uint32_t u[4] = {0u, 0u, 0u, 0u};
-                    if (g < G) {
-                        const float *src = a.qt + (qhead0 + g) * D + 32 * c + 8 * j;
-                        const f32x4 x0 = *reinterpret_cast<const f32x4 *>(src);
-                        const f32x4 x1 = *reinterpret_cast<const f32x4 *>(src + 4);
-                        const float x[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-#pragma unroll
-                        for (int pp = 0; pp < 4; ++pp) {
-                            const uint32_t hi = pack_bf16_rne(x[2 * pp], x[2 * pp + 1]);
-                            const uint32_t lo = pack_bf16_rne(x[2 * pp] - bf16_bits_to_f32(hi & 0xFFFFu),
-                                                              x[2 * pp + 1] - bf16_bits_to_f32(hi >> 16));
-                            u[pp] = part ? lo : hi;
-                        }
-                    }
-                    qa[c] = __builtin_bit_cast(bf16x8, u32x4{u[0], u[1], u[2], u[3]});
-                }
-            }
             // scores: lane (j, n) gets rows 4 j + r = (head 2 j + r / 2,
             // part r % 2) of token slot0 + n
             f32x4 sc = {0.f, 0.f, 0.f, 0.f};
@@ -948,7 +1132,7 @@ struct DecodePlan {
 template <int D, int BITS, int G>
 static void main_kernel_ptr(const void *&f)
 {
-    f = reinterpret_cast<const void *>(&decode_main_kernel<D, BITS, G>);
+    f = reinterpret_cast<const void *>(&decode_main_kernel<D, BITS, G, true>);
 }
 
 // Waves of decode_main_kernel the device keeps resident at once (its
@@ -1045,20 +1229,26 @@ static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq
     return true;
 }
 
+// The main kernel, preceded by decode_qt_kernel unless it forms q~ itself.
 template <int D, int BITS, int G>
-static void launch_main(dim3 grid, hipStream_t s, const DecodeArgs &a)
+static void launch_main(bool form, dim3 grid, hipStream_t s, const DecodeArgs &a)
 {
-    launch("decode_main_kernel", decode_main_kernel<D, BITS, G>, grid, dim3(256), s, a);
+    if (form) {
+        launch("decode_main_kernel", decode_main_kernel<D, BITS, G, true>, grid, dim3(256), s, a);
+    } else {
+        launch("decode_qt_kernel", decode_qt_kernel<D, BITS, G>, dim3(grid.y, grid.z), dim3(256), s, a);
+        launch("decode_main_kernel", decode_main_kernel<D, BITS, G, false>, grid, dim3(256), s, a);
+    }
 }
 
 template <int D, int BITS>
-static void launch_main_g(int G, dim3 grid, hipStream_t s, const DecodeArgs &a)
+static void launch_main_g(int G, bool form, dim3 grid, hipStream_t s, const DecodeArgs &a)
 {
     switch (G) {
-        case 1: launch_main<D, BITS, 1>(grid, s, a); break;
-        case 2: launch_main<D, BITS, 2>(grid, s, a); break;
-        case 4: launch_main<D, BITS, 4>(grid, s, a); break;
-        default: launch_main<D, BITS, 8>(grid, s, a); break;
+        case 1: launch_main<D, BITS, 1>(form, grid, s, a); break;
+        case 2: launch_main<D, BITS, 2>(form, grid, s, a); break;
+        case 4: launch_main<D, BITS, 4>(form, grid, s, a); break;
+        default: launch_main<D, BITS, 8>(form, grid, s, a); break;
     }
 }
 
@@ -1112,10 +1302,10 @@ static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const int32_t G = rs.G;
     uint8_t *ws = reinterpret_cast<uint8_t *>(workspace);
-    float *qt = reinterpret_cast<float *>(ws);
-    uint8_t *qlimb = ws + p.qt_bytes;
-    uint32_t *qaux = reinterpret_cast<uint32_t *>(ws + p.qt_bytes + p.limb_bytes);
-    float *part = reinterpret_cast<float *>(ws + p.qt_bytes + p.limb_bytes + p.aux_bytes);
+    float *part = reinterpret_cast<float *>(ws);
+    float *qt = reinterpret_cast<float *>(ws + p.part_bytes);
+    uint8_t *qlimb = ws + p.part_bytes + p.qt_bytes;
+    uint32_t *qaux = reinterpret_cast<uint32_t *>(ws + p.part_bytes + p.qt_bytes + p.limb_bytes);
 
     DecodeArgs a{};
     a.pages = c->pages;
@@ -1133,10 +1323,13 @@ static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok
     a.units_per_wave = p.units_per_wave;
     a.n_page_splits = p.n_page_splits;
     a.n_splits = p.n_splits;
+    a.q = q;
+    a.tinv = t_k_inv;
+    a.scale = sm_scale * kLog2e;
+    a.part = part;
     a.qt = qt;
     a.qlimb = qlimb;
     a.qaux = qaux;
-    a.part = part;
     a.n_groups = rs.n_groups;
     a.tpg = rs.tpg;
     a.g_real = rs.g_real;
@@ -1144,23 +1337,20 @@ static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok
     a.n_tok = n_tok;
 
     const unsigned rows_z = (unsigned)(c->batch * rs.n_groups);
-    const dim3 gq(c->n_kv_heads, rows_z);
     const dim3 gm(p.n_splits, c->n_kv_heads, rows_z);
     const dim3 gc(c->n_kv_heads * G, rows_z);
-    const float scale = sm_scale * kLog2e;
+    // Each workgroup forms q~ itself when the whole grid is resident at
+    // once (one round: the rows cost each workgroup an L2 read of T^{-1}
+    // that overlaps its first pages).  A grid that runs in rounds would pay
+    // that read once per workgroup, so a small kernel forms q~ first.
+    const int64_t wgs = (int64_t)p.n_splits * c->n_kv_heads * rows_z;
+    const bool form = wgs * 4 <= resident_waves(c->head_dim, c->bits, G);
     const int key = c->head_dim * 10 + c->bits;
-
     switch (key) {
-        case 1282: launch("decode_qt_kernel", decode_qt_kernel<128, 2>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale, a); break;
-        case 1284: launch("decode_qt_kernel", decode_qt_kernel<128, 4>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale, a); break;
-        case 642: launch("decode_qt_kernel", decode_qt_kernel<64, 2>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale, a); break;
-        case 644: launch("decode_qt_kernel", decode_qt_kernel<64, 4>, gq, dim3(256), s, q, t_k_inv, qt, qlimb, qaux, c->n_kv_heads, G, scale, a); break;
-    }
-    switch (key) {
-        case 1282: launch_main_g<128, 2>(G, gm, s, a); break;
-        case 1284: launch_main_g<128, 4>(G, gm, s, a); break;
-        case 642: launch_main_g<64, 2>(G, gm, s, a); break;
-        case 644: launch_main_g<64, 4>(G, gm, s, a); break;
+        case 1282: launch_main_g<128, 2>(G, form, gm, s, a); break;
+        case 1284: launch_main_g<128, 4>(G, form, gm, s, a); break;
+        case 642: launch_main_g<64, 2>(G, form, gm, s, a); break;
+        case 644: launch_main_g<64, 4>(G, form, gm, s, a); break;
     }
     if (c->head_dim == 128) launch("decode_combine_kernel", decode_combine_kernel<128>, gc, dim3(128), s, (const float *)part, out, c->n_kv_heads, G, p.n_splits, a);
     else launch("decode_combine_kernel", decode_combine_kernel<64>, gc, dim3(64), s, (const float *)part, out, c->n_kv_heads, G, p.n_splits, a);

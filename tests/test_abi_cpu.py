@@ -128,14 +128,15 @@ def test_call_specific_validation():
 def test_workspace_bytes_closed_form():
     L = _lib.lib()
     d = _desc()
-    # q~: batch * n_q * d * 4 rounded up to 256; six 128-byte fp8 limbs and
-    # 16 bytes of scales and sum per query head (the latter rounded up to
-    # 256); partials: one (o[d], m, l) per (sequence, kv head, split, query
-    # head of the group).  ceil((1000 - 4)/64) = 16 pages per (sequence,
-    # head), 2 per wave, 8 per four-wave workgroup -> 2 page splits, plus one
-    # workgroup per 64 window slots (192 / 64 = 3) -> 5 splits.
+    # partials: one (o[d], m, l) per (sequence, kv head, split, query head
+    # of the group); then, for grids formed in rounds, q~: batch * n_q * d * 4
+    # rounded up to 256, six 128-byte fp8 limbs and 16 bytes of scales and
+    # sum per query head (the latter rounded up to 256).
+    # ceil((1000 - 4)/64) = 16 pages per (sequence, head), 2 per wave, 8 per
+    # four-wave workgroup -> 2 page splits, plus one workgroup per 64 window
+    # slots (192 / 64 = 3) -> 5 splits.
     ws = L.wushkv_decode_workspace_bytes(ctypes.byref(d), 8, 1000)
-    assert ws == 2 * 8 * 128 * 4 + 2 * 8 * 6 * 128 + 256 + (2 * 2) * 5 * 4 * (128 + 2) * 4
+    assert ws == (2 * 2) * 5 * 4 * (128 + 2) * 4 + 2 * 8 * 128 * 4 + 2 * 8 * 6 * 128 + 256
 
 
 @pytest.mark.parametrize("d,bits", [(64, 2), (64, 4), (128, 2), (128, 4)])
