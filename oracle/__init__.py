@@ -10,7 +10,8 @@ bf16 value of every position plus the codes and fp16 (scale, zero) of the
 quantised positions.  It knows nothing of pages, rings or kernel layouts.
 
 Paper references: Eq. (2) attention, Eq. (3) transform insertion, Eq. (7)
-and Eq. (5) quantisers, Sec. 4.4 windows, Alg. 2 cache management.
+and Eq. (5) quantisers, Sec. 4.4 windows, Alg. 2 cache management, Eq. (1)
+the WUSH transform.
 """
 from __future__ import annotations
 
@@ -385,3 +386,49 @@ def norm_rope(k_bits, positions, theta: float, gain=None, eps: float = 0.0) -> n
     y1, y2 = y[..., :half], y[..., half:]
     out = np.concatenate([y1 * c - y2 * s, y2 * c + y1 * s], axis=-1)
     return f64_to_bf16(out)
+
+
+# --------------------------------------------------------------------------
+# The WUSH transform, Eq. (1) (Sec. 3; used per head by Eq. (4) and Alg. 1)
+# --------------------------------------------------------------------------
+
+def sylvester_hadamard(d: int) -> np.ndarray:
+    """The normalised Hadamard matrix of order d = 2^m in Sylvester's order:
+    entry (i, j) is (-1)^popcount(i & j) / sqrt(d)."""
+    i = np.arange(d)
+    bits = np.bitwise_and(i[:, None], i[None, :])
+    sign = np.ones((d, d))
+    for b in range(int(np.log2(d))):
+        sign *= np.where((bits >> b) & 1, -1.0, 1.0)
+    return sign / np.sqrt(d)
+
+
+def wush_transform(M, H, gamma: float):
+    """T = Wush(M, H, gamma) of Eq. (1) in fp64, with T^{-1}:
+      L L^T = H + gamma tr(H)/d I                 (Cholesky, L lower)
+      U Lam U^T = L^T (M + gamma tr(M)/d I) L     (symmetric eigendecomposition)
+      c = (1 + gamma)^(1/2) tr(M)^(1/2) tr(Lam^(1/2))^(-1/2)
+      T = c Had Lam^(-1/4) U^T L^T
+    The eigendecomposition is unique only up to the order of the eigenpairs
+    and the sign of each eigenvector, and Had mixes them, so T depends on
+    both.  The paper fixes neither; this reading takes the eigenvalues in
+    ascending order and the sign of u_k that makes the largest-magnitude
+    entry of L u_k positive (the first such entry on a tie), with the
+    Hadamard matrix in Sylvester's order.  Returns (T, T^{-1}, Lam)."""
+    M = np.asarray(M, np.float64)
+    H = np.asarray(H, np.float64)
+    d = M.shape[0]
+    I = np.eye(d)
+    L = np.linalg.cholesky(H + gamma * np.trace(H) / d * I)
+    S = L.T @ (M + gamma * np.trace(M) / d * I) @ L
+    lam, U = np.linalg.eigh(0.5 * (S + S.T))   # ascending
+    W = L @ U
+    for k in range(d):
+        i = int(np.argmax(np.abs(W[:, k])))
+        if W[i, k] < 0:
+            U[:, k] = -U[:, k]
+            W[:, k] = -W[:, k]
+    c = np.sqrt(1.0 + gamma) * np.sqrt(np.trace(M)) / np.sqrt(np.sum(np.sqrt(lam)))
+    Had = sylvester_hadamard(d)
+    T = c * Had @ np.diag(lam ** -0.25) @ U.T @ L.T
+    return T, np.linalg.inv(T), lam
