@@ -347,6 +347,9 @@ def main():
     if not args.no_scale:
         scale = bench_decode_scale(torch, wk, synth, dev, args)
 
+    # ---- the transform builder on a whole model's calibration statistics
+    wush = bench_wush(torch, wk, dev, args) if not args.no_scale else None
+
     # ---- oracle baseline on the host
     cpu = None
     if not args.no_cpu:
@@ -387,6 +390,7 @@ def main():
         "append": prefill,
         "decode_at_scale": scale,
         "chunk_attention": chunk,
+        "wush_build": wush,
     }
     print(json.dumps(line), flush=True)
 
@@ -523,6 +527,56 @@ def bench_chunk(torch, wk, caches, reps, k1, tk, tinv, B, NQ, D, max_seq, sm, cf
             "gbps_algorithmic": round(byts / t / 1e9, 1),
             "note": "16-token chunks on the 8192-token Llama-shaped cache; the cache is read "
                     "once per group of two chunk tokens (8 virtual query heads per kv head)"}
+
+
+def bench_wush(torch, wk, dev, args, layers=32, heads=8, d=128, gamma=1e-2, reps=5):
+    """The WUSH transform builder (Eq. (1)) for every key and value head of a
+    Llama-3-8B-shaped model: 32 layers x 8 kv heads x 2 = 512 transforms of
+    d = 128, with T^{-1}, from synthetic calibration statistics of the
+    paper's form (M = K K^T of keys with outlier channels, H = 2 Q Q^T of
+    queries with uneven channel scales; seeded device-side Gaussians).
+    Reported: time per call, transforms per second, and the fp32 arithmetic
+    rate against the vector peak, counting per transform 9 sweeps d^3 (each
+    Jacobi sweep: d - 1 rounds of d / 2 column pairs, three length-d dot
+    products and two rotated length-2d columns) plus 4 d^3 (two Cholesky
+    factorisations, the triangular product and the inverse's product)."""
+    count = layers * heads * 2
+    n = 1024
+    gen = torch.Generator(device=dev).manual_seed(args.seed + 11)
+    K = torch.randn(count, d, n, generator=gen, device=dev)
+    K[:, :8] *= 10.0
+    Q = torch.randn(count, d, n, generator=gen, device=dev) * torch.linspace(0.3, 3.0, d, device=dev)[None, :, None]
+    M = (K @ K.transpose(1, 2) / n).contiguous()
+    Hh = (2.0 * Q @ Q.transpose(1, 2) / n).contiguous()
+    M = 0.5 * (M + M.transpose(1, 2))
+    Hh = (0.5 * (Hh + Hh.transpose(1, 2))).contiguous()
+    M = M.contiguous()
+    del K, Q
+    T = torch.empty_like(M)
+    Ti = torch.empty_like(M)
+    sw = torch.empty(count, dtype=torch.int32, device=dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wk.wushkv_wush_transform(M, Hh, gamma, T, Ti, sweeps_out=sw)
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        e0.record()
+        wk.wushkv_wush_transform(M, Hh, gamma, T, Ti, sweeps_out=sw)
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    ms = float(np.median(times))
+    sweeps = sw.cpu().numpy()
+    flops = float(np.sum(9.0 * sweeps * d ** 3 + 4.0 * d ** 3))
+    tflops = flops / (ms * 1e-3) / 1e12
+    log("wush build: %d transforms of d %d in %.3f ms (%.3g per s), sweeps %.1f mean, "
+        "%.2f TFLOP/s fp32 (%.1f%% of vector peak)" % (count, d, ms, count / (ms * 1e-3),
+                                                        sweeps.mean(), tflops, 100 * tflops / 157.3))
+    return {"workload": "wush-transforms-llama3-8b-kv-heads (512 x d128, gamma 1e-2, with inverse)",
+            "ms_per_call": round(ms, 4), "transforms_per_s": round(count / (ms * 1e-3), 1),
+            "mean_sweeps": round(float(sweeps.mean()), 2),
+            "roofline": {"bound": "alu", "achieved": round(tflops, 3), "peak": 157.3,
+                         "unit": "TFLOP/s", "frac": round(tflops / 157.3, 4), "traffic": None}}
 
 
 def bench_decode_scale(torch, wk, synth, dev, args, calls=24):

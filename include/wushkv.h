@@ -18,6 +18,7 @@
  *   wushkv_append            Alg. 2 steps 3 (keys), 4 and 7-11
  *   wushkv_decode_attention  Alg. 2 steps 3 (queries) and 5, Eq. (2)
  *   wushkv_dequant           the reconstruction of Eq. (7) for stored tokens
+ *   wushkv_wush_transform    the transform T of Eq. (1) (calibration, Alg. 1)
  *
  * Conventions
  *   - Every pointer is a DEVICE pointer unless marked (host), and must be
@@ -316,6 +317,39 @@ int wushkv_dequant(const wushkv_cache *c, int32_t b, int32_t start,
 
 /* Name of a status code. */
 const char *wushkv_status_string(int status);
+
+/*
+ * wushkv_wush_transform -- the WUSH transform of Eq. (1), T = Wush(M, H,
+ * gamma), for `count` independent pairs (one per key or value head, Eq. (4),
+ * Alg. 1):
+ *   L L^T = H + gamma tr(H)/d I,  U Lam U^T = L^T (M + gamma tr(M)/d I) L,
+ *   c = ((1 + gamma) tr(M))^(1/2) tr(Lam^(1/2))^(-1/2),
+ *   T = c Had Lam^(-1/4) U^T L^T   (Had: normalised Sylvester Hadamard).
+ * The eigenpairs are taken in ascending order of Lam, and each eigenvector's
+ * sign makes the largest-magnitude entry of L u_k positive (first on ties);
+ * T depends on both and the paper fixes neither.
+ *
+ *   m, h        fp32 [count][d][d] device, row-major, symmetric (only the
+ *               lower triangle is read): the Gram matrix of the tensor
+ *               quantised and the Hessian of its perturbation.  Both damped
+ *               matrices must be positive definite.
+ *   count       >= 0 pairs; 0 is a no-op.
+ *   d           64 or 128.
+ *   gamma       (host) damping ratio >= 0, finite (the paper uses 1e-2).
+ *   t_out       fp32 [count][d][d]: T (k~ = T k); convert to bf16 for
+ *               wushkv_append's t_k.
+ *   t_inv_out   nullable fp32 [count][d][d]: T^{-1}, as wushkv_decode_attention
+ *               takes it.
+ *   sweeps_out  nullable int32 [count]: Jacobi sweeps each pair took, or -1
+ *               when a damped matrix was not positive definite (its outputs
+ *               are then NaN).
+ * Computed in fp32 with a one-sided Jacobi eigensolver; see the source for
+ * the method.  Errors: WUSHKV_EINVAL for a negative count, bad gamma, null or
+ * unaligned pointers; WUSHKV_EUNSUPPORTED for other d.
+ */
+int wushkv_wush_transform(const float *m, const float *h, int32_t count, int32_t d,
+                          float gamma, float *t_out, float *t_inv_out,
+                          int32_t *sweeps_out, wushkv_stream_t stream);
 
 /*
  * wushkv_quest_alpha -- the clip multiplier alpha_b of Eq. (5): the endpoint

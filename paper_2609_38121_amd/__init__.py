@@ -23,7 +23,8 @@ __all__ = [
     "WushKVCache", "WushKVError", "wushkv_append", "wushkv_decode_attention",
     "wushkv_decode_workspace_bytes", "wushkv_dequant", "wushkv_page_bytes",
     "wushkv_status_string", "wushkv_abi_version", "wushkv_timing_enable",
-    "wushkv_timing_read", "wushkv_quest_alpha", "PAGE_TOKENS", "header_functions",
+    "wushkv_timing_read", "wushkv_quest_alpha", "wushkv_wush_transform", "PAGE_TOKENS",
+    "header_functions",
 ]
 
 
@@ -276,3 +277,29 @@ def wushkv_dequant(cache: WushKVCache, b: int, start: int, count: int, k_out=Non
                                    _ptr(k_out), _ptr(v_out), _stream_handle(stream))
     check(st, "wushkv_dequant")
     return k_out, v_out
+
+
+def wushkv_wush_transform(m, h, gamma: float = 1e-2, t_out=None, t_inv_out=None,
+                          want_inverse: bool = True, sweeps_out=None, stream=None):
+    """T = Wush(M, H, gamma) of Eq. (1) for each of the [count][d][d] fp32
+    (device, symmetric) pairs in m and h.  Returns (T, T^{-1} or None,
+    sweeps int32 [count]: Jacobi sweeps taken, -1 where a damped matrix was
+    not positive definite)."""
+    torch = _torch()
+    if m.shape != h.shape or m.dim() != 3 or m.shape[1] != m.shape[2]:
+        raise ValueError("m and h must both be [count][d][d]")
+    count, d = int(m.shape[0]), int(m.shape[1])
+    for t in (m, h):
+        if t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError("m and h must be contiguous fp32")
+    if t_out is None:
+        t_out = torch.empty_like(m)
+    if want_inverse and t_inv_out is None:
+        t_inv_out = torch.empty_like(m)
+    if sweeps_out is None:
+        sweeps_out = torch.empty(count, dtype=torch.int32, device=m.device)
+    st = _lib.lib().wushkv_wush_transform(_ptr(m), _ptr(h), count, d, float(gamma), _ptr(t_out),
+                                          _ptr(t_inv_out) if want_inverse else None,
+                                          _ptr(sweeps_out), _stream_handle(stream))
+    check(st, "wushkv_wush_transform")
+    return t_out, (t_inv_out if want_inverse else None), sweeps_out

@@ -125,6 +125,21 @@ def test_call_specific_validation():
     assert L.wushkv_dequant(by, 0, 4, 0, FAKE, FAKE, None) == 0
 
 
+@pytest.mark.skipif(gpu_available(), reason="fake device pointers: run only where no GPU exists")
+def test_wush_transform_validation():
+    L = _lib.lib()
+    w = L.wushkv_wush_transform
+    assert w(FAKE, FAKE, 0, 128, 0.01, FAKE, None, None, None) == 0  # empty batch: no-op
+    assert w(FAKE, FAKE, -1, 128, 0.01, FAKE, None, None, None) == -1
+    assert w(FAKE, FAKE, 1, 96, 0.01, FAKE, None, None, None) == -2
+    assert w(FAKE, FAKE, 1, 128, -0.5, FAKE, None, None, None) == -1
+    assert w(FAKE, FAKE, 1, 128, float("nan"), FAKE, None, None, None) == -1
+    assert w(FAKE, FAKE, 1, 128, float("inf"), FAKE, None, None, None) == -1
+    assert w(None, FAKE, 1, 128, 0.01, FAKE, None, None, None) == -1
+    assert w(FAKE, FAKE, 1, 128, 0.01, None, None, None, None) == -1
+    assert w(FAKE, FAKE + 4, 1, 128, 0.01, FAKE, None, None, None) == -1
+
+
 def test_workspace_bytes_closed_form():
     L = _lib.lib()
     d = _desc()
