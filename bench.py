@@ -291,7 +291,7 @@ def main():
     ms_eager = e0.elapsed_time(e1) / KT
     kernels = {}
     for name in ("decode_main_kernel", "decode_qt_kernel", "decode_combine_kernel",
-                 "append_step_kernel", "append_kernel", "append_commit_kernel"):
+                 "append_step_kernel", "append_kernel"):
         n, tot = wk.wushkv_timing_read(name)
         kernels[name] = (tot / n) if n else None
     wk.wushkv_timing_enable(0)

@@ -61,7 +61,7 @@ enum {
 };
 
 #define WUSHKV_PAGE_TOKENS 64
-#define WUSHKV_ABI_VERSION 3
+#define WUSHKV_ABI_VERSION 4
 
 /* Per-token quantisers (wushkv_cache.codec). */
 enum {
@@ -153,6 +153,10 @@ typedef struct wushkv_cache {
     uint16_t *win_v;
     int32_t *seq_len;          /* [batch] S; read and advanced by wushkv_append */
     int32_t *quant_end;        /* [batch] S_quant; read and advanced by wushkv_append */
+    int32_t *commit;           /* [batch] caller-owned scratch, zero before the first
+                                  append: the append's workgroups count their arrivals
+                                  here so that the last of each sequence advances S and
+                                  S_quant; every completed call leaves it zero */
 } wushkv_cache;
 
 /* Bytes of one (page, head) block, or 0 for unsupported (head_dim, bits). */

@@ -79,8 +79,9 @@ class WushKVCache:
     """Device memory of one WUSH-KV cache plus its C descriptor.
 
     Allocates (torch, on ``device``): the page pool, the page table, the bf16
-    windows and the per-sequence counters, all zero-initialised except the
-    windows, which may hold anything (they are only read where live).
+    windows, the per-sequence counters and the append's arrival counts, all
+    zero-initialised except the windows, which may hold anything (they are
+    only read where live).
     ``page_order`` "linear" maps logical page i of sequence b to physical
     page b * max_pages + i; "random" draws a seeded permutation of a pool
     ``pool_factor`` times the needed size.  ``codec`` is "pclip" (Eq. (7),
@@ -131,6 +132,7 @@ class WushKVCache:
                                  device=dev)
         self.seq_len = torch.zeros(batch, dtype=torch.int32, device=dev)
         self.quant_end = torch.zeros(batch, dtype=torch.int32, device=dev)
+        self.commit = torch.zeros(batch, dtype=torch.int32, device=dev)
         self._desc = self._make_desc()
 
     def _make_desc(self) -> CacheDesc:
@@ -140,7 +142,7 @@ class WushKVCache:
             self.kappa_v, {"pclip": _lib.CODEC_PCLIP, "quest": _lib.CODEC_QUEST}[self.codec],
             self.quest_alpha, self.pages.data_ptr(), self.page_table.data_ptr(),
             self.win_k.data_ptr(), self.win_v.data_ptr(), self.seq_len.data_ptr(),
-            self.quant_end.data_ptr())
+            self.quant_end.data_ptr(), self.commit.data_ptr())
 
     @property
     def desc(self) -> CacheDesc:
@@ -150,7 +152,7 @@ class WushKVCache:
         """Deep copy (same layout, same page table, fresh device memory)."""
         new = object.__new__(WushKVCache)
         new.__dict__.update({k: v for k, v in self.__dict__.items() if k != "_desc"})
-        for name in ("pages", "page_table", "win_k", "win_v", "seq_len", "quant_end"):
+        for name in ("pages", "page_table", "win_k", "win_v", "seq_len", "quant_end", "commit"):
             setattr(new, name, getattr(self, name).clone())
         new._desc = new._make_desc()
         return new

@@ -42,6 +42,7 @@ class CacheDesc(ctypes.Structure):
         ("win_v", ctypes.c_void_p),
         ("seq_len", ctypes.c_void_p),
         ("quant_end", ctypes.c_void_p),
+        ("commit", ctypes.c_void_p),
     ]
 
 

@@ -56,11 +56,12 @@ int wushkv_validate_cache(const wushkv_cache *c)
     } else {
         return WUSHKV_EINVAL;
     }
-    if (!c->win_k || !c->win_v || !c->seq_len || !c->quant_end) return WUSHKV_EINVAL;
+    if (!c->win_k || !c->win_v || !c->seq_len || !c->quant_end || !c->commit) return WUSHKV_EINVAL;
     const bool paged = c->n_pages > 0 && c->max_pages_per_seq > 0;
     if (paged && (!c->pages || !c->page_table)) return WUSHKV_EINVAL;
     if (!aligned16(c->win_k) || !aligned16(c->win_v) || !aligned16(c->pages) ||
-        !aligned16(c->page_table) || !aligned16(c->seq_len) || !aligned16(c->quant_end))
+        !aligned16(c->page_table) || !aligned16(c->seq_len) || !aligned16(c->quant_end) ||
+        !aligned16(c->commit))
         return WUSHKV_EINVAL;
     // every element offset the kernels form must fit in int64 with margin
     const double win = (double)c->batch * c->n_kv_heads * c->win_slots * c->head_dim;

@@ -32,8 +32,10 @@ struct AppendArgs {
     const int32_t *page_table;
     uint16_t *win_k;
     uint16_t *win_v;
-    const int32_t *seq_len;
-    const int32_t *quant_end;
+    int32_t *seq_len;
+    int32_t *quant_end;
+    int32_t *commit;     // [batch] arrivals of this launch's workgroups (zero between calls)
+    int32_t arrivals;    // workgroups per sequence that report; 0: this launch does not commit
     int32_t n_kv, s_sink, s_keep, s_flush, win_slots, max_pages, n_pages;
     int32_t lo_k, lo_v;  // quantile positions: lo = floor(kappa (d-1))
     float t_k, t_v;      // and t = kappa (d-1) - lo
@@ -104,6 +106,33 @@ __device__ __forceinline__ void norm_rope_row(float (&x)[D / 32][8], int j, int3
             x[c + kC / 2][e] = hi * co[e] + lo * si[e];
         }
     }
+}
+
+// Sequence b's counters advance from inside the launch that last reads
+// them.  Each workgroup reports once, after its reads of seq_len and
+// quant_end have returned (the values are tied to the report's operand), to
+// the sequence's arrival count (commit_arrive, at the start); the workgroup
+// that was last of a.arrivals writes S_new and S_quant_new and clears the
+// count for the next call (commit_finish, at its end, so that the count's
+// round trip overlaps its work).  Every workgroup of the sequence has read
+// the old values before the last one arrives, so none can see the new ones.
+// Thread 0 only; a launch with a.arrivals = 0 leaves the counters alone.
+__device__ __forceinline__ int32_t commit_arrive(const AppendArgs &a, int b, int32_t s_old, int32_t q_old,
+                                                 int32_t nn, int tid)
+{
+    if (a.arrivals <= 0 || tid != 0) return -1;
+    int32_t one = 1;
+    asm volatile("" : "+v"(one) : "v"(s_old), "v"(q_old), "v"(nn));
+    return __hip_atomic_fetch_add(a.commit + b, one, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void commit_finish(const AppendArgs &a, int b, int32_t arrived, int32_t s_new,
+                                              int32_t q_new, int tid)
+{
+    if (a.arrivals <= 0 || tid != 0 || arrived != a.arrivals - 1) return;
+    a.seq_len[b] = s_new;
+    a.quant_end[b] = q_new;
+    __hip_atomic_store(a.commit + b, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Descending top-KMAX of the values pushed so far; t[0] is the largest.
@@ -495,6 +524,7 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
     nn = nn < 0 ? 0 : (nn > a.max_new ? a.max_new : nn);
     const int32_t s_new = s_old + nn;
     const int32_t q_new = next_quant_end(s_new, q_old, a.s_sink, a.s_keep, a.s_flush);
+    const int32_t arrived = commit_arrive(a, b, s_old, q_old, nn, tid);
     const int32_t start_old = q_old > a.s_sink ? q_old : a.s_sink;
     const int32_t first = s_old < start_old ? s_old : start_old;
     const int32_t ring = a.win_slots - a.s_sink;
@@ -511,7 +541,10 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
         blk_hi = blk_lo + kPage;
     }
     const int32_t lo = max(blk_lo, first), hi = min(blk_hi, s_new);
-    if (lo >= hi) return;
+    if (lo >= hi) {
+        commit_finish(a, b, arrived, s_new, q_new, tid);
+        return;
+    }
 
     const bool do_new = (a.mode & kModeNew) != 0, do_flush = (a.mode & kModeFlush) != 0;
     // position p (lo <= p < hi) is: new if p >= s_old; quantised now if
@@ -689,6 +722,7 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
             a.win_v[(head_win * D) + (int64_t)ch * a.win_slots + slot] = vt[r * kPitch + ch];
         }
     }
+    commit_finish(a, b, arrived, s_new, q_new, tid);
 }
 
 // Appends of at most kStepMax tokens per sequence (decode steps): one
@@ -725,6 +759,7 @@ __global__ void __launch_bounds__(256) append_step_kernel(AppendArgs a)
     nn = nn < 0 ? 0 : (nn > a.max_new ? a.max_new : nn);
     const int32_t s_new = s_old + nn;
     const int32_t q_new = next_quant_end(s_new, q_old, a.s_sink, a.s_keep, a.s_flush);
+    const int32_t arrived = commit_arrive(a, b, s_old, q_old, nn, tid);
     const int32_t start_old = q_old > a.s_sink ? q_old : a.s_sink;
     const int32_t ring = a.win_slots - a.s_sink;
     const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;
@@ -847,20 +882,7 @@ __global__ void __launch_bounds__(256) append_step_kernel(AppendArgs a)
                 *reinterpret_cast<const uint4 *>(kn + t * kPitch + 8 * tid);
         if (tid < D) a.win_v[(head_win * D) + (int64_t)tid * a.win_slots + slot] = new_row(a.v_new, p)[tid];
     }
-}
-
-// Advance seq_len / quant_end after the append kernels have read them.
-__global__ void append_commit_kernel(int32_t *seq_len, int32_t *quant_end, const int32_t *n_new,
-                                     int32_t batch, int32_t max_new, int32_t s_sink,
-                                     int32_t s_keep, int32_t s_flush)
-{
-    const int b = blockIdx.x * blockDim.x + threadIdx.x;
-    if (b >= batch) return;
-    int32_t nn = n_new[b];
-    nn = nn < 0 ? 0 : (nn > max_new ? max_new : nn);
-    const int32_t s_new = seq_len[b] + nn;
-    quant_end[b] = next_quant_end(s_new, quant_end[b], s_sink, s_keep, s_flush);
-    seq_len[b] = s_new;
+    commit_finish(a, b, arrived, s_new, q_new, tid);
 }
 
 template <int D, int BITS>
@@ -917,6 +939,7 @@ static int append_impl(const wushkv_cache *c, const uint16_t *k_new, const uint1
     a.win_v = c->win_v;
     a.seq_len = c->seq_len;
     a.quant_end = c->quant_end;
+    a.commit = c->commit;
     a.n_kv = c->n_kv_heads;
     a.s_sink = c->s_sink;
     a.s_keep = c->s_keep;
@@ -959,10 +982,13 @@ static int append_impl(const wushkv_cache *c, const uint16_t *k_new, const uint1
     const dim3 flush_grid((unsigned)std::min<int64_t>(tiles, a.sink_tiles + (ring + kPage - 1) / kPage + 1),
                           grid.y, grid.z);
 
+    // the launch that appends the new tokens advances the counters (its
+    // workgroups are the last to read them)
     auto go = [&](int mode) -> hipError_t {
         a.mode = mode;
         const char *name = mode == kModeFlush ? "append_flush" : "append_kernel";
         const dim3 g = mode == kModeFlush ? flush_grid : grid;
+        a.arrivals = (mode & kModeNew) ? (int32_t)(g.x * g.y) : 0;
         const int key = c->head_dim * 10 + c->bits;
         switch (key) {
             case 1282: return launch_append<128, 2>(name, a, g, s);
@@ -975,6 +1001,7 @@ static int append_impl(const wushkv_cache *c, const uint16_t *k_new, const uint1
     hipError_t e;
     if (max_new <= kStepMax) {
         const dim3 sgrid((unsigned)c->n_kv_heads, (unsigned)c->batch);
+        a.arrivals = (int32_t)sgrid.x;
         const int key = c->head_dim * 10 + c->bits;
         switch (key) {
             case 1282: e = launch_append_step<128, 2>(a, sgrid, s); break;
@@ -989,9 +1016,6 @@ static int append_impl(const wushkv_cache *c, const uint16_t *k_new, const uint1
         if (e == hipSuccess) e = go(kModeNew);
     }
     if (e != hipSuccess) return WUSHKV_ELAUNCH;
-    launch("append_commit_kernel", append_commit_kernel, dim3((c->batch + 255) / 256), dim3(256), s,
-           c->seq_len, c->quant_end, n_new, c->batch, max_new, c->s_sink, c->s_keep, c->s_flush);
-    if (hipGetLastError() != hipSuccess) return WUSHKV_ELAUNCH;
     return WUSHKV_OK;
 }
 

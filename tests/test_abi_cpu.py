@@ -20,7 +20,7 @@ def test_exports_every_declared_function():
     L = _lib.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert wk.wushkv_abi_version() == 3
+    assert wk.wushkv_abi_version() == 4
 
 
 @pytest.mark.parametrize("d,bits", [(64, 2), (64, 4), (128, 2), (128, 4)])
@@ -47,7 +47,8 @@ FAKE = 0x10000  # 16-byte aligned, never dereferenced: every case below fails va
 def _desc(**over):
     f = dict(batch=2, n_kv_heads=2, head_dim=128, bits=2, s_sink=4, s_keep=128, s_flush=8,
              win_slots=192, max_pages_per_seq=4, n_pages=8, kappa_k=0.96, kappa_v=0.92,
-             pages=FAKE, page_table=FAKE, win_k=FAKE, win_v=FAKE, seq_len=FAKE, quant_end=FAKE)
+             pages=FAKE, page_table=FAKE, win_k=FAKE, win_v=FAKE, seq_len=FAKE, quant_end=FAKE,
+             commit=FAKE)
     f.update(over)
     return _lib.CacheDesc(**f)
 
@@ -58,6 +59,7 @@ BAD = [
     (dict(win_slots=128), -1),  # ring 124 < s_keep + s_flush - 1 = 135
     (dict(kappa_k=0.0), -1), (dict(kappa_v=1.5), -1), (dict(kappa_k=float("nan")), -1),
     (dict(win_k=None), -1), (dict(seq_len=None), -1), (dict(pages=None), -1),
+    (dict(commit=None), -1), (dict(commit=FAKE + 4), -1),
     (dict(win_v=FAKE + 4), -1), (dict(max_pages_per_seq=-1), -1),
     (dict(codec=2), -1), (dict(codec=-1), -1),
     (dict(codec=1, quest_alpha=0.0), -1), (dict(codec=1, quest_alpha=float("inf")), -1),
