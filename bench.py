@@ -54,6 +54,8 @@ def parse():
                     help="only run the append-throughput leg and print its JSON object")
     ap.add_argument("--no-scale", action="store_true",
                     help="skip the decode legs at the long-context and large-batch sizes")
+    ap.add_argument("--wush-only", action="store_true",
+                    help="only the transform-builder leg (all K/V heads of an 8B-shaped model)")
     ap.add_argument("--scale-only", action="store_true",
                     help="only run the long-context / large-batch decode legs")
     ap.add_argument("--seed", type=int, default=0)
@@ -172,6 +174,9 @@ def main():
         return
     if args.scale_only:
         print(json.dumps(bench_decode_scale(torch, wk, synth, dev, args)), flush=True)
+        return
+    if args.wush_only:
+        print(json.dumps(bench_wush(torch, wk, dev, args)), flush=True)
         return
     cfg = synth.CONFIGS["llama8b"]
     w = synth.Workload(cfg, seed=args.seed)

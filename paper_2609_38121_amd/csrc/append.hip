@@ -515,7 +515,16 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int h = blockIdx.y, b = blockIdx.z;
+    // XCD-aware order.  The device hands consecutive workgroups to its 8
+    // XCDs in turn (workgroup L runs on XCD L % 8), so the 8 workgroups of a
+    // turn take 8 consecutive tiles of one (head, sequence), and the next
+    // turns take the same 8 tiles for the other heads and sequences: the
+    // rotary-table rows of a tile's positions are read into one XCD's L2 and
+    // reused there by every head and sequence.  gridDim.x is a multiple of 8.
+    const uint32_t wg = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+    const uint32_t hbs = gridDim.y * gridDim.z, turn = wg / 8;
+    const int tile = (int)(8 * (turn / hbs) + wg % 8);
+    const int h = (int)((turn % hbs) % gridDim.y), b = (int)((turn % hbs) / gridDim.y);
 
     // ---- per-sequence bookkeeping (identical in every workgroup)
     const int32_t s_old = a.seq_len[b];
@@ -531,7 +540,7 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
 
     // ---- which tile
     int k0 = first < a.s_sink ? (first / kPage) - a.sink_tiles : (first - a.s_sink) / kPage;
-    const int k = k0 + (int)blockIdx.x;
+    const int k = k0 + tile;
     int32_t blk_lo, blk_hi;
     if (k < 0) {
         blk_lo = (k + a.sink_tiles) * kPage;
@@ -969,7 +978,9 @@ static int append_impl(const wushkv_cache *c, const uint16_t *k_new, const uint1
     // oldest unflushed position (at most s_keep + s_flush - 1 back) to the
     // new end.
     const int64_t span = (int64_t)max_new + c->s_keep + c->s_flush - 1;
-    const int64_t tiles = a.sink_tiles + (span + kPage - 1) / kPage + 1;
+    // (a multiple of 8: see the tile order in append_kernel; the extra tiles
+    // lie past the new end and exit at once)
+    const int64_t tiles = (a.sink_tiles + (span + kPage - 1) / kPage + 1 + 7) / 8 * 8;
     if (tiles > 0x7FFFFFFF) return WUSHKV_EINVAL;
     dim3 grid((unsigned)tiles, (unsigned)c->n_kv_heads, (unsigned)c->batch);
 
@@ -979,7 +990,7 @@ static int append_impl(const wushkv_cache *c, const uint16_t *k_new, const uint1
     // most the ring's length from the first unflushed one.
     const int64_t ring = (int64_t)c->win_slots - c->s_sink;
     const bool fused = ring >= span;
-    const dim3 flush_grid((unsigned)std::min<int64_t>(tiles, a.sink_tiles + (ring + kPage - 1) / kPage + 1),
+    const dim3 flush_grid((unsigned)std::min<int64_t>(tiles, (a.sink_tiles + (ring + kPage - 1) / kPage + 1 + 7) / 8 * 8),
                           grid.y, grid.z);
 
     // the launch that appends the new tokens advances the counters (its
