@@ -65,7 +65,7 @@ def parse():
     return ap.parse_args()
 
 
-def profiled_traffic(summary, csrc):
+def profiled_traffic(summary, csrc, key="traffic_bytes_per_launch"):
     """HBM bytes per launch from a committed counter summary, or None when
     the kernel sources changed since the counters were taken (the summary
     records a sha256 prefix of each source it covers)."""
@@ -79,7 +79,7 @@ def profiled_traffic(summary, csrc):
             k_, v_ = ln.split(":", 1)
             fields[k_.strip()] = v_.strip()
     try:
-        value = int(fields["traffic_bytes_per_launch"])
+        value = int(fields[key])
         want = dict(x.split("=") for x in fields["source_sha256_prefix"].split())
     except (KeyError, ValueError):
         return None
@@ -470,11 +470,15 @@ def bench_prefill(torch, wk, synth, dev, args):
         log("prefill append (%s): %.1f us/call, %.3g tokens/s, append_kernel %.1f us, %.1f GB/s "
             "(flush-only launch %.1f us)" % (name, ms * 1e3, tokens / (ms * 1e-3), t_kernel * 1e3,
                                              ach, t_flush * 1e3))
+        tkey = {"norm_rope": "traffic_bytes_per_launch", "prenormed": "traffic_bytes_per_launch_prenormed",
+                "quest": "traffic_bytes_per_launch_quest"}[name]
+        traffic = profiled_traffic("append_kernel_prefill_4x16384_2bit.md",
+                                   os.path.join(ROOT, "paper_2609_38121_amd", "csrc"), tkey)
         entry = {"tokens_per_s": round(tokens / (ms * 1e-3), 1), "ms_per_call": round(ms, 4),
                  "bytes_per_call": int(b_),
                  "roofline": {"bound": "hbm", "kernel": "append_kernel", "achieved": round(ach, 2),
                               "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                              "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+                              "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": traffic,
                               "avg_us": round(t_kernel * 1e3, 3)},
                  "flush_launch_us": round(t_flush * 1e3, 3),
                  "roofline_tokens_per_s": round(tokens / (b_ / (PEAK_HBM_GBS * 1e9)), 1)}
