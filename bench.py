@@ -352,6 +352,9 @@ def main():
     if not args.no_scale:
         scale = bench_decode_scale(torch, wk, synth, dev, args)
 
+    # ---- the streaming-read reference on the same device
+    stream_read = bench_stream_read(torch, wk, dev)
+
     # ---- the transform builder on a whole model's calibration statistics
     wush = bench_wush(torch, wk, dev, args) if not args.no_scale else None
 
@@ -396,6 +399,7 @@ def main():
         "decode_at_scale": scale,
         "chunk_attention": chunk,
         "wush_build": wush,
+        "stream_read": stream_read,
     }
     print(json.dumps(line), flush=True)
 
@@ -536,6 +540,33 @@ def bench_chunk(torch, wk, caches, reps, k1, tk, tinv, B, NQ, D, max_seq, sm, cf
             "gbps_algorithmic": round(byts / t / 1e9, 1),
             "note": "16-token chunks on the 8192-token Llama-shaped cache; the cache is read "
                     "once per group of two chunk tokens (8 virtual query heads per kv head)"}
+
+
+def bench_stream_read(torch, wk, dev, gib=2, reps=10):
+    """The reference denominator (not a replacement for the nominal peak): a
+    plain read of a 2 GiB buffer, eight times the Infinity Cache, by the
+    library's read probe with 16-byte vector loads and with the 16-byte
+    direct-to-LDS loads the decode kernel's pages use."""
+    buf = torch.zeros(gib << 30, dtype=torch.uint8, device=dev)
+    sink = torch.empty((gib << 30) // 65536, dtype=torch.int32, device=dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    out = {"bytes": gib << 30}
+    for mode, key in ((0, "vector_loads_gbps"), (1, "lds_dma_loads_gbps")):
+        for _ in range(2):
+            wk.wushkv_read_probe(buf, mode, sink)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            wk.wushkv_read_probe(buf, mode, sink)
+        e1.record()
+        torch.cuda.synchronize()
+        gbs = (gib << 30) * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+        out[key] = round(gbs, 1)
+    log("streaming read of %d GiB: %.1f GB/s (vector loads), %.1f GB/s (direct-to-LDS loads), "
+        "%.0f%% / %.0f%% of 8 TB/s" % (gib, out["vector_loads_gbps"], out["lds_dma_loads_gbps"],
+                                        out["vector_loads_gbps"] / 80, out["lds_dma_loads_gbps"] / 80))
+    del buf
+    return out
 
 
 def bench_wush(torch, wk, dev, args, layers=32, heads=8, d=128, gamma=1e-2, reps=5):

@@ -363,6 +363,17 @@ int wushkv_wush_transform(const float *m, const float *h, int32_t count, int32_t
  */
 double wushkv_quest_alpha(int32_t bits);
 
+/*
+ * wushkv_read_probe -- a plain streaming read of `bytes` (a positive multiple
+ * of 65536) at `buf`: the reference for how much of the nominal HBM peak a
+ * kernel that only reads reaches on this device.  mode 0 reads with 16-byte
+ * vector loads into registers, mode 1 with 16-byte direct-to-LDS loads, the
+ * path of the decode kernel's pages.  sink: uint32 [bytes / 65536] device,
+ * receives one XOR of the data per 64 KB block.  Measurement aid only.
+ */
+int wushkv_read_probe(const void *buf, size_t bytes, int32_t mode, uint32_t *sink,
+                      wushkv_stream_t stream);
+
 /* WUSHKV_ABI_VERSION of the loaded library. */
 int wushkv_abi_version(void);
 

@@ -23,7 +23,8 @@ __all__ = [
     "WushKVCache", "WushKVError", "wushkv_append", "wushkv_decode_attention",
     "wushkv_decode_workspace_bytes", "wushkv_dequant", "wushkv_page_bytes",
     "wushkv_status_string", "wushkv_abi_version", "wushkv_timing_enable",
-    "wushkv_timing_read", "wushkv_quest_alpha", "wushkv_wush_transform", "PAGE_TOKENS",
+    "wushkv_timing_read", "wushkv_quest_alpha", "wushkv_wush_transform", "wushkv_read_probe",
+    "PAGE_TOKENS",
     "header_functions",
 ]
 
@@ -305,3 +306,15 @@ def wushkv_wush_transform(m, h, gamma: float = 1e-2, t_out=None, t_inv_out=None,
                                           _ptr(sweeps_out), _stream_handle(stream))
     check(st, "wushkv_wush_transform")
     return t_out, (t_inv_out if want_inverse else None), sweeps_out
+
+
+def wushkv_read_probe(buf, mode: int, sink=None, stream=None):
+    """Streaming read of the device tensor buf (byte size a multiple of
+    65536), mode 0 vector loads or 1 direct-to-LDS loads.  Returns sink."""
+    torch = _torch()
+    nbytes = buf.numel() * buf.element_size()
+    if sink is None:
+        sink = torch.empty(max(1, nbytes // 65536), dtype=torch.int32, device=buf.device)
+    check(_lib.lib().wushkv_read_probe(_ptr(buf), nbytes, int(mode), _ptr(sink),
+                                       _stream_handle(stream)), "wushkv_read_probe")
+    return sink

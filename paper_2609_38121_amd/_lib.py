@@ -93,6 +93,8 @@ def _declare(L):
     L.wushkv_abi_version.restype = ctypes.c_int
     L.wushkv_wush_transform.argtypes = [P, P, I32, I32, F32, P, P, P, P]
     L.wushkv_wush_transform.restype = ctypes.c_int
+    L.wushkv_read_probe.argtypes = [P, SZ, I32, P, P]
+    L.wushkv_read_probe.restype = ctypes.c_int
     L.wushkv_quest_alpha.argtypes = [I32]
     L.wushkv_quest_alpha.restype = ctypes.c_double
     L.wushkv_timing_enable.argtypes = [I32]

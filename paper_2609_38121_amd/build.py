@@ -19,7 +19,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(BUILD, "libwushkv.so")
-SOURCES = ["api.hip", "append.hip", "decode.hip", "dequant.hip", "wush.hip"]
+SOURCES = ["api.hip", "append.hip", "decode.hip", "dequant.hip", "wush.hip", "probe.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -142,6 +142,16 @@ def test_wush_transform_validation():
     assert w(FAKE, FAKE + 4, 1, 128, 0.01, FAKE, None, None, None) == -1
 
 
+@pytest.mark.skipif(gpu_available(), reason="fake device pointers: run only where no GPU exists")
+def test_read_probe_validation():
+    L = _lib.lib()
+    assert L.wushkv_read_probe(FAKE, 65536 * 3 + 16, 0, FAKE, None) == -1
+    assert L.wushkv_read_probe(FAKE, 0, 0, FAKE, None) == -1
+    assert L.wushkv_read_probe(FAKE, 65536, 2, FAKE, None) == -1
+    assert L.wushkv_read_probe(None, 65536, 0, FAKE, None) == -1
+    assert L.wushkv_read_probe(FAKE, 65536, 1, FAKE + 4, None) == -1
+
+
 def test_workspace_bytes_closed_form():
     L = _lib.lib()
     d = _desc()
