@@ -512,9 +512,15 @@ struct MainLds {
 
 // FORM: the workgroup forms q~ and its limbs itself (the grid fits on the
 // device at once); otherwise decode_qt_kernel has written them.
-template <int D, int BITS, int G, bool FORM>
+// SHARE (chunks, with decode_qt_kernel): the four waves of a workgroup take
+// four consecutive token groups of one sequence and the same work items
+// (one run of pages, or one 64-slot window unit), so that the cache leaves
+// HBM once per four token groups; grid z runs over (sequence, group of four
+// token groups) and every wave writes its own partials.
+template <int D, int BITS, int G, bool FORM, bool SHARE>
 __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
 {
+    static_assert(!(FORM && SHARE), "shared work items take q~ from decode_qt_kernel");
     using L = Layout<D, BITS>;
     using M = MainLds<D, BITS, G>;
     constexpr bool kEarly = FORM && M::kEarly;
@@ -538,8 +544,12 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int j = lane >> 4, n = lane & 15;
     // grid z: (sequence, token group) pairs; see DecodeArgs
-    const int split = blockIdx.x, h = blockIdx.y, bz = blockIdx.z;
-    const int b = bz / a.n_groups, tg = bz % a.n_groups;
+    const int split = blockIdx.x, h = blockIdx.y;
+    const int n_quads = (a.n_groups + 3) / 4;  // SHARE: groups of four token groups
+    const int b = SHARE ? (int)blockIdx.z / n_quads : (int)blockIdx.z / a.n_groups;
+    const int tg = SHARE ? 4 * ((int)blockIdx.z % n_quads) + wave : (int)blockIdx.z % a.n_groups;
+    const bool rows_live = !SHARE || tg < a.n_groups;   // SHARE: this wave has rows
+    const int bz = b * a.n_groups + (rows_live ? tg : 0);  // grid row of this wave's rows
     uint8_t *stage = lds + wave * M::kWave;
     uint8_t *tbuf = stage + M::kStageBytes;
     constexpr int kTP = M::kTPitch;
@@ -558,8 +568,8 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
     // entries of q~, all requested before any page
     const bool page_wg = split < a.n_page_splits;
     const int upw = a.units_per_wave;
-    const int w0 = page_wg ? (split * 4 + wave) * upw : 0;
-    const int w1 = page_wg ? min(w0 + upw, n_qpages) : 0;
+    const int w0 = page_wg ? (SHARE ? split : split * 4 + wave) * upw : 0;
+    const int w1 = page_wg && rows_live ? min(w0 + upw, n_qpages) : 0;
     int32_t tbl = -1;
     if (w0 + lane < w1 && w0 + lane < a.max_pages)
         tbl = a.page_table[(int64_t)b * a.max_pages + w0 + lane];
@@ -894,14 +904,16 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
     } else {
         // ================================================ window slots
         // Workgroup n_page_splits + u owns window unit u (slots 64 u ..
-        // 64 u + 63), wave w its 16 slots 64 u + 16 w .. + 15.  All of a
-        // tile's loads are issued together.
+        // 64 u + 63), wave w its 16 slots 64 u + 16 w .. + 15 (SHARE: every
+        // wave all four 16-slot tiles of the unit, for its own rows, with an
+        // online softmax across them).  All of a tile's loads are issued
+        // together.
         const int32_t ring = a.win_slots - a.s_sink;
         // the ring holds positions [q_hi, S); the oldest sits at ring index a0
         const int32_t a0 = S > q_hi ? (q_hi - a.s_sink) % ring : 0;
         const int32_t ring_live = S > q_hi ? S - q_hi : 0;
         const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;
-        const int32_t slot0 = (split - a.n_page_splits) * kPage + 16 * wave;
+        const int32_t unit0 = (split - a.n_page_splits) * kPage;
 
         const float *qtl;
         if constexpr (FORM) {
@@ -940,19 +952,23 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
         if constexpr (FORM && !kEarly) __syncthreads();  // the rows may now be overwritten
         if (lane < 16) reinterpret_cast<uint32_t *>(tbuf + M::kTRows * kTP)[lane] = 0u;
 
-        // this tile's live slots, one bit per slot (lanes 0..15)
-        bool mine;
-        {
-            const int32_t sl = slot0 + n;
-            if (sl < a.s_sink) mine = sl < S;
-            else mine = ((sl - a.s_sink - a0 + ring) % ring) < ring_live;
-        }
-        const uint32_t vmask = (uint32_t)(__ballot(mine) & 0xFFFFu);
         f32x4 acc[kNT];
 #pragma unroll
         for (int nt = 0; nt < kNT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
         float m_run[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f};
-        if (vmask != 0) {
+        bool formed = FORM;
+        constexpr int kSub = SHARE ? 4 : 1;
+        for (int st = 0; st < (rows_live ? kSub : 0); ++st) {
+            const int32_t slot0 = unit0 + 16 * (SHARE ? st : wave);
+            // this tile's live slots, one bit per slot (lanes 0..15)
+            bool mine;
+            {
+                const int32_t sl = slot0 + n;
+                if (sl < a.s_sink) mine = sl < S;
+                else mine = ((sl - a.s_sink - a0 + ring) % ring) < ring_live;
+            }
+            const uint32_t vmask = (uint32_t)(__ballot(mine) & 0xFFFFu);
+            if (vmask == 0) continue;
             // key slots (token slot0 + n, channels 32 c + 8 j ..) and value
             // slots (channel 16 nt + n, tokens slot0 + 4 j .. + 3)
             const uint16_t *krow = a.win_k + (head_win + slot0 + n) * D + 8 * j;
@@ -964,7 +980,10 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
 #pragma unroll
             for (int nt = 0; nt < kNT; ++nt)
                 vx[nt] = *reinterpret_cast<const u32x2 *>(vrow + (int64_t)(16 * nt + n) * a.win_slots);
-            if constexpr (!FORM) form_qa();
+            if (!formed) {
+                form_qa();
+                formed = true;
+            }
 
             // scores: lane (j, n) gets rows 4 j + r = (head 2 j + r / 2,
             // part r % 2) of token slot0 + n
@@ -993,9 +1012,18 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
             float pr[2];
 #pragma unroll
             for (int e = 0; e < 2; ++e) {
-                m_run[e] = row_max16(lg[e]);
-                pr[e] = m_run[e] == -INFINITY ? 0.0f : fexp2(lg[e] - m_run[e]);
-                lsum[e] = pr[e];
+                // online softmax over the tiles: the running sums are scaled
+                // to the new maximum (a first tile scales zeros)
+                const float m_new = fmaxf(m_run[e], row_max16(lg[e]));
+                const float f_old = m_run[e] == -INFINITY ? 0.0f : fexp2(m_run[e] - m_new);
+                pr[e] = m_new == -INFINITY ? 0.0f : fexp2(lg[e] - m_new);
+                lsum[e] = fmaf(lsum[e], f_old, pr[e]);
+                m_run[e] = m_new;
+#pragma unroll
+                for (int nt = 0; nt < kNT; ++nt) {
+                    acc[nt][2 * e] *= f_old;
+                    acc[nt][2 * e + 1] *= f_old;
+                }
                 const int g = 2 * j + e;
                 if (g < G) {
                     const uint32_t hl = pack_bf16_rne(pr[e], 0.0f) & 0xFFFFu;
@@ -1036,6 +1064,25 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
         }
     }
     __syncthreads();
+
+    if constexpr (SHARE) {
+        // every wave's own rows: its result is that split's partial
+        for (int idx = tid; idx < 4 * G * D; idx += 256) {
+            const int rb = idx / (G * D), gg = (idx / D) % G, ch = idx % D;
+            const int tgr = 4 * ((int)blockIdx.z % n_quads) + rb;
+            if (tgr >= a.n_groups) continue;
+            const int64_t bzr = (int64_t)b * a.n_groups + tgr;
+            float *pr = a.part + ((bzr * a.n_kv + h) * a.n_splits + split) * G * (D + 2);
+            const float mx = sM[rb][gg];
+            pr[gg * (D + 2) + ch] =
+                mx == -INFINITY ? 0.0f : reinterpret_cast<const float(*)[D]>(lds + rb * M::kWave)[gg][ch];
+            if (ch == 0) {
+                pr[gg * (D + 2) + D] = mx;
+                pr[gg * (D + 2) + D + 1] = sL[rb][gg];
+            }
+        }
+        return;
+    }
 
     // ---- merge the four waves
     float *part = a.part + (((int64_t)bz * a.n_kv + h) * a.n_splits + split) * G * (D + 2);
@@ -1132,7 +1179,7 @@ struct DecodePlan {
 template <int D, int BITS, int G>
 static void main_kernel_ptr(const void *&f)
 {
-    f = reinterpret_cast<const void *>(&decode_main_kernel<D, BITS, G, true>);
+    f = reinterpret_cast<const void *>(&decode_main_kernel<D, BITS, G, true, false>);
 }
 
 // Waves of decode_main_kernel the device keeps resident at once (its
@@ -1181,6 +1228,7 @@ static int64_t resident_waves(int D, int bits, int G)
 // query head) pair, and n_groups token groups per sequence (see DecodeArgs).
 struct RowShape {
     int32_t g_real, tpg, G, n_groups, max_tok;
+    bool share;  // several token groups: four waves share each work item
 };
 
 static RowShape row_shape(const wushkv_cache *c, int32_t n_q, int32_t max_tok)
@@ -1192,6 +1240,7 @@ static RowShape row_shape(const wushkv_cache *c, int32_t n_q, int32_t max_tok)
     while (r.g_real * r.tpg * 2 <= 8 && r.tpg < max_tok) r.tpg *= 2;
     r.G = r.g_real * r.tpg;
     r.n_groups = (max_tok + r.tpg - 1) / r.tpg;
+    r.share = r.n_groups > 1;
     return r;
 }
 
@@ -1207,15 +1256,22 @@ static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq
     // 16 pages per wave (when the work cannot fit one round, shorter waves
     // balance the last round better).
     const int64_t wunits = c->win_slots / kPage;
-    const int64_t budget = resident_waves(c->head_dim, c->bits, G) - 4 * heads * wunits;
+    // With shared work items (share_items) the four waves of a workgroup
+    // walk one run together, each for another token group: a workgroup row
+    // is then a (sequence, four token groups, kv head) triple and a split
+    // covers upw pages instead of 4 upw.
+    const int64_t per_split = rs.share ? 1 : 4;
+    const int64_t wg_rows = rs.share ? (int64_t)c->batch * ((rs.n_groups + 3) / 4) * c->n_kv_heads : heads;
+    const int64_t budget = resident_waves(c->head_dim, c->bits, G) - 4 * wg_rows * wunits;
+    const int64_t upw_max = rs.share ? 64 : 16;
     int64_t upw = 2;
-    while (upw < 16 && heads * ((qpages + 4 * upw - 1) / (4 * upw)) * 4 > budget) ++upw;
-    int64_t psplits = (qpages + 4 * upw - 1) / (4 * upw);
+    while (upw < upw_max && wg_rows * ((qpages + per_split * upw - 1) / (per_split * upw)) * 4 > budget) ++upw;
+    int64_t psplits = (qpages + per_split * upw - 1) / (per_split * upw);
     if (psplits + wunits > kMaxSplits) {
         const int64_t room = kMaxSplits - wunits;
         if (room < 1) return false;
-        upw = (qpages + 4 * room - 1) / (4 * room);
-        psplits = (qpages + 4 * upw - 1) / (4 * upw);
+        upw = (qpages + per_split * room - 1) / (per_split * room);
+        psplits = (qpages + per_split * upw - 1) / (per_split * upw);
     }
     const int64_t splits = psplits + wunits;  // and one workgroup per window unit
     if (splits > kMaxSplits || upw > 0x7FFFFFFF / 4 / kMaxSplits) return false;
@@ -1229,26 +1285,32 @@ static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq
     return true;
 }
 
-// The main kernel, preceded by decode_qt_kernel unless it forms q~ itself.
+// The main kernel, preceded by decode_qt_kernel unless it forms q~ itself
+// (rows_z: grid rows of the query rows, one per (sequence, token group)).
 template <int D, int BITS, int G>
-static void launch_main(bool form, dim3 grid, hipStream_t s, const DecodeArgs &a)
+static void launch_main(bool form, bool share, dim3 grid, unsigned rows_z, hipStream_t s,
+                        const DecodeArgs &a)
 {
     if (form) {
-        launch("decode_main_kernel", decode_main_kernel<D, BITS, G, true>, grid, dim3(256), s, a);
-    } else {
-        launch("decode_qt_kernel", decode_qt_kernel<D, BITS, G>, dim3(grid.y, grid.z), dim3(256), s, a);
-        launch("decode_main_kernel", decode_main_kernel<D, BITS, G, false>, grid, dim3(256), s, a);
+        launch("decode_main_kernel", decode_main_kernel<D, BITS, G, true, false>, grid, dim3(256), s, a);
+        return;
     }
+    launch("decode_qt_kernel", decode_qt_kernel<D, BITS, G>, dim3(grid.y, rows_z), dim3(256), s, a);
+    if (share)
+        launch("decode_main_kernel", decode_main_kernel<D, BITS, G, false, true>, grid, dim3(256), s, a);
+    else
+        launch("decode_main_kernel", decode_main_kernel<D, BITS, G, false, false>, grid, dim3(256), s, a);
 }
 
 template <int D, int BITS>
-static void launch_main_g(int G, bool form, dim3 grid, hipStream_t s, const DecodeArgs &a)
+static void launch_main_g(int G, bool form, bool share, dim3 grid, unsigned rows_z, hipStream_t s,
+                          const DecodeArgs &a)
 {
     switch (G) {
-        case 1: launch_main<D, BITS, 1>(form, grid, s, a); break;
-        case 2: launch_main<D, BITS, 2>(form, grid, s, a); break;
-        case 4: launch_main<D, BITS, 4>(form, grid, s, a); break;
-        default: launch_main<D, BITS, 8>(form, grid, s, a); break;
+        case 1: launch_main<D, BITS, 1>(form, share, grid, rows_z, s, a); break;
+        case 2: launch_main<D, BITS, 2>(form, share, grid, rows_z, s, a); break;
+        case 4: launch_main<D, BITS, 4>(form, share, grid, rows_z, s, a); break;
+        default: launch_main<D, BITS, 8>(form, share, grid, rows_z, s, a); break;
     }
 }
 
@@ -1337,20 +1399,24 @@ static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok
     a.n_tok = n_tok;
 
     const unsigned rows_z = (unsigned)(c->batch * rs.n_groups);
-    const dim3 gm(p.n_splits, c->n_kv_heads, rows_z);
+    // several token groups (a chunk of more tokens than one group holds):
+    // the four waves of a workgroup take four of them over the same items
+    const unsigned grid_z = rs.share ? (unsigned)(c->batch * ((rs.n_groups + 3) / 4)) : rows_z;
+    const dim3 gm(p.n_splits, c->n_kv_heads, grid_z);
     const dim3 gc(c->n_kv_heads * G, rows_z);
     // Each workgroup forms q~ itself when the whole grid is resident at
     // once (one round: the rows cost each workgroup an L2 read of T^{-1}
     // that overlaps its first pages).  A grid that runs in rounds would pay
-    // that read once per workgroup, so a small kernel forms q~ first.
-    const int64_t wgs = (int64_t)p.n_splits * c->n_kv_heads * rows_z;
-    const bool form = wgs * 4 <= resident_waves(c->head_dim, c->bits, G);
+    // that read once per workgroup, so a small kernel forms q~ first; so do
+    // grids of shared work items.
+    const int64_t wgs = (int64_t)p.n_splits * c->n_kv_heads * grid_z;
+    const bool form = !rs.share && wgs * 4 <= resident_waves(c->head_dim, c->bits, G);
     const int key = c->head_dim * 10 + c->bits;
     switch (key) {
-        case 1282: launch_main_g<128, 2>(G, form, gm, s, a); break;
-        case 1284: launch_main_g<128, 4>(G, form, gm, s, a); break;
-        case 642: launch_main_g<64, 2>(G, form, gm, s, a); break;
-        case 644: launch_main_g<64, 4>(G, form, gm, s, a); break;
+        case 1282: launch_main_g<128, 2>(G, form, rs.share, gm, rows_z, s, a); break;
+        case 1284: launch_main_g<128, 4>(G, form, rs.share, gm, rows_z, s, a); break;
+        case 642: launch_main_g<64, 2>(G, form, rs.share, gm, rows_z, s, a); break;
+        case 644: launch_main_g<64, 4>(G, form, rs.share, gm, rows_z, s, a); break;
     }
     if (c->head_dim == 128) launch("decode_combine_kernel", decode_combine_kernel<128>, gc, dim3(128), s, (const float *)part, out, c->n_kv_heads, G, p.n_splits, a);
     else launch("decode_combine_kernel", decode_combine_kernel<64>, gc, dim3(64), s, (const float *)part, out, c->n_kv_heads, G, p.n_splits, a);
