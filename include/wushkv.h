@@ -279,6 +279,41 @@ size_t wushkv_decode_workspace_bytes(const wushkv_cache *c,
                                      int32_t n_q_heads, int32_t max_seq_len);
 
 /*
+ * wushkv_decode_step -- one decode step of Alg. 2 (S' = 1) in the
+ * algorithm's own order, in two launches on the stream:
+ *   1. each sequence's new token is appended at bf16 (steps 3-4: k~ = T_K k
+ *      into its window slot) and attention runs over the cache including it
+ *      (step 5), the positions that this step moves out of the recent window
+ *      still at bf16;
+ *   2. the attention splits are merged into out, those positions are
+ *      quantised into their pages (steps 7-11) and seq_len / quant_end
+ *      advance.
+ * On a step that quantises nothing the output and the cache equal those of
+ * wushkv_append followed by wushkv_decode_attention; on a step that does,
+ * that pair (which flushes first) attends to the flushed positions through
+ * their codes instead.
+ *
+ *   k_new, v_new  bf16 [batch][n_kv_heads][head_dim]: each sequence's new key
+ *              (after norm and RoPE) and value.
+ *   n_new      int32 [batch] device: 1 appends sequence b's token, 0 leaves the
+ *              sequence as it is (its query still attends); clamped to [0, 1].
+ *   t_k        bf16 [n_kv_heads][head_dim][head_dim] T_K, 16-byte aligned.
+ *   max_seq_len (host) >= every seq_len[b] + n_new[b]; sizes the split-K grid.
+ *   The other arguments are wushkv_decode_attention's; the workspace needs
+ *   wushkv_decode_workspace_bytes() for the same max_seq_len.
+ * The position seq_len[b] must lie inside the cache's capacity, as for
+ * wushkv_append.  Returns WUSHKV_EUNSUPPORTED when win_slots - s_sink <
+ * s_keep + s_flush (the new token's ring slot could still be live), and
+ * WUSHKV_EINVAL for null or misaligned new-token arguments, besides
+ * wushkv_decode_attention's checks; nothing is enqueued then.
+ */
+int wushkv_decode_step(const wushkv_cache *c, const uint16_t *k_new, const uint16_t *v_new,
+                       const int32_t *n_new, const uint16_t *t_k, const uint16_t *q,
+                       int32_t n_q_heads, int32_t max_seq_len, const float *t_k_inv,
+                       float sm_scale, float *out, void *workspace, size_t workspace_bytes,
+                       wushkv_stream_t stream);
+
+/*
  * wushkv_chunk_attention -- attention of a chunk of new tokens per sequence
  * (Alg. 2 step 5 with S' > 1): Eq. (2) with its causal mask, over the cache
  * as stored after the append that brought the chunk.

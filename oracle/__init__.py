@@ -305,6 +305,29 @@ class OracleCache:
         return out
 
 
+def decode_step(cache: "OracleCache", k_new, v_new, n_new, tk, q, tinv, sm_scale):
+    """One decode step of Alg. 2 (S' = 1) in the algorithm's own order: the
+    new tokens are appended in full precision (steps 3-4), attention runs
+    over the cache (step 5), and only then are the positions that left the
+    recent window quantised (steps 7-11).  So step 5 sees those positions at
+    bf16.  k_new, v_new: bf16 patterns [batch][n_kv][d]; n_new: [batch] of 0
+    or 1.  Returns fp64 [batch][n_q][d]; the cache ends as after append."""
+    k_new = np.ascontiguousarray(k_new, dtype=np.uint16)[:, None]
+    v_new = np.ascontiguousarray(v_new, dtype=np.uint16)[:, None]
+    q_before = cache.quant_end.copy()
+    # append() quantises as well, but it keeps every position's bf16 pattern,
+    # and decode() reads the patterns of positions at or after quant_end: the
+    # attention of step 5 is decode() with the boundary from before the flush
+    cache.append(k_new, v_new, n_new, tk)
+    q_after = cache.quant_end.copy()
+    cache.quant_end[:] = q_before
+    try:
+        out = cache.decode(q, tinv, sm_scale)
+    finally:
+        cache.quant_end[:] = q_after
+    return out
+
+
 def chunk_attention(cache: "OracleCache", q, n_tok, tinv, sm_scale):
     """Attention of a chunk of new tokens (Alg. 2 step 5 with S' > 1; the
     causal mask of Eq. (2)): q bf16 patterns [batch][S'][n_q][d]; sequence b's

@@ -20,7 +20,7 @@ from ._lib import (CacheDesc, WushKVError, PAGE_TOKENS, check, header_functions,
                    status_string)
 
 __all__ = [
-    "WushKVCache", "WushKVError", "wushkv_append", "wushkv_decode_attention",
+    "WushKVCache", "WushKVError", "wushkv_append", "wushkv_decode_attention", "wushkv_decode_step",
     "wushkv_decode_workspace_bytes", "wushkv_dequant", "wushkv_page_bytes",
     "wushkv_status_string", "wushkv_abi_version", "wushkv_timing_enable",
     "wushkv_timing_read", "wushkv_quest_alpha", "wushkv_wush_transform", "wushkv_read_probe",
@@ -229,6 +229,39 @@ def wushkv_decode_attention(cache: WushKVCache, q, t_k_inv, sm_scale=None, max_s
         float(sm_scale), _ptr(out), _ptr(workspace), workspace.numel() * workspace.element_size(),
         _stream_handle(stream))
     check(st, "wushkv_decode_attention")
+    return out
+
+
+def wushkv_decode_step(cache: WushKVCache, k_new, v_new, n_new, t_k, q, t_k_inv, sm_scale=None,
+                       max_seq_len=None, out=None, workspace=None, stream=None):
+    """One decode step in Alg. 2's order: each sequence's new token (n_new[b]
+    of 0 or 1) is appended, attention runs over the cache with it (the
+    positions due for quantisation still at bf16), then the flush.
+    k_new, v_new: bf16 [batch][n_kv][d]; n_new: int32 [batch] on the device;
+    t_k: bf16 [n_kv][d][d]; q: bf16 [batch][n_q][d]; t_k_inv: fp32
+    [n_kv][d][d].  Returns fp32 [batch][n_q][d]."""
+    torch = _torch()
+    _check_2byte(q, "q")
+    _check_2byte(k_new, "k_new")
+    _check_2byte(v_new, "v_new")
+    _check_2byte(t_k, "t_k")
+    n_q = q.shape[1]
+    if max_seq_len is None:
+        max_seq_len = cache.max_seq_len
+    if sm_scale is None:
+        sm_scale = 1.0 / math.sqrt(cache.head_dim)
+    if out is None:
+        out = torch.empty(cache.batch, n_q, cache.head_dim, dtype=torch.float32, device=q.device)
+    need = wushkv_decode_workspace_bytes(cache, n_q, max_seq_len)
+    if need == 0:
+        raise WushKVError(_lib.EINVAL, "wushkv_decode_workspace_bytes")
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    st = _lib.lib().wushkv_decode_step(
+        ctypes.byref(cache.desc), _ptr(k_new), _ptr(v_new), _ptr(n_new), _ptr(t_k), _ptr(q), n_q,
+        int(max_seq_len), _ptr(t_k_inv), float(sm_scale), _ptr(out), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream_handle(stream))
+    check(st, "wushkv_decode_step")
     return out
 
 

@@ -81,6 +81,8 @@ def _declare(L):
     L.wushkv_decode_attention.restype = ctypes.c_int
     L.wushkv_decode_workspace_bytes.argtypes = [D, I32, I32]
     L.wushkv_decode_workspace_bytes.restype = SZ
+    L.wushkv_decode_step.argtypes = [D, P, P, P, P, P, I32, I32, P, F32, P, P, SZ, P]
+    L.wushkv_decode_step.restype = ctypes.c_int
     L.wushkv_chunk_attention.argtypes = [D, P, P, I32, I32, I32, P, F32, P, P, SZ, P]
     L.wushkv_chunk_attention.restype = ctypes.c_int
     L.wushkv_chunk_workspace_bytes.argtypes = [D, I32, I32, I32]

@@ -22,6 +22,7 @@
 //            page already holds.
 //   phase D  bf16 window writes (sink and ring) and the optional k~ output.
 #include "common.h"
+#include "merge.h"
 
 namespace wushkv {
 
@@ -745,13 +746,74 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
 // ring's length.
 constexpr int kStepMax = 16;
 
+// Quantise positions [start, q_new) of (sequence b, kv head h) into their
+// pages, one 64-position block at a time (Alg. 2 steps 7-11).  A position
+// before s_ring comes from the windows' ring (keys row-major, values
+// channel-major); one at or after it is a new token of this call, its key
+// already transformed in kn (LDS, pitch D + 8) and its value in v_new.  kt
+// and vt are 64-row LDS tiles, sh_page one LDS word.  Every thread of the
+// 256-thread workgroup calls it.  kNewRows false: every position comes from
+// the ring (s_ring and kn unused).
+template <int D, int BITS, bool kNewRows>
+__device__ void flush_range(const AppendArgs &a, int b, int h, int32_t start, int32_t q_new,
+                            int32_t s_ring, const uint16_t *kn, uint16_t *kt, uint16_t *vt,
+                            int32_t &sh_page, int tid)
+{
+    using L = Layout<D, BITS>;
+    constexpr int kPitch = D + 8;
+    constexpr int kVec = D / 8;
+    const int32_t ring = a.win_slots - a.s_sink;
+    const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;
+    for (int32_t blk = a.s_sink + (start - a.s_sink) / kPage * kPage; blk < q_new; blk += kPage) {
+        const int32_t lo = max(blk, start), hi = min(blk + kPage, q_new);
+        for (int idx = tid; idx < kPage * kVec; idx += 256) {
+            const int r = idx / kVec, cv = idx % kVec;
+            const int32_t p = blk + r;
+            if (p < lo || p >= hi) continue;
+            uint4 kv, vv;
+            if (kNewRows && p >= s_ring) {
+                kv = *reinterpret_cast<const uint4 *>(kn + (p - s_ring) * kPitch + 8 * cv);
+                vv = *reinterpret_cast<const uint4 *>(
+                    a.v_new + (((int64_t)b * a.max_new + (p - s_ring)) * a.n_kv + h) * D + 8 * cv);
+            } else {
+                const int32_t slot = ring_slot(p, a.s_sink, ring);
+                kv = *reinterpret_cast<const uint4 *>(a.win_k + (head_win + slot) * D + 8 * cv);
+                const uint16_t *vsrc = a.win_v + (head_win * D) + slot;  // channel-major
+                uint16_t e[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) e[q] = vsrc[(int64_t)(8 * cv + q) * a.win_slots];
+                vv.x = e[0] | ((uint32_t)e[1] << 16);
+                vv.y = e[2] | ((uint32_t)e[3] << 16);
+                vv.z = e[4] | ((uint32_t)e[5] << 16);
+                vv.w = e[6] | ((uint32_t)e[7] << 16);
+            }
+            *reinterpret_cast<uint4 *>(kt + r * kPitch + 8 * cv) = kv;
+            *reinterpret_cast<uint4 *>(vt + r * kPitch + 8 * cv) = vv;
+        }
+        if (tid == 0) {
+            const int32_t lp = (blk - a.s_sink) / kPage;
+            int32_t phys = -1;
+            if (lp < a.max_pages) {
+                phys = a.page_table[(int64_t)b * a.max_pages + lp];
+                if (phys < 0 || phys >= a.n_pages) phys = -1;
+            }
+            sh_page = phys;
+        }
+        __syncthreads();
+        const int32_t page = sh_page;
+        uint8_t *pg = page >= 0 ? a.pages + ((int64_t)page * a.n_kv + h) * L::kPageBytes : nullptr;
+        quantise_tile<D, BITS>(a, kt, vt, blk, [&](int32_t p) { return p >= lo && p < hi; }, pg, tid);
+        __syncthreads();
+    }
+}
+
+
 template <int D, int BITS>
 __global__ void __launch_bounds__(256) append_step_kernel(AppendArgs a)
 {
     using L = Layout<D, BITS>;
     constexpr int kPitch = D + 8;
-    constexpr int kParts = 256 / D;   // threads per output channel
-    constexpr int kIn = D / kParts;   // inputs per thread
+    constexpr int kParts = KeyTransform<D>::kParts;  // threads per output channel
     __shared__ __attribute__((aligned(16))) uint16_t kn[kStepMax * kPitch];
     __shared__ __attribute__((aligned(16))) uint16_t kt[kPage * kPitch];
     __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * kPitch];
@@ -778,18 +840,8 @@ __global__ void __launch_bounds__(256) append_step_kernel(AppendArgs a)
 
     // ---- transformed new keys -> kn
     const int o = tid / kParts, part = tid % kParts;
-    uint32_t trow[kIn / 2];
-    {
-        const uint16_t *src = a.tk + ((int64_t)h * D + o) * D + part * kIn;
-#pragma unroll
-        for (int q = 0; q < kIn / 8; ++q) {
-            const uint4 v = *reinterpret_cast<const uint4 *>(src + 8 * q);
-            trow[4 * q + 0] = v.x;
-            trow[4 * q + 1] = v.y;
-            trow[4 * q + 2] = v.z;
-            trow[4 * q + 3] = v.w;
-        }
-    }
+    KeyTransform<D> xf;
+    xf.load(a.tk, h, tid);
     for (int t = 0; t < nn; ++t) {
         if (tid < D) kin[tid] = bf16_bits_to_f32(new_row(a.k_new, s_old + t)[tid]);
         __syncthreads();
@@ -819,14 +871,7 @@ __global__ void __launch_bounds__(256) append_step_kernel(AppendArgs a)
             if (tid < D) kin[tid] = kin2[tid];
             __syncthreads();
         }
-        float acc = 0.0f;
-#pragma unroll
-        for (int i = 0; i < kIn / 2; ++i) {
-            acc = fmaf(bf16_bits_to_f32(trow[i] & 0xFFFFu), kin[part * kIn + 2 * i], acc);
-            acc = fmaf(bf16_bits_to_f32(trow[i] >> 16), kin[part * kIn + 2 * i + 1], acc);
-        }
-#pragma unroll
-        for (int off = 1; off < kParts; off <<= 1) acc += __shfl_xor(acc, off);
+        const float acc = xf.sum(kin, tid);
         if (part == 0) {
             const uint16_t kb = (uint16_t)(pack_bf16_rne(acc, 0.0f) & 0xFFFFu);
             kn[t * kPitch + o] = kb;
@@ -836,50 +881,8 @@ __global__ void __launch_bounds__(256) append_step_kernel(AppendArgs a)
     }
 
     // ---- quantise [start_old, q_new), one page at a time
-    if (start_old < q_new) {
-        for (int32_t blk = a.s_sink + (start_old - a.s_sink) / kPage * kPage; blk < q_new; blk += kPage) {
-            const int32_t lo = max(blk, start_old), hi = min(blk + kPage, q_new);
-            constexpr int kVec = D / 8;
-            for (int idx = tid; idx < kPage * kVec; idx += 256) {
-                const int r = idx / kVec, cv = idx % kVec;
-                const int32_t p = blk + r;
-                if (p < lo || p >= hi) continue;
-                uint4 kv, vv;
-                if (p >= s_old) {
-                    kv = *reinterpret_cast<const uint4 *>(kn + (p - s_old) * kPitch + 8 * cv);
-                    vv = *reinterpret_cast<const uint4 *>(new_row(a.v_new, p) + 8 * cv);
-                } else {
-                    const int32_t slot = ring_slot(p, a.s_sink, ring);
-                    kv = *reinterpret_cast<const uint4 *>(a.win_k + (head_win + slot) * D + 8 * cv);
-                    const uint16_t *vsrc = a.win_v + (head_win * D) + slot;  // channel-major
-                    uint16_t e[8];
-#pragma unroll
-                    for (int q = 0; q < 8; ++q) e[q] = vsrc[(int64_t)(8 * cv + q) * a.win_slots];
-                    vv.x = e[0] | ((uint32_t)e[1] << 16);
-                    vv.y = e[2] | ((uint32_t)e[3] << 16);
-                    vv.z = e[4] | ((uint32_t)e[5] << 16);
-                    vv.w = e[6] | ((uint32_t)e[7] << 16);
-                }
-                *reinterpret_cast<uint4 *>(kt + r * kPitch + 8 * cv) = kv;
-                *reinterpret_cast<uint4 *>(vt + r * kPitch + 8 * cv) = vv;
-            }
-            if (tid == 0) {
-                const int32_t lp = (blk - a.s_sink) / kPage;
-                int32_t phys = -1;
-                if (lp < a.max_pages) {
-                    phys = a.page_table[(int64_t)b * a.max_pages + lp];
-                    if (phys < 0 || phys >= a.n_pages) phys = -1;
-                }
-                sh_page = phys;
-            }
-            __syncthreads();
-            const int32_t page = sh_page;
-            uint8_t *pg = page >= 0 ? a.pages + ((int64_t)page * a.n_kv + h) * L::kPageBytes : nullptr;
-            quantise_tile<D, BITS>(a, kt, vt, blk, [&](int32_t p) { return p >= lo && p < hi; },
-                                   pg, tid);
-            __syncthreads();
-        }
-    }
+    if (start_old < q_new)
+        flush_range<D, BITS, true>(a, b, h, start_old, q_new, s_old, kn, kt, vt, sh_page, tid);
 
     // ---- new tokens that stay bf16: sink, or the ring at or after q_new
     for (int t = 0; t < nn; ++t) {
@@ -909,6 +912,52 @@ static hipError_t launch_append_step(const AppendArgs &a, dim3 grid, hipStream_t
     return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ step
+
+// Second launch of wushkv_decode_step.  Workgroups x < n_q merge the
+// attention splits of query head x of sequence y (as the decode combine
+// does); the n_kv after them then finish Alg. 2 for kv head x - n_q of
+// sequence y after its attention: the positions that left the recent window
+// are quantised from the ring (steps 7-11; the new token, written to its
+// slot by the attention launch, is read from the ring as well), and the
+// last of a sequence's workgroups advances its counters.
+struct FinishArgs {
+    const float *part;  // [batch][n_kv][n_splits][G][D + 2]
+    float *out;         // [batch][n_kv G][D]
+    int32_t G, n_splits;
+};
+
+template <int D, int BITS>
+__global__ void __launch_bounds__(256) step_finish_kernel(AppendArgs a, FinishArgs f)
+{
+    constexpr int kPitch = D + 8;
+    __shared__ __attribute__((aligned(16))) uint16_t kt[kPage * kPitch];
+    __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * kPitch];
+    __shared__ float fw[kMaxSplits];
+    __shared__ float red[D];
+    __shared__ int32_t sh_page;
+    const int tid = threadIdx.x, b = blockIdx.y;
+    const int n_q = a.n_kv * f.G;
+    if ((int)blockIdx.x < n_q) {
+        const int qh = blockIdx.x, h = qh / f.G, g = qh % f.G;
+        const int64_t stride = (int64_t)f.G * (D + 2);
+        const float *pp = f.part + ((int64_t)b * a.n_kv + h) * f.n_splits * stride + g * (D + 2);
+        merge_splits<D>(pp, stride, f.n_splits, f.out + ((int64_t)b * n_q + qh) * D, tid, fw, red);
+        return;
+    }
+    const int h = (int)blockIdx.x - n_q;
+    const int32_t s_old = a.seq_len[b];
+    const int32_t q_old = a.quant_end[b];
+    int32_t nn = a.n_new[b];
+    nn = nn < 0 ? 0 : (nn > 1 ? 1 : nn);
+    const int32_t s_new = s_old + nn;
+    const int32_t q_new = next_quant_end(s_new, q_old, a.s_sink, a.s_keep, a.s_flush);
+    const int32_t arrived = commit_arrive(a, b, s_old, q_old, nn, tid);
+    const int32_t start = q_old > a.s_sink ? q_old : a.s_sink;
+    if (start < q_new) flush_range<D, BITS, false>(a, b, h, start, q_new, s_new, kt, kt, vt, sh_page, tid);
+    commit_finish(a, b, arrived, s_new, q_new, tid);
+}
+
 }  // namespace wushkv
 
 using namespace wushkv;
@@ -927,20 +976,9 @@ static void kappa_position(float kappa, int d, int32_t &lo, float &t)
 
 int wushkv_validate_cache(const wushkv_cache *c);  // api.hip
 
-// Both entry points: rope == nullptr appends keys as given; otherwise the
-// keys are normalised and rotated first (the caller checked the table).
-static int append_impl(const wushkv_cache *c, const uint16_t *k_new, const uint16_t *v_new,
-                       const int32_t *n_new, int32_t max_new, const uint16_t *t_k,
-                       const float *gain, float eps, const float *rope,
-                       uint16_t *k_tilde_out, wushkv_stream_t stream)
+// The cache's part of the kernel arguments (pointers, sizes, quantiser).
+static AppendArgs cache_args(const wushkv_cache *c)
 {
-    int st = wushkv_validate_cache(c);
-    if (st != WUSHKV_OK) return st;
-    if (max_new < 0) return WUSHKV_EINVAL;
-    if (max_new == 0) return WUSHKV_OK;
-    if (!k_new || !v_new || !n_new || !t_k) return WUSHKV_EINVAL;
-
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     AppendArgs a{};
     a.pages = c->pages;
     a.page_table = c->page_table;
@@ -963,16 +1001,35 @@ static int append_impl(const wushkv_cache *c, const uint16_t *k_new, const uint1
     } else {
         a.quest_coef = 2.0 * (double)c->quest_alpha / (double)((1 << c->bits) - 1);
     }
+    a.sink_tiles = (c->s_sink + kPage - 1) / kPage;
+    return a;
+}
+
+// Both entry points: rope == nullptr appends keys as given; otherwise the
+// keys are normalised and rotated first (the caller checked the table).
+static int append_impl(const wushkv_cache *c, const uint16_t *k_new, const uint16_t *v_new,
+                       const int32_t *n_new, int32_t max_new, const uint16_t *t_k,
+                       const float *gain, float eps, const float *rope,
+                       uint16_t *k_tilde_out, wushkv_stream_t stream)
+{
+    int st = wushkv_validate_cache(c);
+    if (st != WUSHKV_OK) return st;
+    if (max_new < 0) return WUSHKV_EINVAL;
+    if (max_new == 0) return WUSHKV_OK;
+    if (!k_new || !v_new || !n_new || !t_k) return WUSHKV_EINVAL;
+
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    AppendArgs a = cache_args(c);
     a.k_new = k_new;
     a.v_new = v_new;
     a.n_new = n_new;
     a.max_new = max_new;
     a.tk = t_k;
     a.k_tilde_out = k_tilde_out;
-    a.sink_tiles = (c->s_sink + kPage - 1) / kPage;
     a.gain = gain;
     a.eps = eps;
     a.rope = rope;
+
 
     // Tiles a sequence can touch: the sink tiles, plus the span from the
     // oldest unflushed position (at most s_keep + s_flush - 1 back) to the
@@ -1052,4 +1109,25 @@ extern "C" int wushkv_append_norm_rope(const wushkv_cache *c, const uint16_t *k_
     if (((uintptr_t)rope_table | (uintptr_t)norm_gain) & 15u) return WUSHKV_EINVAL;
     return append_impl(c, k_raw, v_new, n_new, max_new, t_k, norm_gain, norm_eps, rope_table,
                        k_tilde_out, stream);
+}
+
+// The finishing launch of wushkv_decode_step (its attention launch precedes
+// it on the stream): see step_finish_kernel.  Declared in decode.hip.
+int wushkv_step_finish(const wushkv_cache *c, const int32_t *n_new, const float *part, float *out,
+                       int32_t G, int32_t n_splits, hipStream_t s)
+{
+    AppendArgs a = cache_args(c);
+    a.n_new = n_new;
+    a.max_new = 1;
+    a.arrivals = c->n_kv_heads;  // the flush workgroups of a sequence
+    FinishArgs f{part, out, G, n_splits};
+    const dim3 grid((unsigned)(c->n_kv_heads * G + c->n_kv_heads), (unsigned)c->batch);
+    const int key = c->head_dim * 10 + c->bits;
+    switch (key) {
+        case 1282: launch("step_finish_kernel", step_finish_kernel<128, 2>, grid, dim3(256), s, a, f); break;
+        case 1284: launch("step_finish_kernel", step_finish_kernel<128, 4>, grid, dim3(256), s, a, f); break;
+        case 642: launch("step_finish_kernel", step_finish_kernel<64, 2>, grid, dim3(256), s, a, f); break;
+        default: launch("step_finish_kernel", step_finish_kernel<64, 4>, grid, dim3(256), s, a, f); break;
+    }
+    return hipGetLastError() == hipSuccess ? WUSHKV_OK : WUSHKV_ELAUNCH;
 }

@@ -164,6 +164,49 @@ __device__ __forceinline__ f32x4 mfma16h(f16x8 a, f16x8 b, f32x4 c)
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
 
+// k~ = T_K k for one key (Alg. 2 step 3) on a 256-thread workgroup: output
+// channel o = tid / kParts is summed by kParts = 256 / D neighbouring
+// threads, thread part `part` over inputs part kIn .. part kIn + kIn - 1
+// (kIn = D / kParts) in fp32 fused multiply-adds in index order; the parts
+// are then added across the neighbours (key_transform_sum) and the sum is
+// rounded once to bf16.  Every path that forms k~ uses these two steps, so
+// a token's k~ does not depend on which kernel formed it.
+template <int D>
+struct KeyTransform {
+    static constexpr int kParts = 256 / D;
+    static constexpr int kIn = D / kParts;
+    uint32_t trow[kIn / 2];  // this thread's T_K entries, bf16 pairs
+    // T_K row o (bf16 [D][D] of head h, row-major), this thread's part
+    __device__ __forceinline__ void load(const uint16_t *tk, int h, int tid)
+    {
+        const int o = tid / kParts, part = tid % kParts;
+        const uint16_t *src = tk + ((int64_t)h * D + o) * D + part * kIn;
+#pragma unroll
+        for (int q = 0; q < kIn / 8; ++q) {
+            const uint4 v = *reinterpret_cast<const uint4 *>(src + 8 * q);
+            trow[4 * q + 0] = v.x;
+            trow[4 * q + 1] = v.y;
+            trow[4 * q + 2] = v.z;
+            trow[4 * q + 3] = v.w;
+        }
+    }
+    // the channel's fp32 sum over the whole key kin[0..D) (every thread of
+    // the channel gets it)
+    __device__ __forceinline__ float sum(const float *kin, int tid) const
+    {
+        const int part = tid % kParts;
+        float acc = 0.0f;
+#pragma unroll
+        for (int i = 0; i < kIn / 2; ++i) {
+            acc = fmaf(bf16_bits_to_f32(trow[i] & 0xFFFFu), kin[part * kIn + 2 * i], acc);
+            acc = fmaf(bf16_bits_to_f32(trow[i] >> 16), kin[part * kIn + 2 * i + 1], acc);
+        }
+#pragma unroll
+        for (int off = 1; off < kParts; off <<= 1) acc += __shfl_xor(acc, off);
+        return acc;
+    }
+};
+
 // floor(a / b) for b > 0.
 __host__ __device__ __forceinline__ int64_t floor_div(int64_t a, int64_t b)
 {

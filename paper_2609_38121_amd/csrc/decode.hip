@@ -40,11 +40,11 @@
 // probabilities, again split hi + lo, go through LDS into a 16x16x16 bf16
 // P V product against the channel-major value slots.
 #include "common.h"
+#include "merge.h"
 
 namespace wushkv {
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kMaxSplits = 1024;
 constexpr int kLimbs = 6;
 
 typedef __attribute__((ext_vector_type(8))) int i32x8;
@@ -76,6 +76,15 @@ struct DecodeArgs {
     // head v % g_real).  Decode is the case max_tok = tpg = n_groups = 1.
     int32_t n_groups, tpg, g_real, max_tok;
     const int32_t *n_tok;  // [batch] chunk tokens per sequence, or null (max_tok)
+    // fused step (wushkv_decode_step; null otherwise): sequence b's new token
+    // (n_new[b], clamped to 0 or 1) joins the attention at position
+    // seq_len[b]; the workgroup owning its window slot forms k~ = T_K k,
+    // writes the slot and uses the token from LDS
+    const int32_t *n_new;   // [batch]
+    const uint16_t *k_new;  // bf16 [batch][n_kv][D]
+    const uint16_t *v_new;  // bf16 [batch][n_kv][D]
+    const uint16_t *t_k;    // bf16 [n_kv][D][D]
+    uint16_t *win_kw, *win_vw;  // the windows, written
 };
 
 // Tokens of sequence b's chunk: n_tok[b] (or max_tok), at most max_tok and
@@ -510,6 +519,41 @@ struct MainLds {
     static_assert(QueryLds<D, G>::kBytes <= 4 * kWave, "the query rows fit the page stages");
 };
 
+// Fused step: the new token of (sequence b, kv head h) into window slot
+// `slot`.  k~ = T_K k is formed with the append's arithmetic (KeyTransform),
+// so the stored key does not depend on the path that formed it; k~ and v
+// go to the windows and to tok (LDS: bf16 k~ [D], then v [D]); kin is D
+// floats of LDS.  Every thread of the workgroup calls it; it ends with a
+// barrier.
+template <int D>
+__device__ void step_token(const DecodeArgs &a, int b, int h, int32_t slot, uint16_t *tok,
+                           float *kin, int tid)
+{
+    using X = KeyTransform<D>;
+    X xf;
+    xf.load(a.t_k, h, tid);
+    const int64_t row = ((int64_t)b * a.n_kv + h) * D;
+    uint16_t v = 0;
+    if (tid < D) {
+        kin[tid] = bf16_bits_to_f32(a.k_new[row + tid]);
+        v = a.v_new[row + tid];
+    }
+    __syncthreads();
+    const float acc = xf.sum(kin, tid);
+    const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;
+    if (tid % X::kParts == 0) {
+        const int o = tid / X::kParts;
+        const uint16_t kb = (uint16_t)(pack_bf16_rne(acc, 0.0f) & 0xFFFFu);
+        tok[o] = kb;
+        a.win_kw[(head_win + slot) * D + o] = kb;
+    }
+    if (tid < D) {
+        tok[D + tid] = v;
+        a.win_vw[head_win * D + (int64_t)tid * a.win_slots + slot] = v;  // channel-major
+    }
+    __syncthreads();
+}
+
 // FORM: the workgroup forms q~ and its limbs itself (the grid fits on the
 // device at once); otherwise decode_qt_kernel has written them.
 // SHARE (chunks, with decode_qt_kernel): the four waves of a workgroup take
@@ -555,7 +599,11 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
     constexpr int kTP = M::kTPitch;
     const uint32_t zero_row = lds_addr(tbuf + M::kTRows * kTP);
 
-    const int32_t S = a.seq_len[b];
+    // fused step: the new token is position seq_len[b] and is attended to
+    const int32_t s_old = a.seq_len[b];
+    int32_t nn = a.n_new != nullptr ? a.n_new[b] : 0;
+    nn = nn < 0 ? 0 : (nn > 1 ? 1 : nn);
+    const int32_t S = s_old + nn;
     int32_t qend = a.quant_end[b];
     qend = qend < S ? qend : S;
     const int32_t q_hi = qend > a.s_sink ? qend : a.s_sink;  // quantised: [s_sink, q_hi)
@@ -914,6 +962,20 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
         const int32_t ring_live = S > q_hi ? S - q_hi : 0;
         const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;
         const int32_t unit0 = (split - a.n_page_splits) * kPage;
+        // fused step: the workgroup whose unit holds the new token's slot
+        // writes the token and keeps it in LDS, at the end of wave 3's page
+        // stage (its merge rows, written last, sit at the start)
+        int32_t new_slot = -1;
+        uint16_t *tok = reinterpret_cast<uint16_t *>(lds + 3 * M::kWave + M::kStageBytes - 4 * D);
+        static_assert(G * D * 4 + 8 * D <= M::kStageBytes, "the new token fits the page stage");
+        if (a.n_new != nullptr && nn > 0) {
+            const int32_t slot = s_old < a.s_sink ? s_old : ring_slot(s_old, a.s_sink, ring);
+            if (slot >= unit0 && slot < unit0 + kPage) {
+                new_slot = slot;
+                step_token<D>(a, b, h, slot, tok,
+                              reinterpret_cast<float *>(lds + 3 * M::kWave + M::kStageBytes - 8 * D), tid);
+            }
+        }
 
         const float *qtl;
         if constexpr (FORM) {
@@ -980,6 +1042,24 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
 #pragma unroll
             for (int nt = 0; nt < kNT; ++nt)
                 vx[nt] = *reinterpret_cast<const u32x2 *>(vrow + (int64_t)(16 * nt + n) * a.win_slots);
+            if (new_slot >= slot0 && new_slot < slot0 + 16) {
+                // the new token's slot: its key row (lanes n = t) and its
+                // values (element t % 4 of lanes j = t / 4) from LDS
+                const int t = new_slot - slot0;
+                if (n == t) {
+#pragma unroll
+                    for (int c = 0; c < kC; ++c) kx[c] = *reinterpret_cast<const u32x4 *>(tok + 32 * c + 8 * j);
+                }
+                if (j == (t >> 2)) {
+                    const int e = t & 3;
+#pragma unroll
+                    for (int nt = 0; nt < kNT; ++nt) {
+                        const uint32_t v = tok[D + 16 * nt + n];
+                        const uint32_t w = vx[nt][e >> 1];
+                        vx[nt][e >> 1] = (e & 1) ? ((w & 0xFFFFu) | (v << 16)) : ((w & 0xFFFF0000u) | v);
+                    }
+                }
+            }
             if (!formed) {
                 form_qa();
                 formed = true;
@@ -1141,32 +1221,7 @@ __global__ void __launch_bounds__(D) decode_combine_kernel(const float *part, fl
     }
     const int64_t stride = (int64_t)G * (D + 2);
     const float *pp = part + (((int64_t)bz * n_kv + h) * n_splits) * stride + g * (D + 2);
-    float mx = -INFINITY;
-    for (int s = ch; s < n_splits; s += D) {
-        const float m = pp[s * stride + D];
-        fw[s] = m;
-        mx = fmaxf(mx, m);
-    }
-    red[ch] = mx;
-    __syncthreads();
-    for (int off = D / 2; off > 0; off >>= 1) {
-        if (ch < off) red[ch] = fmaxf(red[ch], red[ch + off]);
-        __syncthreads();
-    }
-    const float M = red[0];
-    for (int s = ch; s < n_splits; s += D)
-        fw[s] = (fw[s] == -INFINITY) ? 0.0f : fexp2(fw[s] - M);
-    __syncthreads();
-    float o = 0.0f, l = 0.0f;
-    if (M != -INFINITY) {
-#pragma unroll 8
-        for (int s = 0; s < n_splits; ++s) {
-            const float f = fw[s];
-            o = fmaf(f, pp[s * stride + ch], o);
-            l = fmaf(f, pp[s * stride + D + 1], l);
-        }
-    }
-    dst[ch] = (l > 0.0f) ? o / l : 0.0f;
+    merge_splits<D>(pp, stride, n_splits, dst, ch, fw, red);
 }
 
 // ------------------------------------------------------------------ host
@@ -1346,9 +1401,19 @@ static size_t workspace_bytes(const wushkv_cache *c, int32_t n_q, int32_t max_to
     return p.qt_bytes + p.limb_bytes + p.aux_bytes + p.part_bytes;
 }
 
+// The new tokens of a fused step (wushkv_decode_step).
+struct StepIn {
+    const int32_t *n_new;
+    const uint16_t *k_new, *v_new, *t_k;
+};
+
+int wushkv_step_finish(const wushkv_cache *c, const int32_t *n_new, const float *part, float *out,
+                       int32_t G, int32_t n_splits, hipStream_t s);  // append.hip
+
 static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok, int32_t max_tok,
                   int32_t n_q_heads, int32_t max_seq_len, const float *t_k_inv, float sm_scale,
-                  float *out, void *workspace, size_t workspace_bytes, wushkv_stream_t stream)
+                  float *out, void *workspace, size_t workspace_bytes, wushkv_stream_t stream,
+                  const StepIn *step = nullptr)
 {
     int st = check_decode_args(c, n_q_heads, max_seq_len);
     if (st != WUSHKV_OK) return st;
@@ -1397,6 +1462,14 @@ static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok
     a.g_real = rs.g_real;
     a.max_tok = rs.max_tok;
     a.n_tok = n_tok;
+    if (step != nullptr) {
+        a.n_new = step->n_new;
+        a.k_new = step->k_new;
+        a.v_new = step->v_new;
+        a.t_k = step->t_k;
+        a.win_kw = c->win_k;
+        a.win_vw = c->win_v;
+    }
 
     const unsigned rows_z = (unsigned)(c->batch * rs.n_groups);
     // several token groups (a chunk of more tokens than one group holds):
@@ -1417,6 +1490,10 @@ static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok
         case 1284: launch_main_g<128, 4>(G, form, rs.share, gm, rows_z, s, a); break;
         case 642: launch_main_g<64, 2>(G, form, rs.share, gm, rows_z, s, a); break;
         case 644: launch_main_g<64, 4>(G, form, rs.share, gm, rows_z, s, a); break;
+    }
+    if (step != nullptr) {
+        if (hipGetLastError() != hipSuccess) return WUSHKV_ELAUNCH;
+        return wushkv_step_finish(c, step->n_new, part, out, G, p.n_splits, s);
     }
     if (c->head_dim == 128) launch("decode_combine_kernel", decode_combine_kernel<128>, gc, dim3(128), s, (const float *)part, out, c->n_kv_heads, G, p.n_splits, a);
     else launch("decode_combine_kernel", decode_combine_kernel<64>, gc, dim3(64), s, (const float *)part, out, c->n_kv_heads, G, p.n_splits, a);
@@ -1458,4 +1535,23 @@ extern "C" int wushkv_chunk_attention(const wushkv_cache *c, const uint16_t *q,
     if (st != WUSHKV_OK) return st;
     return attend(c, q, n_tok, max_tok, n_q_heads, max_seq_len, t_k_inv, sm_scale, out, workspace,
                   workspace_bytes, stream);
+}
+
+extern "C" int wushkv_decode_step(const wushkv_cache *c, const uint16_t *k_new, const uint16_t *v_new,
+                                  const int32_t *n_new, const uint16_t *t_k, const uint16_t *q,
+                                  int32_t n_q_heads, int32_t max_seq_len, const float *t_k_inv,
+                                  float sm_scale, float *out, void *workspace,
+                                  size_t workspace_bytes, wushkv_stream_t stream)
+{
+    int st = wushkv_validate_cache(c);
+    if (st != WUSHKV_OK) return st;
+    if (!k_new || !v_new || !n_new || !t_k) return WUSHKV_EINVAL;
+    if (((uintptr_t)t_k & 15u) || ((uintptr_t)k_new | (uintptr_t)v_new) & 1u || ((uintptr_t)n_new & 3u))
+        return WUSHKV_EINVAL;
+    // the new token's ring slot must be free: the ring holds at most
+    // s_keep + s_flush - 1 live entries before the step
+    if ((int64_t)c->win_slots - c->s_sink < (int64_t)c->s_keep + c->s_flush) return WUSHKV_EUNSUPPORTED;
+    const StepIn in{n_new, k_new, v_new, t_k};
+    return attend(c, q, nullptr, 1, n_q_heads, max_seq_len, t_k_inv, sm_scale, out, workspace,
+                  workspace_bytes, stream, &in);
 }

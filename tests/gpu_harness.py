@@ -118,6 +118,40 @@ class Pair:
         self.k_tilde_log.append((k_rot, kt_np, n_new))
         return kt_np
 
+    def step(self, k: np.ndarray, v: np.ndarray, n_new, q: np.ndarray, tol=TOL, max_seq_len=None):
+        """The fused decode step (wushkv_decode_step) against the oracle's
+        decode_step in Alg. 2's order: k, v bf16 patterns [batch][n_kv][d],
+        n_new [batch] of 0 / 1, q [batch][n_q][d].  The mirror gets the GPU's
+        k~, read back from the window slot the step wrote.  Returns (gpu
+        output, error vs mirror, error vs reference)."""
+        n_new = np.asarray(n_new, np.int32)
+        s_old = self.mirror.seq_len.copy()
+        nd = torch.from_numpy(n_new).to(self.dev)
+        out = wk.wushkv_decode_step(self.gpu, to_dev_bf16(k, self.dev), to_dev_bf16(v, self.dev), nd,
+                                    self.tk_dev, to_dev_bf16(q, self.dev), self.tinv_dev,
+                                    sm_scale=self.sm_scale, max_seq_len=max_seq_len)
+        torch.cuda.synchronize()
+        gpu = out.cpu().numpy()
+        win_k = to_np_bits(self.gpu.win_k)
+        ring = self.gpu.win_slots - self.s_sink
+        kt = np.zeros_like(k)
+        for b in range(self.batch):
+            if n_new[b]:
+                p = int(s_old[b])
+                slot = p if p < self.s_sink else self.s_sink + (p - self.s_sink) % ring
+                kt[b] = win_k[b, :, slot]
+        mir = oracle.decode_step(self.mirror, kt, v, n_new, self.eye, q, self.tinv, self.sm_scale)
+        e_m = rel_err(gpu, mir)
+        e_r = 0.0
+        if self.ref is not None:
+            ref = oracle.decode_step(self.ref, k, v, n_new, self.tk, q, self.tinv, self.sm_scale)
+            e_r = rel_err(gpu, ref)
+        self.k_tilde_log.append((k[:, None], kt[:, None], n_new))
+        assert np.all(np.isfinite(gpu))
+        assert e_m <= tol, "step vs oracle on the GPU's cache: %.3e" % e_m
+        assert e_r <= tol, "step vs oracle from raw inputs: %.3e" % e_r
+        return gpu, e_m, e_r
+
     def k_tilde_vs_ref(self):
         """Check the GPU's bf16 k~ = T_K k against the exact product.  The GPU
         accumulates in fp32 and rounds once to bf16, so each element must lie

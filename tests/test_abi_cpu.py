@@ -81,6 +81,9 @@ def test_validation_rejects_before_launch(over, status):
     assert st == status
     st = L.wushkv_dequant(ctypes.byref(d), 0, 4, 1, FAKE, FAKE, None)
     assert st == status
+    st = L.wushkv_decode_step(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 8, 100, FAKE, 0.1,
+                              FAKE, FAKE, 1 << 30, None)
+    assert st == status
     assert L.wushkv_decode_workspace_bytes(ctypes.byref(d), 8, 100) == 0
 
 
@@ -120,6 +123,28 @@ def test_call_specific_validation():
     need = L.wushkv_decode_workspace_bytes(by, 8, 100)
     assert need > 0
     assert L.wushkv_decode_attention(by, FAKE, 8, 100, FAKE, 0.1, FAKE, FAKE, need - 1, None) == -3
+    # fused step: null or misaligned new-token arguments, then the decode
+    # checks; a ring shorter than s_keep + s_flush is unsupported
+    st_ = L.wushkv_decode_step
+    ok = (FAKE, FAKE, FAKE, FAKE, FAKE, 8, 100, FAKE, 0.1, FAKE, FAKE, 1 << 30, None)
+    for i in range(4):
+        args = list(ok)
+        args[i] = None
+        assert st_(by, *args) == -1
+    args = list(ok)
+    args[3] = FAKE + 2  # t_k
+    assert st_(by, *args) == -1
+    args = list(ok)
+    args[2] = FAKE + 2  # n_new
+    assert st_(by, *args) == -1
+    args = list(ok)
+    args[5] = 7  # n_q not a multiple of n_kv
+    assert st_(by, *args) == -1
+    args = list(ok)
+    args[11] = need - 1  # workspace
+    assert st_(by, *args) == -3
+    short = _desc(s_sink=9, s_keep=180, s_flush=4)  # ring 183 = s_keep + s_flush - 1
+    assert st_(ctypes.byref(short), *ok) == -2
     # dequant: position before the sink end, past the table, bad sequence
     assert L.wushkv_dequant(by, 0, 3, 1, FAKE, FAKE, None) == -1
     assert L.wushkv_dequant(by, 0, 4, 4 * 64 + 1, FAKE, FAKE, None) == -1

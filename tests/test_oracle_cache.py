@@ -258,3 +258,67 @@ def test_chunk_attention_brute_force_causal():
     dec = cache.decode(q_last, tinv, 0.125)
     for b in range(B):
         assert np.array_equal(dec[b], out[b, int(n_tok[b]) - 1])
+
+
+def _brute_decode(cache, b, h, q_row, S, Q, scale):
+    """Softmax attention of one bf16 query over positions [0, S) of (b, h):
+    positions in [s_sink, Q) through their codes, the others at bf16, every
+    row rebuilt here from the stored codes and parameters."""
+    d = cache.d
+    qq = oracle.bf16_to_f32(q_row).astype(np.float64)
+    logits, rows = [], []
+    for p in range(S):
+        if cache.s_sink <= p < Q:
+            s, z = (float(oracle.f16_to_f32(x)) for x in cache.kp[b, h, p])
+            kr = s * cache.kc[b, h, p].astype(np.float64) + z
+            s, z = (float(oracle.f16_to_f32(x)) for x in cache.vp[b, h, p])
+            vr = s * cache.vc[b, h, p].astype(np.float64) + z
+        else:
+            kr = oracle.bf16_to_f32(cache.kbits[b, h, p]).astype(np.float64)
+            vr = oracle.bf16_to_f32(cache.vbits[b, h, p]).astype(np.float64)
+        logits.append(scale * float(qq @ kr))
+        rows.append(vr)
+    w = np.exp(np.array(logits) - max(logits))
+    return (w[:, None] * np.array(rows)).sum(axis=0) / w.sum()
+
+
+def test_decode_step_order_of_alg2():
+    # a run of single-token steps crossing flushes: each step's attention
+    # sees the positions its own flush quantises at bf16 (Alg. 2 quantises
+    # after step 5), and equals append + decode exactly on steps that flush
+    # nothing; the cache ends as after the plain appends
+    rng = np.random.default_rng(21)
+    B, H, G, d, n0, steps = 2, 1, 2, 64, 40, 14
+    k = _rand_bits(rng, (B, n0 + steps, H, d))
+    v = _rand_bits(rng, (B, n0 + steps, H, d))
+    tk = oracle.f32_to_bf16(np.eye(d, dtype=np.float32))[None]
+    tinv = np.eye(d, dtype=np.float32)[None]
+    kw = dict(batch=B, n_kv=H, d=d, bits=2, s_sink=4, s_keep=16, s_flush=8, kappa_k=0.96,
+              kappa_v=0.92, capacity=n0 + steps)
+    fused, plain = oracle.OracleCache(**kw), oracle.OracleCache(**kw)
+    for c in (fused, plain):
+        c.append(k[:, :n0], v[:, :n0], np.array([n0, n0 - 3]), tk)
+    flushes = 0
+    for t in range(steps):
+        n_new = np.array([1, t % 3 != 0])  # sequence 1 skips some steps
+        q = _rand_bits(rng, (B, H * G, d))
+        q_old, s_old = fused.quant_end.copy(), fused.seq_len.copy()
+        pos = s_old.copy()
+        kn = np.stack([k[b, pos[b], :] for b in range(B)])
+        vn = np.stack([v[b, pos[b], :] for b in range(B)])
+        got = oracle.decode_step(fused, kn, vn, n_new, tk, q, tinv, 0.125)
+        plain.append(kn[:, None], vn[:, None], n_new, tk)
+        ref = plain.decode(q, tinv, 0.125)
+        for a, b in zip(_state(fused), _state(plain)):
+            assert np.array_equal(a, b)
+        for b in range(B):
+            S = int(s_old[b] + n_new[b])
+            for g in range(G):
+                want = _brute_decode(fused, b, 0, q[b, g], S, int(q_old[b]), 0.125)
+                assert np.max(np.abs(got[b, g] - want)) < 1e-12
+            if fused.quant_end[b] == q_old[b]:
+                assert np.array_equal(got[b], ref[b])
+            else:
+                flushes += 1
+                assert not np.array_equal(got[b], ref[b])
+    assert flushes >= 2
