@@ -181,3 +181,31 @@ def test_step_llama_shaped(gpu):
                 say("  step %d (b=%d, h=%d) flushing: rel err vs oracle %.2e" % (t, b, h, e))
                 assert e <= TOL
     assert flushing >= 8
+
+
+@pytest.mark.parametrize("s_flush,codec", [(5, "pclip"), (3, "quest"), (8, "pclip")])
+def test_short_flushes_end_inside_value_words(gpu, s_flush, codec):
+    """Flushes of s_flush = 3 or 5 positions end inside value-code words (8
+    tokens each), so the short-flush quantiser (16 lanes per group) must
+    merge its codes with what the page holds; single-token appends and fused
+    steps alternate, over ragged sequences, and the caches stay bit-exact."""
+    rng = np.random.default_rng(400 + s_flush)
+    B, H, G, d = 3, 2, 4, 128
+    say("short flushes s_flush=%d codec=%s" % (s_flush, codec))
+    p = Pair(gpu, B, H, G, d, 2, 4, 16, s_flush, 0.96, 0.92, cap=400, seed=4, codec=codec)
+    k, v = _kv(rng, B, 60, H, d)
+    p.append(k, v, [60, 23, 0])
+    flushes = 0
+    for t in range(40):
+        n_new = [1, 1, 1 if t % 3 else 0]
+        k1, v1 = _kv(rng, B, 1, H, d)
+        q_old = p.mirror.quant_end.copy()
+        if t % 2:
+            p.step(k1[:, 0], v1[:, 0], n_new, _q(rng, B, H * G, d))
+        else:
+            p.append(k1, v1, n_new)
+            p.decode_check(_q(rng, B, H * G, d))
+        p.check_cache()
+        flushes += int(np.count_nonzero(p.mirror.quant_end != q_old))
+    say("  %d flushes" % flushes)
+    assert flushes >= 10
