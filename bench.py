@@ -486,32 +486,42 @@ def bench_prefill(torch, wk, synth, dev, args):
     nn = torch.full((B,), n, dtype=torch.int32, device=dev)
     reps = 10
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # each timed call appends into its own empty cache replica, back to back
+    # on the stream (no reset between calls), so that the time is the GPU's
+    replicas = {"pclip": [cache] + [cache.clone() for _ in range(reps - 1)],
+                "quest": [qcache] + [qcache.clone() for _ in range(reps - 1)]}
     calls = {
-        "norm_rope": (cache, lambda: wk.wushkv_append_norm_rope(cache, k_raw, v, nn, tk, table,
+        "norm_rope": ("pclip", lambda c: wk.wushkv_append_norm_rope(c, k_raw, v, nn, tk, table,
+                                                                    norm_eps=1e-6)),
+        "prenormed": ("pclip", lambda c: wk.wushkv_append(c, k, v, nn, tk)),
+        "quest": ("quest", lambda c: wk.wushkv_append_norm_rope(c, k_raw, v, nn, tk, table,
                                                                 norm_eps=1e-6)),
-        "prenormed": (cache, lambda: wk.wushkv_append(cache, k, v, nn, tk)),
-        "quest": (qcache, lambda: wk.wushkv_append_norm_rope(qcache, k_raw, v, nn, tk, table,
-                                                             norm_eps=1e-6)),
     }
+
+    def reset(cs):
+        for c in cs:
+            c.seq_len.zero_()
+            c.quant_end.zero_()
+        torch.cuda.synchronize()
+
     res = {}
-    for name, (cc, call) in calls.items():
+    for name, (kind, call) in calls.items():
+        cs = replicas[kind]
         times = []
-        for r in range(reps + 2):
-            cc.seq_len.zero_()
-            cc.quant_end.zero_()
-            torch.cuda.synchronize()
+        for rnd in range(3):
+            reset(cs)
             e0.record()
-            call()
+            for c in cs:
+                call(c)
             e1.record()
             torch.cuda.synchronize()
-            if r >= 2:
-                times.append(e0.elapsed_time(e1))
+            if rnd >= 1:
+                times.append(e0.elapsed_time(e1) / reps)
         # the same calls again, each kernel stamped by the library
+        reset(cs)
         wk.wushkv_timing_enable(16 * reps)
-        for r in range(reps):
-            cc.seq_len.zero_()
-            cc.quant_end.zero_()
-            call()
+        for c in cs:
+            call(c)
         torch.cuda.synchronize()
         cnt, tot = wk.wushkv_timing_read("append_kernel")
         fcnt, ftot = wk.wushkv_timing_read("append_flush")

@@ -72,13 +72,19 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
         blk_lo = a.s_sink + k * kPage;
         blk_hi = blk_lo + kPage;
     }
-    const int32_t lo = max(blk_lo, first), hi = min(blk_hi, s_new);
+    const bool do_new = (a.mode & kModeNew) != 0, do_flush = (a.mode & kModeFlush) != 0;
+    int32_t lo = max(blk_lo, first), hi = min(blk_hi, s_new);
+    if (!do_new) {
+        // a flush-only launch touches nothing but the ring positions that
+        // are due: [start_old, q_new) below s_old (an empty cache has none)
+        lo = max(lo, start_old);
+        hi = min(hi, min(s_old, q_new));
+    }
     if (lo >= hi) {
         commit_finish(a, b, arrived, s_new, q_new, tid);
         return;
     }
 
-    const bool do_new = (a.mode & kModeNew) != 0, do_flush = (a.mode & kModeFlush) != 0;
     // position p (lo <= p < hi) is: new if p >= s_old; quantised now if
     // start_old <= p < q_new; otherwise a window entry (sink, or ring if new).
     auto is_new = [&](int32_t p) { return p >= s_old; };
