@@ -59,6 +59,7 @@ struct DecodeArgs {
     int32_t n_kv, s_sink, win_slots, max_pages, n_pages;
     int32_t n_q;
     int32_t units_per_wave, n_page_splits, n_splits;
+    int32_t win_units;     // SHARE: 64-slot window units per window workgroup
     const uint16_t *q;     // bf16 queries (decode [batch][n_q][D]; chunks [batch][max_tok][n_q][D])
     const float *tinv;     // [n_kv][D][D] T_K^{-1}, row-major
     float scale;           // sm_scale log2(e)
@@ -952,16 +953,16 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
     } else {
         // ================================================ window slots
         // Workgroup n_page_splits + u owns window unit u (slots 64 u ..
-        // 64 u + 63), wave w its 16 slots 64 u + 16 w .. + 15 (SHARE: every
-        // wave all four 16-slot tiles of the unit, for its own rows, with an
-        // online softmax across them).  All of a tile's loads are issued
-        // together.
+        // 64 u + 63), wave w its 16 slots 64 u + 16 w .. + 15 (SHARE: the
+        // workgroup owns win_units consecutive units and every wave all their
+        // 16-slot tiles, for its own rows, with an online softmax across
+        // them).  All of a tile's loads are issued together.
         const int32_t ring = a.win_slots - a.s_sink;
         // the ring holds positions [q_hi, S); the oldest sits at ring index a0
         const int32_t a0 = S > q_hi ? (q_hi - a.s_sink) % ring : 0;
         const int32_t ring_live = S > q_hi ? S - q_hi : 0;
         const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;
-        const int32_t unit0 = (split - a.n_page_splits) * kPage;
+        const int32_t unit0 = (split - a.n_page_splits) * kPage * (SHARE ? a.win_units : 1);
         // fused step: the workgroup whose unit holds the new token's slot
         // writes the token and keeps it in LDS, at the end of wave 3's page
         // stage (its merge rows, written last, sit at the start)
@@ -970,7 +971,7 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
         static_assert(G * D * 4 + 8 * D <= M::kStageBytes, "the new token fits the page stage");
         if (a.n_new != nullptr && nn > 0) {
             const int32_t slot = s_old < a.s_sink ? s_old : ring_slot(s_old, a.s_sink, ring);
-            if (slot >= unit0 && slot < unit0 + kPage) {
+            if (slot >= unit0 && slot < unit0 + kPage * (SHARE ? a.win_units : 1)) {
                 new_slot = slot;
                 step_token<D>(a, b, h, slot, tok,
                               reinterpret_cast<float *>(lds + 3 * M::kWave + M::kStageBytes - 8 * D), tid);
@@ -1019,7 +1020,9 @@ __global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
         for (int nt = 0; nt < kNT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
         float m_run[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f};
         bool formed = FORM;
-        constexpr int kSub = SHARE ? 4 : 1;
+        // SHARE: every wave all 16-slot tiles of the workgroup's units, with
+        // an online softmax across them
+        const int kSub = SHARE ? 4 * a.win_units : 1;
         for (int st = 0; st < (rows_live ? kSub : 0); ++st) {
             const int32_t slot0 = unit0 + 16 * (SHARE ? st : wave);
             // this tile's live slots, one bit per slot (lanes 0..15)
@@ -1227,7 +1230,7 @@ __global__ void __launch_bounds__(D) decode_combine_kernel(const float *part, fl
 // ------------------------------------------------------------------ host
 
 struct DecodePlan {
-    int32_t units_per_wave, n_page_splits, n_splits;
+    int32_t units_per_wave, n_page_splits, n_splits, win_units;
     size_t qt_bytes, limb_bytes, aux_bytes, part_bytes;
 };
 
@@ -1311,26 +1314,33 @@ static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq
     // 16 pages per wave (when the work cannot fit one round, shorter waves
     // balance the last round better).
     const int64_t wunits = c->win_slots / kPage;
+    // Window workgroups: one per 64-slot unit, four waves on its four tiles;
+    // with shared work items (share) one per row for all units, since there
+    // every wave walks all the tiles anyway and the page runs then get the
+    // resident slots the other window workgroups would hold.
+    const int64_t win_units = rs.share ? wunits : 1;
+    const int64_t wwgs = (wunits + win_units - 1) / win_units;
     // With shared work items (share_items) the four waves of a workgroup
     // walk one run together, each for another token group: a workgroup row
     // is then a (sequence, four token groups, kv head) triple and a split
     // covers upw pages instead of 4 upw.
     const int64_t per_split = rs.share ? 1 : 4;
     const int64_t wg_rows = rs.share ? (int64_t)c->batch * ((rs.n_groups + 3) / 4) * c->n_kv_heads : heads;
-    const int64_t budget = resident_waves(c->head_dim, c->bits, G) - 4 * wg_rows * wunits;
+    const int64_t budget = resident_waves(c->head_dim, c->bits, G) - 4 * wg_rows * wwgs;
     const int64_t upw_max = rs.share ? 64 : 16;
     int64_t upw = 2;
     while (upw < upw_max && wg_rows * ((qpages + per_split * upw - 1) / (per_split * upw)) * 4 > budget) ++upw;
     int64_t psplits = (qpages + per_split * upw - 1) / (per_split * upw);
-    if (psplits + wunits > kMaxSplits) {
-        const int64_t room = kMaxSplits - wunits;
+    if (psplits + wwgs > kMaxSplits) {
+        const int64_t room = kMaxSplits - wwgs;
         if (room < 1) return false;
         upw = (qpages + per_split * room - 1) / (per_split * room);
         psplits = (qpages + per_split * upw - 1) / (per_split * upw);
     }
-    const int64_t splits = psplits + wunits;  // and one workgroup per window unit
+    const int64_t splits = psplits + wwgs;  // and the window workgroups
     if (splits > kMaxSplits || upw > 0x7FFFFFFF / 4 / kMaxSplits) return false;
     p.units_per_wave = (int32_t)upw;
+    p.win_units = (int32_t)win_units;
     p.n_page_splits = (int32_t)psplits;
     p.n_splits = (int32_t)splits;
     p.qt_bytes = ((size_t)rows_z * n_q * c->head_dim * 4 + 255) / 256 * 256;
@@ -1450,6 +1460,7 @@ static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok
     a.units_per_wave = p.units_per_wave;
     a.n_page_splits = p.n_page_splits;
     a.n_splits = p.n_splits;
+    a.win_units = p.win_units;
     a.q = q;
     a.tinv = t_k_inv;
     a.scale = sm_scale * kLog2e;
