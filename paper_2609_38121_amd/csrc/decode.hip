@@ -153,6 +153,11 @@ struct QueryIn {
                          (D / 4) * wave + 4 * (lane % kQuads);
 #pragma unroll
         for (int r = 0; r < kRr; ++r) t[r] = *reinterpret_cast<const f32x4 *>(T + (int64_t)r * D);
+        load_q(a, b, tg, h, S, tid);
+    }
+    // the raw queries only
+    __device__ __forceinline__ void load_q(const DecodeArgs &a, int b, int tg, int h, int32_t S, int tid)
+    {
         // one load per element, its address chosen first (a load in each of
         // two branches would leave the compiler waiting on both)
         const bool decode = a.max_tok == 1 && a.n_tok == nullptr;
@@ -243,6 +248,52 @@ __device__ void form_qt(const DecodeArgs &a, const QueryIn<D, G> &in, uint8_t *R
             *reinterpret_cast<f32x4 *>(qt + g * D + (D / 4) * wave + 4 * lane) =
                 f32x4{acc[g][0] * a.scale, acc[g][1] * a.scale, acc[g][2] * a.scale, acc[g][3] * a.scale};
     }
+    __syncthreads();
+}
+
+// form_qt on the fp32 matrix instructions, for decode_qt_kernel (which has
+// no pages to overlap and is bound by the products): q~ = q^T T^{-1} as a
+// (16 x D) x (D x D) product of 16x16x4 fp32 tiles, the G query rows padded
+// to 16 with zeros.  Wave w takes the output columns D/4 w .. D/4 w + D/4 - 1
+// (D/64 tiles of 16); lane l supplies A = q[l % 16][k0 + l / 16] and
+// B = T^{-1}[k0 + l / 16][n0 + l % 16] and holds the result rows
+// 4 (l / 16) .. + 3 of column n0 + l % 16.  The T^{-1} column entries of
+// all steps are requested at once.  Same contract as form_qt (q~ scaled,
+// fp32, into R; starts and ends with a barrier); the products are summed in
+// the matrix unit's order, so q~ may differ from form_qt's in the last bits.
+template <int D, int G>
+__device__ void form_qt_mfma(const DecodeArgs &a, int h, uint8_t *R, int tid)
+{
+    constexpr int kTiles = D / 64;   // 16-column tiles per wave
+    constexpr int kSteps = D / 4;    // k steps of 4
+    const uint16_t *qs = reinterpret_cast<const uint16_t *>(R);
+    const int lane = tid & 63, wave = tid >> 6;
+    const int m = lane & 15, kk = lane >> 4;
+    const float *T = a.tinv + (int64_t)h * D * D + (D / 4) * wave + m;
+    float bv[kTiles][kSteps];
+#pragma unroll
+    for (int t = 0; t < kTiles; ++t)
+#pragma unroll
+        for (int st = 0; st < kSteps; ++st) bv[t][st] = T[(int64_t)(4 * st + kk) * D + 16 * t];
+    __syncthreads();  // the staged queries
+    f32x4 acc[kTiles];
+#pragma unroll
+    for (int t = 0; t < kTiles; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < kSteps; ++st) {
+        const float av = m < G ? bf16_bits_to_f32(qs[m * D + 4 * st + kk]) : 0.0f;
+#pragma unroll
+        for (int t = 0; t < kTiles; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv[t][st], acc[t], 0, 0, 0);
+    }
+    __syncthreads();  // the raw queries are read
+    float *qt = reinterpret_cast<float *>(R);
+#pragma unroll
+    for (int t = 0; t < kTiles; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int row = 4 * kk + i;
+            if (row < G) qt[row * D + (D / 4) * wave + 16 * t + m] = acc[t][i] * a.scale;
+        }
     __syncthreads();
 }
 
@@ -353,9 +404,9 @@ __global__ void __launch_bounds__(256) decode_qt_kernel(DecodeArgs a)
     const int b = bz / a.n_groups, tg = bz % a.n_groups;
     const int32_t S = (a.max_tok == 1 && a.n_tok == nullptr) ? 0 : a.seq_len[b];
     QueryIn<D, G> in;
-    in.load(a, b, tg, h, S, tid);
+    in.load_q(a, b, tg, h, S, tid);
     stage_queries<D, G>(in, R, tid);
-    form_qt<D, G>(a, in, R, tid);
+    form_qt_mfma<D, G>(a, h, R, tid);
     const int64_t row0 = ((int64_t)bz * a.n_kv + h) * G;  // first (virtual) query head
     for (int i = tid; i < G * D / 4; i += 256)
         reinterpret_cast<f32x4 *>(a.qt + row0 * D)[i] = reinterpret_cast<const f32x4 *>(R)[i];
