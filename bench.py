@@ -687,13 +687,14 @@ def bench_wush(torch, wk, dev, args, layers=32, heads=8, d=128, gamma=1e-2, reps
 
 def bench_decode_scale(torch, wk, synth, dev, args, calls=24):
     """Decode calls alone on the long-context (131072 tokens, 2 and 4 bits,
-    random page order) and large-batch (64 ragged sequences of 16384-32768
-    tokens) caches.  The caches are filled by the library's own append from
+    random page order), large-batch (64 ragged sequences of 16384-32768
+    tokens) and Qwen3-32B-shaped (8 sequences of 8192 tokens, 64 query heads
+    on 8 kv heads) caches.  The caches are filled by the library's own append from
     seeded device-side Gaussian keys and values (throughput does not depend
     on the values); lengths are the workloads' own.  Replicas are cycled so
     that the calls touch more than twice the 256 MB Infinity Cache."""
     out = {}
-    for name in ("long2", "long4", "bigbatch"):
+    for name in ("long2", "long4", "bigbatch", "qwen32b"):
         cfg = synth.CONFIGS[name]
         w = synth.Workload(cfg, seed=args.seed)
         B, H, NQ, D, BITS = cfg["batch"], cfg["n_kv"], cfg["n_q"], cfg["d"], cfg["bits"]

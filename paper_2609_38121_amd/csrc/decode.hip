@@ -558,8 +558,10 @@ struct MainLds {
     static constexpr int kWave = kStageBytes + kTBytes;
     // Workgroups a compute unit keeps resident, as the variants' register
     // counts allow (three waves per SIMD at most; fewer for the 4-bit and
-    // the eight-head ones); it only decides the query rows' placement.
-    static constexpr int kResident = D == 128 ? (BITS == 2 ? 3 : (G == 8 ? 1 : 2))
+    // the eight-head ones: the 2-bit eight-head decode kernel is given two,
+    // and the registers of a third, so that its page loop does not spill);
+    // it only decides the query rows' placement.
+    static constexpr int kResident = D == 128 ? (BITS == 2 ? (G == 8 ? 2 : 3) : (G == 8 ? 1 : 2))
                                               : (BITS == 2 ? (G == 8 ? 3 : 4) : 3);
     // The query rows get LDS of their own when that keeps the residency:
     // the pages can then be in flight while the rows are formed.  Otherwise
@@ -614,7 +616,8 @@ __device__ void step_token(const DecodeArgs &a, int b, int h, int32_t slot, uint
 // HBM once per four token groups; grid z runs over (sequence, group of four
 // token groups) and every wave writes its own partials.
 template <int D, int BITS, int G, bool FORM, bool SHARE>
-__global__ void __launch_bounds__(256, 3) decode_main_kernel(DecodeArgs a)
+__global__ void __launch_bounds__(256, (D == 128 && BITS == 2 && G == 8 && !SHARE) ? 2 : 3)
+decode_main_kernel(DecodeArgs a)
 {
     static_assert(!(FORM && SHARE), "shared work items take q~ from decode_qt_kernel");
     using L = Layout<D, BITS>;
@@ -1286,39 +1289,41 @@ struct DecodePlan {
 };
 
 template <int D, int BITS, int G>
-static void main_kernel_ptr(const void *&f)
+static void main_kernel_ptr(const void *&f, bool share)
 {
-    f = reinterpret_cast<const void *>(&decode_main_kernel<D, BITS, G, true, false>);
+    if (share) f = reinterpret_cast<const void *>(&decode_main_kernel<D, BITS, G, false, true>);
+    else f = reinterpret_cast<const void *>(&decode_main_kernel<D, BITS, G, true, false>);
 }
 
 // Waves of decode_main_kernel the device keeps resident at once (its
 // occupancy from registers and LDS, times the compute units), cached per
-// variant; 256 compute units at three workgroups each when no device answers.
-static int64_t resident_waves(int D, int bits, int G)
+// variant: the query-forming one, or with share the shared-items one;
+// 256 compute units at three workgroups each when no device answers.
+static int64_t resident_waves(int D, int bits, int G, bool share)
 {
-    static int64_t cache[2][2][4] = {};
+    static int64_t cache[2][2][2][4] = {};
     const int di = D == 128, bi = bits == 4, gi = G == 1 ? 0 : G == 2 ? 1 : G == 4 ? 2 : 3;
-    int64_t &slot = cache[di][bi][gi];
+    int64_t &slot = cache[share][di][bi][gi];
     if (slot > 0) return slot;
     const void *f = nullptr;
     const int key = D * 100 + bits * 10 + gi;
     switch (key) {
-        case 12820: main_kernel_ptr<128, 2, 1>(f); break;
-        case 12821: main_kernel_ptr<128, 2, 2>(f); break;
-        case 12822: main_kernel_ptr<128, 2, 4>(f); break;
-        case 12823: main_kernel_ptr<128, 2, 8>(f); break;
-        case 12840: main_kernel_ptr<128, 4, 1>(f); break;
-        case 12841: main_kernel_ptr<128, 4, 2>(f); break;
-        case 12842: main_kernel_ptr<128, 4, 4>(f); break;
-        case 12843: main_kernel_ptr<128, 4, 8>(f); break;
-        case 6420: main_kernel_ptr<64, 2, 1>(f); break;
-        case 6421: main_kernel_ptr<64, 2, 2>(f); break;
-        case 6422: main_kernel_ptr<64, 2, 4>(f); break;
-        case 6423: main_kernel_ptr<64, 2, 8>(f); break;
-        case 6440: main_kernel_ptr<64, 4, 1>(f); break;
-        case 6441: main_kernel_ptr<64, 4, 2>(f); break;
-        case 6442: main_kernel_ptr<64, 4, 4>(f); break;
-        default: main_kernel_ptr<64, 4, 8>(f); break;
+        case 12820: main_kernel_ptr<128, 2, 1>(f, share); break;
+        case 12821: main_kernel_ptr<128, 2, 2>(f, share); break;
+        case 12822: main_kernel_ptr<128, 2, 4>(f, share); break;
+        case 12823: main_kernel_ptr<128, 2, 8>(f, share); break;
+        case 12840: main_kernel_ptr<128, 4, 1>(f, share); break;
+        case 12841: main_kernel_ptr<128, 4, 2>(f, share); break;
+        case 12842: main_kernel_ptr<128, 4, 4>(f, share); break;
+        case 12843: main_kernel_ptr<128, 4, 8>(f, share); break;
+        case 6420: main_kernel_ptr<64, 2, 1>(f, share); break;
+        case 6421: main_kernel_ptr<64, 2, 2>(f, share); break;
+        case 6422: main_kernel_ptr<64, 2, 4>(f, share); break;
+        case 6423: main_kernel_ptr<64, 2, 8>(f, share); break;
+        case 6440: main_kernel_ptr<64, 4, 1>(f, share); break;
+        case 6441: main_kernel_ptr<64, 4, 2>(f, share); break;
+        case 6442: main_kernel_ptr<64, 4, 4>(f, share); break;
+        default: main_kernel_ptr<64, 4, 8>(f, share); break;
     }
     int dev = 0, ncu = 0, blocks = 0;
     int64_t waves = 256 * 3 * 4;
@@ -1377,7 +1382,7 @@ static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq
     // covers upw pages instead of 4 upw.
     const int64_t per_split = rs.share ? 1 : 4;
     const int64_t wg_rows = rs.share ? (int64_t)c->batch * ((rs.n_groups + 3) / 4) * c->n_kv_heads : heads;
-    const int64_t budget = resident_waves(c->head_dim, c->bits, G) - 4 * wg_rows * wwgs;
+    const int64_t budget = resident_waves(c->head_dim, c->bits, G, rs.share) - 4 * wg_rows * wwgs;
     const int64_t upw_max = rs.share ? 64 : 16;
     int64_t upw = 2;
     while (upw < upw_max && wg_rows * ((qpages + per_split * upw - 1) / (per_split * upw)) * 4 > budget) ++upw;
@@ -1545,7 +1550,7 @@ static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok
     // that read once per workgroup, so a small kernel forms q~ first; so do
     // grids of shared work items.
     const int64_t wgs = (int64_t)p.n_splits * c->n_kv_heads * grid_z;
-    const bool form = !rs.share && wgs * 4 <= resident_waves(c->head_dim, c->bits, G);
+    const bool form = !rs.share && wgs * 4 <= resident_waves(c->head_dim, c->bits, G, false);
     const int key = c->head_dim * 10 + c->bits;
     switch (key) {
         case 1282: launch_main_g<128, 2>(G, form, rs.share, gm, rows_z, s, a); break;

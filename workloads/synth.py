@@ -31,6 +31,11 @@ CONFIGS = {
     "llama8b": dict(batch=8, n_kv=8, n_q=32, d=128, ctx=8192, bits=2, s_sink=4, s_keep=128,
                     s_flush=8, kappa_k=0.96, kappa_v=0.92, k_dist="gauss", outliers=8,
                     outlier_scale=10.0, v_outliers=False, rope_theta=5.0e5),
+    # Qwen3-32B-shaped decode layer: 64 query heads on 8 kv heads (eight per
+    # kv head), same cache recipe as the Llama-shaped one
+    "qwen32b": dict(batch=8, n_kv=8, n_q=64, d=128, ctx=8192, bits=2, s_sink=4, s_keep=128,
+                    s_flush=8, kappa_k=0.96, kappa_v=0.92, k_dist="gauss", outliers=8,
+                    outlier_scale=10.0, v_outliers=False, rope_theta=1.0e6),
     # long context, paged in random physical order
     "long2": dict(batch=1, n_kv=8, n_q=32, d=128, ctx=131072, bits=2, s_sink=4, s_keep=128,
                   s_flush=8, kappa_k=0.96, kappa_v=0.92, k_dist="gauss", outliers=8,
