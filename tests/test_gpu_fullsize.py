@@ -213,6 +213,18 @@ def test_llama8b_bench_configuration(gpu):
 
 
 @pytest.mark.timeout(600)
+def test_qwen32b_shaped_configuration(gpu):
+    """Batch 8, 64 q / 8 kv heads (eight query heads per kv head), d 128,
+    8192-token prefill, then four single-token steps: the 2-bit kernels built
+    for two workgroups per CU, with the query rows formed by their own launch
+    (the grid does not fit at once)."""
+    cfg = synth.CONFIGS["qwen32b"]
+    max_seq = cfg["ctx"] + 200 + 20 + 256
+    _run(gpu, "qwen32b", [(0, 0), (5, 6)], cap=max_seq, decode_len=max_seq, steps=4,
+         split_len=4 * max_seq)
+
+
+@pytest.mark.timeout(600)
 @pytest.mark.parametrize("name", ["long2", "long4"])
 def test_long_context_random_pages(gpu, name):
     """Batch 1, 131072 tokens in 64-token pages placed in random physical

@@ -48,7 +48,7 @@ def test_tiny_config_prefill_then_decode_steps(gpu):
 
 @pytest.mark.parametrize("d,bits,G,symmetric", [(128, 2, 4, True), (128, 4, 4, False),
                                                 (64, 2, 8, False), (64, 4, 1, True),
-                                                (128, 2, 2, False)])
+                                                (128, 2, 2, False), (128, 2, 8, False)])
 def test_ragged_batches(gpu, d, bits, G, symmetric):
     rng = np.random.default_rng(d * 10 + bits + G)
     B, H = 3, 2
