@@ -216,8 +216,9 @@ def test_llama8b_bench_configuration(gpu):
 def test_qwen32b_shaped_configuration(gpu):
     """Batch 8, 64 q / 8 kv heads (eight query heads per kv head), d 128,
     8192-token prefill, then four single-token steps: the 2-bit kernels built
-    for two workgroups per CU, with the query rows formed by their own launch
-    (the grid does not fit at once)."""
+    for two workgroups per CU.  The benchmark's plan fits the grid at once
+    (each workgroup forms its q~); the plan of a four times longer
+    max_seq_len does not (q~ from its own launch), and must agree with it."""
     cfg = synth.CONFIGS["qwen32b"]
     max_seq = cfg["ctx"] + 200 + 20 + 256
     _run(gpu, "qwen32b", [(0, 0), (5, 6)], cap=max_seq, decode_len=max_seq, steps=4,
