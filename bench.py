@@ -604,8 +604,10 @@ def bench_chunk(torch, wk, caches, reps, k1, tk, tinv, B, NQ, D, max_seq, sm, cf
     return {"tokens_per_call": B * T, "call_us": round(t * 1e6, 2),
             "query_tokens_per_s": round(B * T / t, 1), "bytes_per_call": int(byts),
             "gbps_algorithmic": round(byts / t / 1e9, 1),
-            "note": "16-token chunks on the 8192-token Llama-shaped cache; the cache is read "
-                    "once per group of two chunk tokens (8 virtual query heads per kv head)"}
+            "note": "16-token chunks on the 8192-token Llama-shaped cache; bytes_per_call counts "
+                    "the cache once.  Two chunk tokens x 4 query heads make a group of 8 virtual "
+                    "heads, and a workgroup's four waves walk one run of pages for four groups, "
+                    "so each page leaves HBM twice per call"}
 
 
 def bench_stream_read(torch, wk, dev, gib=2, reps=10):
