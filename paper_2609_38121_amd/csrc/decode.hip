@@ -643,7 +643,9 @@ decode_main_kernel(DecodeArgs a)
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int j = lane >> 4, n = lane & 15;
     // grid z: (sequence, token group) pairs; see DecodeArgs
-    const int split = blockIdx.x, h = blockIdx.y;
+    // grid x is the kv head: workgroups are handed to the eight XCDs in
+    // turn, so with eight kv heads each XCD's L2 holds one head's T_K^-1
+    const int h = blockIdx.x, split = blockIdx.y;
     const int n_quads = (a.n_groups + 3) / 4;  // SHARE: groups of four token groups
     const int b = SHARE ? (int)blockIdx.z / n_quads : (int)blockIdx.z / a.n_groups;
     const int tg = SHARE ? 4 * ((int)blockIdx.z % n_quads) + wave : (int)blockIdx.z % a.n_groups;
@@ -1416,7 +1418,7 @@ static void launch_main(bool form, bool share, dim3 grid, unsigned rows_z, hipSt
         launch("decode_main_kernel", decode_main_kernel<D, BITS, G, true, false>, grid, dim3(256), s, a);
         return;
     }
-    launch("decode_qt_kernel", decode_qt_kernel<D, BITS, G>, dim3(grid.y, rows_z), dim3(256), s, a);
+    launch("decode_qt_kernel", decode_qt_kernel<D, BITS, G>, dim3(grid.x, rows_z), dim3(256), s, a);
     if (share)
         launch("decode_main_kernel", decode_main_kernel<D, BITS, G, false, true>, grid, dim3(256), s, a);
     else
@@ -1542,7 +1544,7 @@ static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok
     // several token groups (a chunk of more tokens than one group holds):
     // the four waves of a workgroup take four of them over the same items
     const unsigned grid_z = rs.share ? (unsigned)(c->batch * ((rs.n_groups + 3) / 4)) : rows_z;
-    const dim3 gm(p.n_splits, c->n_kv_heads, grid_z);
+    const dim3 gm(c->n_kv_heads, p.n_splits, grid_z);
     const dim3 gc(c->n_kv_heads * G, rows_z);
     // Each workgroup forms q~ itself when the whole grid is resident at
     // once (one round: the rows cost each workgroup an L2 read of T^{-1}
