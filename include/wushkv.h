@@ -26,8 +26,12 @@
  *     patterns.
  *   - The caller owns all memory.  The library never allocates device memory
  *     on these paths, never frees and never synchronises; all work is
- *     enqueued on the caller's stream.  No call mutates library state, so
- *     calls on different streams with disjoint caches may run concurrently.
+ *     enqueued on the caller's stream.  The only library state the compute
+ *     calls touch is a per-variant cache of the decode kernel's occupancy,
+ *     filled on first use (thread-safe: racing first calls store the same
+ *     value); calls on different streams with disjoint caches may therefore
+ *     run concurrently.  The opt-in kernel timer (wushkv_timing_enable) is
+ *     global and not thread-safe.
  *   - Argument checks happen on the host before anything is enqueued; a
  *     failing check returns a negative status and enqueues nothing.
  *   - Device-resident values (seq_len, quant_end, n_new, page_table) cannot
@@ -264,6 +268,9 @@ int wushkv_append_norm_rope(const wushkv_cache *c,
  *
  * The query of sequence b attends to all positions [0, seq_len[b]): sink
  * and recent windows at bf16, the middle through the stored codes.
+ * Returns WUSHKV_EUNSUPPORTED (and the workspace size is 0) when max_seq_len
+ * would need a page run longer than 64 pages per wave, beyond about
+ * 16.7 M tokens (chunk attention: about 4.19 M).
  */
 int wushkv_decode_attention(const wushkv_cache *c,
                             const uint16_t *q, int32_t n_q_heads,
@@ -425,6 +432,11 @@ int wushkv_abi_version(void);
  */
 int wushkv_timing_enable(int32_t slots);
 int wushkv_timing_read(const char *name_substr, int32_t *count, double *total_ms);
+/* Launches recorded so far, and the kernel name and milliseconds of the
+ * index-th of them (synchronising on its events; WUSHKV_EINVAL for an index
+ * out of range). */
+int wushkv_timing_count(void);
+int wushkv_timing_launch(int32_t index, const char **name, double *ms);
 
 #ifdef __cplusplus
 }

@@ -35,7 +35,9 @@ def build(force: bool = True) -> str:
         return _LIB_PATH
     os.makedirs(os.path.dirname(_LIB_PATH), exist_ok=True)
     tmp = _LIB_PATH + ".tmp%d" % os.getpid()
-    cmd = ["gcc", "-std=c11", "-O2", "-ffp-contract=off", "-fno-fast-math",
+    # -fopenmp only spreads independent (sequence, head) pairs over threads
+    # (orc_*_heads_parallel); every pair's arithmetic is the serial code's
+    cmd = ["gcc", "-std=c11", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
            "-fPIC", "-shared", "-o", tmp, _SRC, "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(tmp, _LIB_PATH)
@@ -92,6 +94,10 @@ def _declare(L):
     L.orc_decode_head.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, _I32, _I32,
                                   _P, _P, _P, _P, _P, _P, _P, _P, _F32, _P]
     L.orc_decode_head.restype = None
+    L.orc_decode_heads_parallel.argtypes = [ctypes.c_int] * 5 + [_P] * 10 + [_F32, _P]
+    L.orc_decode_heads_parallel.restype = ctypes.c_int
+    L.orc_append_heads_parallel.argtypes = [ctypes.c_int] * 8 + [_F32] * 3 + [_P] * 13
+    L.orc_append_heads_parallel.restype = ctypes.c_int
 
 
 def _ptr(a: np.ndarray):
@@ -363,6 +369,71 @@ def decode_head(d, G, s_sink, S, q_end, kbits, vbits, kc, kp, vc, vp, q, tinv, s
     lib().orc_decode_head(d, G, s_sink, S, q_end, *[_ptr(a) for a in args],
                           float(sm_scale), _ptr(out))
     return out
+
+
+def _ptr_array(arrays):
+    return (ctypes.c_void_p * len(arrays))(*[a.ctypes.data for a in arrays])
+
+
+class HeadSet:
+    """Logical caches of independent (sequence, kv head) pairs for the
+    benchmark's CPU baseline: each pair is a one-sequence, one-head cache of
+    capacity ``caps[i]``, filled and decoded with orc_append_head and
+    orc_decode_head, the pairs spread over host threads (OpenMP).  Only the
+    threading differs from OracleCache; every pair's arithmetic is the same."""
+
+    def __init__(self, caps, d, bits, s_sink, s_keep, s_flush, kappa_k, kappa_v):
+        self.d, self.bits = d, bits
+        self.s_sink, self.s_keep, self.s_flush = s_sink, s_keep, s_flush
+        self.kappa_k, self.kappa_v = float(kappa_k), float(kappa_v)
+        self.caps = [int(c) for c in caps]
+        n = len(self.caps)
+        self.kbits = [np.zeros((c, d), np.uint16) for c in self.caps]
+        self.vbits = [np.zeros((c, d), np.uint16) for c in self.caps]
+        self.kc = [np.zeros((c, d), np.uint8) for c in self.caps]
+        self.vc = [np.zeros((c, d), np.uint8) for c in self.caps]
+        self.kp = [np.zeros((c, 2), np.uint16) for c in self.caps]
+        self.vp = [np.zeros((c, 2), np.uint16) for c in self.caps]
+        self.seq_len = np.zeros(n, np.int32)
+        self.quant_end = np.zeros(n, np.int32)
+
+    def append(self, k_new, v_new, tk, threads=0):
+        """k_new[i], v_new[i]: bf16 patterns [n_i][d] of pair i; tk[i]: bf16
+        [d][d].  Returns the threads used."""
+        n = len(self.caps)
+        k_new = [np.ascontiguousarray(k, np.uint16) for k in k_new]
+        v_new = [np.ascontiguousarray(v, np.uint16) for v in v_new]
+        tk = [np.ascontiguousarray(t, np.uint16) for t in tk]
+        n_new = np.array([k.shape[0] for k in k_new], np.int32)
+        assert np.all(self.seq_len + n_new <= np.array(self.caps)), "capacity exceeded"
+        q_new = np.zeros(n, np.int32)
+        used = lib().orc_append_heads_parallel(
+            n, threads, self.d, self.bits, self.s_sink, self.s_keep, self.s_flush, 0,
+            self.kappa_k, self.kappa_v, 0.0, _ptr(self.seq_len.copy()), _ptr(self.quant_end.copy()),
+            _ptr(n_new), _ptr_array(k_new), _ptr_array(v_new), _ptr_array(tk),
+            _ptr_array(self.kbits), _ptr_array(self.vbits), _ptr_array(self.kc),
+            _ptr_array(self.kp), _ptr_array(self.vc), _ptr_array(self.vp), _ptr(q_new))
+        self.seq_len += n_new
+        self.quant_end[:] = q_new
+        return used
+
+    def decode(self, q, tinv, sm_scale, threads=0, pairs=None):
+        """q[i]: bf16 patterns [G][d] of pair i; tinv[i]: fp32 [d][d].
+        Returns (fp64 outputs [n][G][d], threads used).  ``pairs`` restricts
+        the call to those indices."""
+        idx = list(range(len(self.caps))) if pairs is None else list(pairs)
+        q = [np.ascontiguousarray(q[i], np.uint16) for i in idx]
+        tinv = [np.ascontiguousarray(tinv[i], np.float32) for i in idx]
+        G = q[0].shape[0]
+        out = [np.empty((G, self.d), np.float64) for _ in idx]
+        S = np.ascontiguousarray(self.seq_len[idx])
+        Q = np.ascontiguousarray(self.quant_end[idx])
+        pick = lambda arrs: _ptr_array([arrs[i] for i in idx])
+        used = lib().orc_decode_heads_parallel(
+            len(idx), threads, self.d, G, self.s_sink, _ptr(S), _ptr(Q), pick(self.kbits),
+            pick(self.vbits), pick(self.kc), pick(self.kp), pick(self.vc), pick(self.vp),
+            _ptr_array(q), _ptr_array(tinv), float(sm_scale), _ptr_array(out))
+        return np.stack(out), used
 
 
 def attend(q, K, V, scale: float) -> np.ndarray:

@@ -33,6 +33,7 @@
  * project's design notes and repeated at each function below.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -420,4 +421,63 @@ void orc_decode_head(int d, int G, int s_sink, int32_t S, int32_t q_end,
     }
     free(K);
     free(V);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Many (sequence, kv-head) pairs at once, for the benchmark's CPU baseline.  */
+/* ------------------------------------------------------------------------ */
+
+/* The pairs are independent (Eq. (2) attends within one kv head of one
+ * sequence), so they are spread over `threads` host threads (OpenMP,
+ * threads <= 0: the runtime's default); each pair is exactly
+ * orc_decode_head, so the arithmetic is unchanged.  Array arguments hold one
+ * pointer per pair, laid out as orc_decode_head takes them.  Returns the
+ * number of threads that ran. */
+int orc_decode_heads_parallel(int n_pairs, int threads, int d, int G, int s_sink,
+                              const int32_t *S, const int32_t *q_end,
+                              const uint16_t *const *kbits, const uint16_t *const *vbits,
+                              const uint8_t *const *kc, const uint16_t *const *kp,
+                              const uint8_t *const *vc, const uint16_t *const *vp,
+                              const uint16_t *const *q, const float *const *tinv,
+                              float sm_scale, double *const *out)
+{
+    int used = 1;
+    int nt = threads > 0 ? threads : omp_get_max_threads();
+#pragma omp parallel num_threads(nt)
+    {
+#pragma omp single
+        used = omp_get_num_threads();
+#pragma omp for schedule(dynamic, 1)
+        for (int i = 0; i < n_pairs; ++i)
+            orc_decode_head(d, G, s_sink, S[i], q_end[i], kbits[i], vbits[i], kc[i], kp[i],
+                            vc[i], vp[i], q[i], tinv[i], sm_scale, out[i]);
+    }
+    return used;
+}
+
+/* orc_append_head for many pairs, in parallel over the pairs (each pair's
+ * own arguments as orc_append_head takes them; n_new[i] keys at k_new[i]
+ * with row stride d).  q_new[i] receives the pair's new S_quant. */
+int orc_append_heads_parallel(int n_pairs, int threads, int d, int bits, int s_sink, int s_keep,
+                              int s_flush, int codec, float kappa_k, float kappa_v, float alpha,
+                              const int32_t *s_old, const int32_t *q_old, const int32_t *n_new,
+                              const uint16_t *const *k_new, const uint16_t *const *v_new,
+                              const uint16_t *const *tk,
+                              uint16_t *const *kbits, uint16_t *const *vbits,
+                              uint8_t *const *kc, uint16_t *const *kp,
+                              uint8_t *const *vc, uint16_t *const *vp, int32_t *q_new)
+{
+    int used = 1;
+    int nt = threads > 0 ? threads : omp_get_max_threads();
+#pragma omp parallel num_threads(nt)
+    {
+#pragma omp single
+        used = omp_get_num_threads();
+#pragma omp for schedule(dynamic, 1)
+        for (int i = 0; i < n_pairs; ++i)
+            q_new[i] = orc_append_head(d, bits, s_sink, s_keep, s_flush, codec, kappa_k, kappa_v,
+                                       alpha, s_old[i], q_old[i], n_new[i], k_new[i], d, v_new[i],
+                                       d, tk[i], kbits[i], vbits[i], kc[i], kp[i], vc[i], vp[i]);
+    }
+    return used;
 }

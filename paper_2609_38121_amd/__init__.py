@@ -23,7 +23,7 @@ __all__ = [
     "WushKVCache", "WushKVError", "wushkv_append", "wushkv_decode_attention", "wushkv_decode_step",
     "wushkv_decode_workspace_bytes", "wushkv_dequant", "wushkv_page_bytes",
     "wushkv_status_string", "wushkv_abi_version", "wushkv_timing_enable",
-    "wushkv_timing_read", "wushkv_quest_alpha", "wushkv_wush_transform", "wushkv_read_probe",
+    "wushkv_timing_read", "wushkv_timing_launches", "wushkv_quest_alpha", "wushkv_wush_transform", "wushkv_read_probe",
     "PAGE_TOKENS",
     "header_functions",
 ]
@@ -74,6 +74,19 @@ def wushkv_timing_read(name_substr: str = ""):
     check(_lib.lib().wushkv_timing_read(name_substr.encode(), ctypes.byref(cnt),
                                         ctypes.byref(ms)), "wushkv_timing_read")
     return cnt.value, ms.value
+
+
+def wushkv_timing_launches():
+    """[(kernel name, milliseconds)] of every launch recorded since timing
+    was enabled, in launch order."""
+    L = _lib.lib()
+    out = []
+    name = ctypes.c_char_p()
+    ms = ctypes.c_double()
+    for i in range(L.wushkv_timing_count()):
+        check(L.wushkv_timing_launch(i, ctypes.byref(name), ctypes.byref(ms)), "wushkv_timing_launch")
+        out.append((name.value.decode(), ms.value))
+    return out
 
 
 class WushKVCache:

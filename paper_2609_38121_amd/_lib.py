@@ -104,6 +104,11 @@ def _declare(L):
     L.wushkv_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(I32),
                                      ctypes.POINTER(ctypes.c_double)]
     L.wushkv_timing_read.restype = ctypes.c_int
+    L.wushkv_timing_count.argtypes = []
+    L.wushkv_timing_count.restype = ctypes.c_int
+    L.wushkv_timing_launch.argtypes = [I32, ctypes.POINTER(ctypes.c_char_p),
+                                       ctypes.POINTER(ctypes.c_double)]
+    L.wushkv_timing_launch.restype = ctypes.c_int
 
 
 def header_functions() -> list[str]:

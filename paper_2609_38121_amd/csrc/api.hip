@@ -174,3 +174,17 @@ extern "C" int wushkv_timing_read(const char *name_substr, int32_t *count, doubl
     }
     return WUSHKV_OK;
 }
+
+extern "C" int wushkv_timing_launch(int32_t index, const char **name, double *ms)
+{
+    Timing &t = g_timing;
+    if (!name || !ms || index < 0 || index >= t.used) return WUSHKV_EINVAL;
+    if (hipEventSynchronize(t.ev[2 * index + 1]) != hipSuccess) return WUSHKV_ELAUNCH;
+    float f = 0.0f;
+    if (hipEventElapsedTime(&f, t.ev[2 * index], t.ev[2 * index + 1]) != hipSuccess) return WUSHKV_ELAUNCH;
+    *name = t.names[index];
+    *ms = f;
+    return WUSHKV_OK;
+}
+
+extern "C" int wushkv_timing_count(void) { return g_timing.used; }

@@ -35,6 +35,7 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
     __shared__ __attribute__((aligned(16))) uint16_t kt[kPage * kPitch];
     __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * kPitch];
     __shared__ int32_t sh_page[2];  // page index, reduction word
+    __shared__ int32_t sh_cnt[3];   // the sequence's counters (read_counters)
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -50,10 +51,8 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
     const int h = (int)((turn % hbs) % gridDim.y), b = (int)((turn % hbs) / gridDim.y);
 
     // ---- per-sequence bookkeeping (identical in every workgroup)
-    const int32_t s_old = a.seq_len[b];
-    const int32_t q_old = a.quant_end[b];
-    int32_t nn = a.n_new[b];
-    nn = nn < 0 ? 0 : (nn > a.max_new ? a.max_new : nn);
+    const SeqCounters cnt = read_counters(a, b, a.max_new, sh_cnt, tid);
+    const int32_t s_old = cnt.s_old, q_old = cnt.q_old, nn = cnt.nn;
     const int32_t s_new = s_old + nn;
     const int32_t q_new = next_quant_end(s_new, q_old, a.s_sink, a.s_keep, a.s_flush);
     const int32_t arrived = commit_arrive(a, b, s_old, q_old, nn, tid);
@@ -105,7 +104,6 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
     }
 
     const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;  // win_k row base (slots)
-    const uint16_t *tk_h = a.tk + (int64_t)h * D * D;
 
     // new values of this tile: loaded first, so that their latency overlaps
     // the key transform (idx = tid + 256 q is row idx / kVec, 16-byte chunk
@@ -157,32 +155,24 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
             }
             __syncthreads();
         }
-        bf16x8 bop[kNtW][L::kChunks];
-#pragma unroll
-        for (int nt = 0; nt < kNtW; ++nt) {
-            const int o = (wave * kNtW + nt) * 16 + n;
-#pragma unroll
-            for (int c = 0; c < L::kChunks; ++c)
-                bop[nt][c] = *reinterpret_cast<const bf16x8 *>(tk_h + (int64_t)o * D + 32 * c + 8 * j);
-        }
+        KeyTile<D, kNtW> xf;
+        xf.load(a.tk, h, wave * kNtW, lane);
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) {
             const int r = 16 * mt + n;  // A row handled by this lane
             const int32_t p = blk_lo + r;
             const bool ld = (p >= lo && p < hi && is_new(p) && do_new);
             const uint16_t *krow = a.k_new + (((int64_t)b * a.max_new + (p - s_old)) * a.n_kv + h) * D;
-            f32x4 acc[kNtW];
-#pragma unroll
-            for (int nt = 0; nt < kNtW; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            bf16x8 aop[L::kChunks];
 #pragma unroll
             for (int c = 0; c < L::kChunks; ++c) {
                 u32x4 av = {0u, 0u, 0u, 0u};
                 if constexpr (fused) av = *reinterpret_cast<const u32x4 *>(vt + r * kPitch + 32 * c + 8 * j);
                 else if (ld) av = *reinterpret_cast<const u32x4 *>(krow + 32 * c + 8 * j);
-                bf16x8 aop = __builtin_bit_cast(bf16x8, av);
-#pragma unroll
-                for (int nt = 0; nt < kNtW; ++nt) acc[nt] = mfma16(aop, bop[nt][c], acc[nt]);
+                aop[c] = __builtin_bit_cast(bf16x8, av);
             }
+            f32x4 acc[kNtW];
+            xf.apply(aop, acc);
 #pragma unroll
             for (int nt = 0; nt < kNtW; ++nt) {
                 const int ch = (wave * kNtW + nt) * 16 + n;
@@ -264,14 +254,15 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a)
 }
 
 // Appends of at most kStepMax tokens per sequence (decode steps): one
-// workgroup per (kv head, sequence).  The new keys are transformed as
-// matrix-vector products (each thread one output channel over D / kParts
-// inputs, the parts summed across neighbouring lanes, fp32, rounded once to
-// bf16) into LDS; then the newly eligible positions are quantised page by
-// page from the ring or from those new rows (quantise_tile); last, the new
-// tokens that stay bf16 are written to the windows.  Reading the flushed
-// ring slots before writing the new ones makes the order independent of the
-// ring's length.
+// workgroup per (kv head, sequence).  The new keys form one 16-row tile of
+// the key transform (KeyTile, the prefill's own operand order: wave w takes
+// output channels w D/4 .. w D/4 + D/4 - 1; with the fused normalisation
+// and RoPE each wave first applies norm_rope_row to the rows, as the
+// prefill does), rounded once to bf16 into LDS; then the newly eligible
+// positions are quantised page by page from the ring or from those new rows
+// (quantise_tile); last, the new tokens that stay bf16 are written to the
+// windows.  Reading the flushed ring slots before writing the new ones makes
+// the order independent of the ring's length.
 constexpr int kStepMax = 16;
 
 template <int D, int BITS>
@@ -279,21 +270,18 @@ __global__ void __launch_bounds__(256) append_step_kernel(AppendArgs a)
 {
     using L = Layout<D, BITS>;
     constexpr int kPitch = D + 8;
-    constexpr int kParts = KeyTransform<D>::kParts;  // threads per output channel
+    constexpr int kNtW = D / 64;  // 16-channel output tiles per wave
     __shared__ __attribute__((aligned(16))) uint16_t kn[kStepMax * kPitch];
     __shared__ __attribute__((aligned(16))) uint16_t kt[kPage * kPitch];
     __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * kPitch];
-    __shared__ float kin[D];
-    __shared__ float kin2[D];
-    __shared__ float red4[4];
     __shared__ int32_t sh_page[2];  // page index, reduction word
+    __shared__ int32_t sh_cnt[3];   // the sequence's counters (read_counters)
 
     const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
     const int h = blockIdx.x, b = blockIdx.y;
-    const int32_t s_old = a.seq_len[b];
-    const int32_t q_old = a.quant_end[b];
-    int32_t nn = a.n_new[b];
-    nn = nn < 0 ? 0 : (nn > a.max_new ? a.max_new : nn);
+    const SeqCounters cnt = read_counters(a, b, a.max_new, sh_cnt, tid);
+    const int32_t s_old = cnt.s_old, q_old = cnt.q_old, nn = cnt.nn;
     const int32_t s_new = s_old + nn;
     const int32_t q_new = next_quant_end(s_new, q_old, a.s_sink, a.s_keep, a.s_flush);
     const int32_t arrived = commit_arrive(a, b, s_old, q_old, nn, tid);
@@ -304,47 +292,52 @@ __global__ void __launch_bounds__(256) append_step_kernel(AppendArgs a)
         return base + (((int64_t)b * a.max_new + (p - s_old)) * a.n_kv + h) * D;
     };
 
-    // ---- transformed new keys -> kn
-    const int o = tid / kParts, part = tid % kParts;
-    KeyTransform<D> xf;
-    xf.load(a.tk, h, tid);
-    for (int t = 0; t < nn; ++t) {
-        if (tid < D) kin[tid] = bf16_bits_to_f32(new_row(a.k_new, s_old + t)[tid]);
-        __syncthreads();
+    // ---- transformed new keys -> kn (row t: new token t)
+    if (nn > 0) {
+        const int j = lane >> 4, n = lane & 15;
+        KeyTile<D, kNtW> xf;
+        xf.load(a.tk, h, wave * kNtW, lane);
+        const bool ld = n < nn;
+        const uint16_t *krow = new_row(a.k_new, s_old + (ld ? n : 0));
+        bf16x8 aop[L::kChunks];
+        u32x4 av[L::kChunks];
+#pragma unroll
+        for (int c = 0; c < L::kChunks; ++c) {
+            av[c] = u32x4{0u, 0u, 0u, 0u};
+            if (ld) av[c] = *reinterpret_cast<const u32x4 *>(krow + 32 * c + 8 * j);
+        }
         if (a.rope != nullptr) {
-            // RoPE(Norm(k)) of this key (same fp32 steps as norm_rope_row):
-            // the mean square over D channels, then each thread j < D/2
-            // rotates the pair (j, j + D/2) and rounds it to bf16
-            float sq = tid < D ? kin[tid] * kin[tid] : 0.0f;
+            // RoPE(Norm(k)) of row n, rounded to bf16: the prefill's phase A0
+            float x[L::kChunks][8];
 #pragma unroll
-            for (int off = 32; off > 0; off >>= 1) sq += __shfl_xor(sq, off);
-            if ((tid & 63) == 0) red4[tid >> 6] = sq;
-            __syncthreads();
-            float ss = 0.0f;
+            for (int c = 0; c < L::kChunks; ++c)
 #pragma unroll
-            for (int w = 0; w < 4; ++w) ss += red4[w];
-            const float r = 1.0f / sqrtf(ss / (float)D + a.eps);
-            if (tid < D / 2) {
-                const float g0 = a.gain ? a.gain[tid] : 1.0f, g1 = a.gain ? a.gain[tid + D / 2] : 1.0f;
-                const float lo = (kin[tid] * r) * g0, hi = (kin[tid + D / 2] * r) * g1;
-                const float *row = a.rope + (int64_t)(s_old + t) * D;
-                const float co = row[tid], si = row[tid + D / 2];
-                const uint32_t pk = pack_bf16_rne(lo * co - hi * si, hi * co + lo * si);
-                kin2[tid] = bf16_bits_to_f32(pk & 0xFFFFu);
-                kin2[tid + D / 2] = bf16_bits_to_f32(pk >> 16);
+                for (int e = 0; e < 8; ++e) x[c][e] = bf16_bits_to_f32((av[c][e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
+            norm_rope_row<D>(x, j, ld ? s_old + n : 0, a);
+#pragma unroll
+            for (int c = 0; c < L::kChunks; ++c)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) av[c][q] = ld ? pack_bf16_rne(x[c][2 * q], x[c][2 * q + 1]) : 0u;
+        }
+#pragma unroll
+        for (int c = 0; c < L::kChunks; ++c) aop[c] = __builtin_bit_cast(bf16x8, av[c]);
+        f32x4 acc[kNtW];
+        xf.apply(aop, acc);
+#pragma unroll
+        for (int nt = 0; nt < kNtW; ++nt) {
+            const int o = (wave * kNtW + nt) * 16 + n;
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) {
+                const int t = 4 * j + rr;
+                if (t < nn) {
+                    const uint16_t kb = (uint16_t)(pack_bf16_rne(acc[nt][rr], 0.0f) & 0xFFFFu);
+                    kn[t * kPitch + o] = kb;
+                    if (a.k_tilde_out != nullptr) new_row(a.k_tilde_out, s_old + t)[o] = kb;
+                }
             }
-            __syncthreads();
-            if (tid < D) kin[tid] = kin2[tid];
-            __syncthreads();
         }
-        const float acc = xf.sum(kin, tid);
-        if (part == 0) {
-            const uint16_t kb = (uint16_t)(pack_bf16_rne(acc, 0.0f) & 0xFFFFu);
-            kn[t * kPitch + o] = kb;
-            if (a.k_tilde_out != nullptr) new_row(a.k_tilde_out, s_old + t)[o] = kb;
-        }
-        __syncthreads();
     }
+    __syncthreads();
 
     // ---- quantise [start_old, q_new), one page at a time
     if (start_old < q_new)
@@ -400,7 +393,7 @@ __global__ void __launch_bounds__(256) step_finish_kernel(AppendArgs a, FinishAr
     __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * kPitch];
     __shared__ float fw[kMaxSplits];
     __shared__ float red[D];
-    __shared__ int32_t sh[2];
+    __shared__ int32_t sh[5];  // page index, reduction word, the counters (read_counters)
     const int tid = threadIdx.x, b = blockIdx.y;
     const int n_q = a.n_kv * f.G;
     if ((int)blockIdx.x < n_q) {
@@ -411,10 +404,8 @@ __global__ void __launch_bounds__(256) step_finish_kernel(AppendArgs a, FinishAr
         return;
     }
     const int h = (int)blockIdx.x - n_q;
-    const int32_t s_old = a.seq_len[b];
-    const int32_t q_old = a.quant_end[b];
-    int32_t nn = a.n_new[b];
-    nn = nn < 0 ? 0 : (nn > 1 ? 1 : nn);
+    const SeqCounters cnt = read_counters(a, b, 1, sh + 2, tid);
+    const int32_t s_old = cnt.s_old, q_old = cnt.q_old, nn = cnt.nn;
     const int32_t s_new = s_old + nn;
     const int32_t q_new = next_quant_end(s_new, q_old, a.s_sink, a.s_keep, a.s_flush);
     const int32_t arrived = commit_arrive(a, b, s_old, q_old, nn, tid);

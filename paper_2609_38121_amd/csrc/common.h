@@ -164,46 +164,39 @@ __device__ __forceinline__ f32x4 mfma16h(f16x8 a, f16x8 b, f32x4 c)
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
 
-// k~ = T_K k for one key (Alg. 2 step 3) on a 256-thread workgroup: output
-// channel o = tid / kParts is summed by kParts = 256 / D neighbouring
-// threads, thread part `part` over inputs part kIn .. part kIn + kIn - 1
-// (kIn = D / kParts) in fp32 fused multiply-adds in index order; the parts
-// are then added across the neighbours (key_transform_sum) and the sum is
-// rounded once to bf16.  Every path that forms k~ uses these two steps, so
-// a token's k~ does not depend on which kernel formed it.
-template <int D>
-struct KeyTransform {
-    static constexpr int kParts = 256 / D;
-    static constexpr int kIn = D / kParts;
-    uint32_t trow[kIn / 2];  // this thread's T_K entries, bf16 pairs
-    // T_K row o (bf16 [D][D] of head h, row-major), this thread's part
-    __device__ __forceinline__ void load(const uint16_t *tk, int h, int tid)
+// k~ = T_K k (Alg. 2 step 3) for a tile of up to 16 key rows on the
+// 16x16x32 bf16 matrix instruction.  Lane (j, n) of a wave supplies row n's
+// channels 32 c + 8 j .. 32 c + 8 j + 7 (aop[c], c < D / 32) and, from
+// load(), the T_K rows of output channels 16 (nt0 + nt) + n over the same
+// channels (bop[nt][c]).  apply() accumulates the D / 32 chunks in chunk
+// order from zero in fp32; row 4 j + r, output channel 16 (nt0 + nt) + n
+// ends in acc[nt][r], and the caller rounds it once to bf16.  Each output
+// element depends only on its own row and column, and every path that forms
+// k~ (the prefill tiles, short appends and the fused decode step) goes
+// through this with the key in the same operand positions, so a token's k~
+// does not depend on the path that formed it.
+template <int D, int NT>
+struct KeyTile {
+    static constexpr int kC = D / 32;
+    bf16x8 bop[NT][kC];
+    __device__ __forceinline__ void load(const uint16_t *tk, int h, int nt0, int lane)
     {
-        const int o = tid / kParts, part = tid % kParts;
-        const uint16_t *src = tk + ((int64_t)h * D + o) * D + part * kIn;
+        const int j = lane >> 4, n = lane & 15;
 #pragma unroll
-        for (int q = 0; q < kIn / 8; ++q) {
-            const uint4 v = *reinterpret_cast<const uint4 *>(src + 8 * q);
-            trow[4 * q + 0] = v.x;
-            trow[4 * q + 1] = v.y;
-            trow[4 * q + 2] = v.z;
-            trow[4 * q + 3] = v.w;
+        for (int nt = 0; nt < NT; ++nt) {
+            const uint16_t *row = tk + ((int64_t)h * D + 16 * (nt0 + nt) + n) * D + 8 * j;
+#pragma unroll
+            for (int c = 0; c < kC; ++c) bop[nt][c] = *reinterpret_cast<const bf16x8 *>(row + 32 * c);
         }
     }
-    // the channel's fp32 sum over the whole key kin[0..D) (every thread of
-    // the channel gets it)
-    __device__ __forceinline__ float sum(const float *kin, int tid) const
+    __device__ __forceinline__ void apply(const bf16x8 (&aop)[kC], f32x4 (&acc)[NT]) const
     {
-        const int part = tid % kParts;
-        float acc = 0.0f;
 #pragma unroll
-        for (int i = 0; i < kIn / 2; ++i) {
-            acc = fmaf(bf16_bits_to_f32(trow[i] & 0xFFFFu), kin[part * kIn + 2 * i], acc);
-            acc = fmaf(bf16_bits_to_f32(trow[i] >> 16), kin[part * kIn + 2 * i + 1], acc);
-        }
+        for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int off = 1; off < kParts; off <<= 1) acc += __shfl_xor(acc, off);
-        return acc;
+        for (int c = 0; c < kC; ++c)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) acc[nt] = mfma16(aop[c], bop[nt][c], acc[nt]);
     }
 };
 

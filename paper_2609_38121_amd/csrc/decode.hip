@@ -3,8 +3,10 @@
 // compensation q~ = q^T T_K^{-1} of Eq. (3).
 //
 // Two launches on the caller's stream:
-//   decode_main_kernel     grid (splits, kv heads, batch), four waves per
-//                          workgroup.  Each workgroup first forms q~ for its
+//   decode_main_kernel     grid (kv heads, splits, rows: a row is a sequence,
+//                          or a sequence's token group for chunks), four
+//                          waves per workgroup; the kv head on x deals each
+//                          head to one XCD.  Each workgroup first forms q~ for its
 //                          query heads in LDS, scaled by sm_scale log2(e) so
 //                          that the softmax runs in base 2, together with the
 //                          form the quantised-key product consumes: q~ in
@@ -39,6 +41,8 @@
 // rows (head, part) of 16x16x32 bf16 products against the key slots; the
 // probabilities, again split hi + lo, go through LDS into a 16x16x16 bf16
 // P V product against the channel-major value slots.
+#include <atomic>
+
 #include "common.h"
 #include "merge.h"
 
@@ -574,32 +578,40 @@ struct MainLds {
 };
 
 // Fused step: the new token of (sequence b, kv head h) into window slot
-// `slot`.  k~ = T_K k is formed with the append's arithmetic (KeyTransform),
-// so the stored key does not depend on the path that formed it; k~ and v
-// go to the windows and to tok (LDS: bf16 k~ [D], then v [D]); kin is D
-// floats of LDS.  Every thread of the workgroup calls it; it ends with a
-// barrier.
+// `slot`.  k~ = T_K k is formed as the appends form it (KeyTile, the key in
+// operand row 0; wave w takes output channels w D/4 .. w D/4 + D/4 - 1), so
+// the stored key does not depend on the path that formed it; k~ and v go to
+// the windows and to tok (LDS: bf16 k~ [D], then v [D]).  Every thread of
+// the workgroup calls it; it ends with a barrier.
 template <int D>
-__device__ void step_token(const DecodeArgs &a, int b, int h, int32_t slot, uint16_t *tok,
-                           float *kin, int tid)
+__device__ void step_token(const DecodeArgs &a, int b, int h, int32_t slot, uint16_t *tok, int tid)
 {
-    using X = KeyTransform<D>;
-    X xf;
-    xf.load(a.t_k, h, tid);
+    constexpr int kNtW = D / 64;
+    constexpr int kC = D / 32;
+    const int lane = tid & 63, wave = tid >> 6, j = lane >> 4, n = lane & 15;
+    KeyTile<D, kNtW> xf;
+    xf.load(a.t_k, h, wave * kNtW, lane);
     const int64_t row = ((int64_t)b * a.n_kv + h) * D;
-    uint16_t v = 0;
-    if (tid < D) {
-        kin[tid] = bf16_bits_to_f32(a.k_new[row + tid]);
-        v = a.v_new[row + tid];
+    bf16x8 aop[kC];
+#pragma unroll
+    for (int c = 0; c < kC; ++c) {
+        u32x4 av = {0u, 0u, 0u, 0u};
+        if (n == 0) av = *reinterpret_cast<const u32x4 *>(a.k_new + row + 32 * c + 8 * j);
+        aop[c] = __builtin_bit_cast(bf16x8, av);
     }
-    __syncthreads();
-    const float acc = xf.sum(kin, tid);
+    uint16_t v = 0;
+    if (tid < D) v = a.v_new[row + tid];
+    f32x4 acc[kNtW];
+    xf.apply(aop, acc);
     const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;
-    if (tid % X::kParts == 0) {
-        const int o = tid / X::kParts;
-        const uint16_t kb = (uint16_t)(pack_bf16_rne(acc, 0.0f) & 0xFFFFu);
-        tok[o] = kb;
-        a.win_kw[(head_win + slot) * D + o] = kb;
+    if (j == 0) {  // row 0, output channel 16 (w kNtW + nt) + n
+#pragma unroll
+        for (int nt = 0; nt < kNtW; ++nt) {
+            const int o = (wave * kNtW + nt) * 16 + n;
+            const uint16_t kb = (uint16_t)(pack_bf16_rne(acc[nt][0], 0.0f) & 0xFFFFu);
+            tok[o] = kb;
+            a.win_kw[(head_win + slot) * D + o] = kb;
+        }
     }
     if (tid < D) {
         tok[D + tid] = v;
@@ -1029,8 +1041,7 @@ decode_main_kernel(DecodeArgs a)
             const int32_t slot = s_old < a.s_sink ? s_old : ring_slot(s_old, a.s_sink, ring);
             if (slot >= unit0 && slot < unit0 + kPage * (SHARE ? a.win_units : 1)) {
                 new_slot = slot;
-                step_token<D>(a, b, h, slot, tok,
-                              reinterpret_cast<float *>(lds + 3 * M::kWave + M::kStageBytes - 8 * D), tid);
+                step_token<D>(a, b, h, slot, tok, tid);
             }
         }
 
@@ -1300,13 +1311,16 @@ static void main_kernel_ptr(const void *&f, bool share)
 // Waves of decode_main_kernel the device keeps resident at once (its
 // occupancy from registers and LDS, times the compute units), cached per
 // variant: the query-forming one, or with share the shared-items one;
-// 256 compute units at three workgroups each when no device answers.
+// 256 compute units at three workgroups each when no device answers.  The
+// cache entries are atomics: concurrent first calls compute the same value
+// and store it, so the cache is safe to fill from any thread.
 static int64_t resident_waves(int D, int bits, int G, bool share)
 {
-    static int64_t cache[2][2][2][4] = {};
+    static std::atomic<int64_t> cache[2][2][2][4] = {};
     const int di = D == 128, bi = bits == 4, gi = G == 1 ? 0 : G == 2 ? 1 : G == 4 ? 2 : 3;
-    int64_t &slot = cache[share][di][bi][gi];
-    if (slot > 0) return slot;
+    std::atomic<int64_t> &slot = cache[share][di][bi][gi];
+    const int64_t known = slot.load(std::memory_order_relaxed);
+    if (known > 0) return known;
     const void *f = nullptr;
     const int key = D * 100 + bits * 10 + gi;
     switch (key) {
@@ -1336,7 +1350,7 @@ static int64_t resident_waves(int D, int bits, int G, bool share)
         waves = (int64_t)ncu * blocks * 4;
     else
         (void)hipGetLastError();
-    slot = waves;
+    slot.store(waves, std::memory_order_relaxed);
     return waves;
 }
 
@@ -1359,6 +1373,9 @@ static RowShape row_shape(const wushkv_cache *c, int32_t n_q, int32_t max_tok)
     r.share = r.n_groups > 1;
     return r;
 }
+
+// Longest page run of one wave: its page-table entries sit one per lane.
+constexpr int64_t kMaxRunPages = 64;
 
 static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq_len, DecodePlan &p)
 {
@@ -1396,7 +1413,11 @@ static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq
         psplits = (qpages + per_split * upw - 1) / (per_split * upw);
     }
     const int64_t splits = psplits + wwgs;  // and the window workgroups
-    if (splits > kMaxSplits || upw > 0x7FFFFFFF / 4 / kMaxSplits) return false;
+    // a wave keeps the page-table entries of its run in its 64 lanes, one
+    // each (the run's k-th page is lane k's entry), so a run is at most 64
+    // pages long: longer contexts than kMaxSplits runs of 64 cover are not
+    // planned (the caller gets WUSHKV_EUNSUPPORTED)
+    if (splits > kMaxSplits || upw > kMaxRunPages) return false;
     p.units_per_wave = (int32_t)upw;
     p.win_units = (int32_t)win_units;
     p.n_page_splits = (int32_t)psplits;
@@ -1491,7 +1512,7 @@ static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok
     if (!(sm_scale > 0.0f) || sm_scale == INFINITY) return WUSHKV_EINVAL;
     const RowShape rs = row_shape(c, n_q_heads, max_tok);
     DecodePlan p;
-    if (!make_plan(c, rs, max_seq_len, p)) return WUSHKV_EINVAL;
+    if (!make_plan(c, rs, max_seq_len, p)) return WUSHKV_EUNSUPPORTED;
     if (workspace_bytes < p.qt_bytes + p.limb_bytes + p.aux_bytes + p.part_bytes) return WUSHKV_EWORKSPACE;
 
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);

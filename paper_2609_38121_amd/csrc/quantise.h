@@ -93,6 +93,29 @@ __device__ __forceinline__ void norm_rope_row(float (&x)[D / 32][8], int j, int3
     }
 }
 
+// Sequence b's counters as they stand before this launch: thread 0 reads
+// S, S_quant and the new-token count and hands them to the whole workgroup
+// through LDS (sh: three int32 of the caller's), so that every wave works
+// with the very values thread 0's arrival is tied to (commit_arrive).  The
+// count is clamped to [0, max_nn].  Every thread of the workgroup calls it;
+// it contains a barrier.
+struct SeqCounters {
+    int32_t s_old, q_old, nn;
+};
+__device__ __forceinline__ SeqCounters read_counters(const AppendArgs &a, int b, int32_t max_nn,
+                                                     int32_t *sh, int tid)
+{
+    if (tid == 0) {
+        sh[0] = a.seq_len[b];
+        sh[1] = a.quant_end[b];
+        sh[2] = a.n_new[b];
+    }
+    __syncthreads();
+    SeqCounters c{sh[0], sh[1], sh[2]};
+    c.nn = c.nn < 0 ? 0 : (c.nn > max_nn ? max_nn : c.nn);
+    return c;
+}
+
 // Sequence b's counters advance from inside the launch that last reads
 // them.  Each workgroup reports once, after its reads of seq_len and
 // quant_end have returned (the values are tied to the report's operand), to
@@ -100,7 +123,8 @@ __device__ __forceinline__ void norm_rope_row(float (&x)[D / 32][8], int j, int3
 // that was last of a.arrivals writes S_new and S_quant_new and clears the
 // count for the next call (commit_finish, at its end, so that the count's
 // round trip overlaps its work).  Every workgroup of the sequence has read
-// the old values before the last one arrives, so none can see the new ones.
+// the old values before the last one arrives, so none can see the new ones:
+// the other waves of a workgroup use thread 0's reads (read_counters).
 // Thread 0 only; a launch with a.arrivals = 0 leaves the counters alone.
 __device__ __forceinline__ int32_t commit_arrive(const AppendArgs &a, int b, int32_t s_old, int32_t q_old,
                                                  int32_t nn, int tid)

@@ -48,18 +48,61 @@ def eye_bits(n_kv: int, d: int) -> np.ndarray:
     return oracle.f32_to_bf16(np.broadcast_to(np.eye(d, dtype=np.float32), (n_kv, d, d)).copy())
 
 
+def tie_patched(ref: oracle.OracleCache, mirror: oracle.OracleCache):
+    """The end-to-end reference cache ``ref`` (T_K applied in fp64 to the raw
+    keys) with one change: every position whose key codes differ from the
+    GPU's (the mirror's) takes the GPU's bf16 k~ row instead of the fp64 one.
+    Those are the positions where the fp32-accumulated k~ rounded to the
+    other bf16 neighbour of a code decision's tie, so the returned cache
+    differs from ``ref`` exactly there and nowhere else.  Returns (cache,
+    number of substituted positions)."""
+    B, H, d = ref.batch, ref.n_kv, ref.d
+    out = oracle.OracleCache(B, H, d, ref.bits, ref.s_sink, ref.s_keep, ref.s_flush, ref.kappa_k,
+                             ref.kappa_v, ref.cap, codec=ref.codec, quest_alpha=ref.quest_alpha)
+    S = ref.seq_len.astype(np.int64)
+    n = max(1, int(S.max()))
+    k = np.zeros((B, n, H, d), np.uint16)
+    v = np.zeros_like(k)
+    subst = 0
+    for b in range(B):
+        qe = max(int(ref.quant_end[b]), ref.s_sink)
+        for h in range(H):
+            kb = ref.kbits[b, h, :S[b]].copy()
+            if qe > ref.s_sink:
+                sl = slice(ref.s_sink, qe)
+                rows = ref.s_sink + np.nonzero(np.any(ref.kc[b, h, sl] != mirror.kc[b, h, sl], axis=1))[0]
+                kb[rows] = mirror.kbits[b, h, rows]
+                subst += len(rows)
+            k[b, :S[b], h] = kb
+            v[b, :S[b], h] = ref.vbits[b, h, :S[b]]
+    out.append(k, v, S.astype(np.int32), eye_bits(H, d))
+    assert np.array_equal(out.quant_end, ref.quant_end)
+    # every key code now equals the GPU's: the reference's where they agreed,
+    # the GPU's own k~ where they did not
+    for b in range(B):
+        qe = max(int(ref.quant_end[b]), ref.s_sink)
+        assert np.array_equal(out.kc[b, :, ref.s_sink:qe], mirror.kc[b, :, ref.s_sink:qe])
+    return out, subst
+
+
 class Pair:
     def __init__(self, dev, batch, n_kv, G, d, bits, s_sink, s_keep, s_flush, kappa_k, kappa_v,
                  cap, win_slots=None, page_order="linear", pool_factor=1.0, symmetric=True,
-                 seed=0, oracle_ref=True, codec="pclip"):
+                 seed=0, oracle_ref=True, codec="pclip", quest_alpha="oracle"):
+        """quest_alpha (QuEST caches): "oracle" gives the descriptor the
+        oracle's alpha_b, None the library's default (wushkv_quest_alpha);
+        the oracle caches always take the value the descriptor holds."""
         self.dev = dev
         self.batch, self.n_kv, self.G, self.d, self.bits = batch, n_kv, G, d, bits
         self.s_sink = s_sink
+        if codec != "quest":
+            quest_alpha = None
+        elif quest_alpha == "oracle":
+            quest_alpha = oracle.quest_alpha(bits)
         self.gpu = wk.WushKVCache(batch, n_kv, d, bits, s_sink, s_keep, s_flush, kappa_k,
                                   kappa_v, max_seq_len=cap, win_slots=win_slots,
                                   page_order=page_order, pool_factor=pool_factor, seed=seed,
-                                  device=dev, codec=codec,
-                                  quest_alpha=oracle.quest_alpha(bits) if codec == "quest" else None)
+                                  device=dev, codec=codec, quest_alpha=quest_alpha)
         args = (batch, n_kv, d, bits, s_sink, s_keep, s_flush, kappa_k, kappa_v, cap)
         # the oracle gets the clip multiplier exactly as the descriptor holds it
         kw = dict(codec=codec, quest_alpha=self.gpu.quest_alpha)
@@ -231,3 +274,15 @@ class Pair:
         assert e_m <= tol, "decode vs oracle on the GPU's cache: %.3e" % e_m
         assert e_r <= tol, "decode vs oracle from raw inputs: %.3e" % e_r
         return gpu, e_m, e_r
+
+    def reference_for(self, out_fn):
+        """(error of the GPU output against the end-to-end reference, tie
+        positions substituted) where ``out_fn(cache)`` evaluates the oracle's
+        attention on a cache: the reference itself when its key codes equal
+        the GPU's, else the reference with the GPU's k~ at the positions whose
+        codes differ (tie_patched).  The caller asserts the error."""
+        same = all(np.array_equal(self.mirror.kc[b], self.ref.kc[b]) for b in range(self.batch))
+        if same:
+            return out_fn(self.ref), 0
+        patched, n = tie_patched(self.ref, self.mirror)
+        return out_fn(patched), n

@@ -177,6 +177,41 @@ def test_read_probe_validation():
     assert L.wushkv_read_probe(FAKE, 65536, 1, FAKE + 4, None) == -1
 
 
+def test_plans_past_the_page_run_limit_are_unsupported():
+    # a wave caches its run's page-table entries one per lane, so a run is at
+    # most 64 pages: decode (four runs per split, at most 1024 splits minus
+    # the three window workgroups) stops planning past 1021 * 4 * 64 pages,
+    # chunk attention (one run per split, one window workgroup) past
+    # 1023 * 64 pages; the call is then unsupported, the workspace size 0
+    L = _lib.lib()
+    big = _desc(max_pages_per_seq=400000)
+    by = ctypes.byref(big)
+    ok_len = 4 + 1021 * 4 * 64 * 64          # upw = 64 exactly
+    assert L.wushkv_decode_workspace_bytes(by, 8, ok_len) > 0
+    assert L.wushkv_decode_workspace_bytes(by, 8, ok_len + 64) == 0
+    assert L.wushkv_chunk_workspace_bytes(by, 8, 16, 4 + 1023 * 64 * 64) > 0
+    assert L.wushkv_chunk_workspace_bytes(by, 8, 16, 4 + 1023 * 64 * 64 + 64) == 0
+    if not gpu_available():
+        # fake device pointers: the host check answers before any launch
+        st = L.wushkv_decode_attention(by, FAKE, 8, ok_len + 64, FAKE, 0.1, FAKE, FAKE, 1 << 40, None)
+        assert st == -2
+        st = L.wushkv_chunk_attention(by, FAKE, None, 16, 8, 4 + 1023 * 64 * 64 + 64, FAKE, 0.1,
+                                      FAKE, FAKE, 1 << 40, None)
+        assert st == -2
+
+
+def test_quest_alpha_matches_the_oracle():
+    # the library's alpha_b (bisection on the stationarity condition of the
+    # clipping lemma, App. B) against the oracle's (direct minimisation of
+    # the Gaussian grid error, Sec. 4.3): the same optimum of Eq. (5)
+    oracle = pytest.importorskip("oracle")
+    for b in range(1, 9):
+        lib_a = wk.wushkv_quest_alpha(b)
+        orc_a = oracle.quest_alpha(b)
+        assert abs(lib_a - orc_a) <= 1e-6 * orc_a, (b, lib_a, orc_a)
+    assert np.isnan(wk.wushkv_quest_alpha(0)) and np.isnan(wk.wushkv_quest_alpha(9))
+
+
 def test_workspace_bytes_closed_form():
     L = _lib.lib()
     d = _desc()

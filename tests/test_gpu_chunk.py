@@ -1,6 +1,8 @@
 """GPU parity of chunk attention (Alg. 2 step 5 with S' > 1: the causal mask
 of Eq. (2) inside each sequence's chunk of new tokens) against the oracle,
-on the mirror cache (the GPU's own codes) and the end-to-end reference."""
+on the mirror cache (the GPU's own codes) and the end-to-end reference (with
+the GPU's k~ at any position whose codes sit on the other side of a rounding
+tie, see gpu_harness.tie_patched)."""
 import numpy as np
 import pytest
 import torch
@@ -34,14 +36,15 @@ def _check(p, q, n_tok, max_seq_len=None):
     # rows beyond a sequence's chunk are zero
     assert np.all(gpu[~valid] == 0)
     em = rel_err(gpu[valid], mir[valid])
-    same = all(np.array_equal(p.mirror.kc[b], p.ref.kc[b]) for b in range(p.batch))
-    ref = oracle.chunk_attention(p.ref, q, n_tok, p.tinv, p.sm_scale)
+    # the end-to-end reference; where its key codes differ from the GPU's at
+    # a rounding tie of k~, the same reference with the GPU's k~ at exactly
+    # those positions
+    ref, n_sub = p.reference_for(lambda c: oracle.chunk_attention(c, q, n_tok, p.tinv, p.sm_scale))
     er = rel_err(gpu[valid], ref[valid])
-    say("  chunk rel err vs mirror %.2e, vs reference %.2e (codes %s)"
-        % (em, er, "equal" if same else "differ at ties"))
+    say("  chunk rel err vs mirror %.2e, vs reference %.2e (%d tie positions substituted)"
+        % (em, er, n_sub))
     assert em <= TOL
-    if same:
-        assert er <= TOL
+    assert er <= TOL
     return gpu
 
 

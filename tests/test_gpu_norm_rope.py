@@ -7,7 +7,9 @@ RoPE(Norm(k)) evaluated by the oracle in fp64 and rounded to bf16; the GPU
 evaluates it in fp32 and may land on the other bf16 neighbour in rare
 elements, so k~ is checked against the fp64 product within the fp32 bound on
 all but a small fraction of elements, and decode outputs against both caches
-(the reference one only while their codes agree, as in the full-size tests)."""
+(where a key code of the reference sits on the other side of such a rounding
+tie, the reference takes the GPU's k~ at exactly those positions:
+gpu_harness.tie_patched)."""
 import numpy as np
 import pytest
 
@@ -37,15 +39,13 @@ def _check_k_tilde(p, frac=1e-3):
 def _decode(p, q):
     gpu = p.decode(q)
     mir = p.mirror.decode(q, p.tinv, p.sm_scale)
-    ref = p.ref.decode(q, p.tinv, p.sm_scale)
+    ref, n_sub = p.reference_for(lambda c: c.decode(q, p.tinv, p.sm_scale))
     em, er = rel_err(gpu, mir), rel_err(gpu, ref)
-    same = all(np.array_equal(p.mirror.kc[b], p.ref.kc[b]) for b in range(p.batch))
-    say("  decode rel err vs mirror %.2e, vs reference %.2e (codes %s)"
-        % (em, er, "equal" if same else "differ at ties"))
+    say("  decode rel err vs mirror %.2e, vs reference %.2e (%d tie positions substituted)"
+        % (em, er, n_sub))
     assert np.all(np.isfinite(gpu))
     assert em <= TOL
-    if same:
-        assert er <= TOL
+    assert er <= TOL
 
 
 @pytest.mark.parametrize("d,bits,G,use_gain", [(128, 2, 4, True), (128, 4, 4, False),

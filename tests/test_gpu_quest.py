@@ -108,3 +108,31 @@ def test_quest_dequant_bit_exact(gpu):
                 vref = oracle.dequant(m.vc[b, h, 4:qe], m.vp[b, h, 4:qe, 0], m.vp[b, h, 4:qe, 1])
                 assert np.array_equal(ko[h], kref)
                 assert np.array_equal(vo[h], vref)
+
+
+@pytest.mark.parametrize("bits", [2, 4])
+def test_quest_library_default_alpha(gpu, bits):
+    """A QuEST cache built without an explicit clip multiplier uses the
+    library's alpha_b (wushkv_quest_alpha: the stationarity condition of the
+    clipping lemma, App. B); it must be the oracle's Gaussian-optimal alpha_b
+    (Sec. 4.3) within 1e-6, and the cache it builds must equal the oracle's
+    QuEST cache at that same value bit for bit."""
+    import paper_2609_38121_amd as wk
+    rng = np.random.default_rng(110 + bits)
+    B, H, G, d = 2, 2, 4, 128
+    say("quest library-default alpha, bits=%d" % bits)
+    p = Pair(gpu, B, H, G, d, bits, 4, 64, 8, 0.96, 0.92, cap=800, codec="quest",
+             quest_alpha=None)
+    lib_alpha = wk.wushkv_quest_alpha(bits)
+    assert p.gpu.quest_alpha == float(np.float32(lib_alpha))
+    assert abs(lib_alpha - oracle.quest_alpha(bits)) <= 1e-6 * lib_alpha
+    k, v = _kv(rng, B, 600, H, d)
+    p.append(k, v, [600, 257])
+    assert p.check_cache() > 0
+    _, em, er = p.decode_check(_q(rng, B, H * G, d))
+    for _ in range(9):  # single-token steps across a flush
+        k, v = _kv(rng, B, 1, H, d)
+        p.append(k, v, [1, 1])
+        p.check_cache()
+        _, em, er = p.decode_check(_q(rng, B, H * G, d))
+    say("  alpha %.7f: rel err vs mirror %.2e, vs ref %.2e" % (p.gpu.quest_alpha, em, er))

@@ -8,6 +8,7 @@ import numpy as np
 import pytest
 
 import oracle
+from workloads import synth
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "windows_worked_examples.txt")
 
@@ -322,3 +323,38 @@ def test_decode_step_order_of_alg2():
                 flushes += 1
                 assert not np.array_equal(got[b], ref[b])
     assert flushes >= 2
+
+
+def test_parallel_pairs_equal_the_serial_oracle():
+    """The benchmark's OpenMP driver (HeadSet: independent (sequence, head)
+    pairs spread over threads) computes exactly what OracleCache computes
+    pair by pair: same codes, parameters, counters and decode outputs, bit
+    for bit, at any thread count."""
+    rng = np.random.default_rng(77)
+    d, G, bits = 64, 4, 2
+    lens = [300, 0, 41, 130, 257]
+    tk, tinv = synth.make_transform(len(lens), d, 5, False)
+    hs = {}
+    for threads in (1, 3):
+        h = oracle.HeadSet([n + 8 for n in lens], d, bits, 4, 32, 8, 0.96, 0.92)
+        ks = [oracle.f32_to_bf16(rng.standard_normal((n, d)).astype(np.float32)) for n in lens]
+        vs = [oracle.f32_to_bf16(rng.standard_normal((n, d)).astype(np.float32)) for n in lens]
+        if threads == 1:
+            inputs = (ks, vs)
+        ks, vs = inputs
+        used = h.append(ks, vs, [tk[i] for i in range(len(lens))], threads=threads)
+        assert used == threads
+        qs = [oracle.f32_to_bf16(np.random.default_rng(i).standard_normal((G, d)).astype(np.float32))
+              for i in range(len(lens))]
+        out, used = h.decode(qs, [tinv[i] for i in range(len(lens))], 0.125, threads=threads)
+        assert used == threads
+        hs[threads] = (h, out)
+        for i, n in enumerate(lens):
+            oc = oracle.OracleCache(1, 1, d, bits, 4, 32, 8, 0.96, 0.92, n + 8)
+            oc.append(ks[i][None, :, None], vs[i][None, :, None], [n], tk[i:i + 1])
+            assert int(oc.seq_len[0]) == h.seq_len[i] and int(oc.quant_end[0]) == h.quant_end[i]
+            assert np.array_equal(oc.kc[0, 0], h.kc[i]) and np.array_equal(oc.vc[0, 0], h.vc[i])
+            assert np.array_equal(oc.kp[0, 0], h.kp[i]) and np.array_equal(oc.vp[0, 0], h.vp[i])
+            ref = oc.decode(qs[i][None], tinv[i:i + 1], 0.125)[0]
+            assert np.array_equal(ref, out[i]) or (n == 0 and np.all(out[i] == 0))
+    assert np.array_equal(hs[1][1], hs[3][1])
