@@ -286,6 +286,34 @@ size_t wushkv_decode_workspace_bytes(const wushkv_cache *c,
                                      int32_t n_q_heads, int32_t max_seq_len);
 
 /*
+ * wushkv_decode_attention_noalloc -- wushkv_decode_attention for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation): the same arguments without the
+ * workspace, the same kernels and the same results.  Its workspace is a
+ * static device array of WUSHKV_NOALLOC_SCRATCH_BYTES inside the library,
+ * one per GPU, held until the process ends; its address is looked up on the
+ * first call on each device (hipGetSymbolAddress, no allocation).  The call
+ * allocates and frees nothing.
+ *   - A call whose plan needs more than WUSHKV_NOALLOC_SCRATCH_BYTES
+ *     (wushkv_decode_workspace_bytes for the same arguments) returns
+ *     WUSHKV_EWORKSPACE and enqueues nothing: for example batch 64, 32 query
+ *     heads at 32768 tokens need about 14 MB, well inside the limit.
+ *   - Nothing in the array has to start at zero: every call writes all it
+ *     reads (the q~ rows and every split's partial) before reading it.
+ *   - Every call on one GPU shares that GPU's array, which keeps the last
+ *     call's contents: calls that overlap on one GPU (different streams, or
+ *     host threads, without ordering between them) race on it and must not
+ *     be issued.
+ * Returns WUSHKV_ENODEVICE when no device is current or the array cannot be
+ * located, besides wushkv_decode_attention's statuses.
+ */
+#define WUSHKV_NOALLOC_SCRATCH_BYTES (32u << 20)
+int wushkv_decode_attention_noalloc(const wushkv_cache *c, const uint16_t *q,
+                                    int32_t n_q_heads, int32_t max_seq_len,
+                                    const float *t_k_inv, float sm_scale, float *out,
+                                    wushkv_stream_t stream);
+
+/*
  * wushkv_decode_step -- one decode step of Alg. 2 (S' = 1) in the
  * algorithm's own order, in two launches on the stream:
  *   1. each sequence's new token is appended at bf16 (steps 3-4: k~ = T_K k

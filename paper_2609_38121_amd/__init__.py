@@ -20,7 +20,8 @@ from ._lib import (CacheDesc, WushKVError, PAGE_TOKENS, check, header_functions,
                    status_string)
 
 __all__ = [
-    "WushKVCache", "WushKVError", "wushkv_append", "wushkv_decode_attention", "wushkv_decode_step",
+    "WushKVCache", "WushKVError", "wushkv_append", "wushkv_decode_attention",
+    "wushkv_decode_attention_noalloc", "wushkv_decode_step",
     "wushkv_decode_workspace_bytes", "wushkv_dequant", "wushkv_page_bytes",
     "wushkv_status_string", "wushkv_abi_version", "wushkv_timing_enable",
     "wushkv_timing_read", "wushkv_timing_launches", "wushkv_quest_alpha", "wushkv_wush_transform", "wushkv_read_probe",
@@ -242,6 +243,24 @@ def wushkv_decode_attention(cache: WushKVCache, q, t_k_inv, sm_scale=None, max_s
         float(sm_scale), _ptr(out), _ptr(workspace), workspace.numel() * workspace.element_size(),
         _stream_handle(stream))
     check(st, "wushkv_decode_attention")
+    return out
+
+
+def wushkv_decode_attention_noalloc(cache: WushKVCache, q, t_k_inv, out, sm_scale=None,
+                                    max_seq_len=None, stream=None):
+    """wushkv_decode_attention with the library's static workspace: nothing
+    is allocated (``out`` is the caller's fp32 [batch][n_q][d]).  Calls that
+    overlap on one GPU race on that workspace."""
+    _check_2byte(q, "q")
+    n_q = q.shape[1]
+    if max_seq_len is None:
+        max_seq_len = cache.max_seq_len
+    if sm_scale is None:
+        sm_scale = 1.0 / math.sqrt(cache.head_dim)
+    st = _lib.lib().wushkv_decode_attention_noalloc(
+        ctypes.byref(cache.desc), _ptr(q), n_q, int(max_seq_len), _ptr(t_k_inv),
+        float(sm_scale), _ptr(out), _stream_handle(stream))
+    check(st, "wushkv_decode_attention_noalloc")
     return out
 
 

@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(_HERE, "_build", "libwushkv.so")
 HEADER = os.path.join(os.path.dirname(_HERE), "include", "wushkv.h")
 
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, ELAUNCH, ENODEVICE = 0, -1, -2, -3, -4, -5
+NOALLOC_SCRATCH_BYTES = 32 << 20  # WUSHKV_NOALLOC_SCRATCH_BYTES
 CODEC_PCLIP, CODEC_QUEST = 0, 1
 PAGE_TOKENS = 64
 
@@ -79,6 +80,8 @@ def _declare(L):
     L.wushkv_append_norm_rope.restype = ctypes.c_int
     L.wushkv_decode_attention.argtypes = [D, P, I32, I32, P, F32, P, P, SZ, P]
     L.wushkv_decode_attention.restype = ctypes.c_int
+    L.wushkv_decode_attention_noalloc.argtypes = [D, P, I32, I32, P, F32, P, P]
+    L.wushkv_decode_attention_noalloc.restype = ctypes.c_int
     L.wushkv_decode_workspace_bytes.argtypes = [D, I32, I32]
     L.wushkv_decode_workspace_bytes.restype = SZ
     L.wushkv_decode_step.argtypes = [D, P, P, P, P, P, I32, I32, P, F32, P, P, SZ, P]

@@ -42,6 +42,7 @@
 // probabilities, again split hi + lo, go through LDS into a 16x16x16 bf16
 // P V product against the channel-major value slots.
 #include <atomic>
+#include <mutex>
 
 #include "common.h"
 #include "merge.h"
@@ -1604,6 +1605,61 @@ extern "C" int wushkv_decode_attention(const wushkv_cache *c, const uint16_t *q,
 {
     return attend(c, q, nullptr, 1, n_q_heads, max_seq_len, t_k_inv, sm_scale, out, workspace,
                   workspace_bytes, stream);
+}
+
+// ------------------------------------------------------- no-allocation call
+
+// The workspace of wushkv_decode_attention_noalloc: a file-scope device
+// array, one copy per GPU the library runs on, held until the process ends.
+// Host code never uses its name as an address (on the host it stands for a
+// host-side shadow); it takes the device address from hipGetSymbolAddress,
+// once per device, with that device current.
+static __device__ __align__(256) uint8_t scratch[WUSHKV_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+// Device address of the current device's copy of scratch (looked up on the
+// first call on that device), or null when there is no usable device.
+static void *scratch_on_current_device()
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) {
+            (void)hipGetLastError();
+            return nullptr;
+        }
+        g_scratch_ptr[dev] = ptr;
+    }
+    return g_scratch_ptr[dev];
+}
+
+extern "C" int wushkv_decode_attention_noalloc(const wushkv_cache *c, const uint16_t *q,
+                                               int32_t n_q_heads, int32_t max_seq_len,
+                                               const float *t_k_inv, float sm_scale, float *out,
+                                               wushkv_stream_t stream)
+{
+    // the plan's size first: a call that needs more than the array holds is
+    // refused before anything else happens
+    const size_t need = workspace_bytes(c, n_q_heads, 1, max_seq_len);
+    if (need == 0) {
+        const int st = check_decode_args(c, n_q_heads, max_seq_len);
+        return st != WUSHKV_OK ? st : WUSHKV_EUNSUPPORTED;
+    }
+    if (need > (size_t)WUSHKV_NOALLOC_SCRATCH_BYTES) return WUSHKV_EWORKSPACE;
+    void *ws = scratch_on_current_device();
+    if (ws == nullptr) return WUSHKV_ENODEVICE;
+    return attend(c, q, nullptr, 1, n_q_heads, max_seq_len, t_k_inv, sm_scale, out, ws,
+                  (size_t)WUSHKV_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 extern "C" size_t wushkv_chunk_workspace_bytes(const wushkv_cache *c, int32_t n_q_heads,

@@ -200,6 +200,22 @@ def test_plans_past_the_page_run_limit_are_unsupported():
         assert st == -2
 
 
+@pytest.mark.skipif(gpu_available(), reason="fake device pointers: run only where no GPU exists")
+def test_noalloc_decode_host_checks():
+    # the plan is sized before anything else: beyond the static array the
+    # call is refused with EWORKSPACE; within it, with no device, ENODEVICE
+    L = _lib.lib()
+    big = _desc(batch=256, n_kv_heads=8, max_pages_per_seq=2048, n_pages=8)
+    assert L.wushkv_decode_workspace_bytes(ctypes.byref(big), 64, 65536) > _lib.NOALLOC_SCRATCH_BYTES
+    st = L.wushkv_decode_attention_noalloc(ctypes.byref(big), FAKE, 64, 65536, FAKE, 0.1, FAKE, None)
+    assert st == -3
+    d = _desc()
+    assert 0 < L.wushkv_decode_workspace_bytes(ctypes.byref(d), 8, 1000) <= _lib.NOALLOC_SCRATCH_BYTES
+    assert L.wushkv_decode_attention_noalloc(ctypes.byref(d), FAKE, 8, 1000, FAKE, 0.1, FAKE, None) == -5
+    assert L.wushkv_decode_attention_noalloc(ctypes.byref(d), FAKE, 7, 1000, FAKE, 0.1, FAKE, None) == -1
+    assert L.wushkv_decode_attention_noalloc(None, FAKE, 8, 1000, FAKE, 0.1, FAKE, None) == -1
+
+
 def test_quest_alpha_matches_the_oracle():
     # the library's alpha_b (bisection on the stationarity condition of the
     # clipping lemma, App. B) against the oracle's (direct minimisation of
