@@ -872,7 +872,7 @@ def bench_wush(torch, wk, dev, args, layers=32, heads=8, d=128, gamma=1e-2, reps
                          "unit": "TFLOP/s", "frac": round(tflops / 157.3, 4), "traffic": None}}
 
 
-def bench_decode_scale(torch, wk, synth, dev, args, calls=24):
+def bench_decode_scale(torch, wk, synth, dev, args, calls=24, names=("long2", "long4", "qwen32b")):
     """Decode calls alone on the long-context (131072 tokens, 2 and 4 bits,
     random page order) and Qwen3-32B-shaped (8 sequences of 8192 tokens, 64
     query heads on 8 kv heads) caches (the large-batch one is the headline).  The caches are filled by the library's own append from
@@ -880,7 +880,7 @@ def bench_decode_scale(torch, wk, synth, dev, args, calls=24):
     on the values); lengths are the workloads' own.  Replicas are cycled so
     that the calls touch more than twice the 256 MB Infinity Cache."""
     out = {}
-    for name in ("long2", "long4", "qwen32b"):
+    for name in names:
         cfg = synth.CONFIGS[name]
         w = synth.Workload(cfg, seed=args.seed)
         B, H, NQ, D, BITS = cfg["batch"], cfg["n_kv"], cfg["n_q"], cfg["d"], cfg["bits"]

@@ -1031,7 +1031,7 @@ decode_main_kernel(DecodeArgs a)
         const int32_t a0 = S > q_hi ? (q_hi - a.s_sink) % ring : 0;
         const int32_t ring_live = S > q_hi ? S - q_hi : 0;
         const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;
-        const int32_t unit0 = (split - a.n_page_splits) * kPage * (SHARE ? a.win_units : 1);
+        const int32_t unit0 = (split - a.n_page_splits) * kPage * a.win_units;
         // fused step: the workgroup whose unit holds the new token's slot
         // writes the token and keeps it in LDS, at the end of wave 3's page
         // stage (its merge rows, written last, sit at the start)
@@ -1040,7 +1040,7 @@ decode_main_kernel(DecodeArgs a)
         static_assert(G * D * 4 + 8 * D <= M::kStageBytes, "the new token fits the page stage");
         if (a.n_new != nullptr && nn > 0) {
             const int32_t slot = s_old < a.s_sink ? s_old : ring_slot(s_old, a.s_sink, ring);
-            if (slot >= unit0 && slot < unit0 + kPage * (SHARE ? a.win_units : 1)) {
+            if (slot >= unit0 && slot < unit0 + kPage * a.win_units) {
                 new_slot = slot;
                 step_token<D>(a, b, h, slot, tok, tid);
             }
@@ -1090,9 +1090,10 @@ decode_main_kernel(DecodeArgs a)
         bool formed = FORM;
         // SHARE: every wave all 16-slot tiles of the workgroup's units, with
         // an online softmax across them
-        const int kSub = SHARE ? 4 * a.win_units : 1;
+        // (otherwise wave w takes tile w of each of the workgroup's units)
+        const int kSub = SHARE ? 4 * a.win_units : a.win_units;
         for (int st = 0; st < (rows_live ? kSub : 0); ++st) {
-            const int32_t slot0 = unit0 + 16 * (SHARE ? st : wave);
+            const int32_t slot0 = unit0 + 16 * (SHARE ? st : wave + 4 * st);
             // this tile's live slots, one bit per slot (lanes 0..15)
             bool mine;
             {
@@ -1378,7 +1379,8 @@ static RowShape row_shape(const wushkv_cache *c, int32_t n_q, int32_t max_tok)
 // Longest page run of one wave: its page-table entries sit one per lane.
 constexpr int64_t kMaxRunPages = 64;
 
-static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq_len, DecodePlan &p)
+static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq_len, DecodePlan &p,
+                      bool one_window_wg = false)
 {
     const int32_t G = rs.G;
     const int64_t qpages = max_seq_len > c->s_sink ? (max_seq_len - c->s_sink + kPage - 1) / kPage : 0;
@@ -1394,7 +1396,7 @@ static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq
     // with shared work items (share) one per row for all units, since there
     // every wave walks all the tiles anyway and the page runs then get the
     // resident slots the other window workgroups would hold.
-    const int64_t win_units = rs.share ? wunits : 1;
+    const int64_t win_units = (rs.share || one_window_wg) ? wunits : 1;
     const int64_t wwgs = (wunits + win_units - 1) / win_units;
     // With shared work items (share_items) the four waves of a workgroup
     // walk one run together, each for another token group: a workgroup row
@@ -1407,6 +1409,18 @@ static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq
     int64_t upw = 2;
     while (upw < upw_max && wg_rows * ((qpages + per_split * upw - 1) / (per_split * upw)) * 4 > budget) ++upw;
     int64_t psplits = (qpages + per_split * upw - 1) / (per_split * upw);
+    // the same number of runs, evened out (the last one is not left short)
+    if (psplits > 0) {
+        upw = (qpages + per_split * psplits - 1) / (per_split * psplits);
+        psplits = (qpages + per_split * upw - 1) / (per_split * upw);
+    }
+    // A decode grid that cannot be resident at once (it runs in rounds)
+    // takes one window workgroup per row, its waves on every unit's tiles:
+    // a third as many workgroups, each with an online softmax over its
+    // tiles, instead of one per 64-slot unit.
+    if (!rs.share && !one_window_wg && wunits > 1 &&
+        (psplits + wwgs) * heads * 4 > resident_waves(c->head_dim, c->bits, G, false))
+        return make_plan(c, rs, max_seq_len, p, true);
     if (psplits + wwgs > kMaxSplits) {
         const int64_t room = kMaxSplits - wwgs;
         if (room < 1) return false;

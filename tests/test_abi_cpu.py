@@ -180,13 +180,14 @@ def test_read_probe_validation():
 def test_plans_past_the_page_run_limit_are_unsupported():
     # a wave caches its run's page-table entries one per lane, so a run is at
     # most 64 pages: decode (four runs per split, at most 1024 splits minus
-    # the three window workgroups) stops planning past 1021 * 4 * 64 pages,
-    # chunk attention (one run per split, one window workgroup) past
-    # 1023 * 64 pages; the call is then unsupported, the workspace size 0
+    # the window workgroup, one per row when the grid runs in rounds) stops
+    # planning past 1023 * 4 * 64 pages, chunk attention (one run per split,
+    # one window workgroup) past 1023 * 64 pages; the call is then
+    # unsupported, the workspace size 0
     L = _lib.lib()
     big = _desc(max_pages_per_seq=400000)
     by = ctypes.byref(big)
-    ok_len = 4 + 1021 * 4 * 64 * 64          # upw = 64 exactly
+    ok_len = 4 + 1023 * 4 * 64 * 64          # upw = 64 exactly
     assert L.wushkv_decode_workspace_bytes(by, 8, ok_len) > 0
     assert L.wushkv_decode_workspace_bytes(by, 8, ok_len + 64) == 0
     assert L.wushkv_chunk_workspace_bytes(by, 8, 16, 4 + 1023 * 64 * 64) > 0
