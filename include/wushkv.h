@@ -90,7 +90,11 @@ enum {
  * physical page page_table[b * max_pages_per_seq + i].
  *
  * pages: uint8 [n_pages][n_kv_heads][page_bytes], page_bytes =
- *   wushkv_page_bytes(head_dim, bits) = 64 * (2 * head_dim * bits / 8 + 8).
+ *   wushkv_page_bytes(head_dim, bits) = 64 * (2 * head_dim * sb / 8 + 8), where
+ *   sb = bits for 2- and 4-bit codes and sb = 4 for 3-bit codes: a 3-bit code
+ *   is stored in the 4-bit format below, in a 4-bit field whose top bit is
+ *   zero (136 bytes per token-head at d = 128 instead of the dense 104).
+ *   In the rest of this layout description, bits stands for sb.
  *   One (page, head) block is, in order:
  *     K codes   8 * head_dim * bits bytes
  *     V codes   8 * head_dim * bits bytes
@@ -139,7 +143,7 @@ typedef struct wushkv_cache {
     int32_t batch;             /* sequences, >= 1 */
     int32_t n_kv_heads;        /* >= 1 */
     int32_t head_dim;          /* 64 or 128 */
-    int32_t bits;              /* 2 or 4, for keys and values */
+    int32_t bits;              /* 2, 3 or 4, for keys and values (3: stored as 4) */
     int32_t s_sink;            /* >= 0 */
     int32_t s_keep;            /* >= 0 */
     int32_t s_flush;           /* >= 1 */
@@ -163,7 +167,8 @@ typedef struct wushkv_cache {
                                   S_quant; every completed call leaves it zero */
 } wushkv_cache;
 
-/* Bytes of one (page, head) block, or 0 for unsupported (head_dim, bits). */
+/* Bytes of one (page, head) block, or 0 for unsupported (head_dim, bits):
+ * head_dim 64 or 128, bits 2, 3 or 4. */
 size_t wushkv_page_bytes(int32_t head_dim, int32_t bits);
 
 /*

@@ -41,7 +41,7 @@ int wushkv_validate_cache(const wushkv_cache *c)
     if (c == nullptr) return WUSHKV_EINVAL;
     if (c->batch < 1 || c->n_kv_heads < 1) return WUSHKV_EINVAL;
     if (c->head_dim != 64 && c->head_dim != 128) return WUSHKV_EUNSUPPORTED;
-    if (c->bits != 2 && c->bits != 4) return WUSHKV_EUNSUPPORTED;
+    if (c->bits < 2 || c->bits > 4) return WUSHKV_EUNSUPPORTED;
     if (c->s_sink < 0 || c->s_keep < 0 || c->s_flush < 1) return WUSHKV_EINVAL;
     if (c->win_slots < kPage || c->win_slots % kPage != 0) return WUSHKV_EINVAL;
     const int64_t need = (int64_t)c->s_keep + c->s_flush - 1;
@@ -73,8 +73,8 @@ int wushkv_validate_cache(const wushkv_cache *c)
 
 extern "C" size_t wushkv_page_bytes(int32_t head_dim, int32_t bits)
 {
-    if ((head_dim != 64 && head_dim != 128) || (bits != 2 && bits != 4)) return 0;
-    return (size_t)kPage * (2 * head_dim * bits / 8 + 8);
+    if ((head_dim != 64 && head_dim != 128) || bits < 2 || bits > 4) return 0;
+    return (size_t)kPage * (2 * head_dim * storage_bits(bits) / 8 + 8);
 }
 
 extern "C" const char *wushkv_status_string(int status)

@@ -451,6 +451,7 @@ static AppendArgs cache_args(const wushkv_cache *c)
     a.max_pages = c->max_pages_per_seq;
     a.n_pages = c->n_pages;
     a.codec = c->codec;
+    a.levels = (1 << c->bits) - 1;
     if (c->codec == WUSHKV_CODEC_PCLIP) {
         kappa_position(c->kappa_k, c->head_dim, a.lo_k, a.t_k);
         kappa_position(c->kappa_v, c->head_dim, a.lo_v, a.t_v);
@@ -513,7 +514,7 @@ static int append_impl(const wushkv_cache *c, const uint16_t *k_new, const uint1
         const char *name = mode == kModeFlush ? "append_flush" : "append_kernel";
         const dim3 g = mode == kModeFlush ? flush_grid : grid;
         a.arrivals = (mode & kModeNew) ? (int32_t)(g.x * g.y) : 0;
-        const int key = c->head_dim * 10 + c->bits;
+        const int key = c->head_dim * 10 + storage_bits(c->bits);
         switch (key) {
             case 1282: return launch_append<128, 2>(name, a, g, s);
             case 1284: return launch_append<128, 4>(name, a, g, s);
@@ -526,7 +527,7 @@ static int append_impl(const wushkv_cache *c, const uint16_t *k_new, const uint1
     if (max_new <= kStepMax) {
         const dim3 sgrid((unsigned)c->n_kv_heads, (unsigned)c->batch);
         a.arrivals = (int32_t)sgrid.x;
-        const int key = c->head_dim * 10 + c->bits;
+        const int key = c->head_dim * 10 + storage_bits(c->bits);
         switch (key) {
             case 1282: e = launch_append_step<128, 2>(a, sgrid, s); break;
             case 1284: e = launch_append_step<128, 4>(a, sgrid, s); break;
@@ -578,7 +579,7 @@ int wushkv_step_finish(const wushkv_cache *c, const int32_t *n_new, const float 
     a.arrivals = c->n_kv_heads;  // the flush workgroups of a sequence
     FinishArgs f{part, out, G, n_splits};
     const dim3 grid((unsigned)(c->n_kv_heads * G + c->n_kv_heads), (unsigned)c->batch);
-    const int key = c->head_dim * 10 + c->bits;
+    const int key = c->head_dim * 10 + storage_bits(c->bits);
     switch (key) {
         case 1282: launch("step_finish_kernel", step_finish_kernel<128, 2>, grid, dim3(256), s, a, f); break;
         case 1284: launch("step_finish_kernel", step_finish_kernel<128, 4>, grid, dim3(256), s, a, f); break;

@@ -22,6 +22,11 @@ typedef __attribute__((ext_vector_type(2))) _Float16 f16x2;
 
 constexpr int kPage = WUSHKV_PAGE_TOKENS;  // tokens per page
 
+// Bits of the page field that holds one code: 3-bit codes are stored in the
+// 4-bit page format, each in a 4-bit field whose top bit is zero, so that
+// every kernel reads them as 4-bit codes.
+__host__ __device__ constexpr int storage_bits(int bits) { return bits == 3 ? 4 : bits; }
+
 // ---------------------------------------------------------------- formats
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }

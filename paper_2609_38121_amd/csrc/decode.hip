@@ -1404,7 +1404,7 @@ static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq
     // covers upw pages instead of 4 upw.
     const int64_t per_split = rs.share ? 1 : 4;
     const int64_t wg_rows = rs.share ? (int64_t)c->batch * ((rs.n_groups + 3) / 4) * c->n_kv_heads : heads;
-    const int64_t budget = resident_waves(c->head_dim, c->bits, G, rs.share) - 4 * wg_rows * wwgs;
+    const int64_t budget = resident_waves(c->head_dim, storage_bits(c->bits), G, rs.share) - 4 * wg_rows * wwgs;
     const int64_t upw_max = rs.share ? 64 : 16;
     int64_t upw = 2;
     while (upw < upw_max && wg_rows * ((qpages + per_split * upw - 1) / (per_split * upw)) * 4 > budget) ++upw;
@@ -1419,7 +1419,7 @@ static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq
     // a third as many workgroups, each with an online softmax over its
     // tiles, instead of one per 64-slot unit.
     if (!rs.share && !one_window_wg && wunits > 1 &&
-        (psplits + wwgs) * heads * 4 > resident_waves(c->head_dim, c->bits, G, false))
+        (psplits + wwgs) * heads * 4 > resident_waves(c->head_dim, storage_bits(c->bits), G, false))
         return make_plan(c, rs, max_seq_len, p, true);
     if (psplits + wwgs > kMaxSplits) {
         const int64_t room = kMaxSplits - wwgs;
@@ -1588,8 +1588,8 @@ static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok
     // that read once per workgroup, so a small kernel forms q~ first; so do
     // grids of shared work items.
     const int64_t wgs = (int64_t)p.n_splits * c->n_kv_heads * grid_z;
-    const bool form = !rs.share && wgs * 4 <= resident_waves(c->head_dim, c->bits, G, false);
-    const int key = c->head_dim * 10 + c->bits;
+    const bool form = !rs.share && wgs * 4 <= resident_waves(c->head_dim, storage_bits(c->bits), G, false);
+    const int key = c->head_dim * 10 + storage_bits(c->bits);
     switch (key) {
         case 1282: launch_main_g<128, 2>(G, form, rs.share, gm, rows_z, s, a); break;
         case 1284: launch_main_g<128, 4>(G, form, rs.share, gm, rows_z, s, a); break;

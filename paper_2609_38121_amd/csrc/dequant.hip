@@ -65,7 +65,7 @@ extern "C" int wushkv_dequant(const wushkv_cache *c, int32_t b, int32_t start, i
     const int64_t n = (int64_t)count * c->head_dim;
     if ((n + 255) / 256 > 0x7FFFFFFF) return WUSHKV_EINVAL;
     dim3 grid((unsigned)((n + 255) / 256), (unsigned)c->n_kv_heads);
-    const int key = c->head_dim * 10 + c->bits;
+    const int key = c->head_dim * 10 + storage_bits(c->bits);
 #define WUSHKV_DQ(D_, B_)                                                                     \
     launch("dequant_kernel", dequant_kernel<D_, B_>, grid, dim3(256), s, c->pages, c->page_table, \
            c->n_kv_heads, c->s_sink, c->max_pages_per_seq, c->n_pages, b, start, count, k_out,   \

@@ -25,6 +25,7 @@ struct AppendArgs {
     int32_t lo_k, lo_v;  // quantile positions: lo = floor(kappa (d-1))
     float t_k, t_v;      // and t = kappa (d-1) - lo
     int32_t codec;       // WUSHKV_CODEC_PCLIP (Eq. (7)) or WUSHKV_CODEC_QUEST (Eq. (5))
+    int32_t levels;      // 2^b - 1 for b-bit codes (b = 3 codes sit in 4-bit fields)
     double quest_coef;   // QuEST: 2 alpha_b / (2^bits - 1)
     const uint16_t *k_new;
     const uint16_t *v_new;
@@ -301,20 +302,21 @@ __device__ __forceinline__ uint32_t code_of(float x, float z, float inv, float l
 // The zero is the offset of the lowest bin centre, scale (1/2 - 2^(bits-1)),
 // exact in fp32 and rounded to fp16.
 // Eq. (5) parameters from the group's sum of squares ss (fp64).
-template <int D, int BITS>
-__device__ __forceinline__ void quest_finish(double ss, double coef, uint32_t &s16, uint32_t &z16,
-                                             float &z, float &inv)
+// half = 2^(b-1) for b-bit codes.
+template <int D>
+__device__ __forceinline__ void quest_finish(double ss, double coef, float half, uint32_t &s16,
+                                             uint32_t &z16, float &z, float &inv)
 {
     const float step = (float)(coef * sqrt(ss / (double)D));
     s16 = f32_to_f16_bits(step);
     const float s = f16_bits_to_f32(s16);
-    z16 = f32_to_f16_bits(s * (0.5f - (float)(1 << (BITS - 1))));
+    z16 = f32_to_f16_bits(s * (0.5f - half));
     z = f16_bits_to_f32(z16);
     inv = (s > 0.0f) ? 1.0f / s : 0.0f;
 }
 
-template <int D, int BITS>
-__device__ __forceinline__ void quest_params(const uint16_t *row, int hf, double coef,
+template <int D>
+__device__ __forceinline__ void quest_params(const uint16_t *row, int hf, double coef, float h_levels,
                                              uint32_t &s16, uint32_t &z16, float &z, float &inv)
 {
     const uint16_t *half = row + hf * (D / 2);
@@ -335,7 +337,7 @@ __device__ __forceinline__ void quest_params(const uint16_t *row, int hf, double
     const uint32_t plo = __builtin_bit_cast(uint32_t, pair_swap(__builtin_bit_cast(float, (uint32_t)u)));
     const uint32_t phi = __builtin_bit_cast(uint32_t, pair_swap(__builtin_bit_cast(float, (uint32_t)(u >> 32))));
     ss += __builtin_bit_cast(double, ((uint64_t)phi << 32) | plo);
-    quest_finish<D, BITS>(ss, coef, s16, z16, z, inv);
+    quest_finish<D>(ss, coef, h_levels, s16, z16, z, inv);
 }
 
 // clamp(floor(x inv) + 2^(bits-1), 0, levels) of Eq. (5), as code_of.
@@ -457,10 +459,11 @@ __device__ void quantise_tile(const AppendArgs &a, const uint16_t *kt, uint16_t 
             const uint16_t *row = (is_v ? vt : kt) + r * kPitch;
             uint32_t s16, z16;
             float z, inv;
-            constexpr int kLevels = (1 << BITS) - 1;
+            const int kLevels = a.levels;             // 2^b - 1 (b = 3 in 4-bit fields)
+            const float kMid = (float)((kLevels + 1) / 2);  // 2^(b-1)
             const bool quest = a.codec == WUSHKV_CODEC_QUEST;
             if (quest) {
-                quest_params<D, BITS>(row, hf, a.quest_coef, s16, z16, z, inv);
+                quest_params<D>(row, hf, a.quest_coef, kMid, s16, z16, z, inv);
             } else {
                 const int qlo = is_v ? a.lo_v : a.lo_k;
                 const float qt = is_v ? a.t_v : a.t_k;
@@ -522,10 +525,10 @@ __device__ void quantise_tile(const AppendArgs &a, const uint16_t *kt, uint16_t 
                     }
                 }
             };
-            constexpr float kLv = (float)kLevels;
+            const float kLv = (float)kLevels;
             if (quest) {
                 // Eq. (5): clamp(floor(x inv) + 2^(bits-1))
-                write_codes([&](float x) { return quest_code_of(x, inv, (float)(1 << (BITS - 1)), kLv); });
+                write_codes([&](float x) { return quest_code_of(x, inv, kMid, kLv); });
             } else {
                 // Eq. (7): clamp(rne((x - z) inv))
                 write_codes([&](float x) { return code_of(x, z, inv, kLv); });
@@ -613,7 +616,8 @@ __device__ void quantise_few(const AppendArgs &a, uint16_t *kt, uint16_t *vt, in
     using L = Layout<D, BITS>;
     constexpr int kPitch = D + 8;
     constexpr int kPer = D / 16;                 // channels per lane: 8 or 4
-    constexpr int kLevels = (1 << BITS) - 1;
+    const int kLevels = a.levels;                // 2^b - 1 (b = 3 in 4-bit fields)
+    const float kHalf = (float)((kLevels + 1) / 2);  // 2^(b-1)
     constexpr int kPerWord = 32 / BITS;          // key codes per word
     constexpr int kLanesPerWord = kPerWord / kPer;  // 1, 2 or 4
     const int g = tid >> 4, sl = tid & 15;
@@ -652,7 +656,7 @@ __device__ void quantise_few(const AppendArgs &a, uint16_t *kt, uint16_t *vt, in
             add(std::integral_constant<int, 1>{});
             add(std::integral_constant<int, 2>{});
             add(std::integral_constant<int, 3>{});
-            quest_finish<D, BITS>(ss, a.quest_coef, s16, z16, z, inv);
+            quest_finish<D>(ss, a.quest_coef, kHalf, s16, z16, z, inv);
         } else {
             const int qlo = is_v ? a.lo_v : a.lo_k;
             const float qt = is_v ? a.t_v : a.t_k;
@@ -668,11 +672,10 @@ __device__ void quantise_few(const AppendArgs &a, uint16_t *kt, uint16_t *vt, in
             *reinterpret_cast<uint32_t *>(pg + L::kParamOffset + 4 * r + (is_v ? 4 * kPage : 0)) =
                 s16 | (z16 << 16);
         uint32_t code[kPer];
-        constexpr float kLv = (float)kLevels;
+        const float kLv = (float)kLevels;
 #pragma unroll
         for (int e = 0; e < kPer; ++e)
-            code[e] = quest ? quest_code_of(x[e], inv, (float)(1 << (BITS - 1)), kLv)
-                            : code_of(x[e], z, inv, kLv);
+            code[e] = quest ? quest_code_of(x[e], inv, kHalf, kLv) : code_of(x[e], z, inv, kLv);
         if (!is_v) {
             // this lane's channels lie in one key word: word w of 32-channel
             // chunk jc; the lanes sharing the word OR their bits together

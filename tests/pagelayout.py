@@ -25,8 +25,14 @@ import numpy as np
 PAGE = 64
 
 
+def storage_bits(bits: int) -> int:
+    """3-bit codes are stored in the 4-bit format, one per 4-bit field with
+    its top bit zero (the header's description of bits = 3)."""
+    return 4 if bits == 3 else bits
+
+
 def page_bytes(d: int, bits: int) -> int:
-    return PAGE * (2 * d * bits // 8 + 8)
+    return PAGE * (2 * d * storage_bits(bits) // 8 + 8)
 
 
 def _v_field(bits: int, o: int, r: int) -> int:
@@ -78,6 +84,7 @@ def decode_block(block: np.ndarray, d: int, bits: int):
     kparams [64][2], vparams [64][2]) with params as fp16 bit patterns
     (scale, zero)."""
     block = np.ascontiguousarray(block, dtype=np.uint8)
+    code_bits, bits = bits, storage_bits(bits)
     region = 8 * d * bits
     kt, kch, vt, vch, kbit, vbit = _maps(d, bits)
     mask = (1 << bits) - 1
@@ -88,12 +95,14 @@ def decode_block(block: np.ndarray, d: int, bits: int):
     kcodes[kt, kch] = (kw[:, None] >> kbit[None, :]) & mask
     vcodes[vt, vch] = (vw[:, None] >> vbit[None, :]) & mask
     assert (kcodes >= 0).all() and (vcodes >= 0).all(), "layout map is not a bijection"
+    assert kcodes.max() < (1 << code_bits) and vcodes.max() < (1 << code_bits), "code out of range"
     prm = block[2 * region:2 * region + 8 * PAGE].view("<u2").reshape(2, PAGE, 2)
     return kcodes.astype(np.uint8), vcodes.astype(np.uint8), prm[0].copy(), prm[1].copy()
 
 
 def encode_block(kcodes, vcodes, kparams, vparams, d: int, bits: int) -> np.ndarray:
     """Inverse of decode_block (used to check the maps form a bijection)."""
+    bits = storage_bits(bits)
     region = 8 * d * bits
     kt, kch, vt, vch, kbit, vbit = _maps(d, bits)
     kw = (np.asarray(kcodes, np.int64)[kt, kch] << kbit[None, :]).sum(axis=1)

@@ -23,16 +23,19 @@ def test_exports_every_declared_function():
     assert wk.wushkv_abi_version() == 4
 
 
-@pytest.mark.parametrize("d,bits", [(64, 2), (64, 4), (128, 2), (128, 4)])
+@pytest.mark.parametrize("d,bits", [(64, 2), (64, 4), (128, 2), (128, 4), (64, 3), (128, 3)])
 def test_page_bytes_closed_form(d, bits):
-    # per token-head: K and V codes d*bits/8 bytes each, plus 2 x (scale, zero) fp16
-    assert wk.wushkv_page_bytes(d, bits) == 64 * (2 * d * bits // 8 + 8)
+    # per token-head: K and V codes d*bits/8 bytes each, plus 2 x (scale, zero)
+    # fp16; 3-bit codes occupy the 4-bit format
+    sb = 4 if bits == 3 else bits
+    assert wk.wushkv_page_bytes(d, bits) == 64 * (2 * d * sb // 8 + 8)
     assert pagelayout.page_bytes(d, bits) == wk.wushkv_page_bytes(d, bits)
 
 
 def test_page_bytes_rejects_unsupported():
     assert wk.wushkv_page_bytes(96, 2) == 0
-    assert wk.wushkv_page_bytes(128, 3) == 0
+    assert wk.wushkv_page_bytes(128, 1) == 0
+    assert wk.wushkv_page_bytes(128, 5) == 0
 
 
 def test_status_strings():
@@ -54,7 +57,7 @@ def _desc(**over):
 
 
 BAD = [
-    (dict(batch=0), -1), (dict(n_kv_heads=0), -1), (dict(head_dim=96), -2), (dict(bits=3), -2),
+    (dict(batch=0), -1), (dict(n_kv_heads=0), -1), (dict(head_dim=96), -2), (dict(bits=1), -2), (dict(bits=5), -2),
     (dict(s_sink=-1), -1), (dict(s_flush=0), -1), (dict(win_slots=100), -1),
     (dict(win_slots=128), -1),  # ring 124 < s_keep + s_flush - 1 = 135
     (dict(kappa_k=0.0), -1), (dict(kappa_v=1.5), -1), (dict(kappa_k=float("nan")), -1),
@@ -243,7 +246,7 @@ def test_workspace_bytes_closed_form():
     assert ws == (2 * 2) * 5 * 4 * (128 + 2) * 4 + 2 * 8 * 128 * 4 + 2 * 8 * 6 * 128 + 256
 
 
-@pytest.mark.parametrize("d,bits", [(64, 2), (64, 4), (128, 2), (128, 4)])
+@pytest.mark.parametrize("d,bits", [(64, 2), (64, 4), (128, 2), (128, 4), (128, 3)])
 def test_layout_maps_are_bijections(d, bits):
     rng = np.random.default_rng(d + bits)
     kc = rng.integers(0, 1 << bits, (64, d))

@@ -48,7 +48,8 @@ def test_tiny_config_prefill_then_decode_steps(gpu):
 
 @pytest.mark.parametrize("d,bits,G,symmetric", [(128, 2, 4, True), (128, 4, 4, False),
                                                 (64, 2, 8, False), (64, 4, 1, True),
-                                                (128, 2, 2, False), (128, 2, 8, False)])
+                                                (128, 2, 2, False), (128, 2, 8, False),
+                                                (128, 3, 4, False)])
 def test_ragged_batches(gpu, d, bits, G, symmetric):
     rng = np.random.default_rng(d * 10 + bits + G)
     B, H = 3, 2
@@ -165,7 +166,7 @@ def test_page_order_and_determinism(gpu):
 def test_dequant_bit_exact(gpu):
     import paper_2609_38121_amd as wk
     rng = np.random.default_rng(14)
-    for d, bits in [(128, 2), (128, 4), (64, 2), (64, 4)]:
+    for d, bits in [(128, 2), (128, 4), (64, 2), (64, 4), (128, 3), (64, 3)]:
         B, H = 2, 2
         p = Pair(gpu, B, H, 4, d, bits, 4, 32, 8, 0.96, 0.92, cap=500, oracle_ref=False)
         k, v = _kv(rng, B, 450, H, d)

@@ -23,7 +23,8 @@ def _q(rng, B, nq, d):
     return oracle.f32_to_bf16(rng.standard_normal((B, nq, d)).astype(np.float32))
 
 
-@pytest.mark.parametrize("d,bits,G", [(128, 2, 4), (128, 4, 1), (64, 2, 8), (64, 4, 2)])
+@pytest.mark.parametrize("d,bits,G", [(128, 2, 4), (128, 4, 1), (64, 2, 8), (64, 4, 2), (128, 3, 4),
+                                     (64, 3, 2)])
 def test_quest_ragged_prefill_and_steps(gpu, d, bits, G):
     rng = np.random.default_rng(100 + d + bits + G)
     B, H = 3, 2
@@ -91,7 +92,7 @@ def test_quest_fused_norm_rope_prefill(gpu):
 def test_quest_dequant_bit_exact(gpu):
     import paper_2609_38121_amd as wk
     rng = np.random.default_rng(102)
-    for d, bits in [(128, 2), (64, 4)]:
+    for d, bits in [(128, 2), (64, 4), (128, 3)]:
         B, H = 2, 2
         p = Pair(gpu, B, H, 4, d, bits, 4, 32, 8, 0.96, 0.92, cap=500, oracle_ref=False,
                  codec="quest")
@@ -110,7 +111,7 @@ def test_quest_dequant_bit_exact(gpu):
                 assert np.array_equal(vo[h], vref)
 
 
-@pytest.mark.parametrize("bits", [2, 4])
+@pytest.mark.parametrize("bits", [2, 3, 4])
 def test_quest_library_default_alpha(gpu, bits):
     """A QuEST cache built without an explicit clip multiplier uses the
     library's alpha_b (wushkv_quest_alpha: the stationarity condition of the

@@ -31,7 +31,8 @@ def _q(rng, B, nq, d):
 
 @pytest.mark.parametrize("d,bits,G,codec", [(128, 2, 4, "pclip"), (128, 4, 8, "pclip"),
                                             (64, 2, 1, "pclip"), (64, 4, 2, "quest"),
-                                            (128, 2, 4, "quest")])
+                                            (128, 2, 4, "quest"), (128, 3, 4, "quest"),
+                                            (64, 3, 8, "pclip")])
 def test_step_across_flushes(gpu, d, bits, G, codec):
     """Single-token steps from an empty sequence (sink slots), a short one
     and a long one, with some sequences skipping steps, across several
