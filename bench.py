@@ -65,6 +65,8 @@ def parse():
                     help="only the transform-builder leg (all K/V heads of an 8B-shaped model)")
     ap.add_argument("--scale-only", action="store_true",
                     help="only run the long-context / large-batch decode legs")
+    ap.add_argument("--chunk-only", action="store_true",
+                    help="only the Llama-shaped step and chunk-attention legs")
     ap.add_argument("--headline-only", action="store_true",
                     help="only the large-batch decode headline (no oracle, no other legs)")
     ap.add_argument("--seed", type=int, default=0)
@@ -186,6 +188,11 @@ def main():
         return
     if args.wush_only:
         print(json.dumps(bench_wush(torch, wk, dev, args)), flush=True)
+        return
+
+    if args.chunk_only:
+        _, state = bench_llama_step(torch, wk, synth, dev, args)
+        print(json.dumps(bench_chunk(torch, wk, *state)), flush=True)
         return
 
     # ---- headline: large-batch decode (timed first, on a fresh device)
@@ -791,8 +798,9 @@ def bench_chunk(torch, wk, caches, reps, k1, tk, tinv, B, NQ, D, max_seq, sm, cf
             "gbps_algorithmic": round(byts / t / 1e9, 1),
             "note": "16-token chunks on the 8192-token Llama-shaped cache; bytes_per_call counts "
                     "the cache once.  Two chunk tokens x 4 query heads make a group of 8 virtual "
-                    "heads, and a workgroup's four waves walk one run of pages for four groups, "
-                    "so each page leaves HBM twice per call"}
+                    "heads; a page workgroup takes the 64 query rows of all eight groups of a "
+                    "sequence over its run, so each page leaves HBM once per call.  Launches: "
+                    "q~ rows, the page runs, then the window slots merged with the runs"}
 
 
 def bench_stream_read(torch, wk, dev, gib=2, reps=10):

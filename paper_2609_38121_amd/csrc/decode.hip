@@ -1261,6 +1261,707 @@ decode_main_kernel(DecodeArgs a)
     }
 }
 
+// ------------------------------------------------------------------ chunk pages
+
+// The quantised pages of chunk attention (Alg. 2 step 5 with S' > 1) at
+// d = 128.  One workgroup per (kv head, run of pages, sequence, block of
+// eight token groups) takes all 64 query rows of the block -- (chunk token,
+// query head) pairs, eight token groups of G = 8 rows, row r of the block in
+// token group r / 8 -- so that each page leaves HBM once and its codes are
+// unpacked once.  Pages stream through three LDS slots that the four waves
+// share (each wave loads its part of every page).  Per page:
+//   scores  wave w takes rows 16 w .. 16 w + 15: one scaled product per
+//           limb and 16 tokens, whose A rows are the 16 query rows' fp8
+//           digits of that limb (held in registers for the whole run, each
+//           row with its own E8M0 scale) and whose B columns are the fp4 /
+//           fp8 key codes, accumulated over the six limbs; lane (j, n) then
+//           holds rows 16 w + 4 j + r of tokens 4 n .. 4 n + 3, runs their
+//           online softmax and writes their weights (fp16 hi + lo) and
+//           rescale factors to LDS;
+//   P V     wave w takes channel tiles 2 w, 2 w + 1 of all 64 rows: the
+//           weights times its value codes widened to fp16 subnormals.
+// The chunk lies in the recent window (every quantised position precedes
+// it), so no mask applies.  Each row's partial (o, m, l) goes where the
+// decode kernel writes it; the window slots are left to that kernel.
+// Byte offset of byte `byte` of a 128-byte weight row `row`: the 16-byte
+// chunks of row r are stored in the order chunk ^ (r % 8), so that the rows
+// one instruction reads together fall in distinct LDS banks.
+__device__ __forceinline__ uint32_t tbuf_at(int row, int byte)
+{
+    return (uint32_t)(row * 128 + ((((byte >> 4) ^ (row & 7)) << 4) | (byte & 15)));
+}
+
+template <int BITS>
+struct ChunkLds {
+    using L = Layout<128, BITS>;
+    static constexpr int kRows = 64;
+    static constexpr int kSlots = 4;
+    static constexpr int kSlot = (L::kPageBytes + 15) / 16 * 16;
+    static constexpr int kWBytes = 2 * kRows * 128;          // weights: hi plane, lo plane
+    static constexpr int kWAt = 0;                           // two buffers (page parity)
+    static constexpr int kAlphaAt = kWAt + 2 * kWBytes;      // per row: rescale factors, two buffers
+    static constexpr int kZAt = kAlphaAt + 2 * kRows * 4;    // per row at the end: z term, m, l
+    static constexpr int kMAt = kZAt + kRows * 4;
+    static constexpr int kLAt = kMAt + kRows * 4;
+    static constexpr int kSlotAt = kLAt + kRows * 4;
+    static constexpr int kBytes = kSlotAt + kSlots * kSlot;
+};
+
+// One limb's scaled product: A = limb L of 16 query rows, whose E8M0 scale
+// is byte L % 4 of the lane's packed scale word (the instruction's byte
+// select), B = 16 tokens' key codes.
+template <int L, int FMT_B, int SCALE_B>
+__device__ __forceinline__ f32x4 limb_product(const i32x8 &a, const i32x8 &b, int scales, f32x4 c)
+{
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, FMT_B, L % 4, scales, 0, SCALE_B);
+}
+
+template <int BITS>
+__global__ void __launch_bounds__(256, 2) chunk_pages_kernel(DecodeArgs a)
+{
+    constexpr int D = 128, G = 8;
+    using L = Layout<D, BITS>;
+    using C = ChunkLds<BITS>;
+    constexpr int kDma = (L::kPageBytes + 1023) / 1024;  // direct-to-LDS loads per page
+    constexpr int kNTw = L::kNTiles / 4;                  // channel tiles per wave
+    constexpr int kFmtB = BITS == 2 ? 4 : 0;
+    constexpr int kScaleB = BITS == 2 ? 128 : 136;
+    constexpr int kKX = L::kKWordsPerLane / 4;            // key chunks per lane
+    constexpr int kOpw = L::kOpsPerWord;
+    constexpr float kOutScale = BITS == 2 ? 262144.0f : 1048576.0f;
+    __shared__ __attribute__((aligned(16))) uint8_t lds[C::kBytes];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int j = lane >> 4, n = lane & 15;
+    const int h = blockIdx.x, split = blockIdx.y;
+    const int n_blocks = (a.n_groups + 7) / 8;
+    const int b = (int)blockIdx.z / n_blocks, tg0 = 8 * ((int)blockIdx.z % n_blocks);
+    const int32_t S = a.seq_len[b];
+    int32_t qend = a.quant_end[b];
+    qend = qend < S ? qend : S;
+    const int32_t q_hi = qend > a.s_sink ? qend : a.s_sink;  // quantised: [s_sink, q_hi)
+    const int32_t n_qpages = (q_hi - a.s_sink + kPage - 1) / kPage;
+    const int upw = a.units_per_wave;  // pages of a workgroup's run (at most 64)
+    const int w0 = split * upw;
+    const int w1 = min(w0 + upw, n_qpages);
+    int32_t tbl = -1;
+    if (w0 + lane < w1 && w0 + lane < a.max_pages) tbl = a.page_table[(int64_t)b * a.max_pages + w0 + lane];
+
+    // The wave's 16 query rows 16 w .. 16 w + 15 of the block's 64 (rows
+    // past the chunk's token groups have zero limbs).  Lane (j, n) holds the
+    // A operands of row 16 w + n, K bytes 32 j .., one per limb, and that
+    // row's packed limb scales; its scores are rows 16 w + 4 j + r (r < 4),
+    // whose sums of q~ it keeps.
+    auto row_of = [&](int r64) -> int64_t {
+        const int tg = tg0 + r64 / G;
+        return tg < a.n_groups ? (((int64_t)b * a.n_groups + tg) * a.n_kv + h) * G + r64 % G : -1;
+    };
+    i32x8 qa[kLimbs];
+    int sc03 = 0, sc45 = 0;
+    {
+        const int64_t row = row_of(16 * wave + n);
+#pragma unroll
+        for (int l = 0; l < kLimbs; ++l) {
+            u32x4 x0 = {0u, 0u, 0u, 0u}, x1 = x0;
+            if (row >= 0) {
+                const uint8_t *src = a.qlimb + row * (kLimbs * 128) + l * 128 + 32 * j;
+                x0 = *reinterpret_cast<const u32x4 *>(src);
+                x1 = *reinterpret_cast<const u32x4 *>(src + 16);
+            }
+            qa[l] = i32x8{(int)x0[0], (int)x0[1], (int)x0[2], (int)x0[3],
+                          (int)x1[0], (int)x1[1], (int)x1[2], (int)x1[3]};
+        }
+        if (row >= 0) {
+            sc03 = (int)a.qaux[4 * row];
+            sc45 = (int)a.qaux[4 * row + 1];
+        }
+    }
+    float zs[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int64_t row = row_of(16 * wave + 4 * j + r);
+        zs[r] = row >= 0 ? __uint_as_float(a.qaux[4 * row + 2]) : 0.0f;
+    }
+
+    const uint32_t lbase = lds_addr(lds);
+    // This wave's share of each page's loads: loads i = wave, wave + 4, ..
+    constexpr int kMine0 = (kDma + 3) / 4;  // (wave 0 takes the most)
+    const int n_mine = (kDma - wave + 3) / 4;
+    auto issue = [&](int u, int slot) {
+        int32_t phys = __builtin_amdgcn_readlane(tbl, u - w0);
+        if (phys < 0 || phys >= a.n_pages) phys = 0;  // (its data is never used)
+        const uint8_t *src = a.pages + ((int64_t)phys * a.n_kv + h) * L::kPageBytes + 16 * lane;
+        const uint32_t dst = __builtin_amdgcn_readfirstlane(lbase + C::kSlotAt + slot * C::kSlot);
+#pragma unroll
+        for (int i0 = 0; i0 < kMine0; ++i0) {
+            const int i = wave + 4 * i0;
+            if (i < kDma && (i + 1 < kDma || 1024 * i + 16 * lane < L::kPageBytes))
+                dma16(src + 1024 * i, dst + 1024 * i);
+        }
+    };
+    // at most `pages` of this wave's page loads still in flight
+    auto wait_pages = [&](int pages) {
+        const int after = pages * n_mine;
+        if (after <= 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        else if (after == 1) asm volatile("s_waitcnt vmcnt(1)" ::: "memory");
+        else if (after == 2) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+        else asm volatile("s_waitcnt vmcnt(3)" ::: "memory");
+    };
+    static_assert(kMine0 <= 3, "at most three loads per wave and page");
+
+    // per-row state of the lane's score rows 16 w + 4 j + r, in units of
+    // 2^-off (the value widening's field offset, as in decode)
+    const float off = BITS == 2 ? 2.0f * (n & 1) : 0.0f;
+    float m_run[4], lc[4], zc[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        m_run[r] = -INFINITY;
+        lc[r] = zc[r] = 0.0f;
+    }
+    f32x4 acc[4][kNTw];
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+        for (int c = 0; c < kNTw; ++c) acc[rt][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // Page u sits in slot (u - w0) % 4 and writes its weights and rescale
+    // factors to buffer (u - w0) % 2; its P V runs in the next iteration.
+    auto slot_at = [&](int u) -> uint32_t { return lbase + C::kSlotAt + ((u - w0) & 3) * C::kSlot; };
+    auto wbuf_at = [&](int u) -> uint32_t { return lbase + C::kWAt + ((u - w0) & 1) * C::kWBytes; };
+    auto alpha_at = [&](int u) -> float * {
+        return reinterpret_cast<float *>(lds + C::kAlphaAt) + ((u - w0) & 1) * C::kRows;
+    };
+    // tokens of page u that hold keys (0 for an entry outside the pool)
+    auto page_valid = [&](int u) -> int32_t {
+        const int32_t phys = __builtin_amdgcn_readlane(tbl, u - w0);
+        return (phys < 0 || phys >= a.n_pages) ? 0 : min(kPage, q_hi - (a.s_sink + u * kPage));
+    };
+    // the score products of page u: c[t][r] = q~ . codes of row 16 w + 4 j
+    // + r and token 4 n + t, the limbs accumulated in order (each product's
+    // block sums are exact); kp, vp the key and value parameters of the
+    // lane's tokens
+    auto score_products = [&](int u, f32x4 (&c)[4], u32x4 &kp, u32x4 &vp) {
+        const uint32_t pg = slot_at(u);
+        u32x4 kx[kKX];
+#pragma unroll
+        for (int q4 = 0; q4 < kKX; ++q4) kx[q4] = lds_read16(pg + 4 * L::k_word(lane, 4 * q4));
+        kp = lds_read16(pg + L::kParamOffset + 16 * n);
+        vp = lds_read16(pg + L::kParamOffset + 4 * kPage + 16 * n);
+        i32x8 bop[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            uint32_t w[BITS];
+#pragma unroll
+            for (int i = 0; i < BITS; ++i) w[i] = kx[(BITS * t + i) / 4][(BITS * t + i) % 4];
+            if constexpr (BITS == 2) {
+                bop[t] = i32x8{(int)(w[0] & 0x33333333u), (int)((w[0] >> 2) & 0x33333333u),
+                               (int)(w[1] & 0x33333333u), (int)((w[1] >> 2) & 0x33333333u), 0, 0, 0, 0};
+            } else {
+                bop[t] = i32x8{(int)(w[0] & 0x0F0F0F0Fu), (int)((w[0] >> 4) & 0x0F0F0F0Fu),
+                               (int)(w[1] & 0x0F0F0F0Fu), (int)((w[1] >> 4) & 0x0F0F0F0Fu),
+                               (int)(w[2] & 0x0F0F0F0Fu), (int)((w[2] >> 4) & 0x0F0F0F0Fu),
+                               (int)(w[3] & 0x0F0F0F0Fu), (int)((w[3] >> 4) & 0x0F0F0F0Fu)};
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) c[t] = limb_product<0, kFmtB, kScaleB>(qa[0], bop[t], sc03, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+        for (int t = 0; t < 4; ++t) c[t] = limb_product<1, kFmtB, kScaleB>(qa[1], bop[t], sc03, c[t]);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) c[t] = limb_product<2, kFmtB, kScaleB>(qa[2], bop[t], sc03, c[t]);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) c[t] = limb_product<3, kFmtB, kScaleB>(qa[3], bop[t], sc03, c[t]);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) c[t] = limb_product<4, kFmtB, kScaleB>(qa[4], bop[t], sc45, c[t]);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) c[t] = limb_product<5, kFmtB, kScaleB>(qa[5], bop[t], sc45, c[t]);
+    };
+    // the online softmax of page u over the products: the weights (fp16
+    // hi + lo) and rescale factors of the wave's rows into LDS; tail: mask
+    // the tokens past nvalid
+    auto softmax = [&](int u, const f32x4 (&c)[4], const u32x4 &kp, const u32x4 &vp, bool tail,
+                       int32_t nvalid) {
+        const uint32_t wbase = wbuf_at(u);
+        float *alpha = alpha_at(u);
+        float ks[4], kz[4], vs[4], vz[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            ks[t] = f16_bits_to_f32(kp[t] & 0xFFFFu);
+            kz[t] = f16_bits_to_f32(kp[t] >> 16);
+            vs[t] = f16_bits_to_f32(vp[t] & 0xFFFFu);
+            vz[t] = f16_bits_to_f32(vp[t] >> 16);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int rz = 16 * wave + 4 * j + r;  // the row, in the block's 64
+            float lg[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) lg[t] = fmaf(ks[t], c[t][r], kz[t] * zs[r]);
+            if (tail) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    if (4 * n + t >= nvalid) lg[t] = -INFINITY;
+            }
+            // online softmax of row rz over this page's tokens 4 n .. 4 n + 3
+            const float mx = row_max16(fmaxf(fmaxf(lg[0], lg[1]), fmaxf(lg[2], lg[3])));
+            const float m_new = fmaxf(m_run[r], mx);
+            const float al = m_new == -INFINITY ? 1.0f : fexp2(m_run[r] - m_new);
+            lc[r] *= al;
+            zc[r] *= al;
+            m_run[r] = m_new;
+            alpha[rz] = al;  // (the row's 16 lanes store the same value)
+            const float mo = m_new == -INFINITY ? 0.0f : m_new + off;
+            float wgt[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const float pw = fexp2(lg[t] - mo);
+                lc[r] += pw;
+                zc[r] = fmaf(pw, vz[t], zc[r]);
+                wgt[t] = fmaf(pw, vs[t], 0.0f);
+            }
+            const uint32_t h01 = pack_f16_rne(wgt[0], wgt[1]);
+            const uint32_t h23 = pack_f16_rne(wgt[2], wgt[3]);
+            const uint32_t l01 = pack_f16_rne(fmaf(-1.0f, f16_bits_to_f32(h01 & 0xFFFFu), wgt[0]),
+                                              fmaf(-1.0f, f16_bits_to_f32(h01 >> 16), wgt[1]));
+            const uint32_t l23 = pack_f16_rne(fmaf(-1.0f, f16_bits_to_f32(h23 & 0xFFFFu), wgt[2]),
+                                              fmaf(-1.0f, f16_bits_to_f32(h23 >> 16), wgt[3]));
+            lds_write8(wbase + tbuf_at(rz, 8 * n), h01, h23);
+            lds_write8(wbase + C::kRows * 128 + tbuf_at(rz, 8 * n), l01, l23);
+        }
+    };
+    // P V of page u: all 64 rows, this wave's channel tiles
+    auto pv = [&](int u) {
+        // lane (j, n) holds query rows 16 rt + 4 j + i (i < 4) of row tile
+        // rt; the hi and lo weights are two products into the same sums
+        const uint32_t pg = slot_at(u);
+        const uint32_t wbase = wbuf_at(u);
+        const float *alpha = alpha_at(u);
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) {
+            const f32x4 al = *reinterpret_cast<const f32x4 *>(alpha + 16 * rt + 4 * j);
+#pragma unroll
+            for (int c = 0; c < kNTw; ++c)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[rt][c][i] *= al[i];
+        }
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) {
+            // this wave's value codes for tokens 32 kc .., channel tiles
+            // kNTw w .. (words vw = nt / kOpw of the lane)
+            uint32_t op[kNTw][4];
+#pragma unroll
+            for (int cw = 0; cw < kNTw / kOpw; ++cw) {
+                const int vw = (kNTw * wave) / kOpw + cw;
+                const uint32_t word = *(const __attribute__((address_space(3))) uint32_t *)(uintptr_t)(
+                    pg + L::kRegionBytes + 4 * L::v_word(lane, kc * 2 * L::kNw + vw));
+                uint32_t wide[L::kCodesPerWord / 2];
+                widen_word_f16<BITS>(word, wide);
+#pragma unroll
+                for (int o = 0; o < kOpw; ++o)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) op[cw * kOpw + o][q] = wide[4 * o + q];
+            }
+#pragma unroll
+            for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+                for (int part = 0; part < 2; ++part) {
+                    const f16x8 A = __builtin_bit_cast(
+                        f16x8, lds_read16(wbase + part * C::kRows * 128 + tbuf_at(16 * rt + n, 64 * kc + 16 * j)));
+#pragma unroll
+                    for (int c = 0; c < kNTw; ++c) acc[rt][c] = mfma16h(A, as_op_h(op[c]), acc[rt][c]);
+                }
+        }
+    };
+
+    // Software pipeline over the run, one barrier per page: iteration u
+    // waits for page u's loads, then (barrier) issues page u + 2 into the
+    // slot page u - 2 has left, runs the P V of page u - 1 (its weights
+    // complete) and the scores of page u.
+    const bool run = a.n_pages > 0 && w0 < w1;
+    if (run) {
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // the page table and query reads have returned
+        issue(w0, 0);
+        if (w0 + 1 < w1) issue(w0 + 1, 1);
+        wait_pages(w0 + 1 < w1 ? 1 : 0);
+        __syncthreads();
+        if (w0 + 2 < w1) issue(w0 + 2, 2);
+        {
+            f32x4 c[4];
+            u32x4 kp, vp;
+            const int32_t nv = page_valid(w0);
+            score_products(w0, c, kp, vp);
+            softmax(w0, c, kp, vp, nv < kPage, nv);
+        }
+        for (int u = w0 + 1; u < w1; ++u) {
+            wait_pages(u + 1 < w1 ? 1 : 0);
+            __syncthreads();  // page u is in; page u - 1's weights are written
+            if (u + 2 < w1) issue(u + 2, (u + 2 - w0) & 3);
+            const int32_t nv = page_valid(u);
+            f32x4 c[4];
+            u32x4 kp, vp;
+            if (nv == kPage) {
+                // a full page: one branch-free region, page u's products and
+                // page u - 1's P V interleaved with the softmax arithmetic
+                score_products(u, c, kp, vp);
+                pv(u - 1);
+                softmax(u, c, kp, vp, false, kPage);
+#pragma unroll
+                for (int i = 0; i < 24; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // a score product
+                    __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);  // vector arithmetic
+                }
+#pragma unroll
+                for (int i = 0; i < 32; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // a P V product
+                    __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+                }
+            } else {
+                pv(u - 1);
+                score_products(u, c, kp, vp);
+                softmax(u, c, kp, vp, true, nv);
+            }
+        }
+        __syncthreads();
+        pv(w1 - 1);
+    }
+
+    // ---- partials: each row's m, l and z term from its owner wave, then
+    // every wave its channel tiles of o
+    float *zrow = reinterpret_cast<float *>(lds + C::kZAt);
+    float *mrow = reinterpret_cast<float *>(lds + C::kMAt);
+    float *lrow = reinterpret_cast<float *>(lds + C::kLAt);
+    {
+        const float f = ldexpf(1.0f, (int)off);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float zt = row_sum16(zc[r] * f);
+            const float lt = row_sum16(lc[r] * f);
+            if (n == 0) {
+                const int rz = 16 * wave + 4 * j + r;
+                zrow[rz] = zt;
+                mrow[rz] = m_run[r];
+                lrow[rz] = lt;
+            }
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = 16 * rt + 4 * j + i;
+            const int tg = tg0 + r / G;
+            if (tg >= a.n_groups) continue;
+            const int64_t bzr = (int64_t)b * a.n_groups + tg;
+            float *pr = a.part + ((bzr * a.n_kv + h) * a.n_splits + split) * G * (D + 2) + (r % G) * (D + 2);
+            const float mx = mrow[r];
+#pragma unroll
+            for (int c = 0; c < kNTw; ++c) {
+                const int ch = 16 * (kNTw * wave + c) + n;
+                pr[ch] = mx == -INFINITY ? 0.0f : fmaf(acc[rt][c][i], kOutScale, zrow[r]);
+            }
+            if (wave == 0 && n == 0) {
+                pr[D] = mx;
+                pr[D + 1] = lrow[r];
+            }
+        }
+}
+
+// ------------------------------------------------------------------ chunk windows
+
+// The bf16 window slots of chunk attention at d = 128, merged with the page
+// runs of chunk_pages_kernel into the output (so no combine launch follows).
+// One workgroup per (kv head, sequence, block of eight token groups): the
+// block's 64 query rows, wave w rows 16 w .. 16 w + 15, as in the page
+// kernel.  The window streams through LDS one 64-slot unit at a time (keys
+// and channel-major values, two buffers, filled by direct-to-LDS loads);
+// per unit and wave:
+//   scores  q~ in bf16 hi + lo parts (A, 16 rows) times the unit's keys,
+//           tile t column n the slot 4 n + t, so that lane (j, n) holds rows
+//           4 j + r of slots 4 n .. 4 n + 3; causal and live-slot masks;
+//   softmax online across the units; the lane's rows are its P V rows, so
+//           the rescale stays in the lane;
+//   P V     weights (bf16 hi, lo: two products) through a per-wave LDS
+//           buffer, times the values (dead slots' values zeroed).
+// Then each row's window result and its page-run partials merge by
+// log-sum-exp, as decode_combine_kernel does.
+struct ChunkWinLds {
+    static constexpr int kUnitK = 64 * 256;                 // [slot][16 chunks of 16 B]
+    static constexpr int kUnitV = 128 * 128;                // [channel][8 chunks of 16 B]
+    static constexpr int kKAt = 0;                          // two unit buffers each
+    static constexpr int kVAt = kKAt + 2 * kUnitK;
+    static constexpr int kPWave = 2 * 16 * 128;             // [part][16 rows][64 slots] bf16
+    static constexpr int kPAt = kVAt + 2 * kUnitV;
+    static constexpr int kBytes = kPAt + 4 * kPWave;
+};
+
+__global__ void __launch_bounds__(256, 1) chunk_window_kernel(DecodeArgs a, float *out)
+{
+    constexpr int D = 128, G = 8;
+    using W = ChunkWinLds;
+    __shared__ __attribute__((aligned(16))) uint8_t lds[W::kBytes];
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int j = lane >> 4, n = lane & 15;
+    const int h = blockIdx.x;
+    const int n_blocks = (a.n_groups + 7) / 8;
+    const int b = (int)blockIdx.y / n_blocks, tg0 = 8 * ((int)blockIdx.y % n_blocks);
+    const int32_t S = a.seq_len[b];
+    int32_t qend = a.quant_end[b];
+    qend = qend < S ? qend : S;
+    const int32_t q_hi = qend > a.s_sink ? qend : a.s_sink;
+    const int32_t ring = a.win_slots - a.s_sink;
+    // the ring holds positions [q_hi, S); the oldest sits at ring index a0
+    const int32_t a0 = S > q_hi ? (q_hi - a.s_sink) % ring : 0;
+    const int32_t ring_live = S > q_hi ? S - q_hi : 0;
+    const int32_t nb = chunk_tokens(a.n_tok, a.max_tok, b, S);
+    const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;
+    const int n_units = a.win_slots / kPage;
+    const uint32_t lbase = lds_addr(lds);
+
+    // row rr of the block (0 .. 63): its q~ row, chunk token and query head
+    auto qt_row = [&](int rr) -> int64_t {
+        const int tg = tg0 + rr / G;
+        return tg < a.n_groups ? (((int64_t)b * a.n_groups + tg) * a.n_kv + h) * G + rr % G : -1;
+    };
+    auto chunk_tok = [&](int rr) -> int32_t { return (tg0 + rr / G) * a.tpg + (rr % G) / a.g_real; };
+
+    // unit u's keys and values into buffer u % 2: wave w the 1 KB rows
+    // w, w + 4, .. of each; LDS chunk p of the keys is slot p / 16, chunk
+    // (p % 16) ^ ((slot / 4) % 16); of the values channel p / 8, chunk
+    // (p % 8) ^ (channel % 8) (the readers' bank swizzles)
+    auto issue = [&](int u) {
+        const int32_t unit0 = u * kPage;
+        const uint32_t kdst = lbase + W::kKAt + (u & 1) * W::kUnitK;
+        const uint32_t vdst = lbase + W::kVAt + (u & 1) * W::kUnitV;
+#pragma unroll
+        for (int i0 = 0; i0 < 4; ++i0) {
+            const int i = wave + 4 * i0;
+            const int pk = 64 * i + lane;
+            const int slot = pk >> 4, ck = (pk & 15) ^ ((slot >> 2) & 15);
+            dma16(a.win_k + (head_win + unit0 + slot) * D + 8 * ck, __builtin_amdgcn_readfirstlane(kdst + 1024 * i));
+            const int ch = pk >> 3, cv = (pk & 7) ^ (ch & 7);
+            dma16(a.win_v + head_win * D + (int64_t)ch * a.win_slots + unit0 + 8 * cv,
+                  __builtin_amdgcn_readfirstlane(vdst + 1024 * i));
+        }
+    };
+    if (n_units > 0) issue(0);
+
+    // A operands: q~ of row 16 w + n (lane n), channels 32 c + 8 j .., as
+    // bf16 hi and lo parts
+    bf16x8 qh[4], ql[4];
+    {
+        const int64_t row = qt_row(16 * wave + n);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
+            if (row >= 0) {
+                const float *src = a.qt + row * D + 32 * c + 8 * j;
+                const f32x4 x0 = *reinterpret_cast<const f32x4 *>(src);
+                const f32x4 x1 = *reinterpret_cast<const f32x4 *>(src + 4);
+                const float x[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+#pragma unroll
+                for (int pp = 0; pp < 4; ++pp) {
+                    hi[pp] = pack_bf16_rne(x[2 * pp], x[2 * pp + 1]);
+                    lo[pp] = pack_bf16_rne(x[2 * pp] - bf16_bits_to_f32(hi[pp] & 0xFFFFu),
+                                           x[2 * pp + 1] - bf16_bits_to_f32(hi[pp] >> 16));
+                }
+            }
+            qh[c] = __builtin_bit_cast(bf16x8, u32x4{hi[0], hi[1], hi[2], hi[3]});
+            ql[c] = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], lo[2], lo[3]});
+        }
+    }
+    // the lane's rows 16 w + 4 j + r: chunk token (or -1: no such row)
+    int32_t trow[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int rr = 16 * wave + 4 * j + r;
+        trow[r] = qt_row(rr) >= 0 ? chunk_tok(rr) : -1;
+    }
+
+    float m_run[4], lsum[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        m_run[r] = -INFINITY;
+        lsum[r] = 0.0f;
+    }
+    f32x4 acc[8];  // P V: lane (j, n) rows 4 j + i, channel 16 nt + n
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const uint32_t pbuf = lbase + W::kPAt + wave * W::kPWave;
+
+    for (int u = 0; u < n_units; ++u) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's loads of unit u
+        __syncthreads();  // every wave's loads of unit u; unit u - 1's buffers are read
+        if (u + 1 < n_units) issue(u + 1);
+        const int32_t unit0 = u * kPage;
+        const uint32_t kb = lbase + W::kKAt + (u & 1) * W::kUnitK;
+        const uint32_t vb = lbase + W::kVAt + (u & 1) * W::kUnitV;
+        // the lane's slots 4 n + t: live, and their positions
+        int32_t pos[4];
+        bool live[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int32_t sl = unit0 + 4 * n + t;
+            const int32_t ri = (sl - a.s_sink - a0 + ring) % ring;
+            live[t] = sl < a.s_sink ? sl < S : ri < ring_live;
+            pos[t] = sl < a.s_sink ? sl : q_hi + ri;
+        }
+        // slots of the unit that hold a position (bit s: slot unit0 + s,
+        // lane s answers)
+        uint64_t live_mask;
+        {
+            const int32_t sl = unit0 + lane;
+            const int32_t ri = (sl - a.s_sink - a0 + ring) % ring;
+            live_mask = __ballot(sl < a.s_sink ? sl < S : ri < ring_live);
+        }
+        if (live_mask == 0) continue;
+
+        // ---- scores
+        f32x4 sc[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            sc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+            const uint32_t krow = kb + (4 * n + t) * 256;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const bf16x8 kk = __builtin_bit_cast(bf16x8, lds_read16(krow + 16 * ((4 * c + j) ^ n)));
+                sc[t] = mfma16(qh[c], kk, sc[t]);
+                sc[t] = mfma16(ql[c], kk, sc[t]);
+            }
+        }
+        // ---- online softmax of the lane's rows over the unit
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            float lg[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const bool vis = live[t] && trow[r] >= 0 && trow[r] < nb && pos[t] <= S - nb + trow[r];
+                lg[t] = vis ? sc[t][r] : -INFINITY;
+            }
+            const float mx = row_max16(fmaxf(fmaxf(lg[0], lg[1]), fmaxf(lg[2], lg[3])));
+            const float m_new = fmaxf(m_run[r], mx);
+            const float al = m_new == -INFINITY ? 1.0f : fexp2(m_run[r] - m_new);
+            m_run[r] = m_new;
+            lsum[r] *= al;
+#pragma unroll
+            for (int nt = 0; nt < 8; ++nt) acc[nt][r] *= al;
+            uint32_t hw[2], lw[2];
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+                const float p0 = m_new == -INFINITY ? 0.0f : fexp2(lg[2 * e] - m_new);
+                const float p1 = m_new == -INFINITY ? 0.0f : fexp2(lg[2 * e + 1] - m_new);
+                lsum[r] += p0 + p1;
+                hw[e] = pack_bf16_rne(p0, p1);
+                lw[e] = pack_bf16_rne(p0 - bf16_bits_to_f32(hw[e] & 0xFFFFu), p1 - bf16_bits_to_f32(hw[e] >> 16));
+            }
+            lds_write8(pbuf + tbuf_at(4 * j + r, 8 * n), hw[0], hw[1]);
+            lds_write8(pbuf + 16 * 128 + tbuf_at(4 * j + r, 8 * n), lw[0], lw[1]);
+        }
+        // ---- P V (the weight buffer is the wave's own: no barrier)
+        const bool dead = ~live_mask != 0;
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) {
+            const bf16x8 ph = __builtin_bit_cast(bf16x8, lds_read16(pbuf + tbuf_at(n, 64 * kc + 16 * j)));
+            const bf16x8 pl = __builtin_bit_cast(bf16x8, lds_read16(pbuf + 16 * 128 + tbuf_at(n, 64 * kc + 16 * j)));
+            // dead slots 32 kc + 8 j + e: their values are zeroed
+            uint32_t msk[4] = {~0u, ~0u, ~0u, ~0u};
+            if (dead) {
+                const uint32_t bits8 = (uint32_t)(live_mask >> (32 * kc + 8 * j)) & 0xFFu;
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    msk[q] = ((bits8 >> (2 * q)) & 1u ? 0x0000FFFFu : 0u) | ((bits8 >> (2 * q + 1)) & 1u ? 0xFFFF0000u : 0u);
+            }
+#pragma unroll
+            for (int nt = 0; nt < 8; ++nt) {
+                const int ch = 16 * nt + n;
+                u32x4 v = lds_read16(vb + ch * 128 + 16 * ((4 * kc + j) ^ (ch & 7)));
+#pragma unroll
+                for (int q = 0; q < 4; ++q) v[q] &= msk[q];
+                const bf16x8 vv = __builtin_bit_cast(bf16x8, v);
+                acc[nt] = mfma16(ph, vv, acc[nt]);
+                acc[nt] = mfma16(pl, vv, acc[nt]);
+            }
+        }
+    }
+
+    // ---- merge with the page runs and write the rows.  The window
+    // partials go through LDS (the unit buffers are free now); then thread
+    // (row tid / 4, channels 32 (tid % 4) ..) merges its row's splits, the
+    // loads of several splits in flight together.
+#pragma unroll
+    for (int r = 0; r < 4; ++r) lsum[r] = row_sum16(lsum[r]);
+    __syncthreads();  // every wave is past its last unit
+    float *wo = reinterpret_cast<float *>(lds + W::kKAt);  // [64 rows][D]
+    float *wml = wo + 64 * D;                               // [64 rows][m, l]
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int rr = 16 * wave + 4 * j + i;
+#pragma unroll
+        for (int nt = 0; nt < 8; ++nt) wo[rr * D + 16 * nt + n] = acc[nt][i];
+        if (n == 0) {
+            wml[2 * rr] = m_run[i];
+            wml[2 * rr + 1] = lsum[i];
+        }
+    }
+    __syncthreads();
+    const int rr = tid >> 2, c0 = 32 * (tid & 3);
+    if (qt_row(rr) < 0) return;
+    const int32_t t = chunk_tok(rr);
+    if (t >= a.max_tok) return;
+    float *dst = out + (((int64_t)b * a.max_tok + t) * a.n_kv * a.g_real + h * a.g_real + (rr % G) % a.g_real) * D + c0;
+    if (t >= nb) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) reinterpret_cast<f32x4 *>(dst)[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+        return;
+    }
+    const int64_t bzr = (int64_t)b * a.n_groups + tg0 + rr / G;
+    const float *pp = a.part + ((bzr * a.n_kv + h) * a.n_splits) * G * (D + 2) + (rr % G) * (D + 2);
+    const int64_t stride = (int64_t)G * (D + 2);
+    const int P = a.n_page_splits;
+    const float mw = wml[2 * rr];
+    float M = mw;
+    for (int s0 = 0; s0 < P; s0 += 8) {
+        float ms[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ms[e] = s0 + e < P ? pp[(s0 + e) * stride + D] : -INFINITY;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) M = fmaxf(M, ms[e]);
+    }
+    f32x4 o[8];
+    const float fw = (M == -INFINITY || mw == -INFINITY) ? 0.0f : fexp2(mw - M);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        const f32x4 x = *reinterpret_cast<const f32x4 *>(wo + rr * D + c0 + 4 * q);
+        o[q] = f32x4{fw * x[0], fw * x[1], fw * x[2], fw * x[3]};
+    }
+    float l = fw * wml[2 * rr + 1];
+    for (int s0 = 0; s0 < P; s0 += 2) {
+        f32x4 x[2][8];
+        float ms[2], ls[2];
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int sp = s0 + e < P ? s0 + e : s0;  // (a repeat of s0 weighs 0)
+            const float *src = pp + sp * stride;
+            ms[e] = s0 + e < P ? src[D] : -INFINITY;
+            ls[e] = src[D + 1];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) x[e][q] = *reinterpret_cast<const f32x4 *>(src + c0 + 4 * q);
+        }
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const float f = (M == -INFINITY || ms[e] == -INFINITY) ? 0.0f : fexp2(ms[e] - M);
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+#pragma unroll
+                for (int k = 0; k < 4; ++k) o[q][k] = fmaf(f, x[e][q][k], o[q][k]);
+            l = fmaf(f, ls[e], l);
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+        reinterpret_cast<f32x4 *>(dst)[q] = l > 0.0f ? f32x4{o[q][0] / l, o[q][1] / l, o[q][2] / l, o[q][3] / l}
+                                                  : f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
 // ------------------------------------------------------------------ combine
 
 // One workgroup per (query head, sequence): the split maxima and weights go
@@ -1356,6 +2057,24 @@ static int64_t resident_waves(int D, int bits, int G, bool share)
     return waves;
 }
 
+// Compute units of the current device (256 when no device answers),
+// cached like resident_waves.
+static int64_t device_cus()
+{
+    static std::atomic<int64_t> cache{0};
+    const int64_t known = cache.load(std::memory_order_relaxed);
+    if (known > 0) return known;
+    int dev = 0, ncu = 0;
+    int64_t v = 256;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && ncu > 0)
+        v = ncu;
+    else
+        (void)hipGetLastError();
+    cache.store(v, std::memory_order_relaxed);
+    return v;
+}
+
 // Query rows of a call: G virtual heads per kv head, each a (chunk token,
 // query head) pair, and n_groups token groups per sequence (see DecodeArgs).
 struct RowShape {
@@ -1396,8 +2115,8 @@ static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq
     // with shared work items (share) one per row for all units, since there
     // every wave walks all the tiles anyway and the page runs then get the
     // resident slots the other window workgroups would hold.
-    const int64_t win_units = (rs.share || one_window_wg) ? wunits : 1;
-    const int64_t wwgs = (wunits + win_units - 1) / win_units;
+    int64_t win_units = (rs.share || one_window_wg) ? wunits : 1;
+    int64_t wwgs = (wunits + win_units - 1) / win_units;
     // With shared work items (share_items) the four waves of a workgroup
     // walk one run together, each for another token group: a workgroup row
     // is then a (sequence, four token groups, kv head) triple and a split
@@ -1413,6 +2132,22 @@ static bool make_plan(const wushkv_cache *c, const RowShape &rs, int32_t max_seq
     if (psplits > 0) {
         upw = (qpages + per_split * psplits - 1) / (per_split * psplits);
         psplits = (qpages + per_split * upw - 1) / (per_split * upw);
+    }
+    // Chunks at d = 128 run their pages in chunk_pages_kernel: a workgroup
+    // per run of upw pages takes the 64 rows of eight token groups; the
+    // runs are sized for about two such workgroups per compute unit, one
+    // round.  The window slots and the merge follow in chunk_window_kernel,
+    // so the splits are the page runs alone.
+    if (rs.share && c->head_dim == 128 && G == 8) {
+        const int64_t per_cu = 2;
+        const int64_t crows = (int64_t)c->batch * ((rs.n_groups + 7) / 8) * c->n_kv_heads;
+        int64_t runs = (per_cu * device_cus() + crows - 1) / crows;
+        runs = runs < 1 ? 1 : (runs > qpages ? qpages : runs);
+        upw = qpages > 0 ? (qpages + runs - 1) / runs : 1;
+        if (upw > kMaxRunPages) upw = kMaxRunPages;
+        psplits = (qpages + upw - 1) / upw;
+        win_units = 1;
+        wwgs = 0;
     }
     // A decode grid that cannot be resident at once (it runs in rounds)
     // takes one window workgroup per row, its waves on every unit's tiles:
@@ -1590,7 +2325,24 @@ static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok
     const int64_t wgs = (int64_t)p.n_splits * c->n_kv_heads * grid_z;
     const bool form = !rs.share && wgs * 4 <= resident_waves(c->head_dim, storage_bits(c->bits), G, false);
     const int key = c->head_dim * 10 + storage_bits(c->bits);
-    switch (key) {
+    if (rs.share && c->head_dim == 128 && G == 8) {
+        // chunks: q~ rows, the pages (chunk_pages_kernel, splits 0 ..
+        // n_page_splits - 1), then the window slots merged with the page
+        // runs into the output (chunk_window_kernel)
+        const unsigned blocks = (unsigned)(c->batch * ((rs.n_groups + 7) / 8));
+        const dim3 gp(c->n_kv_heads, p.n_page_splits, blocks);
+        const dim3 gw(c->n_kv_heads, blocks);
+        if (key == 1282) {
+            launch("decode_qt_kernel", decode_qt_kernel<128, 2, 8>, dim3(c->n_kv_heads, rows_z), dim3(256), s, a);
+            if (p.n_page_splits > 0) launch("chunk_pages_kernel", chunk_pages_kernel<2>, gp, dim3(256), s, a);
+        } else {
+            launch("decode_qt_kernel", decode_qt_kernel<128, 4, 8>, dim3(c->n_kv_heads, rows_z), dim3(256), s, a);
+            if (p.n_page_splits > 0) launch("chunk_pages_kernel", chunk_pages_kernel<4>, gp, dim3(256), s, a);
+        }
+        launch("chunk_window_kernel", chunk_window_kernel, gw, dim3(256), s, a, out);
+        if (hipGetLastError() != hipSuccess) return WUSHKV_ELAUNCH;
+        return WUSHKV_OK;
+    } else switch (key) {
         case 1282: launch_main_g<128, 2>(G, form, rs.share, gm, rows_z, s, a); break;
         case 1284: launch_main_g<128, 4>(G, form, rs.share, gm, rows_z, s, a); break;
         case 642: launch_main_g<64, 2>(G, form, rs.share, gm, rows_z, s, a); break;

@@ -184,22 +184,22 @@ def test_plans_past_the_page_run_limit_are_unsupported():
     # a wave caches its run's page-table entries one per lane, so a run is at
     # most 64 pages: decode (four runs per split, at most 1024 splits minus
     # the window workgroup, one per row when the grid runs in rounds) stops
-    # planning past 1023 * 4 * 64 pages, chunk attention (one run per split,
-    # one window workgroup) past 1023 * 64 pages; the call is then
-    # unsupported, the workspace size 0
+    # planning past 1023 * 4 * 64 pages, chunk attention at d = 128 (one run
+    # per split; its window slots take no split) past 1024 * 64 pages; the
+    # call is then unsupported, the workspace size 0
     L = _lib.lib()
     big = _desc(max_pages_per_seq=400000)
     by = ctypes.byref(big)
     ok_len = 4 + 1023 * 4 * 64 * 64          # upw = 64 exactly
     assert L.wushkv_decode_workspace_bytes(by, 8, ok_len) > 0
     assert L.wushkv_decode_workspace_bytes(by, 8, ok_len + 64) == 0
-    assert L.wushkv_chunk_workspace_bytes(by, 8, 16, 4 + 1023 * 64 * 64) > 0
-    assert L.wushkv_chunk_workspace_bytes(by, 8, 16, 4 + 1023 * 64 * 64 + 64) == 0
+    assert L.wushkv_chunk_workspace_bytes(by, 8, 16, 4 + 1024 * 64 * 64) > 0
+    assert L.wushkv_chunk_workspace_bytes(by, 8, 16, 4 + 1024 * 64 * 64 + 64) == 0
     if not gpu_available():
         # fake device pointers: the host check answers before any launch
         st = L.wushkv_decode_attention(by, FAKE, 8, ok_len + 64, FAKE, 0.1, FAKE, FAKE, 1 << 40, None)
         assert st == -2
-        st = L.wushkv_chunk_attention(by, FAKE, None, 16, 8, 4 + 1023 * 64 * 64 + 64, FAKE, 0.1,
+        st = L.wushkv_chunk_attention(by, FAKE, None, 16, 8, 4 + 1024 * 64 * 64 + 64, FAKE, 0.1,
                                       FAKE, FAKE, 1 << 40, None)
         assert st == -2
 
