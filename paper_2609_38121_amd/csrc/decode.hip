@@ -130,6 +130,9 @@ __host__ __device__ constexpr int limb_pos(int ch)
 // scale bytes and sum(q~) of each head follow it.
 template <int D, int G>
 struct QueryLds {
+    // the raw queries' row pitch in bf16 elements: rows 16 bytes apart in
+    // the LDS banks, so that a column read across rows does not conflict
+    static constexpr int kQPitch = D + 8;
     static constexpr int kRegion = G * D * 4 > G * kLimbs * 128 ? G * D * 4 : G * kLimbs * 128;
     static constexpr int kAux = kRegion;  // uint32 [G][4]: limb scales (E8M0 bytes, limbs
                                           // 0-3 then 4-5), sum(q~) (fp32 bits), unused
@@ -192,10 +195,13 @@ struct QueryIn {
 template <int D, int G>
 __device__ __forceinline__ void stage_queries(const QueryIn<D, G> &in, uint8_t *R, int tid)
 {
-    uint16_t *qs = reinterpret_cast<uint16_t *>(R);  // bf16 [G][D]
+    uint16_t *qs = reinterpret_cast<uint16_t *>(R);  // bf16 [G][kQPitch]
+    constexpr int kP = QueryLds<D, G>::kQPitch;
 #pragma unroll
-    for (int k = 0; k < QueryIn<D, G>::kPer; ++k)
-        if (tid + 256 * k < G * D) qs[tid + 256 * k] = in.q[k];
+    for (int k = 0; k < QueryIn<D, G>::kPer; ++k) {
+        const int i = tid + 256 * k;
+        if (i < G * D) qs[(i / D) * kP + i % D] = in.q[k];
+    }
 }
 
 // q~ = q^T T^{-1} for the workgroup's G query rows (Alg. 2 step 3, Eq. (3)),
@@ -225,10 +231,10 @@ __device__ void form_qt(const DecodeArgs &a, const QueryIn<D, G> &in, uint8_t *R
         for (int g = 0; g < G; ++g) {
             uint32_t ww[4];
             if constexpr (kRv == 8) {
-                const uint4 w = *reinterpret_cast<const uint4 *>(qs + g * D + part * C::kRr + r0);
+                const uint4 w = *reinterpret_cast<const uint4 *>(qs + g * QueryLds<D, G>::kQPitch + part * C::kRr + r0);
                 ww[0] = w.x; ww[1] = w.y; ww[2] = w.z; ww[3] = w.w;
             } else {
-                const uint2 w = *reinterpret_cast<const uint2 *>(qs + g * D + part * C::kRr + r0);
+                const uint2 w = *reinterpret_cast<const uint2 *>(qs + g * QueryLds<D, G>::kQPitch + part * C::kRr + r0);
                 ww[0] = w.x; ww[1] = w.y;
             }
 #pragma unroll
@@ -256,6 +262,25 @@ __device__ void form_qt(const DecodeArgs &a, const QueryIn<D, G> &in, uint8_t *R
     __syncthreads();
 }
 
+// The T^{-1} entries lane l of wave w supplies to form_qt_mfma: column
+// D/4 w + 16 t + l % 16 at rows 4 st + l / 16.  Loaded on their own so that
+// a kernel can request them together with the raw queries (one round trip).
+template <int D>
+struct TColumns {
+    static constexpr int kTiles = D / 64;  // 16-column tiles per wave
+    static constexpr int kSteps = D / 4;   // k steps of 4
+    float bv[kTiles][kSteps];
+    __device__ __forceinline__ void load(const DecodeArgs &a, int h, int tid)
+    {
+        const int lane = tid & 63, wave = tid >> 6;
+        const float *T = a.tinv + (int64_t)h * D * D + (D / 4) * wave + (lane & 15);
+#pragma unroll
+        for (int t = 0; t < kTiles; ++t)
+#pragma unroll
+            for (int st = 0; st < kSteps; ++st) bv[t][st] = T[(int64_t)(4 * st + (lane >> 4)) * D + 16 * t];
+    }
+};
+
 // form_qt on the fp32 matrix instructions, for decode_qt_kernel (which has
 // no pages to overlap and is bound by the products): q~ = q^T T^{-1} as a
 // (16 x D) x (D x D) product of 16x16x4 fp32 tiles, the G query rows padded
@@ -263,30 +288,25 @@ __device__ void form_qt(const DecodeArgs &a, const QueryIn<D, G> &in, uint8_t *R
 // (D/64 tiles of 16); lane l supplies A = q[l % 16][k0 + l / 16] and
 // B = T^{-1}[k0 + l / 16][n0 + l % 16] and holds the result rows
 // 4 (l / 16) .. + 3 of column n0 + l % 16.  The T^{-1} column entries of
-// all steps are requested at once.  Same contract as form_qt (q~ scaled,
+// all steps come loaded in tc.  Same contract as form_qt (q~ scaled,
 // fp32, into R; starts and ends with a barrier); the products are summed in
 // the matrix unit's order, so q~ may differ from form_qt's in the last bits.
 template <int D, int G>
-__device__ void form_qt_mfma(const DecodeArgs &a, int h, uint8_t *R, int tid)
+__device__ void form_qt_mfma(const DecodeArgs &a, const TColumns<D> &tc, uint8_t *R, int tid)
 {
-    constexpr int kTiles = D / 64;   // 16-column tiles per wave
-    constexpr int kSteps = D / 4;    // k steps of 4
+    constexpr int kTiles = TColumns<D>::kTiles;
+    constexpr int kSteps = TColumns<D>::kSteps;
     const uint16_t *qs = reinterpret_cast<const uint16_t *>(R);
     const int lane = tid & 63, wave = tid >> 6;
     const int m = lane & 15, kk = lane >> 4;
-    const float *T = a.tinv + (int64_t)h * D * D + (D / 4) * wave + m;
-    float bv[kTiles][kSteps];
-#pragma unroll
-    for (int t = 0; t < kTiles; ++t)
-#pragma unroll
-        for (int st = 0; st < kSteps; ++st) bv[t][st] = T[(int64_t)(4 * st + kk) * D + 16 * t];
+    const auto &bv = tc.bv;
     __syncthreads();  // the staged queries
     f32x4 acc[kTiles];
 #pragma unroll
     for (int t = 0; t < kTiles; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int st = 0; st < kSteps; ++st) {
-        const float av = m < G ? bf16_bits_to_f32(qs[m * D + 4 * st + kk]) : 0.0f;
+        const float av = m < G ? bf16_bits_to_f32(qs[m * QueryLds<D, G>::kQPitch + 4 * st + kk]) : 0.0f;
 #pragma unroll
         for (int t = 0; t < kTiles; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv[t][st], acc[t], 0, 0, 0);
     }
@@ -408,10 +428,12 @@ __global__ void __launch_bounds__(256) decode_qt_kernel(DecodeArgs a)
     const int h = blockIdx.x, bz = blockIdx.y;
     const int b = bz / a.n_groups, tg = bz % a.n_groups;
     const int32_t S = (a.max_tok == 1 && a.n_tok == nullptr) ? 0 : a.seq_len[b];
+    TColumns<D> tc;
+    tc.load(a, h, tid);
     QueryIn<D, G> in;
     in.load_q(a, b, tg, h, S, tid);
     stage_queries<D, G>(in, R, tid);
-    form_qt_mfma<D, G>(a, h, R, tid);
+    form_qt_mfma<D, G>(a, tc, R, tid);
     const int64_t row0 = ((int64_t)bz * a.n_kv + h) * G;  // first (virtual) query head
     for (int i = tid; i < G * D / 4; i += 256)
         reinterpret_cast<f32x4 *>(a.qt + row0 * D)[i] = reinterpret_cast<const f32x4 *>(R)[i];
@@ -419,6 +441,46 @@ __global__ void __launch_bounds__(256) decode_qt_kernel(DecodeArgs a)
     for (int i = tid; i < G * kLimbs * 128 / 16; i += 256)
         reinterpret_cast<u32x4 *>(a.qlimb + row0 * kLimbs * 128)[i] = reinterpret_cast<const u32x4 *>(R)[i];
     if (tid < G * 4) a.qaux[row0 * 4 + tid] = reinterpret_cast<const uint32_t *>(R + Q::kAux)[tid];
+}
+
+// Chunks at d = 128 (eight virtual heads per token group): one workgroup
+// per (kv head, sequence, pair of token groups) forms the 16 rows of both
+// groups at once, which fills the 16-row products of form_qt_mfma and reads
+// T^{-1} once per pair; each group's rows go where decode_qt_kernel puts
+// them.
+template <int BITS>
+__global__ void __launch_bounds__(256) chunk_qt_kernel(DecodeArgs a)
+{
+    constexpr int D = 128, G = 8, G2 = 16;
+    using Q = QueryLds<D, G2>;
+    __shared__ __attribute__((aligned(16))) uint8_t R[Q::kBytes];
+    const int tid = threadIdx.x;
+    const int h = blockIdx.x;
+    const int n_pairs = (a.n_groups + 1) / 2;
+    const int b = (int)blockIdx.y / n_pairs, tg = 2 * ((int)blockIdx.y % n_pairs);
+    const int32_t S = a.seq_len[b];
+    // virtual head v of the pair: token tg tpg + v / g_real, which is token
+    // group tg + v / 8, virtual head v % 8 of that group
+    TColumns<D> tc;
+    tc.load(a, h, tid);
+    QueryIn<D, G2> in;
+    in.load_q(a, b, tg, h, S, tid);
+    stage_queries<D, G2>(in, R, tid);
+    form_qt_mfma<D, G2>(a, tc, R, tid);
+    const int n_mine = tg + 1 < a.n_groups ? 2 : 1;
+    for (int e = 0; e < n_mine; ++e) {
+        const int64_t row0 = (((int64_t)b * a.n_groups + tg + e) * a.n_kv + h) * G;
+        for (int i = tid; i < G * D / 4; i += 256)
+            reinterpret_cast<f32x4 *>(a.qt + row0 * D)[i] = reinterpret_cast<const f32x4 *>(R)[e * G * D / 4 + i];
+    }
+    form_limbs<D, BITS, G2>(R, tid);
+    for (int e = 0; e < n_mine; ++e) {
+        const int64_t row0 = (((int64_t)b * a.n_groups + tg + e) * a.n_kv + h) * G;
+        for (int i = tid; i < G * kLimbs * 128 / 16; i += 256)
+            reinterpret_cast<u32x4 *>(a.qlimb + row0 * kLimbs * 128)[i] =
+                reinterpret_cast<const u32x4 *>(R)[e * G * kLimbs * 128 / 16 + i];
+        if (tid < G * 4) a.qaux[row0 * 4 + tid] = reinterpret_cast<const uint32_t *>(R + Q::kAux)[e * G * 4 + tid];
+    }
 }
 
 // ------------------------------------------------------------------ main
@@ -1670,27 +1732,26 @@ __global__ void __launch_bounds__(256, 2) chunk_pages_kernel(DecodeArgs a)
 
 // The bf16 window slots of chunk attention at d = 128, merged with the page
 // runs of chunk_pages_kernel into the output (so no combine launch follows).
-// One workgroup per (kv head, sequence, block of eight token groups): the
-// block's 64 query rows, wave w rows 16 w .. 16 w + 15, as in the page
-// kernel.  The window streams through LDS one 64-slot unit at a time (keys
-// and channel-major values, two buffers, filled by direct-to-LDS loads);
-// per unit and wave:
-//   scores  q~ in bf16 hi + lo parts (A, 16 rows) times the unit's keys,
-//           tile t column n the slot 4 n + t, so that lane (j, n) holds rows
-//           4 j + r of slots 4 n .. 4 n + 3; causal and live-slot masks;
-//   softmax online across the units; the lane's rows are its P V rows, so
-//           the rescale stays in the lane;
+// One workgroup per (kv head, sequence, block of eight token groups, quarter
+// of the block's 64 query rows): its 16 rows, the rows of chunk_pages_kernel's
+// wave of the same index.  Wave w takes the 64-slot window units w, w + 4,
+// .., each staged whole in the wave's own LDS buffer (keys and channel-major
+// values, direct-to-LDS loads).  Per unit:
+//   scores  q~ in bf16 hi + lo parts (A, the 16 rows) times the keys, tile t
+//           column n the slot 4 n + t, so that lane (j, n) holds rows 4 j + r
+//           of slots 4 n .. 4 n + 3; causal and live-slot masks;
+//   softmax online across the wave's units; the lane's rows are its P V
+//           rows, so the rescale stays in the lane;
 //   P V     weights (bf16 hi, lo: two products) through a per-wave LDS
 //           buffer, times the values (dead slots' values zeroed).
-// Then each row's window result and its page-run partials merge by
-// log-sum-exp, as decode_combine_kernel does.
+// Then the four waves' results and the row's page-run partials merge by
+// log-sum-exp (as decode_combine_kernel does), eight splits' loads at a time.
 struct ChunkWinLds {
     static constexpr int kUnitK = 64 * 256;                 // [slot][16 chunks of 16 B]
     static constexpr int kUnitV = 128 * 128;                // [channel][8 chunks of 16 B]
-    static constexpr int kKAt = 0;                          // two unit buffers each
-    static constexpr int kVAt = kKAt + 2 * kUnitK;
+    static constexpr int kUnit = kUnitK + kUnitV;           // one per wave
     static constexpr int kPWave = 2 * 16 * 128;             // [part][16 rows][64 slots] bf16
-    static constexpr int kPAt = kVAt + 2 * kUnitV;
+    static constexpr int kPAt = 4 * kUnit;
     static constexpr int kBytes = kPAt + 4 * kPWave;
 };
 
@@ -1703,7 +1764,8 @@ __global__ void __launch_bounds__(256, 1) chunk_window_kernel(DecodeArgs a, floa
     const int j = lane >> 4, n = lane & 15;
     const int h = blockIdx.x;
     const int n_blocks = (a.n_groups + 7) / 8;
-    const int b = (int)blockIdx.y / n_blocks, tg0 = 8 * ((int)blockIdx.y % n_blocks);
+    const int blk = (int)blockIdx.y >> 2, r0 = 16 * ((int)blockIdx.y & 3);
+    const int b = blk / n_blocks, tg0 = 8 * (blk % n_blocks);
     const int32_t S = a.seq_len[b];
     int32_t qend = a.quant_end[b];
     qend = qend < S ? qend : S;
@@ -1717,39 +1779,38 @@ __global__ void __launch_bounds__(256, 1) chunk_window_kernel(DecodeArgs a, floa
     const int n_units = a.win_slots / kPage;
     const uint32_t lbase = lds_addr(lds);
 
-    // row rr of the block (0 .. 63): its q~ row, chunk token and query head
+    // row rr of the block (0 .. 63): its q~ row (-1: past the token groups)
+    // and chunk token
     auto qt_row = [&](int rr) -> int64_t {
         const int tg = tg0 + rr / G;
         return tg < a.n_groups ? (((int64_t)b * a.n_groups + tg) * a.n_kv + h) * G + rr % G : -1;
     };
     auto chunk_tok = [&](int rr) -> int32_t { return (tg0 + rr / G) * a.tpg + (rr % G) / a.g_real; };
 
-    // unit u's keys and values into buffer u % 2: wave w the 1 KB rows
-    // w, w + 4, .. of each; LDS chunk p of the keys is slot p / 16, chunk
-    // (p % 16) ^ ((slot / 4) % 16); of the values channel p / 8, chunk
-    // (p % 8) ^ (channel % 8) (the readers' bank swizzles)
+    // unit u's keys and values into the wave's buffer: LDS chunk p of the
+    // keys is slot p / 16, chunk (p % 16) ^ ((slot / 4) % 16); of the values
+    // channel p / 8, chunk (p % 8) ^ (channel % 8) (the readers' bank
+    // swizzles)
+    const uint32_t kb = lbase + wave * W::kUnit, vb = kb + W::kUnitK;
     auto issue = [&](int u) {
         const int32_t unit0 = u * kPage;
-        const uint32_t kdst = lbase + W::kKAt + (u & 1) * W::kUnitK;
-        const uint32_t vdst = lbase + W::kVAt + (u & 1) * W::kUnitV;
-#pragma unroll
-        for (int i0 = 0; i0 < 4; ++i0) {
-            const int i = wave + 4 * i0;
+#pragma unroll 4
+        for (int i = 0; i < 16; ++i) {
             const int pk = 64 * i + lane;
             const int slot = pk >> 4, ck = (pk & 15) ^ ((slot >> 2) & 15);
-            dma16(a.win_k + (head_win + unit0 + slot) * D + 8 * ck, __builtin_amdgcn_readfirstlane(kdst + 1024 * i));
+            dma16(a.win_k + (head_win + unit0 + slot) * D + 8 * ck, __builtin_amdgcn_readfirstlane(kb + 1024 * i));
             const int ch = pk >> 3, cv = (pk & 7) ^ (ch & 7);
             dma16(a.win_v + head_win * D + (int64_t)ch * a.win_slots + unit0 + 8 * cv,
-                  __builtin_amdgcn_readfirstlane(vdst + 1024 * i));
+                  __builtin_amdgcn_readfirstlane(vb + 1024 * i));
         }
     };
-    if (n_units > 0) issue(0);
+    if (wave < n_units) issue(wave);
 
-    // A operands: q~ of row 16 w + n (lane n), channels 32 c + 8 j .., as
+    // A operands: q~ of row r0 + n (lane n), channels 32 c + 8 j .., as
     // bf16 hi and lo parts
     bf16x8 qh[4], ql[4];
     {
-        const int64_t row = qt_row(16 * wave + n);
+        const int64_t row = qt_row(r0 + n);
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
             uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
@@ -1769,11 +1830,11 @@ __global__ void __launch_bounds__(256, 1) chunk_window_kernel(DecodeArgs a, floa
             ql[c] = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], lo[2], lo[3]});
         }
     }
-    // the lane's rows 16 w + 4 j + r: chunk token (or -1: no such row)
+    // the lane's rows r0 + 4 j + r: chunk token (or -1: no such row)
     int32_t trow[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        const int rr = 16 * wave + 4 * j + r;
+        const int rr = r0 + 4 * j + r;
         trow[r] = qt_row(rr) >= 0 ? chunk_tok(rr) : -1;
     }
 
@@ -1788,14 +1849,17 @@ __global__ void __launch_bounds__(256, 1) chunk_window_kernel(DecodeArgs a, floa
     for (int nt = 0; nt < 8; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     const uint32_t pbuf = lbase + W::kPAt + wave * W::kPWave;
 
-    for (int u = 0; u < n_units; ++u) {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's loads of unit u
-        __syncthreads();  // every wave's loads of unit u; unit u - 1's buffers are read
-        if (u + 1 < n_units) issue(u + 1);
+    for (int u = wave; u < n_units; u += 4) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the wave's loads of unit u
         const int32_t unit0 = u * kPage;
-        const uint32_t kb = lbase + W::kKAt + (u & 1) * W::kUnitK;
-        const uint32_t vb = lbase + W::kVAt + (u & 1) * W::kUnitV;
-        // the lane's slots 4 n + t: live, and their positions
+        // slots of the unit that hold a position (bit s: slot unit0 + s,
+        // lane s answers), and the lane's slots 4 n + t with their positions
+        uint64_t live_mask;
+        {
+            const int32_t sl = unit0 + lane;
+            const int32_t ri = (sl - a.s_sink - a0 + ring) % ring;
+            live_mask = __ballot(sl < a.s_sink ? sl < S : ri < ring_live);
+        }
         int32_t pos[4];
         bool live[4];
 #pragma unroll
@@ -1805,159 +1869,164 @@ __global__ void __launch_bounds__(256, 1) chunk_window_kernel(DecodeArgs a, floa
             live[t] = sl < a.s_sink ? sl < S : ri < ring_live;
             pos[t] = sl < a.s_sink ? sl : q_hi + ri;
         }
-        // slots of the unit that hold a position (bit s: slot unit0 + s,
-        // lane s answers)
-        uint64_t live_mask;
-        {
-            const int32_t sl = unit0 + lane;
-            const int32_t ri = (sl - a.s_sink - a0 + ring) % ring;
-            live_mask = __ballot(sl < a.s_sink ? sl < S : ri < ring_live);
-        }
-        if (live_mask == 0) continue;
-
-        // ---- scores
-        f32x4 sc[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            sc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-            const uint32_t krow = kb + (4 * n + t) * 256;
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const bf16x8 kk = __builtin_bit_cast(bf16x8, lds_read16(krow + 16 * ((4 * c + j) ^ n)));
-                sc[t] = mfma16(qh[c], kk, sc[t]);
-                sc[t] = mfma16(ql[c], kk, sc[t]);
-            }
-        }
-        // ---- online softmax of the lane's rows over the unit
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            float lg[4];
+        if (live_mask != 0) {
+            // ---- scores
+            f32x4 sc[4];
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-                const bool vis = live[t] && trow[r] >= 0 && trow[r] < nb && pos[t] <= S - nb + trow[r];
-                lg[t] = vis ? sc[t][r] : -INFINITY;
-            }
-            const float mx = row_max16(fmaxf(fmaxf(lg[0], lg[1]), fmaxf(lg[2], lg[3])));
-            const float m_new = fmaxf(m_run[r], mx);
-            const float al = m_new == -INFINITY ? 1.0f : fexp2(m_run[r] - m_new);
-            m_run[r] = m_new;
-            lsum[r] *= al;
+                sc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+                const uint32_t krow = kb + (4 * n + t) * 256;
 #pragma unroll
-            for (int nt = 0; nt < 8; ++nt) acc[nt][r] *= al;
-            uint32_t hw[2], lw[2];
-#pragma unroll
-            for (int e = 0; e < 2; ++e) {
-                const float p0 = m_new == -INFINITY ? 0.0f : fexp2(lg[2 * e] - m_new);
-                const float p1 = m_new == -INFINITY ? 0.0f : fexp2(lg[2 * e + 1] - m_new);
-                lsum[r] += p0 + p1;
-                hw[e] = pack_bf16_rne(p0, p1);
-                lw[e] = pack_bf16_rne(p0 - bf16_bits_to_f32(hw[e] & 0xFFFFu), p1 - bf16_bits_to_f32(hw[e] >> 16));
+                for (int c = 0; c < 4; ++c) {
+                    const bf16x8 kk = __builtin_bit_cast(bf16x8, lds_read16(krow + 16 * ((4 * c + j) ^ n)));
+                    sc[t] = mfma16(qh[c], kk, sc[t]);
+                    sc[t] = mfma16(ql[c], kk, sc[t]);
+                }
             }
-            lds_write8(pbuf + tbuf_at(4 * j + r, 8 * n), hw[0], hw[1]);
-            lds_write8(pbuf + 16 * 128 + tbuf_at(4 * j + r, 8 * n), lw[0], lw[1]);
+            // ---- online softmax of the lane's rows over the unit
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                float lg[4];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const bool vis = live[t] && trow[r] >= 0 && trow[r] < nb && pos[t] <= S - nb + trow[r];
+                    lg[t] = vis ? sc[t][r] : -INFINITY;
+                }
+                const float mx = row_max16(fmaxf(fmaxf(lg[0], lg[1]), fmaxf(lg[2], lg[3])));
+                const float m_new = fmaxf(m_run[r], mx);
+                const float al = m_new == -INFINITY ? 1.0f : fexp2(m_run[r] - m_new);
+                m_run[r] = m_new;
+                lsum[r] *= al;
+#pragma unroll
+                for (int nt = 0; nt < 8; ++nt) acc[nt][r] *= al;
+                uint32_t hw[2], lw[2];
+#pragma unroll
+                for (int e = 0; e < 2; ++e) {
+                    const float p0 = m_new == -INFINITY ? 0.0f : fexp2(lg[2 * e] - m_new);
+                    const float p1 = m_new == -INFINITY ? 0.0f : fexp2(lg[2 * e + 1] - m_new);
+                    lsum[r] += p0 + p1;
+                    hw[e] = pack_bf16_rne(p0, p1);
+                    lw[e] = pack_bf16_rne(p0 - bf16_bits_to_f32(hw[e] & 0xFFFFu),
+                                          p1 - bf16_bits_to_f32(hw[e] >> 16));
+                }
+                lds_write8(pbuf + tbuf_at(4 * j + r, 8 * n), hw[0], hw[1]);
+                lds_write8(pbuf + 16 * 128 + tbuf_at(4 * j + r, 8 * n), lw[0], lw[1]);
+            }
+            // ---- P V (the weight buffer is the wave's own: no barrier)
+            const bool dead = ~live_mask != 0;
+#pragma unroll
+            for (int kc = 0; kc < 2; ++kc) {
+                const bf16x8 ph = __builtin_bit_cast(bf16x8, lds_read16(pbuf + tbuf_at(n, 64 * kc + 16 * j)));
+                const bf16x8 pl =
+                    __builtin_bit_cast(bf16x8, lds_read16(pbuf + 16 * 128 + tbuf_at(n, 64 * kc + 16 * j)));
+                // dead slots 32 kc + 8 j + e: their values are zeroed
+                uint32_t msk[4] = {~0u, ~0u, ~0u, ~0u};
+                if (dead) {
+                    const uint32_t bits8 = (uint32_t)(live_mask >> (32 * kc + 8 * j)) & 0xFFu;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        msk[q] = ((bits8 >> (2 * q)) & 1u ? 0x0000FFFFu : 0u) |
+                                 ((bits8 >> (2 * q + 1)) & 1u ? 0xFFFF0000u : 0u);
+                }
+#pragma unroll
+                for (int nt = 0; nt < 8; ++nt) {
+                    const int ch = 16 * nt + n;
+                    u32x4 v = lds_read16(vb + ch * 128 + 16 * ((4 * kc + j) ^ (ch & 7)));
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) v[q] &= msk[q];
+                    const bf16x8 vv = __builtin_bit_cast(bf16x8, v);
+                    acc[nt] = mfma16(ph, vv, acc[nt]);
+                    acc[nt] = mfma16(pl, vv, acc[nt]);
+                }
+            }
         }
-        // ---- P V (the weight buffer is the wave's own: no barrier)
-        const bool dead = ~live_mask != 0;
-#pragma unroll
-        for (int kc = 0; kc < 2; ++kc) {
-            const bf16x8 ph = __builtin_bit_cast(bf16x8, lds_read16(pbuf + tbuf_at(n, 64 * kc + 16 * j)));
-            const bf16x8 pl = __builtin_bit_cast(bf16x8, lds_read16(pbuf + 16 * 128 + tbuf_at(n, 64 * kc + 16 * j)));
-            // dead slots 32 kc + 8 j + e: their values are zeroed
-            uint32_t msk[4] = {~0u, ~0u, ~0u, ~0u};
-            if (dead) {
-                const uint32_t bits8 = (uint32_t)(live_mask >> (32 * kc + 8 * j)) & 0xFFu;
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    msk[q] = ((bits8 >> (2 * q)) & 1u ? 0x0000FFFFu : 0u) | ((bits8 >> (2 * q + 1)) & 1u ? 0xFFFF0000u : 0u);
-            }
-#pragma unroll
-            for (int nt = 0; nt < 8; ++nt) {
-                const int ch = 16 * nt + n;
-                u32x4 v = lds_read16(vb + ch * 128 + 16 * ((4 * kc + j) ^ (ch & 7)));
-#pragma unroll
-                for (int q = 0; q < 4; ++q) v[q] &= msk[q];
-                const bf16x8 vv = __builtin_bit_cast(bf16x8, v);
-                acc[nt] = mfma16(ph, vv, acc[nt]);
-                acc[nt] = mfma16(pl, vv, acc[nt]);
-            }
+        if (u + 4 < n_units) {
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the unit's reads are done
+            issue(u + 4);
         }
     }
 
-    // ---- merge with the page runs and write the rows.  The window
-    // partials go through LDS (the unit buffers are free now); then thread
-    // (row tid / 4, channels 32 (tid % 4) ..) merges its row's splits, the
-    // loads of several splits in flight together.
+    // ---- merge: the four waves' results through LDS (the unit buffers are
+    // free once every wave is past its units), then thread (row tid / 16,
+    // channels 8 (tid % 16) ..) adds its row's page-run partials
 #pragma unroll
     for (int r = 0; r < 4; ++r) lsum[r] = row_sum16(lsum[r]);
-    __syncthreads();  // every wave is past its last unit
-    float *wo = reinterpret_cast<float *>(lds + W::kKAt);  // [64 rows][D]
-    float *wml = wo + 64 * D;                               // [64 rows][m, l]
+    __syncthreads();
+    float *wo = reinterpret_cast<float *>(lds);  // [wave][16 rows][D]
+    float *wml = wo + 4 * 16 * D;                // [wave][16 rows][m, l]
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int rr = 16 * wave + 4 * j + i;
+        const int ri = 4 * j + i;
 #pragma unroll
-        for (int nt = 0; nt < 8; ++nt) wo[rr * D + 16 * nt + n] = acc[nt][i];
+        for (int nt = 0; nt < 8; ++nt) wo[(wave * 16 + ri) * D + 16 * nt + n] = acc[nt][i];
         if (n == 0) {
-            wml[2 * rr] = m_run[i];
-            wml[2 * rr + 1] = lsum[i];
+            wml[2 * (wave * 16 + ri)] = m_run[i];
+            wml[2 * (wave * 16 + ri) + 1] = lsum[i];
         }
     }
     __syncthreads();
-    const int rr = tid >> 2, c0 = 32 * (tid & 3);
+    const int ri = tid >> 4, c0 = 8 * (tid & 15), rr = r0 + ri;
     if (qt_row(rr) < 0) return;
     const int32_t t = chunk_tok(rr);
     if (t >= a.max_tok) return;
     float *dst = out + (((int64_t)b * a.max_tok + t) * a.n_kv * a.g_real + h * a.g_real + (rr % G) % a.g_real) * D + c0;
-    if (t >= nb) {
+    f32x4 o[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+    float l = 0.0f, M = -INFINITY;
+    if (t < nb) {
+        // running (M, o, l); a batch of partials joins with the new maximum
+        auto join = [&](float mb) -> float {
+            const float m_new = fmaxf(M, mb);
+            const float f = (M == -INFINITY) ? 0.0f : fexp2(M - m_new);
+            o[0] = f32x4{f * o[0][0], f * o[0][1], f * o[0][2], f * o[0][3]};
+            o[1] = f32x4{f * o[1][0], f * o[1][1], f * o[1][2], f * o[1][3]};
+            l *= f;
+            M = m_new;
+            return m_new;
+        };
+        auto add = [&](float ms, float ls, const f32x4 &x0, const f32x4 &x1) {
+            const float f = (ms == -INFINITY) ? 0.0f : fexp2(ms - M);
 #pragma unroll
-        for (int q = 0; q < 8; ++q) reinterpret_cast<f32x4 *>(dst)[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-        return;
-    }
-    const int64_t bzr = (int64_t)b * a.n_groups + tg0 + rr / G;
-    const float *pp = a.part + ((bzr * a.n_kv + h) * a.n_splits) * G * (D + 2) + (rr % G) * (D + 2);
-    const int64_t stride = (int64_t)G * (D + 2);
-    const int P = a.n_page_splits;
-    const float mw = wml[2 * rr];
-    float M = mw;
-    for (int s0 = 0; s0 < P; s0 += 8) {
-        float ms[8];
+            for (int k = 0; k < 4; ++k) {
+                o[0][k] = fmaf(f, x0[k], o[0][k]);
+                o[1][k] = fmaf(f, x1[k], o[1][k]);
+            }
+            l = fmaf(f, ls, l);
+        };
+        float mw[4];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) ms[e] = s0 + e < P ? pp[(s0 + e) * stride + D] : -INFINITY;
+        for (int w = 0; w < 4; ++w) mw[w] = wml[2 * (w * 16 + ri)];
+        join(fmaxf(fmaxf(mw[0], mw[1]), fmaxf(mw[2], mw[3])));
 #pragma unroll
-        for (int e = 0; e < 8; ++e) M = fmaxf(M, ms[e]);
-    }
-    f32x4 o[8];
-    const float fw = (M == -INFINITY || mw == -INFINITY) ? 0.0f : fexp2(mw - M);
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        const f32x4 x = *reinterpret_cast<const f32x4 *>(wo + rr * D + c0 + 4 * q);
-        o[q] = f32x4{fw * x[0], fw * x[1], fw * x[2], fw * x[3]};
-    }
-    float l = fw * wml[2 * rr + 1];
-    for (int s0 = 0; s0 < P; s0 += 2) {
-        f32x4 x[2][8];
-        float ms[2], ls[2];
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-            const int sp = s0 + e < P ? s0 + e : s0;  // (a repeat of s0 weighs 0)
-            const float *src = pp + sp * stride;
-            ms[e] = s0 + e < P ? src[D] : -INFINITY;
-            ls[e] = src[D + 1];
-#pragma unroll
-            for (int q = 0; q < 8; ++q) x[e][q] = *reinterpret_cast<const f32x4 *>(src + c0 + 4 * q);
+        for (int w = 0; w < 4; ++w) {
+            const float *src = wo + (w * 16 + ri) * D + c0;
+            add(mw[w], wml[2 * (w * 16 + ri) + 1], *reinterpret_cast<const f32x4 *>(src),
+                *reinterpret_cast<const f32x4 *>(src + 4));
         }
+        const int64_t bzr = (int64_t)b * a.n_groups + tg0 + rr / G;
+        const float *pp = a.part + ((bzr * a.n_kv + h) * a.n_splits) * G * (D + 2) + (rr % G) * (D + 2);
+        const int64_t stride = (int64_t)G * (D + 2);
+        for (int s0 = 0; s0 < a.n_page_splits; s0 += 8) {
+            float ms[8], ls[8];
+            f32x4 x[8][2];
 #pragma unroll
-        for (int e = 0; e < 2; ++e) {
-            const float f = (M == -INFINITY || ms[e] == -INFINITY) ? 0.0f : fexp2(ms[e] - M);
+            for (int e = 0; e < 8; ++e) {
+                const bool in = s0 + e < a.n_page_splits;
+                const float *src = pp + (in ? s0 + e : s0) * stride;  // (a repeat weighs 0)
+                ms[e] = in ? src[D] : -INFINITY;
+                ls[e] = src[D + 1];
+                x[e][0] = *reinterpret_cast<const f32x4 *>(src + c0);
+                x[e][1] = *reinterpret_cast<const f32x4 *>(src + c0 + 4);
+            }
+            float mb = ms[0];
 #pragma unroll
-            for (int q = 0; q < 8; ++q)
+            for (int e = 1; e < 8; ++e) mb = fmaxf(mb, ms[e]);
+            join(mb);
 #pragma unroll
-                for (int k = 0; k < 4; ++k) o[q][k] = fmaf(f, x[e][q][k], o[q][k]);
-            l = fmaf(f, ls[e], l);
+            for (int e = 0; e < 8; ++e) add(ms[e], ls[e], x[e][0], x[e][1]);
         }
     }
 #pragma unroll
-    for (int q = 0; q < 8; ++q)
+    for (int q = 0; q < 2; ++q)
         reinterpret_cast<f32x4 *>(dst)[q] = l > 0.0f ? f32x4{o[q][0] / l, o[q][1] / l, o[q][2] / l, o[q][3] / l}
                                                   : f32x4{0.f, 0.f, 0.f, 0.f};
 }
@@ -2326,17 +2395,18 @@ static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok
     const bool form = !rs.share && wgs * 4 <= resident_waves(c->head_dim, storage_bits(c->bits), G, false);
     const int key = c->head_dim * 10 + storage_bits(c->bits);
     if (rs.share && c->head_dim == 128 && G == 8) {
-        // chunks: q~ rows, the pages (chunk_pages_kernel, splits 0 ..
+        // chunks: q~ rows (chunk_qt_kernel), the pages (chunk_pages_kernel, splits 0 ..
         // n_page_splits - 1), then the window slots merged with the page
         // runs into the output (chunk_window_kernel)
         const unsigned blocks = (unsigned)(c->batch * ((rs.n_groups + 7) / 8));
         const dim3 gp(c->n_kv_heads, p.n_page_splits, blocks);
-        const dim3 gw(c->n_kv_heads, blocks);
+        const dim3 gw(c->n_kv_heads, 4 * blocks);
+        const dim3 gq(c->n_kv_heads, (unsigned)(c->batch * ((rs.n_groups + 1) / 2)));
         if (key == 1282) {
-            launch("decode_qt_kernel", decode_qt_kernel<128, 2, 8>, dim3(c->n_kv_heads, rows_z), dim3(256), s, a);
+            launch("chunk_qt_kernel", chunk_qt_kernel<2>, gq, dim3(256), s, a);
             if (p.n_page_splits > 0) launch("chunk_pages_kernel", chunk_pages_kernel<2>, gp, dim3(256), s, a);
         } else {
-            launch("decode_qt_kernel", decode_qt_kernel<128, 4, 8>, dim3(c->n_kv_heads, rows_z), dim3(256), s, a);
+            launch("chunk_qt_kernel", chunk_qt_kernel<4>, gq, dim3(256), s, a);
             if (p.n_page_splits > 0) launch("chunk_pages_kernel", chunk_pages_kernel<4>, gp, dim3(256), s, a);
         }
         launch("chunk_window_kernel", chunk_window_kernel, gw, dim3(256), s, a, out);
