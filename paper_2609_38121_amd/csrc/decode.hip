@@ -1153,7 +1153,10 @@ decode_main_kernel(DecodeArgs a)
         // SHARE: every wave all 16-slot tiles of the workgroup's units, with
         // an online softmax across them
         // (otherwise wave w takes tile w of each of the workgroup's units)
-        const int kSub = SHARE ? 4 * a.win_units : a.win_units;
+        // (the query-forming variant runs only plans of one unit per window
+        // workgroup: its loop is a single tile, kept compile-time so that it
+        // costs no registers)
+        const int kSub = SHARE ? 4 * a.win_units : (FORM ? 1 : a.win_units);
         for (int st = 0; st < (rows_live ? kSub : 0); ++st) {
             const int32_t slot0 = unit0 + 16 * (SHARE ? st : wave + 4 * st);
             // this tile's live slots, one bit per slot (lanes 0..15)
@@ -2392,7 +2395,8 @@ static int attend(const wushkv_cache *c, const uint16_t *q, const int32_t *n_tok
     // that read once per workgroup, so a small kernel forms q~ first; so do
     // grids of shared work items.
     const int64_t wgs = (int64_t)p.n_splits * c->n_kv_heads * grid_z;
-    const bool form = !rs.share && wgs * 4 <= resident_waves(c->head_dim, storage_bits(c->bits), G, false);
+    const bool form = !rs.share && p.win_units == 1 &&
+                      wgs * 4 <= resident_waves(c->head_dim, storage_bits(c->bits), G, false);
     const int key = c->head_dim * 10 + storage_bits(c->bits);
     if (rs.share && c->head_dim == 128 && G == 8) {
         // chunks: q~ rows (chunk_qt_kernel), the pages (chunk_pages_kernel, splits 0 ..
