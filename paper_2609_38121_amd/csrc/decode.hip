@@ -625,11 +625,12 @@ struct MainLds {
     static constexpr int kWave = kStageBytes + kTBytes;
     // Workgroups a compute unit keeps resident, as the variants' register
     // counts allow (three waves per SIMD at most; fewer for the 4-bit and
-    // the eight-head ones: the 2-bit eight-head decode kernel is given two,
-    // and the registers of a third, so that its page loop does not spill);
-    // it only decides the query rows' placement.
+    // the eight-head ones: the 2-bit eight-head decode kernel at d = 128 and
+    // the 4-bit eight-head kernels at d = 64 are given two, and the
+    // registers of a third, so that their page loops do not spill); it only
+    // decides the query rows' placement.
     static constexpr int kResident = D == 128 ? (BITS == 2 ? (G == 8 ? 2 : 3) : (G == 8 ? 1 : 2))
-                                              : (BITS == 2 ? (G == 8 ? 3 : 4) : 3);
+                                              : (BITS == 2 ? (G == 8 ? 3 : 4) : (G == 8 ? 2 : 3));
     // The query rows get LDS of their own when that keeps the residency:
     // the pages can then be in flight while the rows are formed.  Otherwise
     // they borrow the start of the page stages, and the pages wait for them.
@@ -691,7 +692,7 @@ __device__ void step_token(const DecodeArgs &a, int b, int h, int32_t slot, uint
 // HBM once per four token groups; grid z runs over (sequence, group of four
 // token groups) and every wave writes its own partials.
 template <int D, int BITS, int G, bool FORM, bool SHARE>
-__global__ void __launch_bounds__(256, (D == 128 && BITS == 2 && G == 8 && !SHARE) ? 2 : 3)
+__global__ void __launch_bounds__(256, ((D == 128 && BITS == 2 && G == 8 && !SHARE) || (D == 64 && BITS == 4 && G == 8)) ? 2 : 3)
 decode_main_kernel(DecodeArgs a)
 {
     static_assert(!(FORM && SHARE), "shared work items take q~ from decode_qt_kernel");
