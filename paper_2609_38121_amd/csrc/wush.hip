@@ -19,7 +19,7 @@
 //      L columns are L U: the eigendecomposition without forming L^T M_d L,
 //      and with the eigenvalues' relative accuracy of a one-sided method.
 //      The d/2 disjoint pairs of a round (a round-robin tournament) rotate in
-//      parallel, each by 512/d threads;
+//      parallel, each by 1024/d threads (512 per workgroup);
 //   4. the eigenpairs in ascending order, each eigenvector's sign fixed so
 //      that the largest-magnitude entry of L u_k is positive (the paper
 //      fixes neither; Had mixes them, so T depends on both);
@@ -32,20 +32,55 @@
 namespace wushkv {
 
 constexpr int kWushMaxSweeps = 40;
+// Threads of a workgroup: eight waves, two per SIMD, so that one wave's LDS
+// and barrier waits overlap the other's arithmetic (the frame's LDS admits
+// one workgroup per compute unit).
+constexpr int kWushThreads = 512;
+constexpr int kWushWaves = kWushThreads / 64;
 
+// Sum of one value per wave (in red[wave]) in a fixed order.
+__device__ __forceinline__ float wave_total(const float *red)
+{
+    float t = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kWushWaves; ++w) t += red[w];
+    return t;
+}
+
+// Column stride of the LDS frame: 16-byte aligned, and 16 banks apart for
+// neighbouring columns, so that the Jacobi rounds' 16-byte reads of the
+// pairs' columns by consecutive lanes fall on distinct banks.
 template <int D>
 struct WushLds {
-    static constexpr int kP = 2 * D + 1;  // column stride (odd: columns on different banks)
+    static constexpr int kP = 2 * D + 16;
 };
 
 // Lane exchange within aligned groups of N lanes (N a power of two <= 64):
-// the sum over the group, the same value in every lane of the group.
+// the sum over the group, the same value in every lane of the group (each
+// step adds the same two partial sums in every lane, so all lanes agree bit
+// for bit).  Groups of up to 16 lanes sum by DPP inside the lanes' row:
+// quad permutations, then the half-row and the row mirrors, which pair each
+// quad (each half row) with the other one of its group.
+template <int CTRL>
+__device__ __forceinline__ float wush_dpp(float x)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF,
+                                                                  0xF, false));
+}
 template <int N>
 __device__ __forceinline__ float group_sum(float x)
 {
+    if constexpr (N <= 16) {
+        if constexpr (N >= 2) x += wush_dpp<0xB1>(x);   // quad_perm [1, 0, 3, 2]
+        if constexpr (N >= 4) x += wush_dpp<0x4E>(x);   // quad_perm [2, 3, 0, 1]
+        if constexpr (N >= 8) x += wush_dpp<0x141>(x);  // row_half_mirror
+        if constexpr (N >= 16) x += wush_dpp<0x140>(x); // row_mirror
+        return x;
+    } else {
 #pragma unroll
-    for (int off = 1; off < N; off <<= 1) x += __shfl_xor(x, off);
-    return x;
+        for (int off = 1; off < N; off <<= 1) x += __shfl_xor(x, off);
+        return x;
+    }
 }
 
 // In-place Cholesky of the symmetric matrix held in rows off .. off + D - 1
@@ -66,12 +101,12 @@ __device__ bool cholesky(float *X, int off, int tid)
         if (tid == 0 && !(piv > 0.0f)) bad = 1;
         const float inv = piv > 0.0f ? 1.0f / ljj : 0.0f;
         __syncthreads();  // every thread has read the pivot
-        for (int i = j + 1 + tid; i < D; i += 256) cj[i] *= inv;
+        for (int i = j + 1 + tid; i < D; i += kWushThreads) cj[i] *= inv;
         if (tid == 0) cj[j] = ljj;
         __syncthreads();
         // trailing update of the lower triangle: A[i][k] -= l_i l_k, i >= k > j
         const int n = D - 1 - j;
-        for (int e = tid; e < n * n; e += 256) {
+        for (int e = tid; e < n * n; e += kWushThreads) {
             const int kk = e / n, ii = e % n;
             if (ii < kk) continue;
             const int k = j + 1 + kk, i = j + 1 + ii;
@@ -79,7 +114,7 @@ __device__ bool cholesky(float *X, int off, int tid)
         }
         __syncthreads();
     }
-    for (int e = tid; e < D * D; e += 256) {
+    for (int e = tid; e < D * D; e += kWushThreads) {
         const int k = e / D, i = e % D;
         if (i < k) X[k * P + off + i] = 0.0f;
     }
@@ -94,13 +129,13 @@ __device__ float load_damped(const float *A, float *X, int off, float gamma, int
 {
     constexpr int P = WushLds<D>::kP;
     float t = 0.0f;
-    for (int i = tid; i < D; i += 256) t += A[i * D + i];
+    for (int i = tid; i < D; i += kWushThreads) t += A[i * D + i];
     t = group_sum<64>(t);
     if ((tid & 63) == 0) red[tid >> 6] = t;
     __syncthreads();
-    const float tr = (red[0] + red[1]) + (red[2] + red[3]);
+    const float tr = wave_total(red);
     const float damp = gamma * tr / (float)D;
-    for (int e = tid; e < D * D; e += 256) {
+    for (int e = tid; e < D * D; e += kWushThreads) {
         const int i = e / D, k = e % D;  // row-major read, coalesced
         if (i >= k) X[k * P + off + i] = A[e] + (i == k ? damp : 0.0f);
     }
@@ -115,7 +150,7 @@ __device__ void fwht_columns(float *X, int tid)
 {
     constexpr int P = WushLds<D>::kP;
     for (int h = 1; h < D; h <<= 1) {
-        for (int e = tid; e < D * (D / 2); e += 256) {
+        for (int e = tid; e < D * (D / 2); e += kWushThreads) {
             const int col = e / (D / 2), m = e % (D / 2);
             const int r0 = (m / h) * 2 * h + m % h, r1 = r0 + h;
             float *c = X + col * P;
@@ -128,18 +163,18 @@ __device__ void fwht_columns(float *X, int tid)
 }
 
 template <int D>
-__global__ void __launch_bounds__(256) wush_kernel(const float *m_all, const float *h_all, float gamma,
+__global__ void __launch_bounds__(kWushThreads) wush_kernel(const float *m_all, const float *h_all, float gamma,
                                                    float *t_all, float *tinv_all, int32_t *sweeps_out)
 {
     constexpr int P = WushLds<D>::kP;
     constexpr int kPairs = D / 2;
-    constexpr int kTpp = 256 / kPairs;  // threads per pair: 4 (d 128) or 8 (d 64)
+    constexpr int kTpp = kWushThreads / kPairs;  // threads per pair: 8 (d 128) or 16 (d 64)
     constexpr int kRows = D / kTpp;     // rows of each half per thread
     constexpr float kTol = 4.0f * (D == 128 ? 11.3137085f : 8.0f) * 5.9604645e-8f;
-    __shared__ float X[D * P];
+    __shared__ __attribute__((aligned(16))) float X[D * P];
     __shared__ float lam[D], scl[D];
     __shared__ int perm[D];
-    __shared__ float red[4];
+    __shared__ float red[kWushWaves];
     const int tid = threadIdx.x;
     const int64_t pair = blockIdx.x;
     const float *M = m_all + pair * D * D;
@@ -153,7 +188,7 @@ __global__ void __launch_bounds__(256) wush_kernel(const float *m_all, const flo
     const float trM = load_damped<D>(M, X, 0, gamma, tid, red);
     ok = cholesky<D>(X, 0, tid) && ok;
     if (!ok) {
-        for (int e = tid; e < D * D; e += 256) {
+        for (int e = tid; e < D * D; e += kWushThreads) {
             T[e] = NAN;
             if (Ti != nullptr) Ti[e] = NAN;
         }
@@ -169,7 +204,7 @@ __global__ void __launch_bounds__(256) wush_kernel(const float *m_all, const flo
         for (int a = 0; a < 8; ++a)
 #pragma unroll
             for (int b = 0; b < 8; ++b) acc[a][b] = 0.0f;
-        const int tile = tid;  // D = 128: 256 tiles, one per thread; D = 64: 64 tiles
+        const int tile = tid;  // D = 128: 256 tiles, D = 64: 64 tiles, one per thread
         const bool have = tile < kT * kT;
         const int ti = have ? tile / kT : 0, tj = have ? tile % kT : 0;
         if (have) {
@@ -209,17 +244,22 @@ __global__ void __launch_bounds__(256) wush_kernel(const float *m_all, const flo
             auto at = [&](int pos) { return pos == 0 ? 0 : 1 + (pos - 1 + round) % (D - 1); };
             const int p = at(pm), q = at(D - 1 - pm);
             // this thread's rows of the two B halves stay in registers from
-            // the dot products to the rotation
-            float *cp = X + p * P + part * kRows, *cq = X + q * P + part * kRows;
-            float xb[kRows], yb[kRows];
+            // the dot products to the rotation: the 4-row pieces
+            // 4 (kTpp k + part) .. + 3, one 16-byte access each
+            float *cp = X + p * P, *cq = X + q * P;
+            f32x4 xb[kRows / 4], yb[kRows / 4];
             float al = 0.0f, be = 0.0f, ga = 0.0f;
 #pragma unroll
-            for (int e = 0; e < kRows; ++e) {
-                xb[e] = cp[e];
-                yb[e] = cq[e];
-                al = fmaf(xb[e], xb[e], al);
-                be = fmaf(yb[e], yb[e], be);
-                ga = fmaf(xb[e], yb[e], ga);
+            for (int k = 0; k < kRows / 4; ++k) {
+                const int r = 4 * (kTpp * k + part);
+                xb[k] = *reinterpret_cast<const f32x4 *>(cp + r);
+                yb[k] = *reinterpret_cast<const f32x4 *>(cq + r);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    al = fmaf(xb[k][i], xb[k][i], al);
+                    be = fmaf(yb[k][i], yb[k][i], be);
+                    ga = fmaf(xb[k][i], yb[k][i], ga);
+                }
             }
             al = group_sum<kTpp>(al);
             be = group_sum<kTpp>(be);
@@ -232,15 +272,30 @@ __global__ void __launch_bounds__(256) wush_kernel(const float *m_all, const flo
                 const float cs = 1.0f / sqrtf(1.0f + t * t);
                 const float sn = cs * t;
 #pragma unroll
-                for (int e = 0; e < kRows; ++e) {
-                    cp[e] = cs * xb[e] - sn * yb[e];
-                    cq[e] = sn * xb[e] + cs * yb[e];
+                for (int k = 0; k < kRows / 4; ++k) {
+                    const int r = 4 * (kTpp * k + part);
+                    f32x4 u, v;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        u[i] = fmaf(cs, xb[k][i], -sn * yb[k][i]);
+                        v[i] = fmaf(sn, xb[k][i], cs * yb[k][i]);
+                    }
+                    *reinterpret_cast<f32x4 *>(cp + r) = u;
+                    *reinterpret_cast<f32x4 *>(cq + r) = v;
                 }
-#pragma unroll 8
-                for (int e = 0; e < kRows; ++e) {
-                    const float x = cp[D + e], y = cq[D + e];
-                    cp[D + e] = cs * x - sn * y;
-                    cq[D + e] = sn * x + cs * y;
+#pragma unroll
+                for (int k = 0; k < kRows / 4; ++k) {
+                    const int r = D + 4 * (kTpp * k + part);
+                    const f32x4 x = *reinterpret_cast<const f32x4 *>(cp + r);
+                    const f32x4 y = *reinterpret_cast<const f32x4 *>(cq + r);
+                    f32x4 u, v;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        u[i] = fmaf(cs, x[i], -sn * y[i]);
+                        v[i] = fmaf(sn, x[i], cs * y[i]);
+                    }
+                    *reinterpret_cast<f32x4 *>(cp + r) = u;
+                    *reinterpret_cast<f32x4 *>(cq + r) = v;
                 }
                 rotated = 1;
             }
@@ -250,7 +305,7 @@ __global__ void __launch_bounds__(256) wush_kernel(const float *m_all, const flo
     }
 
     // ---- 4. eigenvalues, their order, the eigenvector signs, c
-    for (int k = tid; k < D; k += 256) {
+    for (int k = tid; k < D; k += kWushThreads) {
         const float *ck = X + k * P;
         float s = 0.0f;
         for (int i = 0; i < D; ++i) s = fmaf(ck[i], ck[i], s);
@@ -268,34 +323,34 @@ __global__ void __launch_bounds__(256) wush_kernel(const float *m_all, const flo
     }
     // (every slot of perm holds a valid column even if non-finite norms
     // left ranks tied)
-    for (int r = tid; r < D; r += 256) perm[r] = r;
+    for (int r = tid; r < D; r += kWushThreads) perm[r] = r;
     __syncthreads();
-    for (int k = tid; k < D; k += 256) {
+    for (int k = tid; k < D; k += kWushThreads) {
         int rank = 0;
         const float lk = lam[k];
         for (int j = 0; j < D; ++j) rank += (lam[j] < lk) || (lam[j] == lk && j < k);
         perm[rank] = k;
     }
     float rs = 0.0f;
-    for (int k = tid; k < D; k += 256) rs += sqrtf(lam[k]);
+    for (int k = tid; k < D; k += kWushThreads) rs += sqrtf(lam[k]);
     rs = group_sum<64>(rs);
     __syncthreads();
     if ((tid & 63) == 0) red[tid >> 6] = rs;
     __syncthreads();
-    const float sum_sqrt = (red[0] + red[1]) + (red[2] + red[3]);
+    const float sum_sqrt = wave_total(red);
     const float c = sqrtf((1.0f + gamma) * trM) / sqrtf(sum_sqrt);
     const float had = 1.0f / sqrtf((float)D);
 
     // ---- 5a. T: column j of the B halves gets y_r[j] = s_k lam_k^(-1/4)
     // (L u_k)[j], k = perm[r]; the transform along r gives row r of Had Y
-    for (int e = tid; e < D * D; e += 256) {
+    for (int e = tid; e < D * D; e += kWushThreads) {
         const int j = e / D, r = e % D;
         const int k = perm[r];
         X[j * P + r] = scl[k] * powf(lam[k], -0.25f) * X[k * P + D + j];
     }
     __syncthreads();
     fwht_columns<D>(X, tid);
-    for (int e = tid; e < D * D; e += 256) {
+    for (int e = tid; e < D * D; e += kWushThreads) {
         const int i = e / D, j = e % D;  // row-major write, coalesced
         T[e] = (c * had) * X[j * P + i];
     }
@@ -307,7 +362,7 @@ __global__ void __launch_bounds__(256) wush_kernel(const float *m_all, const flo
     // (column j holds M_d[.][j]), Z = M_d W in 8 x 8 tiles, row i of Z into
     // column i, then the transform along each row
     const float damp = gamma * trM / (float)D;
-    for (int e = tid; e < D * D; e += 256) {
+    for (int e = tid; e < D * D; e += kWushThreads) {
         const int i = e / D, j = e % D;
         const float v = i >= j ? M[e] : M[j * D + i];  // the lower triangle, mirrored
         X[j * P + i] = v + (i == j ? damp : 0.0f);
@@ -357,7 +412,7 @@ __global__ void __launch_bounds__(256) wush_kernel(const float *m_all, const flo
         __syncthreads();
     }
     fwht_columns<D>(X, tid);
-    for (int e = tid; e < D * D; e += 256) {
+    for (int e = tid; e < D * D; e += kWushThreads) {
         const int i = e / D, r = e % D;
         Ti[e] = had * X[i * P + r];
     }
@@ -381,9 +436,9 @@ extern "C" int wushkv_wush_transform(const float *m, const float *h, int32_t cou
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const dim3 grid((unsigned)count);
     if (d == 128)
-        launch("wush_kernel", wush_kernel<128>, grid, dim3(256), s, m, h, gamma, t_out, t_inv_out, sweeps_out);
+        launch("wush_kernel", wush_kernel<128>, grid, dim3(kWushThreads), s, m, h, gamma, t_out, t_inv_out, sweeps_out);
     else
-        launch("wush_kernel", wush_kernel<64>, grid, dim3(256), s, m, h, gamma, t_out, t_inv_out, sweeps_out);
+        launch("wush_kernel", wush_kernel<64>, grid, dim3(kWushThreads), s, m, h, gamma, t_out, t_inv_out, sweeps_out);
     if (hipGetLastError() != hipSuccess) return WUSHKV_ELAUNCH;
     return WUSHKV_OK;
 }
