@@ -47,12 +47,14 @@ __device__ __forceinline__ float wave_total(const float *red)
     return t;
 }
 
-// Column stride of the LDS frame: 16-byte aligned, and 16 banks apart for
-// neighbouring columns, so that the Jacobi rounds' 16-byte reads of the
-// pairs' columns by consecutive lanes fall on distinct banks.
+// Column stride of the LDS frame: 16-byte aligned, and 32 banks apart for
+// neighbouring columns.  In a Jacobi round the eight lanes of a pair read
+// 32 consecutive floats of its column (32 banks) and the next eight lanes
+// the neighbouring column, so a 16-lane group's reads fall on distinct
+// banks.
 template <int D>
 struct WushLds {
-    static constexpr int kP = 2 * D + 16;
+    static constexpr int kP = 2 * D + 32;
 };
 
 // Lane exchange within aligned groups of N lanes (N a power of two <= 64):
