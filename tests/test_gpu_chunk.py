@@ -48,7 +48,7 @@ def _check(p, q, n_tok, max_seq_len=None):
     return gpu
 
 
-@pytest.mark.parametrize("d,bits,G", [(128, 2, 4), (128, 4, 8), (64, 2, 1), (64, 4, 2)])
+@pytest.mark.parametrize("d,bits,G", [(128, 2, 4), (128, 4, 8), (128, 3, 2), (64, 2, 1), (64, 4, 2)])
 def test_chunk_attention_ragged(gpu, d, bits, G):
     rng = np.random.default_rng(200 + d + bits + G)
     B, H, T = 3, 2, 16
