@@ -42,6 +42,7 @@
 // probabilities, again split hi + lo, go through LDS into a 16x16x16 bf16
 // P V product against the channel-major value slots.
 #include <atomic>
+#include <cfloat>
 #include <mutex>
 
 #include "common.h"
@@ -1481,9 +1482,11 @@ __global__ void __launch_bounds__(256, 2) chunk_pages_kernel(DecodeArgs a)
     float m_run[4], lc[4], zc[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        m_run[r] = -INFINITY;
+        m_run[r] = -FLT_MAX;
         lc[r] = zc[r] = 0.0f;
     }
+    float one;
+    asm("v_mov_b32 %0, 1.0" : "=v"(one));
     f32x4 acc[4][kNTw];
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt)
@@ -1569,13 +1572,16 @@ __global__ void __launch_bounds__(256, 2) chunk_pages_kernel(DecodeArgs a)
             }
             // online softmax of row rz over this page's tokens 4 n .. 4 n + 3
             const float mx = row_max16(fmaxf(fmaxf(lg[0], lg[1]), fmaxf(lg[2], lg[3])));
+            // (m_run starts at -FLT_MAX, so m_new is finite: a first page
+            // scales zeros by exp2(-huge) = 0, and a row with no key yet
+            // keeps weights exp2(-inf) = 0)
             const float m_new = fmaxf(m_run[r], mx);
-            const float al = m_new == -INFINITY ? 1.0f : fexp2(m_run[r] - m_new);
+            const float al = fexp2(m_run[r] - m_new);
             lc[r] *= al;
             zc[r] *= al;
             m_run[r] = m_new;
             alpha[rz] = al;  // (the row's 16 lanes store the same value)
-            const float mo = m_new == -INFINITY ? 0.0f : m_new + off;
+            const float mo = m_new + off;
             float wgt[4];
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
@@ -1584,12 +1590,15 @@ __global__ void __launch_bounds__(256, 2) chunk_pages_kernel(DecodeArgs a)
                 zc[r] = fmaf(pw, vz[t], zc[r]);
                 wgt[t] = fmaf(pw, vs[t], 0.0f);
             }
+            // fp16 hi parts, then the lo parts w - hi in one rounding each
+            // (one mixed-precision fma per weight: `one` is opaque to the
+            // compiler, which would otherwise fold the product away)
             const uint32_t h01 = pack_f16_rne(wgt[0], wgt[1]);
             const uint32_t h23 = pack_f16_rne(wgt[2], wgt[3]);
-            const uint32_t l01 = pack_f16_rne(fmaf(-1.0f, f16_bits_to_f32(h01 & 0xFFFFu), wgt[0]),
-                                              fmaf(-1.0f, f16_bits_to_f32(h01 >> 16), wgt[1]));
-            const uint32_t l23 = pack_f16_rne(fmaf(-1.0f, f16_bits_to_f32(h23 & 0xFFFFu), wgt[2]),
-                                              fmaf(-1.0f, f16_bits_to_f32(h23 >> 16), wgt[3]));
+            const uint32_t l01 = pack_f16_rne(fmaf(-f16_bits_to_f32(h01 & 0xFFFFu), one, wgt[0]),
+                                              fmaf(-f16_bits_to_f32(h01 >> 16), one, wgt[1]));
+            const uint32_t l23 = pack_f16_rne(fmaf(-f16_bits_to_f32(h23 & 0xFFFFu), one, wgt[2]),
+                                              fmaf(-f16_bits_to_f32(h23 >> 16), one, wgt[3]));
             lds_write8(wbase + tbuf_at(rz, 8 * n), h01, h23);
             lds_write8(wbase + C::kRows * 128 + tbuf_at(rz, 8 * n), l01, l23);
         }
@@ -1704,7 +1713,7 @@ __global__ void __launch_bounds__(256, 2) chunk_pages_kernel(DecodeArgs a)
             if (n == 0) {
                 const int rz = 16 * wave + 4 * j + r;
                 zrow[rz] = zt;
-                mrow[rz] = m_run[r];
+                mrow[rz] = m_run[r] == -FLT_MAX ? -INFINITY : m_run[r];  // no key: -inf
                 lrow[rz] = lt;
             }
         }
