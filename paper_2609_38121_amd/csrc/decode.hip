@@ -2,23 +2,30 @@
 // bf16 / packed-code cache (Alg. 2 step 5, Eq. (2)), with the query-side
 // compensation q~ = q^T T_K^{-1} of Eq. (3).
 //
-// Two launches on the caller's stream:
+// Launches on the caller's stream:
+//   decode_qt_kernel       (only when the main grid runs in several
+//                          residency rounds) q~ and its limbs per (kv head,
+//                          row), into the workspace; otherwise each main
+//                          workgroup forms them itself in LDS.
 //   decode_main_kernel     grid (kv heads, splits, rows: a row is a sequence,
 //                          or a sequence's token group for chunks), four
 //                          waves per workgroup; the kv head on x deals each
-//                          head to one XCD.  Each workgroup first forms q~ for its
-//                          query heads in LDS, scaled by sm_scale log2(e) so
-//                          that the softmax runs in base 2, together with the
-//                          form the quantised-key product consumes: q~ in
+//                          head to one XCD.  q~ is scaled by sm_scale log2(e)
+//                          so that the softmax runs in base 2, and comes with
+//                          the form the quantised-key product consumes: q~ in
 //                          24-bit fixed point as six fp8 digit "limbs" with
 //                          one power-of-two scale each, and sum(q~).
-//                          Workgroups 0 .. n_page_splits - 1 then scan the
+//                          Workgroups 0 .. n_page_splits - 1 scan the
 //                          quantised pages, each wave a contiguous run; the
-//                          others scan the bf16 sink + ring slots, one
-//                          64-slot unit per workgroup, 16 slots per wave.
-//                          Each workgroup writes one partial (m, l, o) per
-//                          query head.
+//                          others scan the bf16 sink + ring slots: one
+//                          64-slot unit per workgroup, 16 slots per wave, or,
+//                          when the grid runs in rounds, one workgroup per
+//                          row whose waves walk all the units.  Each
+//                          workgroup writes one partial (m, l, o) per query
+//                          head.
 //   decode_combine_kernel  log-sum-exp merge of the splits.
+// Chunks at d = 128 run chunk_qt_kernel, chunk_pages_kernel and
+// chunk_window_kernel instead (below).
 //
 // Quantised pages.  A stored key is k = s c + z per token, so
 //   q~ . k = s (q~ . c) + z sum(q~).
