@@ -513,8 +513,9 @@ def bench_llama_step(torch, wk, synth, dev, args):
                 step(done + i)
     torch.cuda.current_stream().wait_stream(cap_stream)
     torch.cuda.synchronize()
-    # the capture enqueued nothing; replays advance every replica by one token
-    n_rep = max(1, steps // reps)
+    # the capture enqueued nothing; replays advance every replica by one
+    # token; at least `steps` steps are timed (whole replays)
+    n_rep = max(1, -(-steps // reps))
     K = n_rep * reps
     g.replay()  # one untimed replay (warm)
     torch.cuda.synchronize()
