@@ -124,8 +124,11 @@ __global__ void __launch_bounds__(256, (BITS == 4 && ROPE) ? 3 : 4) append_kerne
     }
 
     // ---- phase A: transformed keys -> kt, values -> vt
-    bool any_new = false;
-    for (int32_t p = lo; p < hi; ++p) any_new |= (do_new && is_new(p));
+    // the tile's new positions are [new_lo, hi); window writes go to those
+    // below s_sink or at or above q_new
+    const int32_t new_lo = max(lo, s_old);
+    const bool any_new = do_new && new_lo < hi;
+    const bool any_window = any_new && (new_lo < a.s_sink || hi > q_new);
     if (any_new) {
         // Wave w produces output channels [w D/4, (w+1) D/4) for all 64 rows.
         constexpr int kNtW = D / 64;  // N-tiles per wave
@@ -228,8 +231,9 @@ __global__ void __launch_bounds__(256, (BITS == 4 && ROPE) ? 3 : 4) append_kerne
     quantise_tile<D, BITS>(a, kt, vt, blk_lo, [&](int32_t p) { return p >= lo && p < hi && quant_now(p); },
                            pg, sh_page + 1, tid);
 
-    // ---- phase D: bf16 windows and the optional k~ output
-    {
+    // ---- phase D: bf16 windows and the optional k~ output (a tile of
+    // the quantised region of a prefill has neither)
+    if (any_window || (any_new && a.k_tilde_out != nullptr)) {
         constexpr int kVec = D / 8;
         for (int idx = tid; idx < kPage * kVec; idx += 256) {
             const int r = idx / kVec, cv = idx % kVec;
@@ -245,7 +249,7 @@ __global__ void __launch_bounds__(256, (BITS == 4 && ROPE) ? 3 : 4) append_kerne
             }
         }
         // values, channel-major: consecutive threads write consecutive slots
-        for (int idx = tid; idx < kPage * D; idx += 256) {
+        for (int idx = tid; any_window && idx < kPage * D; idx += 256) {
             const int ch = idx / kPage, r = idx % kPage;
             const int32_t p = blk_lo + r;
             if (p < lo || p >= hi || !window_write(p)) continue;

@@ -145,22 +145,39 @@ __device__ __forceinline__ void commit_finish(const AppendArgs &a, int b, int32_
     __hip_atomic_store(a.commit + b, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// max and min of two values as medians of three against an infinity held in
+// a register (inf: +inf for the max, -inf for the min): one instruction
+// each, where fmaxf / fminf first quiet an operand that might be a
+// signalling NaN, a second instruction per call.  Equal to fmaxf / fminf for
+// every non-NaN operand.  The infinity comes from opaque_inf: a literal one
+// would be folded back into fmaxf / fminf.
+__device__ __forceinline__ float opaque_inf(bool negative)
+{
+    float v = negative ? -INFINITY : INFINITY;
+    asm volatile("" : "+v"(v));
+    return v;
+}
+__device__ __forceinline__ float max_m3(float x, float y, float pinf) { return __builtin_amdgcn_fmed3f(x, y, pinf); }
+__device__ __forceinline__ float min_m3(float x, float y, float ninf) { return __builtin_amdgcn_fmed3f(x, y, ninf); }
+
 // Descending top-KMAX of the values pushed so far; t[0] is the largest.
 // Inserting a into a sorted list is one median-of-three per slot:
-// new t[i] = med3(t[i-1], t[i], a).
+// new t[i] = med3(t[i-1], t[i], a), and new t[0] = max(t[0], a).
 template <int KMAX>
 struct TopK {
     float t[KMAX];
+    float pinf;
     __device__ __forceinline__ void init()
     {
 #pragma unroll
         for (int i = 0; i < KMAX; ++i) t[i] = -1.0f;
+        pinf = opaque_inf(false);
     }
     __device__ __forceinline__ void push(float a)
     {
 #pragma unroll
         for (int i = KMAX - 1; i >= 1; --i) t[i] = __builtin_amdgcn_fmed3f(t[i - 1], t[i], a);
-        t[0] = fmaxf(t[0], a);
+        t[0] = max_m3(t[0], a, pinf);
     }
     // t[k] for a runtime k, as a chain of selects.  The empty assembly step
     // keeps the chain in registers: without it the compiler turns the chain
@@ -186,15 +203,18 @@ __device__ __forceinline__ float pair_swap(float x)
 }
 
 // a_lo and a_{lo+1} of the ascending sort of |x| over a bf16 row in LDS,
-// for lo >= D - KMAX, with the row's min and max.  The lane pair (2 r,
-// 2 r + 1) shares row r: each lane keeps the top KMAX of |x| over its half of
-// the row, then inserts its partner's list, so that both hold the top KMAX
-// of the whole row (the same multiset, hence the same sorted list).
-template <int D, int KMAX>
-__device__ __forceinline__ void order_stats_topk(const uint16_t *row, int hf, int lo, float &a_lo,
-                                                 float &a_hi, float &mn, float &mx)
+// for lo = D - K (a_lo is the K-th largest), with the row's min and max.
+// The lane pair (2 r, 2 r + 1) shares row r: each lane keeps the sorted top
+// K of |x| over its half of the row.  The top K of the whole row are then
+// max(t[i], t'[K-1-i]), i < K, with t' the partner's list (a descending list
+// against an ascending one: each pair's larger value is in the top K of the
+// union, and each smaller one is not); a_lo and a_{lo+1} are the smallest and
+// the second smallest of these.  Both lanes form the same multiset.
+template <int D, int K>
+__device__ __forceinline__ void order_stats_topk(const uint16_t *row, int hf, float &a_lo, float &a_hi,
+                                                 float &mn, float &mx)
 {
-    TopK<KMAX> tk;
+    TopK<K> tk;
     tk.init();
     mn = INFINITY;
     mx = -INFINITY;
@@ -214,16 +234,24 @@ __device__ __forceinline__ void order_stats_topk(const uint16_t *row, int hf, in
             }
         }
     }
-    float other[KMAX];
+    const float ninf = opaque_inf(true);
+    float c[K];
 #pragma unroll
-    for (int i = 0; i < KMAX; ++i) other[i] = pair_swap(tk.t[i]);
+    for (int i = 0; i < K; ++i) c[i] = max_m3(tk.t[i], pair_swap(tk.t[K - 1 - i]), tk.pinf);
+    if constexpr (K == 1) {
+        a_lo = a_hi = c[0];
+    } else {
+        float m1 = min_m3(c[0], c[1], ninf), m2 = max_m3(c[0], c[1], tk.pinf);
 #pragma unroll
-    for (int i = 0; i < KMAX; ++i) tk.push(other[i]);
+        for (int i = 2; i < K; ++i) {
+            m2 = __builtin_amdgcn_fmed3f(m1, m2, c[i]);  // m1 <= m2: the new second smallest
+            m1 = min_m3(m1, c[i], ninf);
+        }
+        a_lo = m1;
+        a_hi = m2;
+    }
     mn = fminf(mn, pair_swap(mn));
     mx = fmaxf(mx, pair_swap(mx));
-    const int K = D - lo;  // a_lo is the K-th largest
-    a_lo = tk.get(K - 1);
-    a_hi = (K >= 2) ? tk.get(K - 2) : a_lo;
 }
 
 // Same order statistics by counting ranks: any lo, O(D^2) work.  Used when
@@ -347,16 +375,14 @@ __device__ __forceinline__ uint32_t quest_code_of(float x, float inv, float h, f
     return __float_as_uint(c + 8388608.0f) - 0x4B000000u;
 }
 
-template <int D, int BITS>
-__device__ void order_stats(const uint16_t *row, int hf, int lo, float &a_lo, float &a_hi,
-                            float &mn, float &mx)
+// The selection for K = D - lo: the top-K lists for K = KC .. 16 (each its
+// own exact length), the rank count beyond.
+template <int D, int KC = 1>
+__device__ __forceinline__ void order_stats(const uint16_t *row, int hf, int lo, float &a_lo, float &a_hi,
+                                            float &mn, float &mx)
 {
-    const int K = D - lo;
-    if (K <= 2) order_stats_topk<D, 2>(row, hf, lo, a_lo, a_hi, mn, mx);
-    else if (K <= 4) order_stats_topk<D, 4>(row, hf, lo, a_lo, a_hi, mn, mx);
-    else if (K <= 8) order_stats_topk<D, 8>(row, hf, lo, a_lo, a_hi, mn, mx);
-    else if (K <= 12) order_stats_topk<D, 12>(row, hf, lo, a_lo, a_hi, mn, mx);
-    else if (K <= 16) order_stats_topk<D, 16>(row, hf, lo, a_lo, a_hi, mn, mx);
+    if (D - lo == KC) order_stats_topk<D, KC>(row, hf, a_lo, a_hi, mn, mx);
+    else if constexpr (KC < 16) order_stats<D, KC + 1>(row, hf, lo, a_lo, a_hi, mn, mx);
     else order_stats_rank<D>(row, hf, lo, a_lo, a_hi, mn, mx);
 }
 
@@ -468,7 +494,7 @@ __device__ void quantise_tile(const AppendArgs &a, const uint16_t *kt, uint16_t 
                 const int qlo = is_v ? a.lo_v : a.lo_k;
                 const float qt = is_v ? a.t_v : a.t_k;
                 float a_lo, a_hi, mn, mx;
-                order_stats<D, BITS>(row, hf, qlo, a_lo, a_hi, mn, mx);
+                order_stats<D>(row, hf, qlo, a_lo, a_hi, mn, mx);
                 quant_params(a_lo, a_hi, qt, qlo + 1 < D, mn, mx, kLevels, s16, z16, z, inv);
             }
             if (hf == 0)
