@@ -108,20 +108,24 @@ __global__ void __launch_bounds__(256, (BITS == 4 && ROPE) ? 3 : 4) append_kerne
 
     const int64_t head_win = ((int64_t)b * a.n_kv + h) * a.win_slots;  // win_k row base (slots)
 
-    // new values of this tile: loaded first, so that their latency overlaps
-    // the key transform (idx = tid + 256 q is row idx / kVec, 16-byte chunk
-    // idx % kVec)
+    // new values of this tile, loaded early so that their latency overlaps
+    // the key transform: first of all, or (with the fused normalisation,
+    // whose registers are full until it ends) right after the keys are
+    // staged (idx = tid + 256 q is row idx / kVec, 16-byte chunk idx % kVec)
     constexpr int kVec = D / 8;                   // uint4 per row
     constexpr int kVPer = kPage * kVec / 256;     // uint4 per thread
     uint4 vpre[kVPer];
+    auto load_values = [&]() {
 #pragma unroll
-    for (int q = 0; q < kVPer; ++q) {
-        const int idx = tid + 256 * q, r = idx / kVec, cv = idx % kVec;
-        const int32_t p = blk_lo + r;
-        if (p >= lo && p < hi && do_new && is_new(p))
-            vpre[q] = *reinterpret_cast<const uint4 *>(
-                a.v_new + (((int64_t)b * a.max_new + (p - s_old)) * a.n_kv + h) * D + 8 * cv);
-    }
+        for (int q = 0; q < kVPer; ++q) {
+            const int idx = tid + 256 * q, r = idx / kVec, cv = idx % kVec;
+            const int32_t p = blk_lo + r;
+            if (p >= lo && p < hi && do_new && is_new(p))
+                vpre[q] = *reinterpret_cast<const uint4 *>(
+                    a.v_new + (((int64_t)b * a.max_new + (p - s_old)) * a.n_kv + h) * D + 8 * cv);
+        }
+    };
+    if constexpr (!ROPE) load_values();
 
     // ---- phase A: transformed keys -> kt, values -> vt
     // the tile's new positions are [new_lo, hi); window writes go to those
@@ -134,24 +138,47 @@ __global__ void __launch_bounds__(256, (BITS == 4 && ROPE) ? 3 : 4) append_kerne
         constexpr int kNtW = D / 64;  // N-tiles per wave
         const int j = lane >> 4, n = lane & 15;
         constexpr bool fused = ROPE;
-        if constexpr (fused) {
-            // phase A0: RoPE(Norm(k)) of each new row once (wave w rows
-            // 16 w .. 16 w + 15), rounded to bf16 into the value rows, which
-            // serve as the key operand's staging until the values arrive
-            const int r = 16 * wave + n;
-            const int32_t p = blk_lo + r;
-            const bool ld = (p >= lo && p < hi && is_new(p) && do_new);
-            const uint16_t *krow = a.k_new + (((int64_t)b * a.max_new + (p - s_old)) * a.n_kv + h) * D;
+        // this wave's rows of T_K, in flight while the keys are staged (the
+        // fused variant loads them after the normalisation: its registers
+        // are full until then)
+        KeyTile<D, kNtW> xf;
+        if constexpr (!fused) xf.load(a.tk, h, wave * kNtW, lane);
+        // phase A0: each new row once (wave w rows 16 w .. 16 w + 15, one
+        // load per lane and chunk for the whole tile) into the value rows,
+        // which serve as the key operand's staging until the values arrive:
+        // RoPE(Norm(k)) rounded to bf16 when fused, else k as it came
+        // A row that is not new loads the first row of k_new (in bounds;
+        // it is replaced by zeros), so that every load of the tile is
+        // issued at once, with no branch between them.
+        const int r0 = 16 * wave + n;
+        const int32_t p0 = blk_lo + r0;
+        const bool ld0 = (p0 >= lo && p0 < hi && is_new(p0) && do_new);
+        const uint16_t *krow0 =
+            a.k_new + (ld0 ? (((int64_t)b * a.max_new + (p0 - s_old)) * a.n_kv + h) * D : (int64_t)0);
+        u32x4 kin[L::kChunks];
+#pragma unroll
+        for (int c = 0; c < L::kChunks; ++c) kin[c] = *reinterpret_cast<const u32x4 *>(krow0 + 32 * c + 8 * j);
+        if constexpr (!fused) {
+#pragma unroll
+            for (int c = 0; c < L::kChunks; ++c) {
+                const u32x4 zero = {0u, 0u, 0u, 0u};
+                *reinterpret_cast<u32x4 *>(vt + r0 * kPitch + 32 * c + 8 * j) = ld0 ? kin[c] : zero;
+            }
+        } else {
+            const int r = r0;
+            const bool ld = ld0;
+            float rt[D / 64][16];
+            load_rope<D>(a, j, ld ? p0 : 0, rt);
             float x[L::kChunks][8];
 #pragma unroll
             for (int c = 0; c < L::kChunks; ++c) {
-                u32x4 av = {0u, 0u, 0u, 0u};
-                if (ld) av = *reinterpret_cast<const u32x4 *>(krow + 32 * c + 8 * j);
 #pragma unroll
-                for (int e = 0; e < 8; ++e) x[c][e] = bf16_bits_to_f32((av[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
+                for (int e = 0; e < 8; ++e)
+                    x[c][e] = ld ? bf16_bits_to_f32((kin[c][e >> 1] >> (16 * (e & 1))) & 0xFFFFu) : 0.0f;
             }
             // (a row not loaded is zero: its result is discarded below)
-            norm_rope_row<D>(x, j, ld ? p : 0, a);
+            norm_rope_row<D>(x, j, rt, a);
+            load_values();
 #pragma unroll
             for (int c = 0; c < L::kChunks; ++c) {
                 u32x4 pk;
@@ -159,24 +186,16 @@ __global__ void __launch_bounds__(256, (BITS == 4 && ROPE) ? 3 : 4) append_kerne
                 for (int q = 0; q < 4; ++q) pk[q] = ld ? pack_bf16_rne(x[c][2 * q], x[c][2 * q + 1]) : 0u;
                 *reinterpret_cast<u32x4 *>(vt + r * kPitch + 32 * c + 8 * j) = pk;
             }
-            __syncthreads();
         }
-        KeyTile<D, kNtW> xf;
-        xf.load(a.tk, h, wave * kNtW, lane);
+        __syncthreads();
+        if constexpr (fused) xf.load(a.tk, h, wave * kNtW, lane);
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) {
             const int r = 16 * mt + n;  // A row handled by this lane
-            const int32_t p = blk_lo + r;
-            const bool ld = (p >= lo && p < hi && is_new(p) && do_new);
-            const uint16_t *krow = a.k_new + (((int64_t)b * a.max_new + (p - s_old)) * a.n_kv + h) * D;
             bf16x8 aop[L::kChunks];
 #pragma unroll
-            for (int c = 0; c < L::kChunks; ++c) {
-                u32x4 av = {0u, 0u, 0u, 0u};
-                if constexpr (fused) av = *reinterpret_cast<const u32x4 *>(vt + r * kPitch + 32 * c + 8 * j);
-                else if (ld) av = *reinterpret_cast<const u32x4 *>(krow + 32 * c + 8 * j);
-                aop[c] = __builtin_bit_cast(bf16x8, av);
-            }
+            for (int c = 0; c < L::kChunks; ++c)
+                aop[c] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(vt + r * kPitch + 32 * c + 8 * j));
             f32x4 acc[kNtW];
             xf.apply(aop, acc);
 #pragma unroll
@@ -193,7 +212,7 @@ __global__ void __launch_bounds__(256, (BITS == 4 && ROPE) ? 3 : 4) append_kerne
         }
         // the value rows are about to be overwritten: every wave must have
         // read its key operands from them
-        if constexpr (fused) __syncthreads();
+        __syncthreads();
     }
     // ring-sourced keys (flush) and all values, 16 B per thread-step
     {

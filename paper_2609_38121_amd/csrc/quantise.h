@@ -46,9 +46,30 @@ struct AppendArgs {
 // j = 0..3 of a 16-lane column group): lane j holds channels 32 c + 8 j + e
 // (c = 0..3, e = 0..7) in x[c][e].  The rotary partner of channel i < D/2
 // is i + D/2, chunk c + D/64 of the same lane, so the rotation is local.
-// Each step is a separately rounded fp32 operation.
+// Each step is a separately rounded fp32 operation.  The rotary table's
+// entries for this lane (cos in rt[c][0..7], sin in rt[c][8..15] for the
+// chunks c < D/64 of position pos) come from load_rope, so that their load
+// can be issued with the row's own.
 template <int D>
-__device__ __forceinline__ void norm_rope_row(float (&x)[D / 32][8], int j, int32_t pos,
+__device__ __forceinline__ void load_rope(const AppendArgs &a, int j, int32_t pos, float (&rt)[D / 64][16])
+{
+    const float *row = a.rope + (int64_t)pos * D;
+#pragma unroll
+    for (int c = 0; c < D / 64; ++c) {
+        const float *cs = row + 32 * c + 8 * j;
+        const float4 c0 = *reinterpret_cast<const float4 *>(cs);
+        const float4 c1 = *reinterpret_cast<const float4 *>(cs + 4);
+        const float4 s0 = *reinterpret_cast<const float4 *>(cs + D / 2);
+        const float4 s1 = *reinterpret_cast<const float4 *>(cs + D / 2 + 4);
+        const float v[16] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w,
+                             s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+#pragma unroll
+        for (int e = 0; e < 16; ++e) rt[c][e] = v[e];
+    }
+}
+
+template <int D>
+__device__ __forceinline__ void norm_rope_row(float (&x)[D / 32][8], int j, const float (&rt)[D / 64][16],
                                               const AppendArgs &a)
 {
     constexpr int kC = D / 32;
@@ -75,23 +96,23 @@ __device__ __forceinline__ void norm_rope_row(float (&x)[D / 32][8], int j, int3
 #pragma unroll
         for (int e = 0; e < 8; ++e) x[c][e] = (x[c][e] * r) * g[e];
     }
-    const float *row = a.rope + (int64_t)pos * D;
 #pragma unroll
     for (int c = 0; c < kC / 2; ++c) {
-        const float *cs = row + 32 * c + 8 * j;
-        const float4 c0 = *reinterpret_cast<const float4 *>(cs);
-        const float4 c1 = *reinterpret_cast<const float4 *>(cs + 4);
-        const float4 s0 = *reinterpret_cast<const float4 *>(cs + D / 2);
-        const float4 s1 = *reinterpret_cast<const float4 *>(cs + D / 2 + 4);
-        const float co[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
-        const float si[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             const float lo = x[c][e], hi = x[c + kC / 2][e];
-            x[c][e] = lo * co[e] - hi * si[e];
-            x[c + kC / 2][e] = hi * co[e] + lo * si[e];
+            x[c][e] = lo * rt[c][e] - hi * rt[c][8 + e];
+            x[c + kC / 2][e] = hi * rt[c][e] + lo * rt[c][8 + e];
         }
     }
+}
+
+template <int D>
+__device__ __forceinline__ void norm_rope_row(float (&x)[D / 32][8], int j, int32_t pos, const AppendArgs &a)
+{
+    float rt[D / 64][16];
+    load_rope<D>(a, j, pos, rt);
+    norm_rope_row<D>(x, j, rt, a);
 }
 
 // Sequence b's counters as they stand before this launch: thread 0 reads
