@@ -37,7 +37,7 @@ __global__ void __launch_bounds__(256, (BITS == 4 && ROPE) ? 3 : 4) append_kerne
     constexpr int kPitch = D + 8;  // bf16 elements per LDS row (16 B pad)
     __shared__ __attribute__((aligned(16))) uint16_t kt[kPage * kPitch];
     __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * kPitch];
-    __shared__ int32_t sh_page[2];  // page index, reduction word
+    __shared__ int32_t sh_page[1];  // page index
     __shared__ int32_t sh_cnt[3];   // the sequence's counters (read_counters)
 
     const int tid = threadIdx.x;
@@ -247,8 +247,14 @@ __global__ void __launch_bounds__(256, (BITS == 4 && ROPE) ? 3 : 4) append_kerne
     uint8_t *pg = page >= 0 ? a.pages + ((int64_t)page * a.n_kv + h) * L::kPageBytes : nullptr;
 
     // ---- phases B and C
+    // quant_now holds for every position of [blk_lo, blk_lo + 64) when the
+    // range lies in [lo, hi) and [start_old, q_new), its new positions are
+    // appended and its old ones flushed by this launch
+    const int32_t blk_end = blk_lo + kPage;
+    const bool all_quant = lo <= blk_lo && blk_end <= hi && start_old <= blk_lo && blk_end <= q_new &&
+                           (blk_end <= s_old || do_new) && (blk_lo >= s_old || do_flush);
     quantise_tile<D, BITS>(a, kt, vt, blk_lo, [&](int32_t p) { return p >= lo && p < hi && quant_now(p); },
-                           pg, sh_page + 1, tid);
+                           all_quant, pg, tid);
 
     // ---- phase D: bf16 windows and the optional k~ output (a tile of
     // the quantised region of a prefill has neither)
@@ -300,7 +306,7 @@ __global__ void __launch_bounds__(256) append_step_kernel(AppendArgs a)
     __shared__ __attribute__((aligned(16))) uint16_t kn[kStepMax * kPitch];
     __shared__ __attribute__((aligned(16))) uint16_t kt[kPage * kPitch];
     __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * kPitch];
-    __shared__ int32_t sh_page[2];  // page index, reduction word
+    __shared__ int32_t sh_page[1];  // page index
     __shared__ int32_t sh_cnt[3];   // the sequence's counters (read_counters)
 
     const int tid = threadIdx.x;
@@ -419,7 +425,7 @@ __global__ void __launch_bounds__(256) step_finish_kernel(AppendArgs a, FinishAr
     __shared__ __attribute__((aligned(16))) uint16_t vt[kPage * kPitch];
     __shared__ float fw[kMaxSplits];
     __shared__ float red[D];
-    __shared__ int32_t sh[5];  // page index, reduction word, the counters (read_counters)
+    __shared__ int32_t sh[4];  // page index, the counters (read_counters)
     const int tid = threadIdx.x, b = blockIdx.y;
     const int n_q = a.n_kv * f.G;
     if ((int)blockIdx.x < n_q) {
@@ -430,7 +436,7 @@ __global__ void __launch_bounds__(256) step_finish_kernel(AppendArgs a, FinishAr
         return;
     }
     const int h = (int)blockIdx.x - n_q;
-    const SeqCounters cnt = read_counters(a, b, 1, sh + 2, tid);
+    const SeqCounters cnt = read_counters(a, b, 1, sh + 1, tid);
     const int32_t s_old = cnt.s_old, q_old = cnt.q_old, nn = cnt.nn;
     const int32_t s_new = s_old + nn;
     const int32_t q_new = next_quant_end(s_new, q_old, a.s_sink, a.s_keep, a.s_flush);

@@ -476,24 +476,18 @@ __device__ void value_words(uint16_t *vt, int32_t blk_lo, Pred quant, bool full,
 // one page (pg, or null when the page is outside the pool): quantise every
 // position p with quant(p) from its bf16 rows in kt / vt (row p - blk_lo),
 // write its parameters and key words, then assemble the value words, merging
-// words only partly covered with what the page holds.  Every thread of the
-// workgroup must call it (it synchronises); red is one LDS word of the
-// caller's, used for a workgroup-wide AND (so that the kernels that inline
-// this need no LDS of the runtime's for it).
+// words only partly covered with what the page holds.  all_quant: the
+// caller's statement that quant(p) holds for every p of [blk_lo, blk_lo +
+// 64) (the common case of a prefill); the value words are then assembled
+// without per-code checks or merges.  Every thread of the workgroup must
+// call it (it synchronises).
 template <int D, int BITS, typename Pred>
 __device__ void quantise_tile(const AppendArgs &a, const uint16_t *kt, uint16_t *vt,
-                              int32_t blk_lo, Pred quant, uint8_t *pg, int32_t *red, int tid)
+                              int32_t blk_lo, Pred quant, bool all_quant, uint8_t *pg, int tid)
 {
     using L = Layout<D, BITS>;
     constexpr int kPitch = D + 8;
-    // every position of the tile quantised now (the common case of a
-    // prefill): the value words are then assembled without per-code checks
-    // or merges
-    if (tid == 0) *red = 1;
-    __syncthreads();
-    if (!(quant(blk_lo + ((tid >> 1) & (kPage - 1))) && pg != nullptr)) *red = 0;
-    __syncthreads();
-    const bool full = *red != 0;
+    const bool full = all_quant && pg != nullptr;
     // ---- phase B: quantise.  Lanes 2 r and 2 r + 1 share group r (rows
     // 0-63 keys, 64-127 values), one half of its channels each, so that all
     // four waves take part.
@@ -761,7 +755,7 @@ __device__ void quantise_few(const AppendArgs &a, uint16_t *kt, uint16_t *vt, in
 // before s_ring comes from the windows' ring (keys row-major, values
 // channel-major); one at or after it is a new token of this call, its key
 // already transformed in kn (LDS, pitch D + 8) and its value in v_new.  kt
-// and vt are 64-row LDS tiles, sh two LDS words.  Every thread of the
+// and vt are 64-row LDS tiles, sh one LDS word.  Every thread of the
 // 256-thread workgroup calls it.  kNewRows false: every position comes from
 // the ring (s_ring and kn unused).
 template <int D, int BITS, bool kNewRows>
@@ -818,8 +812,8 @@ __device__ void flush_range(const AppendArgs &a, int b, int h, int32_t start, in
         if (few)
             quantise_few<D, BITS>(a, kt, vt, blk, lo, hi, pg, tid);
         else
-            quantise_tile<D, BITS>(a, kt, vt, blk, [&](int32_t p) { return p >= lo && p < hi; }, pg, sh + 1,
-                                   tid);
+            quantise_tile<D, BITS>(a, kt, vt, blk, [&](int32_t p) { return p >= lo && p < hi; },
+                                   lo <= blk && blk + kPage <= hi, pg, tid);
         __syncthreads();
     }
 }
