@@ -164,7 +164,9 @@ typedef struct wushkv_cache {
     int32_t *commit;           /* [batch] caller-owned scratch, zero before the first
                                   append: the append's workgroups count their arrivals
                                   here so that the last of each sequence advances S and
-                                  S_quant; every completed call leaves it zero */
+                                  S_quant (an append of more than 64 tiles per sequence
+                                  advances them in a one-workgroup launch of its own
+                                  instead); every completed call leaves it zero */
 } wushkv_cache;
 
 /* Bytes of one (page, head) block, or 0 for unsupported (head_dim, bits):

@@ -58,7 +58,6 @@ __global__ void __launch_bounds__(256, (BITS == 4 && ROPE) ? 3 : 4) append_kerne
     const int32_t s_old = cnt.s_old, q_old = cnt.q_old, nn = cnt.nn;
     const int32_t s_new = s_old + nn;
     const int32_t q_new = next_quant_end(s_new, q_old, a.s_sink, a.s_keep, a.s_flush);
-    const int32_t arrived = commit_arrive(a, b, s_old, q_old, nn, tid);
     const int32_t start_old = q_old > a.s_sink ? q_old : a.s_sink;
     const int32_t first = s_old < start_old ? s_old : start_old;
     const int32_t ring = a.win_slots - a.s_sink;
@@ -83,7 +82,7 @@ __global__ void __launch_bounds__(256, (BITS == 4 && ROPE) ? 3 : 4) append_kerne
         hi = min(hi, min(s_old, q_new));
     }
     if (lo >= hi) {
-        commit_finish(a, b, arrived, s_new, q_new, tid);
+        commit_finish(a, b, commit_arrive(a, b, s_old, q_old, nn, tid), s_new, q_new, tid);
         return;
     }
 
@@ -214,6 +213,12 @@ __global__ void __launch_bounds__(256, (BITS == 4 && ROPE) ? 3 : 4) append_kerne
         // read its key operands from them
         __syncthreads();
     }
+    // The arrival (thread 0) comes after the tile's key and value loads
+    // have landed: an atomic on the sequence's count, shared by every tile
+    // of the sequence, can take long to return, and the vector memory
+    // counter would make every later wait for a load wait for it too.  Its
+    // result is needed only at the end.
+    const int32_t arrived = commit_arrive(a, b, s_old, q_old, nn, tid);
     // ring-sourced keys (flush) and all values, 16 B per thread-step
     {
 #pragma unroll
@@ -396,6 +401,24 @@ static hipError_t launch_append(const char *name, const AppendArgs &a, dim3 grid
     return hipGetLastError();
 }
 
+// S and S_quant of every sequence advanced after an append launch of many
+// tiles, which then counts no arrivals (thousands of workgroups of one
+// sequence would queue their device-scope atomics at one address, and each
+// holds its slot until its own returns).  Launched after it on the stream,
+// so that every tile has read the old values.  One thread per sequence; the
+// new-token count is clamped as read_counters clamps it.
+__global__ void __launch_bounds__(256) append_commit_kernel(AppendArgs a, int32_t batch)
+{
+    const int b = (int)(blockIdx.x * 256 + threadIdx.x);
+    if (b >= batch) return;
+    const int32_t s_old = a.seq_len[b], q_old = a.quant_end[b];
+    int32_t nn = a.n_new[b];
+    nn = nn < 0 ? 0 : (nn > a.max_new ? a.max_new : nn);
+    const int32_t s_new = s_old + nn;
+    a.seq_len[b] = s_new;
+    a.quant_end[b] = next_quant_end(s_new, q_old, a.s_sink, a.s_keep, a.s_flush);
+}
+
 template <int D, int BITS>
 static hipError_t launch_append_step(const AppendArgs &a, dim3 grid, hipStream_t s)
 {
@@ -539,21 +562,31 @@ static int append_impl(const wushkv_cache *c, const uint16_t *k_new, const uint1
     const dim3 flush_grid((unsigned)std::min<int64_t>(tiles, (a.sink_tiles + (ring + kPage - 1) / kPage + 1 + 7) / 8 * 8),
                           grid.y, grid.z);
 
-    // the launch that appends the new tokens advances the counters (its
-    // workgroups are the last to read them)
+    // The launch that appends the new tokens advances the counters (its
+    // workgroups are the last to read them): its last arriving workgroup
+    // does, or, beyond kArrivalsMax workgroups per sequence, a launch of its
+    // own right after it.
+    constexpr int64_t kArrivalsMax = 64;
     auto go = [&](int mode) -> hipError_t {
         a.mode = mode;
         const char *name = mode == kModeFlush ? "append_flush" : "append_kernel";
         const dim3 g = mode == kModeFlush ? flush_grid : grid;
-        a.arrivals = (mode & kModeNew) ? (int32_t)(g.x * g.y) : 0;
+        const bool commit_launch = (mode & kModeNew) && (int64_t)g.x * g.y > kArrivalsMax;
+        a.arrivals = (mode & kModeNew) && !commit_launch ? (int32_t)(g.x * g.y) : 0;
         const int key = c->head_dim * 10 + storage_bits(c->bits);
+        hipError_t e = hipErrorInvalidValue;
         switch (key) {
-            case 1282: return launch_append<128, 2>(name, a, g, s);
-            case 1284: return launch_append<128, 4>(name, a, g, s);
-            case 642: return launch_append<64, 2>(name, a, g, s);
-            case 644: return launch_append<64, 4>(name, a, g, s);
+            case 1282: e = launch_append<128, 2>(name, a, g, s); break;
+            case 1284: e = launch_append<128, 4>(name, a, g, s); break;
+            case 642: e = launch_append<64, 2>(name, a, g, s); break;
+            case 644: e = launch_append<64, 4>(name, a, g, s); break;
         }
-        return hipErrorInvalidValue;
+        if (e == hipSuccess && commit_launch) {
+            launch("append_commit", append_commit_kernel, dim3((unsigned)((c->batch + 255) / 256)), dim3(256), s, a,
+                   (int32_t)c->batch);
+            e = hipGetLastError();
+        }
+        return e;
     };
     hipError_t e;
     if (max_new <= kStepMax) {
