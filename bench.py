@@ -741,8 +741,10 @@ def bench_prefill(torch, wk, synth, dev, args):
         torch.cuda.synchronize()
         cnt, tot = wk.wushkv_timing_read("append_kernel")
         fcnt, ftot = wk.wushkv_timing_read("append_flush")
+        ccnt, ctot = wk.wushkv_timing_read("append_commit")
         wk.wushkv_timing_enable(0)
-        res[name] = (float(np.median(times)), tot / cnt, ftot / fcnt if fcnt else 0.0)
+        res[name] = (float(np.median(times)), tot / cnt, ftot / fcnt if fcnt else 0.0,
+                     ctot / ccnt if ccnt else 0.0)
     tokens = B * n
     Q = int(cache.quant_end[0].item())
     n_quant = Q - cfg["s_sink"]
@@ -750,12 +752,12 @@ def bench_prefill(torch, wk, synth, dev, args):
     table_bytes = n * D * 4  # the rotary table rows of the positions written
     out = None
     for name in ("norm_rope", "prenormed", "quest"):
-        ms, t_kernel, t_flush = res[name]
+        ms, t_kernel, t_flush, t_commit = res[name]
         b_ = byts + (table_bytes if name != "prenormed" else 0)
         ach = b_ / (t_kernel * 1e-3) / 1e9
         log("prefill append (%s): %.1f us/call, %.3g tokens/s, append_kernel %.1f us, %.1f GB/s "
-            "(flush-only launch %.1f us)" % (name, ms * 1e3, tokens / (ms * 1e-3), t_kernel * 1e3,
-                                             ach, t_flush * 1e3))
+            "(flush-only launch %.1f us, counter launch %.1f us)"
+            % (name, ms * 1e3, tokens / (ms * 1e-3), t_kernel * 1e3, ach, t_flush * 1e3, t_commit * 1e3))
         tkey = {"norm_rope": "traffic_bytes_per_launch", "prenormed": "traffic_bytes_per_launch_prenormed",
                 "quest": "traffic_bytes_per_launch_quest"}[name]
         traffic = profiled_traffic("append_kernel_prefill_4x16384_2bit.md",
@@ -767,6 +769,7 @@ def bench_prefill(torch, wk, synth, dev, args):
                               "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": traffic,
                               "avg_us": round(t_kernel * 1e3, 3)},
                  "flush_launch_us": round(t_flush * 1e3, 3),
+                 "counter_launch_us": round(t_commit * 1e3, 3),
                  "roofline_tokens_per_s": round(tokens / (b_ / (PEAK_HBM_GBS * 1e9)), 1)}
         if out is None:
             out = dict(entry, workload="prefill-append-4x16384-2bit, RMS norm + RoPE fused",
