@@ -168,14 +168,14 @@ __global__ void __launch_bounds__(256, (BITS == 4 && ROPE) ? 3 : 4) append_kerne
             const bool ld = ld0;
             float rt[D / 64][16];
             load_rope<D>(a, j, ld ? p0 : 0, rt);
+            // (a row that is not new holds the first row of k_new here: its
+            // result is replaced by zeros below)
             float x[L::kChunks][8];
 #pragma unroll
             for (int c = 0; c < L::kChunks; ++c) {
 #pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    x[c][e] = ld ? bf16_bits_to_f32((kin[c][e >> 1] >> (16 * (e & 1))) & 0xFFFFu) : 0.0f;
+                for (int e = 0; e < 8; ++e) x[c][e] = bf16_bits_to_f32((kin[c][e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
             }
-            // (a row not loaded is zero: its result is discarded below)
             norm_rope_row<D>(x, j, rt, a);
             load_values();
 #pragma unroll

@@ -81,20 +81,21 @@ __device__ __forceinline__ void norm_rope_row(float (&x)[D / 32][8], int j, cons
     ss += __shfl_xor(ss, 16);
     ss += __shfl_xor(ss, 32);
     const float r = 1.0f / sqrtf(ss / (float)D + a.eps);
+    // (x r) g, or x r with no gain (a product by 1 is exact)
+    if (a.gain != nullptr) {
 #pragma unroll
-    for (int c = 0; c < kC; ++c) {
-        float g[8];
-        if (a.gain != nullptr) {
+        for (int c = 0; c < kC; ++c) {
             const float4 g0 = *reinterpret_cast<const float4 *>(a.gain + 32 * c + 8 * j);
             const float4 g1 = *reinterpret_cast<const float4 *>(a.gain + 32 * c + 8 * j + 4);
-            g[0] = g0.x; g[1] = g0.y; g[2] = g0.z; g[3] = g0.w;
-            g[4] = g1.x; g[5] = g1.y; g[6] = g1.z; g[7] = g1.w;
-        } else {
+            const float g[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
 #pragma unroll
-            for (int e = 0; e < 8; ++e) g[e] = 1.0f;
+            for (int e = 0; e < 8; ++e) x[c][e] = (x[c][e] * r) * g[e];
         }
+    } else {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) x[c][e] = (x[c][e] * r) * g[e];
+        for (int c = 0; c < kC; ++c)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[c][e] = x[c][e] * r;
     }
 #pragma unroll
     for (int c = 0; c < kC / 2; ++c) {
