@@ -113,15 +113,19 @@ __global__ void __launch_bounds__(256, (BITS == 4 && ROPE) ? 3 : 4) append_kerne
     // staged (idx = tid + 256 q is row idx / kVec, 16-byte chunk idx % kVec)
     constexpr int kVec = D / 8;                   // uint4 per row
     constexpr int kVPer = kPage * kVec / 256;     // uint4 per thread
+    constexpr int kVRows = 256 / kVec;            // rows between a thread's chunks
     uint4 vpre[kVPer];
     auto load_values = [&]() {
+        // the thread's chunks lie kVRows token rows apart in v_new: one
+        // address, then a constant step
+        const int r0v = tid / kVec, cv = tid % kVec;
+        const int64_t step = (int64_t)kVRows * a.n_kv * D;
+        const uint16_t *src = a.v_new + (((int64_t)b * a.max_new + (blk_lo + r0v - s_old)) * a.n_kv + h) * D + 8 * cv;
 #pragma unroll
         for (int q = 0; q < kVPer; ++q) {
-            const int idx = tid + 256 * q, r = idx / kVec, cv = idx % kVec;
-            const int32_t p = blk_lo + r;
+            const int32_t p = blk_lo + r0v + kVRows * q;
             if (p >= lo && p < hi && do_new && is_new(p))
-                vpre[q] = *reinterpret_cast<const uint4 *>(
-                    a.v_new + (((int64_t)b * a.max_new + (p - s_old)) * a.n_kv + h) * D + 8 * cv);
+                vpre[q] = *reinterpret_cast<const uint4 *>(src + q * step);
         }
     };
     if constexpr (!ROPE) load_values();
