@@ -82,6 +82,10 @@ __device__ __forceinline__ void norm_rope_row(float (&x)[D / 32][8], int j, cons
     ss += __shfl_xor(ss, 32);
     const float r = 1.0f / sqrtf(ss / (float)D + a.eps);
     // (x r) g, or x r with no gain (a product by 1 is exact)
+#pragma unroll
+    for (int c = 0; c < kC; ++c)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[c][e] = x[c][e] * r;
     if (a.gain != nullptr) {
 #pragma unroll
         for (int c = 0; c < kC; ++c) {
@@ -89,13 +93,8 @@ __device__ __forceinline__ void norm_rope_row(float (&x)[D / 32][8], int j, cons
             const float4 g1 = *reinterpret_cast<const float4 *>(a.gain + 32 * c + 8 * j + 4);
             const float g[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
 #pragma unroll
-            for (int e = 0; e < 8; ++e) x[c][e] = (x[c][e] * r) * g[e];
+            for (int e = 0; e < 8; ++e) x[c][e] = x[c][e] * g[e];
         }
-    } else {
-#pragma unroll
-        for (int c = 0; c < kC; ++c)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) x[c][e] = x[c][e] * r;
     }
 #pragma unroll
     for (int c = 0; c < kC / 2; ++c) {
