@@ -141,13 +141,15 @@ __device__ __forceinline__ SeqCounters read_counters(const AppendArgs &a, int b,
 // Sequence b's counters advance from inside the launch that last reads
 // them.  Each workgroup reports once, after its reads of seq_len and
 // quant_end have returned (the values are tied to the report's operand), to
-// the sequence's arrival count (commit_arrive, at the start); the workgroup
-// that was last of a.arrivals writes S_new and S_quant_new and clears the
-// count for the next call (commit_finish, at its end, so that the count's
-// round trip overlaps its work).  Every workgroup of the sequence has read
-// the old values before the last one arrives, so none can see the new ones:
-// the other waves of a workgroup use thread 0's reads (read_counters).
-// Thread 0 only; a launch with a.arrivals = 0 leaves the counters alone.
+// the sequence's arrival count (commit_arrive, early in the workgroup's
+// work); the workgroup that was last of a.arrivals writes S_new and
+// S_quant_new and clears the count for the next call (commit_finish, at its
+// end, so that the count's round trip overlaps its work).  Every workgroup
+// of the sequence has read the old values before the last one arrives, so
+// none can see the new ones: the other waves of a workgroup use thread 0's
+// reads (read_counters).  Thread 0 only; a launch with a.arrivals = 0 leaves
+// the counters alone (a launch of many workgroups per sequence does, and
+// append_commit_kernel advances them after it).
 __device__ __forceinline__ int32_t commit_arrive(const AppendArgs &a, int b, int32_t s_old, int32_t q_old,
                                                  int32_t nn, int tid)
 {
