@@ -28,10 +28,9 @@
 namespace wushkv {
 
 // Four workgroups per compute unit (their LDS fits four times): the
-// registers are held to what four waves per SIMD leave (the 4-bit variant
-// with the fused normalisation would spill there, so it keeps three).
+// registers are held to what four waves per SIMD leave.
 template <int D, int BITS, bool ROPE>
-__global__ void __launch_bounds__(256, (BITS == 4 && ROPE) ? 3 : 4) append_kernel(AppendArgs a)
+__global__ void __launch_bounds__(256, 4) append_kernel(AppendArgs a)
 {
     using L = Layout<D, BITS>;
     constexpr int kPitch = D + 8;  // bf16 elements per LDS row (16 B pad)
