@@ -424,6 +424,41 @@ def bench_bigbatch(torch, wk, synth, dev, args):
     return res, sample
 
 
+def bench_dequant(torch, wk, cache, B, H, D, bits, s_sink):
+    """Reconstruction of stored entries (wushkv_dequant, Eq. (7)'s x =
+    scale code + zero) of every quantised position of each sequence of a
+    Llama-shaped cache: one launch per sequence, fp32 K and V out
+    [kv heads][positions][d], the outputs rotated over four buffer pairs
+    (beyond the 256 MB Infinity Cache).  Algorithmic bytes per launch: the
+    codes and the two (scale, zero) pairs per token-head read (d bits / 4 +
+    8 B: 72 B at d 128, 2 bits), 8 d B per token-head written; timed by the
+    library's per-launch events."""
+    qe = cache.quant_end.cpu().numpy()
+    count = int(qe.min()) - s_sink
+    outs = [(torch.empty((H, count, D), dtype=torch.float32, device=cache.device),
+             torch.empty((H, count, D), dtype=torch.float32, device=cache.device)) for _ in range(4)]
+    for b in range(B):
+        wk.wushkv_dequant(cache, b, s_sink, count, *outs[b % 4])
+    torch.cuda.synchronize()
+    rounds = 4
+    wk.wushkv_timing_enable(rounds * B + 8)
+    for r in range(rounds):
+        for b in range(B):
+            wk.wushkv_dequant(cache, b, s_sink, count, *outs[(r * B + b) % 4])
+    torch.cuda.synchronize()
+    cnt, tot = wk.wushkv_timing_read("dequant_kernel")
+    wk.wushkv_timing_enable(0)
+    t = tot / cnt * 1e-3  # seconds per launch
+    per_launch = H * count * (D * bits // 4 + 8 + 8 * D)
+    ach = per_launch / t / 1e9
+    del outs
+    log("dequant: %d positions x %d kv heads per launch, %.1f us, %.1f GB/s" % (count, H, t * 1e6, ach))
+    return {"positions_per_launch": count, "kv_heads": H, "launches": int(cnt),
+            "roofline": {"bound": "hbm", "kernel": "dequant_kernel", "achieved": round(ach, 2),
+                         "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
+                         "traffic": None, "avg_us": round(t * 1e6, 3), "bytes_per_launch": int(per_launch)}}
+
+
 def bench_llama_step(torch, wk, synth, dev, args):
     """The Llama-3-8B-shaped decode layer (batch 8, 32 query / 8 kv heads,
     d 128, 8192-token context, 2-bit): one step appends one token per
@@ -459,6 +494,7 @@ def bench_llama_step(torch, wk, synth, dev, args):
     wk.wushkv_append(base, as_dev(k), as_dev(v), torch.full((B,), ctx, dtype=torch.int32, device=dev), tk)
     torch.cuda.synchronize()
     del k, v
+    dequant = bench_dequant(torch, wk, base, B, H, D, BITS, cfg["s_sink"])
     cache_bytes = base.pages.numel() + 2 * base.win_k.numel() * 2
     reps = max(1, math.ceil(2 * MALL_BYTES / cache_bytes))
     caches = [base] + [base.clone() for _ in range(reps - 1)]
@@ -671,6 +707,7 @@ def bench_llama_step(torch, wk, synth, dev, args):
         "decode_call_us": round(ms_dec * 1e3, 3),
         "eager_step_us": round(ms_eager * 1e3, 3),
         "kernel_avg_us": {k_: (round(v_ * 1e3, 3) if v_ else None) for k_, v_ in kernels.items()},
+        "dequant": dequant,
     }
     state = (caches, reps, k1, tk, tinv_d, B, NQ, D, max_seq, sm, cfg, lengths_at, done)
     return fused, state

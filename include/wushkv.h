@@ -386,7 +386,8 @@ size_t wushkv_chunk_workspace_bytes(const wushkv_cache *c, int32_t n_q_heads,
 /*
  * wushkv_dequant -- reconstruct stored entries x = scale * code + zero
  * (Eq. (7), last term) of sequence b, positions [start, start + count).
- *   k_out, v_out  fp32 [n_kv_heads][count][head_dim] (either may be null).
+ *   k_out, v_out  fp32 [n_kv_heads][count][head_dim] (either may be null;
+ *                 16-byte aligned, or the call fails with WUSHKV_EINVAL).
  * Positions must satisfy start >= s_sink and start + count <= s_sink + 64 *
  * max_pages_per_seq (host-checked).  The pages are decoded as stored,
  * whether or not quant_end has reached the position; a logical page whose

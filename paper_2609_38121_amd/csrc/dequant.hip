@@ -1,6 +1,7 @@
 // wushkv_dequant: reconstruct stored entries x = scale * code + zero
 // (Eq. (7), last term) straight from the packed pages.  One thread per
-// (position, channel); reads the page layout of include/wushkv.h.
+// (position, four consecutive channels), written as one 16-byte store per
+// output; reads the page layout of include/wushkv.h.
 #include "common.h"
 
 namespace wushkv {
@@ -12,36 +13,55 @@ __global__ void __launch_bounds__(256) dequant_kernel(const uint8_t *pages, cons
                                                       int32_t count, float *k_out, float *v_out)
 {
     using L = Layout<D, BITS>;
+    constexpr int kQuads = D / 4;  // threads per position
+    // four consecutive channels from a multiple of 4 share one key word:
+    // a word spans 32 / BITS >= 8 channels, aligned to its span
+    static_assert(32 / BITS >= 8, "four key channels per word");
     const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int h = blockIdx.y;
-    if (idx >= (int64_t)count * D) return;
-    const int32_t pos = start + (int32_t)(idx / D);
-    const int ch = (int)(idx % D);
+    if (idx >= (int64_t)count * kQuads) return;
+    const int32_t pos = start + (int32_t)(idx / kQuads);
+    const int ch0 = 4 * (int)(idx % kQuads);
     const int32_t rel = pos - s_sink;
     const int32_t lp = rel / kPage, t = rel % kPage;
     const int32_t phys = lp < max_pages ? page_table[(int64_t)b * max_pages + lp] : -1;
-    const int64_t o = ((int64_t)h * count + (pos - start)) * D + ch;
+    const int64_t o = ((int64_t)h * count + (pos - start)) * D + ch0;
     if (phys < 0 || phys >= n_pages) {
-        if (k_out) k_out[o] = NAN;
-        if (v_out) v_out[o] = NAN;
+        const float4 nan4 = make_float4(NAN, NAN, NAN, NAN);
+        if (k_out) *reinterpret_cast<float4 *>(k_out + o) = nan4;
+        if (v_out) *reinterpret_cast<float4 *>(v_out + o) = nan4;
         return;
     }
     const uint8_t *pg = pages + ((int64_t)phys * n_kv + h) * L::kPageBytes;
     const uint32_t *w = reinterpret_cast<const uint32_t *>(pg);
     const uint32_t *pk = reinterpret_cast<const uint32_t *>(pg + L::kParamOffset);
     const uint32_t mask = (1u << BITS) - 1u;
-    int word, bit;
     if (k_out) {
-        L::k_pos(t, ch, word, bit);
-        const uint32_t code = (w[word] >> bit) & mask;
+        int word, bit;
+        L::k_pos(t, ch0, word, bit);
+        const uint32_t kw = w[word];
         const uint32_t prm = pk[t];
-        k_out[o] = fmaf(f16_bits_to_f32(prm & 0xFFFFu), (float)code, f16_bits_to_f32(prm >> 16));
+        const float sc = f16_bits_to_f32(prm & 0xFFFFu), zr = f16_bits_to_f32(prm >> 16);
+        float r[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            int we, be;
+            L::k_pos(t, ch0 + e, we, be);
+            r[e] = fmaf(sc, (float)((kw >> be) & mask), zr);
+        }
+        *reinterpret_cast<float4 *>(k_out + o) = make_float4(r[0], r[1], r[2], r[3]);
     }
     if (v_out) {
-        L::v_pos(t, ch, word, bit);
-        const uint32_t code = (w[L::kRegionBytes / 4 + word] >> bit) & mask;
         const uint32_t prm = pk[kPage + t];
-        v_out[o] = fmaf(f16_bits_to_f32(prm & 0xFFFFu), (float)code, f16_bits_to_f32(prm >> 16));
+        const float sc = f16_bits_to_f32(prm & 0xFFFFu), zr = f16_bits_to_f32(prm >> 16);
+        float r[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            int we, be;
+            L::v_pos(t, ch0 + e, we, be);
+            r[e] = fmaf(sc, (float)((w[L::kRegionBytes / 4 + we] >> be) & mask), zr);
+        }
+        *reinterpret_cast<float4 *>(v_out + o) = make_float4(r[0], r[1], r[2], r[3]);
     }
 }
 
@@ -60,9 +80,9 @@ extern "C" int wushkv_dequant(const wushkv_cache *c, int32_t b, int32_t start, i
     if ((int64_t)start + count > (int64_t)c->s_sink + (int64_t)kPage * c->max_pages_per_seq)
         return WUSHKV_EINVAL;
     if (count == 0 || (!k_out && !v_out)) return WUSHKV_OK;
-    if (((uintptr_t)k_out | (uintptr_t)v_out) & 3u) return WUSHKV_EINVAL;
+    if (((uintptr_t)k_out | (uintptr_t)v_out) & 15u) return WUSHKV_EINVAL;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const int64_t n = (int64_t)count * c->head_dim;
+    const int64_t n = (int64_t)count * (c->head_dim / 4);
     if ((n + 255) / 256 > 0x7FFFFFFF) return WUSHKV_EINVAL;
     dim3 grid((unsigned)((n + 255) / 256), (unsigned)c->n_kv_heads);
     const int key = c->head_dim * 10 + storage_bits(c->bits);
