@@ -116,15 +116,16 @@ __global__ void __launch_bounds__(256, 4) append_kernel(AppendArgs a)
     uint4 vpre[kVPer];
     auto load_values = [&]() {
         // the thread's chunks lie kVRows token rows apart in v_new: one
-        // address, then a constant step
+        // element offset, then a constant step (negative for rows before
+        // the new ones, which are not loaded)
         const int r0v = tid / kVec, cv = tid % kVec;
         const int64_t step = (int64_t)kVRows * a.n_kv * D;
-        const uint16_t *src = a.v_new + (((int64_t)b * a.max_new + (blk_lo + r0v - s_old)) * a.n_kv + h) * D + 8 * cv;
+        const int64_t off0 = (((int64_t)b * a.max_new + (blk_lo + r0v - s_old)) * a.n_kv + h) * D + 8 * cv;
 #pragma unroll
         for (int q = 0; q < kVPer; ++q) {
             const int32_t p = blk_lo + r0v + kVRows * q;
             if (p >= lo && p < hi && do_new && is_new(p))
-                vpre[q] = *reinterpret_cast<const uint4 *>(src + q * step);
+                vpre[q] = *reinterpret_cast<const uint4 *>(a.v_new + (off0 + q * step));
         }
     };
     if constexpr (!ROPE) load_values();
